@@ -1,0 +1,19 @@
+"""CPU oracle for the convolution hot path.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the bench's CPU
+baseline may import this package; the product library never does.  It shares
+no code with the HIP path.  See ``ref_conv.c`` for the operator definition it
+writes out, and ``ref.py`` for the numpy-facing wrapper.
+"""
+from .ref import (  # noqa: F401
+    build,
+    lib_path,
+    out_dims,
+    conv2d,
+    conv2d_bf16,
+    dwconv2d,
+    maxpool2d,
+    add_act,
+    f32_to_bf16,
+    bf16_to_f32,
+)
