@@ -1,0 +1,210 @@
+"""Conv hot-path benchmark on one MI355X.
+
+A step is one pass of a network's whole conv stack, layer by layer, over one
+batch of seeded synthetic input already resident in HBM: every layer's input,
+weights and bias are drawn once (their own seeds, the configuration's value
+distributions) and every layer writes its own output buffer, so the timed
+region holds only conv kernels.  The default workload is the ResNet-50 v1
+conv stack at batch 1 in fp32 (53 convs); --config picks another.
+
+Prints one JSON line with the conv TFLOP/s of the step, ms per image, the
+roofline of the dominant kernel (the kernel with the largest summed time,
+timed live with HIP events around each of its launches on the launch
+stream) and the CPU oracle timed on a bounded sample of the same stack.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_BF16_MFMA_TFLOPS = 2516.6
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--batch", type=int, default=None, help="override the config's batch")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="budget for the CPU-oracle baseline (0 disables it)")
+    ap.add_argument("--layers", action="store_true", help="also print a per-layer table to stderr")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1907_02154_amd import miconv
+    from paper_1907_02154_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    miconv.lib()
+    wk = wl.workload(args.config, args.batch)
+    bf16 = wk.dtype == "bf16"
+
+    # Resident inputs, weights, biases and outputs for every layer.
+    layers = []
+    for i, l in enumerate(wk.layers):
+        x, w, b = wl.layer_tensors(args.config, i, l)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        if bf16:
+            tx = torch.from_numpy(wl.to_bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
+            tw = torch.from_numpy(wl.to_bf16_bits(w).view(np.int16)).cuda().view(torch.bfloat16)
+        else:
+            tx = torch.from_numpy(x).cuda()
+            tw = torch.from_numpy(w).cuda()
+        tb = torch.from_numpy(b).cuda()
+        ty = torch.empty((l.N, l.K, P, Q), device="cuda")
+        name, launches = miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad,
+                                                l.groups, wk.dtype)
+        fl = wl.flops(l, P, Q)
+        elem_in = 2 if bf16 else 4
+        nbytes = (x.size + w.size) * elem_in + (b.size + l.N * l.K * P * Q) * 4
+        layers.append(dict(layer=l, idx=i, x=tx, w=tw, b=tb, y=ty, P=P, Q=Q, kernel=name,
+                           launches=launches, flops=fl, bytes=nbytes, host=(x, w, b)))
+    torch.cuda.synchronize()
+
+    def launch(d):
+        l = d["layer"]
+        if bf16:
+            miconv.conv2d_fwd_bf16(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu)
+        elif l.kind == "dw":
+            miconv.dwconv2d_fwd(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.relu)
+        else:
+            miconv.conv2d_fwd(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu)
+
+    for _ in range(args.warmup):
+        for d in layers:
+            launch(d)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    K = args.steps
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in layers] for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for k in range(K):
+        for j, d in enumerate(layers):
+            ev[k][j][0].record(stream)
+            launch(d)
+            ev[k][j][1].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_per_step = ms_total / K
+
+    per_layer_ms = np.array([[ev[k][j][0].elapsed_time(ev[k][j][1]) for j in range(len(layers))]
+                             for k in range(K)])
+    layer_ms = per_layer_ms.mean(axis=0)
+    step_flops = sum(d["flops"] for d in layers)
+    tflops = step_flops / (ms_per_step * 1e-3) / 1e12
+
+    # Dominant kernel: the largest summed time per kernel name.
+    groups = {}
+    for j, d in enumerate(layers):
+        g = groups.setdefault(d["kernel"], dict(ms=0.0, flops=0, bytes=0, launches=0, layers=[]))
+        g["ms"] += layer_ms[j]
+        g["flops"] += d["flops"]
+        g["bytes"] += d["bytes"]
+        g["launches"] += d["launches"]
+        g["layers"].append(d["layer"].name)
+    dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
+    avg_launch_us = dom["ms"] / dom["launches"] * 1e3
+    if dom_name.startswith("dw"):
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(achieved, 2), peak=PEAK_HBM_GBS, unit="GB/s",
+                    frac=round(achieved / PEAK_HBM_GBS, 4))
+    else:
+        peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
+        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
+                    frac=round(achieved / peak, 4))
+    roof.update(traffic=None, kernel=dom_name, launches_per_step=dom["launches"],
+                avg_launch_us=round(avg_launch_us, 3),
+                share_of_step=round(dom["ms"] / float(layer_ms.sum()), 4))
+
+    if args.layers:
+        for j, d in enumerate(layers):
+            l = d["layer"]
+            t = layer_ms[j]
+            print(f"{j:3d} {l.name:10s} {d['kernel']:45s} {t * 1e3:9.2f} us "
+                  f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s",
+                  file=sys.stderr)
+
+    # CPU baseline: the oracle on a bounded prefix of the same layers.
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        done_flops, t_cpu, sample = 0, 0.0, []
+        for d in layers:
+            l = d["layer"]
+            x, w, b = d["host"]
+            t0 = time.perf_counter()
+            if bf16:
+                oracle.conv2d_bf16(wl.to_bf16_bits(x), wl.to_bf16_bits(w), b, l.stride, l.pad,
+                                   l.groups, l.relu)
+            elif l.kind == "dw":
+                oracle.dwconv2d(x, w, b, l.stride, l.pad, l.relu)
+            else:
+                oracle.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+            t_cpu += time.perf_counter() - t0
+            done_flops += d["flops"]
+            sample.append(l.name)
+            if t_cpu > args.cpu_seconds:
+                break
+        cpu = dict(value=round(done_flops / t_cpu / 1e12, 6), unit="TFLOP/s",
+                   cores=oracle.num_threads(), kind="oracle",
+                   sample=f"{len(sample)} of {len(layers)} layers ({sample[0]}..{sample[-1]}), "
+                          f"{done_flops / 1e9:.3f} GFLOP in {t_cpu:.2f} s, fp64 accumulation")
+
+    out = {
+        "metric": "conv TFLOP/s and ms/image (ResNet-50 convs, b=1 & b=64); % MFMA/HBM peak",
+        "value": round(tflops, 4),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_image": round(ms_per_step / wk.layers[0].N, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-in/f32-acc" if bf16 else "f32",
+        "data": "synthetic (seeded uniform/He-normal per layer, resident in HBM)",
+        "config": {"workload": wk.name, "convs": len(layers), "batch": wk.layers[0].N,
+                   "gflop_per_step": round(step_flops / 1e9, 4), "device": torch.cuda.get_device_name(0),
+                   "wall_s_timed": round(wall, 4)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

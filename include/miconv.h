@@ -1,0 +1,133 @@
+/*
+ * miconv — the convolution hot path of CNN inference on AMD Instinct MI355X
+ * (gfx950): dense conv2d, depthwise conv2d and the glue operators of the
+ * evaluated networks.  C ABI, no C++ or framework types.
+ *
+ * The paper optimises the Conv2D operator of CNN inference (Sec. 3.2.2:
+ * spatial packing / loop tiling, output channels split across work-groups,
+ * feature map split along its height, unrolled loop nests) and keeps the
+ * operator's semantics (Sec. 4.2, Sec. 5).  The operator computed here is:
+ *
+ *   P = floor((H + 2*pad - R) / stride) + 1,   Q = floor((W + 2*pad - S) / stride) + 1
+ *   y[n][k][p][q] = act( bias[k] + sum_{c < C/groups, r < R, s < S}
+ *                        x[n][g*(C/groups) + c][p*stride - pad + r][q*stride - pad + s]
+ *                        * w[k][c][r][s] ),     g = k / (K/groups)
+ *
+ * cross-correlation (no kernel flip), symmetric zero padding, act = ReLU when
+ * relu != 0 else identity.
+ *
+ * Conventions shared by every entry point
+ *  - Layouts (all contiguous, row-major): x [N][C][H][W], w [K][C/groups][R][S],
+ *    bias [K] (may be NULL: no bias), y [N][K][P][Q].
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never frees them.  x, w, bias must not overlap y.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Calls are asynchronous: they validate, enqueue kernels on `stream` and
+ *    return.  Launch errors are returned; faults inside a kernel surface at
+ *    the caller's next synchronisation.
+ *  - Return 0 (MICONV_OK) on success or a negative miconv_status.  On a
+ *    validation error nothing is enqueued.
+ *  - Tensor extents are limited to 2^31-1 elements each (MICONV_ERR_TOO_LARGE).
+ *  - Dilation is not supported (the evaluated networks use none).
+ *  - Entry points are thread-safe.  The split-K path of the dense conv keeps
+ *    fp32 partial sums in a library-owned device workspace, one per
+ *    (device, stream) pair, allocated by the first call on that stream that
+ *    needs it and grown (hipMalloc) only when a larger layer arrives; it is
+ *    released at process exit.  Calls on one stream are ordered by the
+ *    stream, so they never race on it.  Capture such calls in a graph only
+ *    after one eager call of the same or a larger layer on that stream.
+ */
+#ifndef MICONV_H
+#define MICONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum miconv_status {
+    MICONV_OK = 0,
+    MICONV_ERR_NULL = -1,        /* x, w or y is NULL */
+    MICONV_ERR_SHAPE = -2,       /* a dim <= 0, stride < 1, pad < 0, or P or Q < 1 */
+    MICONV_ERR_GROUPS = -3,      /* C % groups or K % groups != 0; depthwise needs groups == C == K */
+    MICONV_ERR_UNSUPPORTED = -4, /* valid but not provided (e.g. depthwise filter wider than 7) */
+    MICONV_ERR_TOO_LARGE = -5,   /* a tensor exceeds 2^31-1 elements */
+    MICONV_ERR_ALIGN = -6,       /* a pointer is not aligned to its element size */
+    MICONV_ERR_HIP = -7          /* a HIP call failed; see miconv_last_hip_error() */
+};
+
+/* Dense-conv algorithm selector for conv2d_fwd_algo (tests and A/B runs). */
+enum miconv_algo {
+    MICONV_ALGO_AUTO = 0,   /* shape-based choice, what conv2d_fwd does */
+    MICONV_ALGO_DIRECT = 1, /* one output per lane, plain FMA loop: any shape and groups */
+    MICONV_ALGO_IGEMM = 2   /* implicit GEMM on MFMA with LDS-staged tiles (+ split-K when small) */
+};
+
+/* Output extent: floor((H + 2*pad - R)/stride) + 1 and likewise for W.
+ * Writes *P and *Q; returns MICONV_ERR_SHAPE if either is < 1. */
+int miconv_out_dims(int H, int W, int R, int S, int stride, int pad, int *P, int *Q);
+
+/* Dense or grouped conv2d forward in fp32 (the Conv2D operator of Sec. 3.2.2).
+ * x fp32 [N][C][H][W], w fp32 [K][C/groups][R][S], bias fp32 [K] or NULL,
+ * y fp32 [N][K][P][Q].  When groups == C == K the call is the depthwise
+ * operator and is served by the depthwise kernel. */
+int conv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+               int groups, const float *x, const float *w, const float *bias, float *y,
+               int relu, void *stream);
+
+/* conv2d_fwd with an explicit algorithm (enum miconv_algo). */
+int conv2d_fwd_algo(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                    int groups, const float *x, const float *w, const float *bias, float *y,
+                    int relu, int algo, void *stream);
+
+/* Same operator with x and w stored as bf16 (raw bit patterns, uint16),
+ * products accumulated in fp32, bias and y in fp32. */
+int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                    int groups, const uint16_t *x, const uint16_t *w, const float *bias,
+                    float *y, int relu, void *stream);
+
+/* Depthwise conv2d forward in fp32 (MobileNet's per-channel filter, Sec. 4.2
+ * discusses its cost): requires groups == C == K; w fp32 [C][1][R][S] with
+ * R, S <= 7; otherwise the same conventions as conv2d_fwd. */
+int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                 int groups, const float *x, const float *w, const float *bias, float *y,
+                 int relu, void *stream);
+
+/* Glue operators of the evaluated networks (not part of the conv operator). */
+
+/* Max-pool fp32 NCHW with an R x S window, stride and symmetric pad
+ * (pad < R and pad < S); padded positions never win. y [N][C][P][Q]. */
+int maxpool2d_fwd(int N, int C, int H, int W, int R, int S, int stride, int pad,
+                  const float *x, float *y, void *stream);
+
+/* Residual join: y[i] = act(a[i] + b[i]) for i < count, fp32.  y may alias a or b. */
+int add_act_fwd(long count, const float *a, const float *b, float *y, int relu, void *stream);
+
+/* fp32 -> bf16 bit patterns, round to nearest even (NaN stays NaN). */
+int cast_f32_to_bf16(long count, const float *x, uint16_t *y, void *stream);
+
+/* Names the kernels conv2d_fwd_algo (dtype 0) or conv2d_fwd_bf16 (dtype 1)
+ * would launch for this shape on the current device, as a profiler prints
+ * them (template arguments included, namespaces omitted), joined by " + ";
+ * writes at most buflen bytes (NUL-terminated) into buf and the number of
+ * kernel launches into *launches.  Validates like the conv entry points
+ * (pointer alignment is taken as 256 bytes); enqueues nothing. */
+int conv2d_describe(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                    int groups, int dtype, int algo, char *buf, int buflen, int *launches);
+
+/* Human-readable text for a miconv_status. */
+const char *miconv_strerror(int status);
+
+/* The hipError_t of the last failed HIP call made by this thread (0 if none). */
+int miconv_last_hip_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int miconv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MICONV_H */

@@ -8,6 +8,7 @@ writes out, and ``ref.py`` for the numpy-facing wrapper.
 from .ref import (  # noqa: F401
     build,
     lib_path,
+    num_threads,
     out_dims,
     conv2d,
     conv2d_bf16,

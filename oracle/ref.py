@@ -61,12 +61,18 @@ def _load():
                 lib.ref_maxpool2d_f32.argtypes = [i] * 8 + [p, p]
                 lib.ref_add_act_f32.argtypes = [v, p, p, p, i]
                 lib.ref_f32_to_bf16.argtypes = [v, p, p]
-                for f in ("ref_out_dims", "ref_conv2d_f32", "ref_conv2d_bf16",
+                lib.ref_num_threads.argtypes = []
+                for f in ("ref_num_threads", "ref_out_dims", "ref_conv2d_f32", "ref_conv2d_bf16",
                           "ref_dwconv2d_f32", "ref_maxpool2d_f32", "ref_add_act_f32",
                           "ref_f32_to_bf16"):
                     getattr(lib, f).restype = i
                 _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().ref_num_threads())
 
 
 def _ptr(a):

@@ -37,6 +37,9 @@
 #include <stdlib.h>
 #include <string.h>
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define REF_OK 0
 #define REF_EINVAL -1
@@ -57,6 +60,16 @@ int ref_out_dims(int H, int W, int R, int S, int stride, int pad, int *P, int *Q
     *P = (int)ref_extent(H, R, stride, pad);
     *Q = (int)ref_extent(W, S, stride, pad);
     return REF_OK;
+}
+
+/* Threads an OpenMP region of this library uses. */
+int ref_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }
 
 /* bf16 bit pattern -> its exact fp32 value (bf16 is the top half of fp32). */

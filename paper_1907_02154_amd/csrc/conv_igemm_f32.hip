@@ -1,0 +1,317 @@
+// Dense conv2d in fp32 as an implicit GEMM on the gfx950 matrix cores.
+//
+// GEMM view (per group g): D[k][m] = sum_kr Wg[k][kr] * X[kr][m] with
+//   k  = output channel          (GEMM rows,    "output channels divided", Sec. 3.2.2)
+//   m  = (n, p, q) output pixel  (GEMM columns, the feature map split across work-groups)
+//   kr = (c, r, s) filter tap    (reduction, Kred = C/groups * R * S)
+// X is never materialised: each work-group gathers its [KRC x BPX] slice of
+// the im2col matrix straight from NCHW x into LDS (the loop tiling / spatial
+// packing of Sec. 3.2.2), zero-filling taps that fall in the padding.
+//
+// Data path per work-group (BKC channels x BPX pixels, 4 wavefronts):
+//   HBM/L2 --(coalesced loads along q / along kr)--> VGPR --> LDS (double buffer)
+//   LDS --(one fp32 per lane per operand)--> v_mfma_f32_32x32x2_f32 --> AGPR acc
+// The next chunk's global loads are issued before the MFMAs on the current
+// chunk, so memory latency hides behind matrix work; one barrier per chunk.
+//
+// MFMA 32x32x2 f32 operand layout (lane l of 64):
+//   A[i][kk] with i = l % 32, kk = l / 32   -> output channel i, tap kk
+//   B[kk][j] with j = l % 32, kk = l / 32   -> tap kk, pixel j
+//   D reg v: i = 8*(v/4) + 4*(l/32) + v%4,  j = l % 32
+// Pixels sit on j, so every accumulator store writes 32 consecutive pixels of
+// one channel: 128-byte contiguous NCHW segments.
+//
+// Small layers (batch 1, late stages) do not fill 256 CUs with output tiles;
+// there the reduction is split over grid.z.  The work-groups of one output
+// tile leave fp32 partials in a workspace and the last to finish sums them
+// in split order inside the same launch, so results are run-to-run
+// deterministic and every conv is a single kernel launch.
+#include "internal.h"
+
+#include <cstdio>
+
+namespace miconv {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+template <int R_, int S_, int BKC, int BPX, int WK, int WP, int KRC>
+__global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
+{
+    constexpr int NT = 64 * WK * WP;
+    constexpr int WTK = BKC / WK, WTP = BPX / WP;
+    constexpr int BI = WTK / 32, BJ = WTP / 32;
+    static_assert(WTK % 32 == 0 && WTP % 32 == 0, "wave tile must be a multiple of 32x32");
+    static_assert(NT % BPX == 0 && KRC % (NT / BPX) == 0, "B loader shape");
+    static_assert(NT % KRC == 0 && BKC % (NT / KRC) == 0, "A loader shape");
+    constexpr int APAD = 4, BPAD = 4;
+    constexpr int B_RPP = NT / BPX;          // B rows (taps) per loader pass
+    constexpr int B_LOADS = KRC / B_RPP;
+    constexpr int A_KPP = NT / KRC;          // A rows (channels) per loader pass
+    constexpr int A_LOADS = BKC / A_KPP;
+
+    __shared__ float As[2][KRC][BKC + APAD];
+    __shared__ float Bs[2][KRC][BPX + BPAD];
+
+    const float *__restrict__ x = static_cast<const float *>(a.x);
+    const float *__restrict__ w = static_cast<const float *>(a.w);
+    const int R = R_ ? R_ : a.R;
+    const int S = S_ ? S_ : a.S;
+    const int RS = R * S;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wk = wid / WP, wp = wid % WP;
+    const int g = blockIdx.z % a.groups;
+    const int split = blockIdx.z / a.groups;
+    const int m0 = blockIdx.x * BPX;
+    const int k0 = blockIdx.y * BKC;
+    const int kr_begin = split * a.kr_per_split;
+    const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
+
+    // B (im2col) loader: this lane always gathers pixel column bcol.
+    const int bcol = tid % BPX;
+    const int brow0 = tid / BPX;
+    const int mB = m0 + bcol;
+    const bool mvalid = mB < a.M;
+    int ih0 = 0, iw0 = 0, nB = 0;
+    if (mvalid) {
+        nB = mB / a.PQ;
+        const int pq = mB - nB * a.PQ;
+        const int p = pq / a.Q;
+        const int q = pq - p * a.Q;
+        ih0 = p * a.stride - a.pad;
+        iw0 = q * a.stride - a.pad;
+    }
+    const float *xg = x + ((long)nB * a.C + (long)g * a.Cg) * a.HW;
+
+    // A (weights) loader: consecutive lanes walk the reduction axis of one row.
+    const int acol = tid % KRC;
+    const int arow0 = tid / KRC;
+    const float *wg = w + (long)g * a.Kg * a.Kred;
+
+    float breg[B_LOADS], areg[A_LOADS];
+    auto gload = [&](int kr0) {
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+            const int kr = kr0 + brow0 + i * B_RPP;
+            const int c = kr / RS;
+            const int rs = kr - c * RS;
+            const int r = rs / S;
+            const int s = rs - r * S;
+            const int ih = ih0 + r, iw = iw0 + s;
+            const bool ok = mvalid && kr < kr_end && (unsigned)ih < (unsigned)a.H &&
+                            (unsigned)iw < (unsigned)a.W;
+            breg[i] = ok ? xg[(long)c * a.HW + ih * a.W + iw] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) {
+            const int k = k0 + arow0 + i * A_KPP;
+            const int kr = kr0 + acol;
+            const bool ok = k < a.Kg && kr < kr_end;
+            areg[i] = ok ? wg[(long)k * a.Kred + kr] : 0.f;
+        }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) Bs[buf][brow0 + i * B_RPP][bcol] = breg[i];
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) As[buf][acol][arow0 + i * A_KPP] = areg[i];
+    };
+
+    floatx16 acc[BI][BJ];
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[bi][bj][v] = 0.f;
+
+    const int nchunks = kr_end > kr_begin ? ceil_div(kr_end - kr_begin, KRC) : 0;
+    if (nchunks > 0) {
+        gload(kr_begin);
+        sstore(0);
+    }
+    __syncthreads();
+    const int hl = lane >> 5, ll = lane & 31;
+    for (int t = 0; t < nchunks; ++t) {
+        const int cur = t & 1;
+        const bool more = t + 1 < nchunks;
+        if (more) gload(kr_begin + (t + 1) * KRC);
+#pragma unroll
+        for (int kk = 0; kk < KRC; kk += 2) {
+            float av[BI], bv[BJ];
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi) av[bi] = As[cur][kk + hl][wk * WTK + bi * 32 + ll];
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj) bv[bj] = Bs[cur][kk + hl][wp * WTP + bj * 32 + ll];
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+                for (int bj = 0; bj < BJ; ++bj)
+                    acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[bi], bv[bj], acc[bi][bj],
+                                                                      0, 0, 0);
+        }
+        if (more) sstore(cur ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue.  Without a split: bias + activation and the NCHW store.
+    // With a split: every work-group of a tile stores its fp32 partials, and
+    // the last one to arrive (per-tile arrival counter) sums all partials in
+    // split order, so the result does not depend on arrival order.
+    if (a.splits > 1) {
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj) {
+            const int m = m0 + wp * WTP + bj * 32 + ll;
+            if (m >= a.M) continue;
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int k = k0 + wk * WTK + bi * 32 + 8 * (v >> 2) + 4 * hl + (v & 3);
+                    if (k < a.Kg)
+                        a.ws[((long)split * a.K + g * a.Kg + k) * a.M + m] = acc[bi][bj][v];
+                }
+        }
+        __threadfence();
+        __syncthreads();
+        __shared__ int s_last;
+        if (tid == 0) {
+            const int tile = (g * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+            const int prev = atomicAdd(&a.counters[tile], 1);
+            s_last = prev == a.splits - 1;
+            if (s_last) atomicExch(&a.counters[tile], 0);   // ready for the next call
+        }
+        __syncthreads();
+        if (!s_last) return;
+        __threadfence();
+    }
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj) {
+        const int m = m0 + wp * WTP + bj * 32 + ll;
+        if (m >= a.M) continue;
+        const int n = m / a.PQ;
+        const int pq = m - n * a.PQ;
+        const long ybase = (long)n * a.K * a.PQ + pq;
+#pragma unroll
+        for (int bi = 0; bi < BI; ++bi) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int k = k0 + wk * WTK + bi * 32 + 8 * (v >> 2) + 4 * hl + (v & 3);
+                if (k >= a.Kg) continue;
+                const int kg = g * a.Kg + k;
+                float val = acc[bi][bj][v];
+                if (a.splits > 1) {
+                    val = 0.f;
+                    for (int sp = 0; sp < a.splits; ++sp)
+                        val += sp == split ? acc[bi][bj][v] : a.ws[((long)sp * a.K + kg) * a.M + m];
+                }
+                val += a.bias ? a.bias[kg] : 0.f;
+                if (a.relu) val = fmaxf(val, 0.f);
+                a.y[ybase + (long)kg * a.PQ] = val;
+            }
+        }
+    }
+}
+
+struct TileInfo {
+    int bkc, bpx, wk, wp, krc;
+};
+// Tile table: 0 = 128x128 (large layers), 1 = 64x64, 2 = 32 channels x 64 pixels.
+const TileInfo kTiles[] = {{128, 128, 2, 2, 16}, {64, 64, 2, 2, 16}, {32, 64, 1, 2, 16}};
+
+int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
+
+template <int R_, int S_>
+hipError_t launch_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    switch (tile) {
+    case 0:
+        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 128, 128, 2, 2, 16>), grid, dim3(256), 0, st, a);
+        break;
+    case 1:
+        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 64, 64, 2, 2, 16>), grid, dim3(256), 0, st, a);
+        break;
+    default:
+        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 32, 64, 1, 2, 16>), grid, dim3(128), 0, st, a);
+        break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// Pick the tile and the reduction split: the biggest tile that still gives
+// about two work-groups per CU, else the smallest tile plus a split of the
+// reduction (chunks of 16 taps, at least 4 chunks per split).
+IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus)
+{
+    IgemmPlan plan{2, 1, 0, 0};
+    const long target = 2L * num_cus;
+    for (int t = 0; t < 3; ++t) {
+        const long tiles = (long)ceil_div(p.M, kTiles[t].bpx) * ceil_div(p.Kg, kTiles[t].bkc) * p.groups;
+        if (tiles >= target || t == 2) {
+            plan.tile = t;
+            const int krc = kTiles[t].krc;
+            const int chunks = ceil_div(p.Kred, krc);
+            int splits = 1;
+            if (tiles < target) {
+                splits = (int)((target + tiles - 1) / tiles);
+                const int max_splits = chunks / 4;
+                if (splits > max_splits) splits = max_splits;
+                if (splits < 1) splits = 1;
+            }
+            const int chunks_per = ceil_div(chunks, splits);
+            splits = ceil_div(chunks, chunks_per);   // no empty splits
+            plan.splits = splits;
+            plan.kr_per_split = chunks_per * krc;
+            const size_t tiles_total = (size_t)tiles;
+            plan.counters = splits > 1 ? (int)tiles_total : 0;
+            plan.ws_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
+            break;
+        }
+    }
+    return plan;
+}
+
+void describe_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, char *buf, int len,
+                        int *launches)
+{
+    const TileInfo &t = kTiles[plan.tile];
+    int R = rs_template(p.R), S = rs_template(p.S);
+    if (R == 0 || S == 0 || R != S) R = S = 0;
+    snprintf(buf, len, "igemm_f32_kernel<%d, %d, %d, %d, %d, %d, %d>", R, S, t.bkc, t.bpx, t.wk,
+             t.wp, t.krc);
+    *launches = 1;
+}
+
+hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const float *x,
+                            const float *w, const float *bias, float *y, float *ws, int *counters,
+                            hipStream_t st)
+{
+    ConvArgs a = make_args(p);
+    a.x = x;
+    a.w = w;
+    a.bias = bias;
+    a.y = y;
+    a.ws = plan.splits > 1 ? ws : nullptr;
+    a.counters = plan.splits > 1 ? counters : nullptr;
+    a.splits = plan.splits;
+    a.kr_per_split = plan.kr_per_split;
+    const TileInfo &ti = kTiles[plan.tile];
+    dim3 grid(ceil_div(p.M, ti.bpx), ceil_div(p.Kg, ti.bkc), p.groups * plan.splits);
+    hipError_t e;
+    if (p.R == 1 && p.S == 1)
+        e = launch_rs<1, 1>(a, plan.tile, grid, st);
+    else if (p.R == 3 && p.S == 3)
+        e = launch_rs<3, 3>(a, plan.tile, grid, st);
+    else if (p.R == 7 && p.S == 7)
+        e = launch_rs<7, 7>(a, plan.tile, grid, st);
+    else
+        e = launch_rs<0, 0>(a, plan.tile, grid, st);
+    return e;
+}
+
+}  // namespace miconv

@@ -1,0 +1,126 @@
+// Glue operators of the evaluated networks, outside the conv operator:
+// max-pool (ResNet stem 3x3/2 pad 1, VGG 2x2/2), the residual join
+// act(a + b) of a bottleneck block, and the fp32 -> bf16 rounding that feeds
+// a bf16 conv from an fp32 activation.  All are elementwise or near it and
+// bound by HBM bandwidth; lanes walk contiguous memory.
+#include "internal.h"
+
+namespace miconv {
+namespace {
+
+__global__ __launch_bounds__(256) void maxpool_kernel(const float *__restrict__ x,
+                                                      float *__restrict__ y, int H, int W, int R,
+                                                      int S, int stride, int pad, int P, int Q,
+                                                      long total)
+{
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const int q = (int)(i % Q);
+        const long t = i / Q;
+        const int p = (int)(t % P);
+        const long plane = t / P;
+        const float *xp = x + plane * (long)H * W;
+        float m = -INFINITY;
+        for (int r = 0; r < R; ++r) {
+            const int h = p * stride - pad + r;
+            if ((unsigned)h >= (unsigned)H) continue;
+            for (int s = 0; s < S; ++s) {
+                const int ww = q * stride - pad + s;
+                if ((unsigned)ww >= (unsigned)W) continue;
+                m = fmaxf(m, xp[(long)h * W + ww]);
+            }
+        }
+        y[i] = m;
+    }
+}
+
+__global__ __launch_bounds__(256) void add_act_vec4_kernel(const float4 *__restrict__ a,
+                                                           const float4 *__restrict__ b,
+                                                           float4 *__restrict__ y, long n4,
+                                                           int relu)
+{
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+         i += (long)gridDim.x * blockDim.x) {
+        float4 u = a[i], v = b[i];
+        float4 o = make_float4(u.x + v.x, u.y + v.y, u.z + v.z, u.w + v.w);
+        if (relu) {
+            o.x = fmaxf(o.x, 0.f);
+            o.y = fmaxf(o.y, 0.f);
+            o.z = fmaxf(o.z, 0.f);
+            o.w = fmaxf(o.w, 0.f);
+        }
+        y[i] = o;
+    }
+}
+
+__global__ __launch_bounds__(256) void add_act_kernel(const float *a, const float *b, float *y,
+                                                      long n, int relu)
+{
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (long)gridDim.x * blockDim.x) {
+        float o = a[i] + b[i];
+        y[i] = relu ? fmaxf(o, 0.f) : o;
+    }
+}
+
+// Round to nearest even on the raw bits: add 0x7FFF plus the lowest kept bit,
+// then keep the upper half.  A NaN keeps its sign and gets the quiet bit.
+__device__ inline uint16_t f32_to_bf16_rne(float f)
+{
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
+        return (uint16_t)((u >> 16) | 0x0040u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__global__ __launch_bounds__(256) void cast_bf16_kernel(const float *__restrict__ x,
+                                                        uint16_t *__restrict__ y, long n)
+{
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (long)gridDim.x * blockDim.x)
+        y[i] = f32_to_bf16_rne(x[i]);
+}
+
+unsigned grid_for(long n)
+{
+    long b = (n + 255) / 256;
+    if (b < 1) b = 1;
+    if (b > 65536) b = 65536;
+    return (unsigned)b;
+}
+
+}  // namespace
+
+hipError_t launch_maxpool_f32(int N, int C, int H, int W, int R, int S, int stride, int pad,
+                              int P, int Q, const float *x, float *y, hipStream_t st)
+{
+    const long total = (long)N * C * P * Q;
+    hipLaunchKernelGGL(maxpool_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, y, H, W, R, S,
+                       stride, pad, P, Q, total);
+    return hipGetLastError();
+}
+
+hipError_t launch_add_act_f32(long count, const float *a, const float *b, float *y, int relu,
+                              hipStream_t st)
+{
+    if (count == 0) return hipSuccess;
+    const bool vec = (count % 4 == 0) && ((uintptr_t)a % 16 == 0) && ((uintptr_t)b % 16 == 0) &&
+                     ((uintptr_t)y % 16 == 0);
+    if (vec) {
+        hipLaunchKernelGGL(add_act_vec4_kernel, dim3(grid_for(count / 4)), dim3(256), 0, st,
+                           (const float4 *)a, (const float4 *)b, (float4 *)y, count / 4, relu);
+    } else {
+        hipLaunchKernelGGL(add_act_kernel, dim3(grid_for(count)), dim3(256), 0, st, a, b, y, count,
+                           relu);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t st)
+{
+    if (count == 0) return hipSuccess;
+    hipLaunchKernelGGL(cast_bf16_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, y, count);
+    return hipGetLastError();
+}
+
+}  // namespace miconv

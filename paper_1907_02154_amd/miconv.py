@@ -1,0 +1,223 @@
+"""Thin Python binding over libmiconv.so (``include/miconv.h``).
+
+Argument marshalling only: every function checks dtype / device / layout,
+reads the extents off the tensor shapes and passes raw device pointers plus
+torch's current HIP stream to the C entry point of the same name.  PyTorch
+provides device memory and streams; all arithmetic runs in the library's HIP
+kernels.  If the library is missing the import of any entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmiconv.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "miconv.h")
+
+OK = 0
+ERR_NULL, ERR_SHAPE, ERR_GROUPS, ERR_UNSUPPORTED, ERR_TOO_LARGE, ERR_ALIGN, ERR_HIP = range(-1, -8, -1)
+ALGO_AUTO, ALGO_DIRECT, ALGO_IGEMM = 0, 1, 2
+
+_lib = None
+
+
+class MiconvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {strerror(status)} ({status})")
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmiconv.so (built by ``paper_1907_02154_amd.build``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        i, p, l = ctypes.c_int, ctypes.c_void_p, ctypes.c_long
+        conv = [i] * 10 + [p, p, p, p, i, p]
+        L.conv2d_fwd.argtypes = conv
+        L.conv2d_fwd_bf16.argtypes = conv
+        L.dwconv2d_fwd.argtypes = conv
+        L.conv2d_fwd_algo.argtypes = [i] * 10 + [p, p, p, p, i, i, p]
+        L.miconv_out_dims.argtypes = [i] * 6 + [ctypes.POINTER(i)] * 2
+        L.maxpool2d_fwd.argtypes = [i] * 8 + [p, p, p]
+        L.add_act_fwd.argtypes = [l, p, p, p, i, p]
+        L.cast_f32_to_bf16.argtypes = [l, p, p, p]
+        L.conv2d_describe.argtypes = [i] * 12 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
+        L.conv2d_describe.restype = i
+        L.miconv_strerror.argtypes = [i]
+        L.miconv_strerror.restype = ctypes.c_char_p
+        L.miconv_last_hip_error.argtypes = []
+        L.miconv_version.argtypes = []
+        for f in ("conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd", "conv2d_fwd_algo",
+                  "miconv_out_dims", "maxpool2d_fwd", "add_act_fwd", "cast_f32_to_bf16",
+                  "miconv_last_hip_error", "miconv_version"):
+            getattr(L, f).restype = i
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions ``include/miconv.h`` declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def strerror(status: int) -> str:
+    return lib().miconv_strerror(status).decode()
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise MiconvError(rc, what)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims")
+
+
+def out_dims(H: int, W: int, R: int, S: int, stride: int, pad: int):
+    P, Q = ctypes.c_int(), ctypes.c_int()
+    rc = lib().miconv_out_dims(H, W, R, S, stride, pad, ctypes.byref(P), ctypes.byref(Q))
+    _check(rc, "miconv_out_dims")
+    return P.value, Q.value
+
+
+def _conv_common(fn, x, w, bias, y, stride, pad, groups, relu, stream, xdtype, extra=()):
+    _dev(x, xdtype, "x", 4)
+    _dev(w, xdtype, "w", 4)
+    _dev(y, torch.float32, "y", 4)
+    if bias is not None:
+        _dev(bias, torch.float32, "bias", 1)
+    N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if groups <= 0 or Cg * groups != C:
+        raise ValueError("w.shape[1] * groups must equal C")
+    if bias is not None and bias.shape[0] != K:
+        raise ValueError("bias must have K entries")
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, K, P, Q):
+        raise ValueError(f"y must have shape {(N, K, P, Q)}, got {tuple(y.shape)}")
+    rc = fn(N, C, H, W, K, R, S, stride, pad, groups, _ptr(x), _ptr(w), _ptr(bias), _ptr(y),
+            1 if relu else 0, *extra, _stream(stream))
+    _check(rc, fn.__name__)
+    return y
+
+
+def conv2d_fwd(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, stream=None):
+    """fp32 conv2d: x [N][C][H][W], w [K][C/groups][R][S], bias [K] or None -> y [N][K][P][Q]."""
+    return _conv_common(lib().conv2d_fwd, x, w, bias, y, stride, pad, groups, relu, stream,
+                        torch.float32)
+
+
+def conv2d_fwd_algo(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO,
+                    stream=None):
+    """conv2d_fwd with an explicit algorithm (ALGO_AUTO / ALGO_DIRECT / ALGO_IGEMM)."""
+    f = lib().conv2d_fwd_algo
+    _dev(x, torch.float32, "x", 4)
+    return _conv_common(f, x, w, bias, y, stride, pad, groups, relu, stream, torch.float32,
+                        extra=(int(algo),))
+
+
+def conv2d_fwd_bf16(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, stream=None):
+    """bf16 x and w (torch.bfloat16), fp32 bias and y."""
+    return _conv_common(lib().conv2d_fwd_bf16, x, w, bias, y, stride, pad, groups, relu, stream,
+                        torch.bfloat16)
+
+
+def dwconv2d_fwd(x, w, bias, y, stride=1, pad=1, relu=False, stream=None):
+    """Depthwise conv: w [C][1][R][S], groups = C = K."""
+    C = x.shape[1]
+    return _conv_common(lib().dwconv2d_fwd, x, w, bias, y, stride, pad, C, relu, stream,
+                        torch.float32)
+
+
+def maxpool2d_fwd(x, y, R, S, stride, pad=0, stream=None):
+    _dev(x, torch.float32, "x", 4)
+    _dev(y, torch.float32, "y", 4)
+    N, C, H, W = x.shape
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, C, P, Q):
+        raise ValueError(f"y must have shape {(N, C, P, Q)}")
+    _check(lib().maxpool2d_fwd(N, C, H, W, R, S, stride, pad, _ptr(x), _ptr(y), _stream(stream)),
+           "maxpool2d_fwd")
+    return y
+
+
+def add_act_fwd(a, b, y, relu=True, stream=None):
+    for t, n in ((a, "a"), (b, "b"), (y, "y")):
+        _dev(t, torch.float32, n)
+    if a.shape != b.shape or a.shape != y.shape:
+        raise ValueError("a, b, y must have one shape")
+    _check(lib().add_act_fwd(a.numel(), _ptr(a), _ptr(b), _ptr(y), 1 if relu else 0,
+                             _stream(stream)), "add_act_fwd")
+    return y
+
+
+def cast_f32_to_bf16(x, y, stream=None):
+    _dev(x, torch.float32, "x")
+    _dev(y, torch.bfloat16, "y")
+    if x.shape != y.shape:
+        raise ValueError("x and y must have one shape")
+    _check(lib().cast_f32_to_bf16(x.numel(), _ptr(x), _ptr(y), _stream(stream)), "cast_f32_to_bf16")
+    return y
+
+
+def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", algo=ALGO_AUTO):
+    """(kernel names, launch count) the library would use for this conv shape."""
+    buf = ctypes.create_string_buffer(256)
+    n = ctypes.c_int()
+    rc = lib().conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups,
+                               1 if dtype == "bf16" else 0, int(algo), buf, 256, ctypes.byref(n))
+    _check(rc, "conv2d_describe")
+    return buf.value.decode(), n.value
+
+
+# Allocating conveniences (output buffers come from torch's caching allocator).
+
+def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO, stream=None):
+    N, _, H, W = x.shape
+    K, _, R, S = w.shape
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    y = torch.empty((N, K, P, Q), device=x.device, dtype=torch.float32)
+    if x.dtype == torch.bfloat16:
+        return conv2d_fwd_bf16(x, w, bias, y, stride, pad, groups, relu, stream)
+    if algo == ALGO_AUTO:
+        return conv2d_fwd(x, w, bias, y, stride, pad, groups, relu, stream)
+    return conv2d_fwd_algo(x, w, bias, y, stride, pad, groups, relu, algo, stream)
+
+
+def dwconv2d(x, w, bias=None, stride=1, pad=1, relu=False, stream=None):
+    N, C, H, W = x.shape
+    P, Q = out_dims(H, W, w.shape[2], w.shape[3], stride, pad)
+    y = torch.empty((N, C, P, Q), device=x.device, dtype=torch.float32)
+    return dwconv2d_fwd(x, w, bias, y, stride, pad, relu, stream)

@@ -1,0 +1,84 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+The library must load, export every function ``include/miconv.h`` declares,
+and reject invalid arguments before any HIP call (so these run on a machine
+without a GPU).  The fake pointers below are never dereferenced: every call
+here fails validation first.
+"""
+import ctypes
+
+import pytest
+
+from paper_1907_02154_amd import miconv
+
+FAKE = 4096   # aligned, non-null, never touched
+
+
+@pytest.fixture(scope="module")
+def L():
+    return miconv.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = miconv.header_functions()
+    for expected in ("conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd", "conv2d_fwd_algo",
+                     "miconv_out_dims", "maxpool2d_fwd", "add_act_fwd", "cast_f32_to_bf16",
+                     "miconv_strerror", "miconv_last_hip_error", "miconv_version"):
+        assert expected in names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_out_dims(L):
+    assert miconv.out_dims(224, 224, 7, 7, 2, 3) == (112, 112)
+    assert miconv.out_dims(112, 112, 3, 3, 2, 1) == (56, 56)
+    assert miconv.out_dims(14, 14, 1, 1, 2, 0) == (7, 7)
+    assert miconv.out_dims(5, 6, 3, 2, 2, 0) == (2, 3)
+    P, Q = ctypes.c_int(), ctypes.c_int()
+    assert L.miconv_out_dims(2, 2, 3, 3, 1, 0, ctypes.byref(P), ctypes.byref(Q)) == miconv.ERR_SHAPE
+    assert L.miconv_out_dims(2, 2, 3, 3, 0, 0, ctypes.byref(P), ctypes.byref(Q)) == miconv.ERR_SHAPE
+    assert L.miconv_out_dims(2, 2, 3, 3, 1, 0, None, None) == miconv.ERR_NULL
+
+
+def _call(L, fn, N=1, C=4, H=8, W=8, K=4, R=3, S=3, stride=1, pad=1, groups=1,
+          x=FAKE, w=FAKE, b=None, y=FAKE):
+    return getattr(L, fn)(N, C, H, W, K, R, S, stride, pad, groups, x, w, b, y, 0, None)
+
+
+@pytest.mark.parametrize("fn", ["conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd"])
+def test_validation_errors(L, fn):
+    assert _call(L, fn, x=None) == miconv.ERR_NULL
+    assert _call(L, fn, w=None) == miconv.ERR_NULL
+    assert _call(L, fn, y=None) == miconv.ERR_NULL
+    for bad in (dict(N=0), dict(C=-1), dict(H=0), dict(W=0), dict(K=0), dict(R=0), dict(S=0),
+                dict(stride=0), dict(pad=-1), dict(H=2, W=2, pad=0)):
+        assert _call(L, fn, **bad) == miconv.ERR_SHAPE, bad
+    assert _call(L, fn, groups=3) == miconv.ERR_GROUPS
+    assert _call(L, fn, groups=0) == miconv.ERR_GROUPS
+    assert _call(L, fn, N=70000, C=1024, H=64, W=64, K=4, groups=1) == miconv.ERR_TOO_LARGE
+    assert _call(L, fn, x=FAKE + 1) == miconv.ERR_ALIGN
+    assert _call(L, fn, y=FAKE + 2) == miconv.ERR_ALIGN
+
+
+def test_depthwise_specific_errors(L):
+    assert _call(L, "dwconv2d_fwd", groups=1) == miconv.ERR_GROUPS
+    assert _call(L, "dwconv2d_fwd", C=4, K=8, groups=4) == miconv.ERR_GROUPS
+    assert _call(L, "dwconv2d_fwd", C=4, K=4, groups=4, R=9, S=9, pad=4) == miconv.ERR_UNSUPPORTED
+
+
+def test_algo_and_glue_errors(L):
+    assert L.conv2d_fwd_algo(1, 4, 8, 8, 4, 3, 3, 1, 1, 1, FAKE, FAKE, None, FAKE, 0, 7, None) == \
+        miconv.ERR_UNSUPPORTED
+    assert L.maxpool2d_fwd(1, 1, 4, 4, 2, 2, 2, 2, FAKE, FAKE, None) == miconv.ERR_SHAPE   # pad >= R
+    assert L.maxpool2d_fwd(1, 1, 4, 4, 2, 2, 2, 0, None, FAKE, None) == miconv.ERR_NULL
+    assert L.add_act_fwd(-1, FAKE, FAKE, FAKE, 1, None) == miconv.ERR_SHAPE
+    assert L.add_act_fwd(4, None, FAKE, FAKE, 1, None) == miconv.ERR_NULL
+    assert L.cast_f32_to_bf16(4, FAKE, FAKE + 1, None) == miconv.ERR_ALIGN
+
+
+def test_strerror_and_version(L):
+    for s in range(0, -8, -1):
+        assert miconv.strerror(s)
+    assert miconv.strerror(-99) == "unknown status"
+    assert L.miconv_version() >= 100
+    assert L.miconv_last_hip_error() == 0

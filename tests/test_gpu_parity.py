@@ -1,0 +1,244 @@
+"""GPU parity: the HIP kernels behind the C ABI against the CPU oracle.
+
+* Small-integer data (|x|, |w| <= 4, |bias| <= 8) keep every partial sum
+  exact in fp32, so any summation order must reproduce the oracle bit for
+  bit: this checks indexing, padding, strides, groups, tiling edges and the
+  split-K reduction of every kernel independently of rounding.
+* Random data at the layer shapes of the five evaluation configurations are
+  held to the gate e = max|y - y_ref| / max|y_ref| <= 1e-4 (fp32 path) and
+  <= 2e-2 (bf16 inputs, fp32 accumulation), with the GPU running the full
+  batch in the same launch configuration the bench times.  Where the oracle
+  would take minutes (VGG-16 at batch 8, ResNet-50 at batch 64) it is run on
+  a sample that it computes exactly: a few images and a subset of output
+  channels (each output channel depends only on its own filter and each
+  image only on itself).
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1907_02154_amd import miconv
+from paper_1907_02154_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-4
+TOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    miconv.lib()   # fails loudly if the library is missing
+
+
+def dev(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dtype)
+
+
+def dev_bf16_bits(bits):
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+    return t.view(torch.bfloat16)
+
+
+def gpu_conv(x, w, b, stride, pad, groups, relu, algo):
+    y = miconv.conv2d(dev(x), dev(w), None if b is None else dev(b), stride, pad, groups, relu,
+                      algo=algo)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def err_inf(y, ref):
+    d = np.max(np.abs(y.astype(np.float64) - ref.astype(np.float64)))
+    s = np.max(np.abs(ref.astype(np.float64)))
+    return d / s if s > 0 else d
+
+
+def ints(shape, lo, hi, seed):
+    return wl.small_ints(shape, lo, hi, seed)
+
+
+# (N, C, H, W, K, R, S, stride, pad, groups): several tiles and ragged tails
+DENSE_CASES = [
+    (1, 1, 1, 1, 1, 1, 1, 1, 0, 1),
+    (1, 3, 5, 7, 2, 3, 3, 1, 1, 1),
+    (2, 3, 17, 19, 70, 7, 7, 2, 3, 1),       # stem-like, ragged M and K
+    (1, 40, 19, 19, 70, 3, 3, 1, 1, 1),      # Kred 360, several chunks
+    (2, 64, 15, 13, 130, 1, 1, 1, 0, 1),     # 1x1, ragged tiles
+    (1, 96, 14, 14, 200, 1, 1, 2, 0, 1),     # 1x1 stride 2
+    (1, 512, 7, 7, 96, 3, 3, 1, 1, 1),       # small M, long reduction -> split-K
+    (3, 33, 9, 11, 65, 3, 3, 2, 1, 1),
+    (1, 16, 10, 10, 24, 3, 5, 1, 2, 1),      # R != S, generic path
+    (1, 12, 9, 9, 18, 3, 3, 1, 1, 3),        # grouped
+    (2, 32, 8, 8, 64, 3, 3, 1, 1, 2),        # grouped with Cg >= 8
+    (1, 8, 6, 6, 4, 3, 3, 1, 4, 1),          # padding wider than the filter
+    (1, 130, 130, 1, 3, 1, 1, 1, 0, 1),      # W = 1
+]
+
+
+@pytest.mark.parametrize("case", DENSE_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("algo", [miconv.ALGO_DIRECT, miconv.ALGO_IGEMM, miconv.ALGO_AUTO])
+def test_dense_small_int_bitwise(oracle_lib, case, algo):
+    N, C, H, W, K, R, S, st, pad, g = case
+    seed = 1000 + sum(case)
+    x = ints((N, C, H, W), -4, 4, seed)
+    w = ints((K, C // g, R, S), -4, 4, seed + 1)
+    b = ints((K,), -8, 8, seed + 2)
+    for relu in (False, True):
+        ref = oracle_lib.conv2d(x, w, b, st, pad, g, relu)
+        y = gpu_conv(x, w, b, st, pad, g, relu, algo)
+        np.testing.assert_array_equal(y, ref, err_msg=f"{case} relu={relu} algo={algo}")
+    y = gpu_conv(x, w, None, st, pad, g, False, algo)
+    np.testing.assert_array_equal(y, oracle_lib.conv2d(x, w, None, st, pad, g, False))
+
+
+DW_CASES = [  # (N, C, H, W, R, stride, pad)
+    (1, 32, 112, 112, 3, 1, 1), (1, 64, 112, 112, 3, 2, 1), (2, 128, 28, 28, 3, 2, 1),
+    (2, 5, 14, 14, 3, 1, 1), (1, 7, 7, 7, 3, 1, 1), (1, 3, 14, 14, 3, 2, 1),
+    (1, 4, 130, 130, 3, 1, 1),          # row wider than one lane group: several segments
+    (1, 4, 9, 13, 3, 1, 1), (2, 3, 11, 10, 3, 2, 1),   # odd sizes
+    (1, 6, 12, 12, 5, 3, 2), (1, 2, 8, 8, 7, 1, 3), (1, 3, 6, 6, 1, 1, 0), (1, 2, 5, 5, 3, 1, 0),
+]
+
+
+@pytest.mark.parametrize("case", DW_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_depthwise_small_int_bitwise(oracle_lib, case):
+    N, C, H, W, R, st, pad = case
+    seed = 2000 + sum(case)
+    x = ints((N, C, H, W), -4, 4, seed)
+    w = ints((C, 1, R, R), -4, 4, seed + 1)
+    b = ints((C,), -8, 8, seed + 2)
+    for relu in (False, True):
+        ref = oracle_lib.dwconv2d(x, w, b, st, pad, relu)
+        y = miconv.dwconv2d(dev(x), dev(w), dev(b), st, pad, relu)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"{case} relu={relu}")
+        # conv2d_fwd with groups == C == K reaches the same kernel
+        y2 = gpu_conv(x, w, b, st, pad, C, relu, miconv.ALGO_AUTO)
+        np.testing.assert_array_equal(y2, ref)
+
+
+@pytest.mark.parametrize("case", DENSE_CASES[:9], ids=lambda c: "x".join(map(str, c)))
+def test_bf16_small_int_bitwise(oracle_lib, case):
+    N, C, H, W, K, R, S, st, pad, g = case
+    seed = 3000 + sum(case)
+    x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
+    w = wl.to_bf16_bits(ints((K, C // g, R, S), -4, 4, seed + 1))
+    b = ints((K,), -8, 8, seed + 2)
+    ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
+    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), ref)
+
+
+def _layers(config):
+    """Unique layer shapes of a config with the index of their first use."""
+    seen, out = set(), []
+    for i, l in enumerate(wl.workload(config).layers):
+        key = (l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad, l.groups, l.relu)
+        if key not in seen:
+            seen.add(key)
+            out.append((i, l))
+    return out
+
+
+def _layer_ids(config):
+    return [f"c{config}-{i}-{l.name}" for i, l in _layers(config)]
+
+
+def _check_layer(oracle_lib, config, i, l, images=None, kmax=None, tol=TOL_F32):
+    x, w, b = wl.layer_tensors(config, i, l)
+    bf16 = wl.workload(config).dtype == "bf16"
+    if bf16:
+        xb, wb = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+        y = miconv.conv2d(dev_bf16_bits(xb), dev_bf16_bits(wb), dev(b), l.stride, l.pad, l.groups, l.relu)
+    elif l.kind == "dw":
+        y = miconv.dwconv2d(dev(x), dev(w), dev(b), l.stride, l.pad, l.relu)
+    else:
+        y = miconv.conv2d(dev(x), dev(w), dev(b), l.stride, l.pad, l.groups, l.relu)
+    torch.cuda.synchronize()
+    y = y.cpu().numpy()
+    imgs = list(range(l.N)) if images is None else images
+    if kmax is None or l.groups != 1 or kmax >= l.K:
+        ks = np.arange(l.K)
+    else:   # first, last and evenly spread output channels
+        ks = np.unique(np.concatenate([np.linspace(0, l.K - 1, kmax).astype(int), [0, l.K - 1]]))
+    for n in imgs:
+        if bf16:
+            ref = oracle_lib.conv2d_bf16(xb[n:n + 1], wb[ks], b[ks], l.stride, l.pad, l.groups, l.relu)
+        elif l.kind == "dw":
+            ref = oracle_lib.dwconv2d(x[n:n + 1], w, b, l.stride, l.pad, l.relu)
+        else:
+            ref = oracle_lib.conv2d(x[n:n + 1], w[ks], b[ks], l.stride, l.pad, l.groups, l.relu)
+        got = y[n:n + 1, ks] if l.kind != "dw" else y[n:n + 1]
+        e = err_inf(got, ref)
+        assert e <= tol, f"config {config} layer {i} {l.name} image {n}: e={e:.3e}"
+    return y
+
+
+@pytest.mark.parametrize("config", [1, 2, 3])
+def test_configs_full_oracle(oracle_lib, config):
+    """Configs 1-3 (batch 1, fp32): every layer against the whole oracle output."""
+    for i, l in _layers(config):
+        print(f"config {config} layer {i} {l.name}", flush=True)
+        _check_layer(oracle_lib, config, i, l)
+
+
+def test_config4_vgg_sampled(oracle_lib):
+    """VGG-16 at batch 8: images 0 and 7, 24 output channels per layer."""
+    for i, l in _layers(4):
+        print(f"config 4 layer {i} {l.name}", flush=True)
+        _check_layer(oracle_lib, 4, i, l, images=[0, l.N - 1], kmax=24)
+
+
+def test_config5_resnet_bf16_sampled(oracle_lib):
+    """ResNet-50 at batch 64 with bf16 x and w: images 0 and 63, 24 channels."""
+    for i, l in _layers(5):
+        print(f"config 5 layer {i} {l.name}", flush=True)
+        _check_layer(oracle_lib, 5, i, l, images=[0, l.N - 1], kmax=24, tol=TOL_BF16)
+
+
+def test_dense_deterministic():
+    l = wl.workload(2).layers[-2]      # s5 3x3: small M, split-K
+    x, w, b = wl.layer_tensors(2, 51, l)
+    X, Wt, B = dev(x), dev(w), dev(b)
+    y1 = miconv.conv2d(X, Wt, B, l.stride, l.pad, 1, l.relu)
+    y2 = miconv.conv2d(X, Wt, B, l.stride, l.pad, 1, l.relu)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+def test_maxpool_add_cast(oracle_lib):
+    rng = np.random.default_rng(0)
+    for (N, C, H, W, R, st, pad) in [(1, 64, 112, 112, 3, 2, 1), (2, 64, 224, 224, 2, 2, 0), (1, 3, 7, 9, 3, 2, 1)]:
+        x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+        P, Q = oracle_lib.out_dims(H, W, R, R, st, pad)
+        y = torch.empty((N, C, P, Q), device="cuda")
+        miconv.maxpool2d_fwd(dev(x), y, R, R, st, pad)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), oracle_lib.maxpool2d(x, R, R, st, pad))
+    for n in (1, 7, 4096, 1 << 20):
+        a = rng.standard_normal(n).astype(np.float32)
+        b = rng.standard_normal(n).astype(np.float32)
+        for relu in (True, False):
+            y = torch.empty(n, device="cuda")
+            miconv.add_act_fwd(dev(a), dev(b), y, relu)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(y.cpu().numpy(), oracle_lib.add_act(a, b, relu))
+    bits = rng.integers(0, 2 ** 32, 1 << 18, dtype=np.uint64).astype(np.uint32)
+    f = bits.view(np.float32)
+    f = f[np.isfinite(f)]
+    y = torch.empty(f.shape, device="cuda", dtype=torch.bfloat16)
+    miconv.cast_f32_to_bf16(dev(f), y)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.view(torch.int16).cpu().numpy().view(np.uint16), oracle_lib.f32_to_bf16(f))
+
+
+def test_rejects_wrong_shapes_from_python():
+    x = torch.zeros((1, 4, 8, 8), device="cuda")
+    w = torch.zeros((4, 4, 3, 3), device="cuda")
+    with pytest.raises(ValueError):
+        miconv.conv2d_fwd(x, w, None, torch.zeros((1, 4, 7, 7), device="cuda"), 1, 1)
+    with pytest.raises(TypeError):
+        miconv.conv2d_fwd(x.double(), w, None, torch.zeros((1, 4, 8, 8), device="cuda"), 1, 1)
