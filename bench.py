@@ -7,6 +7,9 @@ distributions) and every layer writes its own output buffer, so the timed
 region holds only conv kernels.  The default workload is the ResNet-50 v1
 conv stack at batch 1 in fp32 (53 convs); --config picks another.
 
+The passes run through the library's stack executor: W eager passes, then
+one HIP graph holding exactly K passes (after one untimed replay of it).
+
 Prints one JSON line with the conv TFLOP/s of the step, ms per image, the
 roofline of the dominant kernel (the kernel with the largest summed time,
 timed live with HIP events around each of its launches on the launch
@@ -85,58 +88,82 @@ def main():
                            launches=launches, flops=fl, bytes=nbytes, host=(x, w, b)))
     torch.cuda.synchronize()
 
-    def launch(d):
+    ops = []
+    for d in layers:
         l = d["layer"]
-        if bf16:
-            miconv.conv2d_fwd_bf16(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu)
-        elif l.kind == "dw":
-            miconv.dwconv2d_fwd(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.relu)
-        else:
-            miconv.conv2d_fwd(d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu)
-
-    for _ in range(args.warmup):
-        for d in layers:
-            launch(d)
-    torch.cuda.synchronize()
+        op = miconv.OP_CONV_BF16 if bf16 else (miconv.OP_DWCONV_F32 if l.kind == "dw" else miconv.OP_CONV_F32)
+        ops.append((op, d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu))
+    stack = miconv.Stack(ops)
+    for j, d in enumerate(layers):
+        assert stack.describe(j) == d["kernel"], (stack.describe(j), d["kernel"])
+    n_launch = stack.launches
+    launch_info = [stack.launch_info(j) for j in range(n_launch)]
 
     stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):          # eager passes: planning, workspace, caches
+        stack.launch(stream)
+    torch.cuda.synchronize()
+
+    # The timed region: one HIP graph holding exactly K passes, with an event
+    # before every layer (per-kernel durations) and after the last one.
     K = args.steps
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in layers] for _ in range(K)]
+    stack.capture(K, timed=True, stream=stream)
+    stack.replay(stream)                  # first replay of a fresh graph: untimed
+    torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
-    for k in range(K):
-        for j, d in enumerate(layers):
-            ev[k][j][0].record(stream)
-            launch(d)
-            ev[k][j][1].record(stream)
+    stack.replay(stream)
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / K
+    per_launch_ms = stack.times()
 
-    per_layer_ms = np.array([[ev[k][j][0].elapsed_time(ev[k][j][1]) for j in range(len(layers))]
-                             for k in range(K)])
-    layer_ms = per_layer_ms.mean(axis=0)
+    # The same K passes without the per-layer events, for the cost of timing.
+    stack.capture(K, timed=False, stream=stream)
+    stack.replay(stream)
+    torch.cuda.synchronize()
+    u0 = torch.cuda.Event(enable_timing=True)
+    u1 = torch.cuda.Event(enable_timing=True)
+    u0.record(stream)
+    stack.replay(stream)
+    u1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step_untimed = u0.elapsed_time(u1) / K
+    stack.close()
+
+    launch_ms = per_launch_ms.mean(axis=0)          # mean over the K passes, per kernel launch
+    layer_ms = np.zeros(len(layers))
+    for j in range(n_launch):
+        layer_ms[launch_info[j][0]] += launch_ms[j]
     step_flops = sum(d["flops"] for d in layers)
     tflops = step_flops / (ms_per_step * 1e-3) / 1e12
 
-    # Dominant kernel: the largest summed time per kernel name.
+    # Dominant kernel: the kernel name with the largest summed time.  Its
+    # algorithmic work is that of the layers whose main kernel it is (a split
+    # reduction's own launches are attributed to splitk_reduce_kernel, which
+    # then carries the layers' output bytes but no FLOPs).
     groups = {}
-    for j, d in enumerate(layers):
-        g = groups.setdefault(d["kernel"], dict(ms=0.0, flops=0, bytes=0, launches=0, layers=[]))
-        g["ms"] += layer_ms[j]
-        g["flops"] += d["flops"]
-        g["bytes"] += d["bytes"]
-        g["launches"] += d["launches"]
+    for j in range(n_launch):
+        li, name = launch_info[j]
+        d = layers[li]
+        g = groups.setdefault(name, dict(ms=0.0, flops=0, bytes=0, launches=0, layers=[]))
+        g["ms"] += float(launch_ms[j])
+        g["launches"] += 1
+        main = j == 0 or launch_info[j - 1][0] != li
+        if main:
+            g["flops"] += d["flops"]
+            g["bytes"] += d["bytes"]
+        else:
+            l = d["layer"]
+            g["bytes"] += l.N * l.K * d["P"] * d["Q"] * 4
         g["layers"].append(d["layer"].name)
     dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
     avg_launch_us = dom["ms"] / dom["launches"] * 1e3
-    if dom_name.startswith("dw"):
+    if dom_name.startswith("dw") or dom["flops"] == 0:
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(achieved, 2), peak=PEAK_HBM_GBS, unit="GB/s",
                     frac=round(achieved / PEAK_HBM_GBS, 4))
@@ -147,12 +174,12 @@ def main():
                     frac=round(achieved / peak, 4))
     roof.update(traffic=None, kernel=dom_name, launches_per_step=dom["launches"],
                 avg_launch_us=round(avg_launch_us, 3),
-                share_of_step=round(dom["ms"] / float(layer_ms.sum()), 4))
+                share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
 
     if args.layers:
         for j, d in enumerate(layers):
             l = d["layer"]
-            t = layer_ms[j]
+            t = float(layer_ms[j])
             print(f"{j:3d} {l.name:10s} {d['kernel']:45s} {t * 1e3:9.2f} us "
                   f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s",
                   file=sys.stderr)
@@ -189,7 +216,7 @@ def main():
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": args.warmup + K,
         "ms_per_step": round(ms_per_step, 5),
         "ms_per_image": round(ms_per_step / wk.layers[0].N, 5),
         "higher_is_better": True,
@@ -199,7 +226,8 @@ def main():
         "data": "synthetic (seeded uniform/He-normal per layer, resident in HBM)",
         "config": {"workload": wk.name, "convs": len(layers), "batch": wk.layers[0].N,
                    "gflop_per_step": round(step_flops / 1e9, 4), "device": torch.cuda.get_device_name(0),
-                   "wall_s_timed": round(wall, 4)},
+                   "wall_s_timed": round(wall, 4), "timing": "one HIP graph of K passes, an event "
+                   "before every layer", "ms_per_step_graph_without_events": round(ms_per_step_untimed, 5)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -108,6 +108,76 @@ int add_act_fwd(long count, const float *a, const float *b, float *y, int relu, 
 /* fp32 -> bf16 bit patterns, round to nearest even (NaN stays NaN). */
 int cast_f32_to_bf16(long count, const float *x, uint16_t *y, void *stream);
 
+/* ---- Stack executor: a network's conv layers planned once and replayed ----
+ *
+ * Batch-1 inference (the latency setting of Sec. 4.2) runs layers of a few
+ * microseconds, so the executor validates and plans every layer once, owns
+ * one split-K workspace for the whole stack, and can capture repeated passes
+ * into a single HIP graph.  Tensor pointers are borrowed: they must stay
+ * valid and keep their contents' meaning for the executor's lifetime (a
+ * replay reads x/w/bias and writes y of every layer). */
+
+enum miconv_op {
+    MICONV_OP_CONV_F32 = 0,    /* conv2d_fwd */
+    MICONV_OP_CONV_BF16 = 1,   /* conv2d_fwd_bf16 (x, w are bf16 bit patterns) */
+    MICONV_OP_DWCONV_F32 = 2   /* dwconv2d_fwd */
+};
+
+typedef struct miconv_conv_desc {
+    int op;                    /* enum miconv_op */
+    int N, C, H, W, K, R, S, stride, pad, groups, relu;
+    const void *x;             /* device, layout as the matching entry point */
+    const void *w;
+    const float *bias;         /* may be NULL */
+    float *y;
+} miconv_conv_desc;
+
+typedef struct miconv_stack miconv_stack;
+
+/* Validate and plan n layers (each as its entry point would); allocate the
+ * executor and its split-K workspace on the current device.  On error
+ * nothing is allocated and *out is NULL. */
+int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **out);
+
+/* Number of layers. */
+int miconv_stack_size(const miconv_stack *s);
+
+/* Kernel names of one layer (as conv2d_describe); returns its launch count. */
+int miconv_stack_describe(const miconv_stack *s, int layer, char *buf, int buflen);
+
+/* Kernel launches in one pass (a layer with a split reduction launches two). */
+int miconv_stack_launches(const miconv_stack *s);
+
+/* Kernel name of launch `launch` of a pass; returns the index of its layer. */
+int miconv_stack_launch_info(const miconv_stack *s, int launch, char *buf, int buflen);
+
+/* Enqueue every layer once, in order, on `stream`. */
+int miconv_stack_launch(miconv_stack *s, void *stream);
+
+/* Enqueue `steps` passes eagerly with an event before every kernel launch and
+ * after the last one (read them with miconv_stack_times once the stream is done).
+ * Drops any captured graph. */
+int miconv_stack_launch_timed(miconv_stack *s, int steps, void *stream);
+
+/* Capture `steps` consecutive passes into one HIP graph, replacing any
+ * previous capture (nothing executes; the NULL stream is served by a private
+ * capture stream).  With timed != 0 an event is recorded before every kernel
+ * launch of every pass and after the last one.  Workspace and events are owned by
+ * the executor, so a replay allocates nothing. */
+int miconv_stack_capture(miconv_stack *s, int steps, int timed, void *stream);
+
+/* Launch the captured graph on `stream` (MICONV_ERR_UNSUPPORTED if none). */
+int miconv_stack_replay(miconv_stack *s, void *stream);
+
+/* After a timed replay (or miconv_stack_launch_timed) has completed:
+ * ms[k*L + j] = time from the event before launch j of pass k to the next
+ * event (L = miconv_stack_launches).  capacity is the length of ms, at least
+ * steps*L. */
+int miconv_stack_times(const miconv_stack *s, float *ms, long capacity);
+
+/* Free the graph, events, workspace and the executor (NULL is a no-op). */
+int miconv_stack_destroy(miconv_stack *s);
+
 /* Names the kernels conv2d_fwd_algo (dtype 0) or conv2d_fwd_bf16 (dtype 1)
  * would launch for this shape on the current device, as a profiler prints
  * them (template arguments included, namespaces omitted), joined by " + ";

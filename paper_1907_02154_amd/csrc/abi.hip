@@ -119,34 +119,25 @@ int cu_count()
     return n;
 }
 
-// Split-K workspace, one per (device, stream): an array of per-tile arrival
-// counters (zeroed once when allocated; every launch leaves them at zero)
-// followed by the fp32 partial sums.
+// Split-K workspace (fp32 partials), one per (device, stream).
 struct Workspace {
     void *ptr = nullptr;
-    size_t counter_bytes = 0;
-    size_t partial_bytes = 0;
+    size_t bytes = 0;
 };
 
-size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
-
-int get_workspace(hipStream_t st, const IgemmPlan &plan, float **partials, int **counters)
+int get_workspace(hipStream_t st, size_t need, float **out)
 {
     static std::mutex mu;
     static std::map<std::pair<int, hipStream_t>, Workspace> table;
-    *partials = nullptr;
-    *counters = nullptr;
-    if (plan.splits <= 1) return MICONV_OK;
-    const size_t need_c = round_up((size_t)plan.counters * sizeof(int), 256);
-    const size_t need_p = round_up(plan.ws_bytes, 256);
+    *out = nullptr;
+    if (need == 0) return MICONV_OK;
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e);
     std::lock_guard<std::mutex> lk(mu);
     Workspace &ws = table[{dev, st}];
-    if (ws.counter_bytes < need_c || ws.partial_bytes < need_p) {
-        const size_t cb = std::max(std::max(need_c, ws.counter_bytes), (size_t)16384);
-        const size_t pb = std::max(std::max(need_p, ws.partial_bytes), (size_t)(1u << 20));
+    if (ws.bytes < need) {
+        const size_t bytes = std::max(need, (size_t)(1u << 20));
         if (ws.ptr) {
             // Kernels already queued on this stream may still use the old buffer.
             e = hipStreamSynchronize(st);
@@ -155,34 +146,101 @@ int get_workspace(hipStream_t st, const IgemmPlan &plan, float **partials, int *
             if (e != hipSuccess) return hip_fail(e);
             ws = Workspace{};
         }
-        void *ptr = nullptr;
-        e = hipMalloc(&ptr, cb + pb);
-        if (e != hipSuccess) return hip_fail(e);
-        e = hipMemset(ptr, 0, cb);
+        e = hipMalloc(&ws.ptr, bytes);
         if (e != hipSuccess) {
-            hipFree(ptr);
+            ws.ptr = nullptr;
             return hip_fail(e);
         }
-        ws.ptr = ptr;
-        ws.counter_bytes = cb;
-        ws.partial_bytes = pb;
+        ws.bytes = bytes;
     }
-    *counters = static_cast<int *>(ws.ptr);
-    *partials = reinterpret_cast<float *>(static_cast<char *>(ws.ptr) + ws.counter_bytes);
+    *out = static_cast<float *>(ws.ptr);
     return MICONV_OK;
 }
 
 int finish(hipError_t e) { return e == hipSuccess ? MICONV_OK : hip_fail(e); }
 
-int run_igemm_f32(const ConvProblem &p, const float *x, const float *w, const float *bias, float *y,
-                  hipStream_t st)
+}  // namespace
+
+int set_hip_error(hipError_t e) { return hip_fail(e); }
+
+// Validate one conv call and fix the kernel that serves it.
+int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S, int stride,
+            int pad, int groups, const void *x, const void *w, const float *bias, float *y,
+            int relu, Resolved *out)
 {
-    const IgemmPlan plan = plan_igemm_f32(p, cu_count());
-    float *ws = nullptr;
-    int *counters = nullptr;
-    int rc = get_workspace(st, plan, &ws, &counters);
+    Resolved r{};
+    const size_t elem = kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
+    int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, elem, &r.p);
     if (rc != MICONV_OK) return rc;
-    return finish(launch_igemm_f32(p, plan, x, w, bias, y, ws, counters, st));
+    if ((rc = check_bias(bias)) != MICONV_OK) return rc;
+    if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_IGEMM) return MICONV_ERR_UNSUPPORTED;
+    r.p.relu = relu ? 1 : 0;
+    r.kind = kind;
+    r.x = x;
+    r.w = w;
+    r.bias = bias;
+    r.y = y;
+    const bool depthwise = groups > 1 && groups == C && K == C;
+    if (kind == OP_DW_F32) {
+        if (!depthwise) return MICONV_ERR_GROUPS;
+        if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
+        r.impl = IMPL_DW;
+    } else if (kind == OP_DENSE_BF16) {
+        r.impl = IMPL_DIRECT;
+    } else if (kind == OP_DENSE_F32) {
+        if (algo == MICONV_ALGO_AUTO) {
+            if (depthwise && R <= 7 && S <= 7)
+                r.impl = IMPL_DW;
+            else
+                r.impl = (groups == 1 || r.p.Cg >= 8) ? IMPL_IGEMM : IMPL_DIRECT;
+        } else {
+            r.impl = algo == MICONV_ALGO_DIRECT ? IMPL_DIRECT : IMPL_IGEMM;
+        }
+    } else {
+        return MICONV_ERR_UNSUPPORTED;
+    }
+    if (r.impl == IMPL_IGEMM) r.plan = plan_igemm_f32(r.p, cu_count());
+    *out = r;
+    return MICONV_OK;
+}
+
+hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook)
+{
+    const float *xf = static_cast<const float *>(r.x), *wf = static_cast<const float *>(r.w);
+    if (r.impl == IMPL_IGEMM) return launch_igemm_f32(r.p, r.plan, xf, wf, r.bias, r.y, ws, st, hook);
+    if (hook) {
+        hipError_t e = hook->before_launch(hook->ctx, st);
+        if (e != hipSuccess) return e;
+    }
+    switch (r.impl) {
+    case IMPL_DW: return launch_dwconv_f32(r.p, xf, wf, r.bias, r.y, st);
+    default:
+        if (r.kind == OP_DENSE_BF16)
+            return launch_conv_direct_bf16(r.p, static_cast<const uint16_t *>(r.x),
+                                           static_cast<const uint16_t *>(r.w), r.bias, r.y, st);
+        return launch_conv_direct_f32(r.p, xf, wf, r.bias, r.y, st);
+    }
+}
+
+void describe(const Resolved &r, char *buf, int len, int *launches)
+{
+    switch (r.impl) {
+    case IMPL_DW: describe_dwconv(r.p, buf, len, launches); break;
+    case IMPL_IGEMM: describe_igemm_f32(r.p, r.plan, buf, len, launches); break;
+    default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;
+    }
+}
+
+namespace {
+
+int run(const Resolved &r, hipStream_t st)
+{
+    float *ws = nullptr;
+    if (r.impl == IMPL_IGEMM) {
+        int rc = get_workspace(st, r.plan.ws_bytes, &ws);
+        if (rc != MICONV_OK) return rc;
+    }
+    return finish(enqueue(r, ws, st));
 }
 
 }  // namespace
@@ -206,20 +264,10 @@ int conv2d_fwd_algo(int N, int C, int H, int W, int K, int R, int S, int stride,
                     int groups, const float *x, const float *w, const float *bias, float *y,
                     int relu, int algo, void *stream)
 {
-    ConvProblem p;
-    int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, sizeof(float), &p);
-    if (rc != MICONV_OK) return rc;
-    if ((rc = check_bias(bias)) != MICONV_OK) return rc;
-    if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_IGEMM) return MICONV_ERR_UNSUPPORTED;
-    p.relu = relu ? 1 : 0;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const bool depthwise = groups > 1 && groups == C && K == C;
-    if (algo == MICONV_ALGO_AUTO) {
-        if (depthwise && R <= 7 && S <= 7) return finish(launch_dwconv_f32(p, x, w, bias, y, st));
-        algo = (groups == 1 || p.Cg >= 8) ? MICONV_ALGO_IGEMM : MICONV_ALGO_DIRECT;
-    }
-    if (algo == MICONV_ALGO_DIRECT) return finish(launch_conv_direct_f32(p, x, w, bias, y, st));
-    return run_igemm_f32(p, x, w, bias, y, st);
+    Resolved r;
+    int rc = resolve(OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y,
+                     relu, &r);
+    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
 }
 
 int conv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
@@ -233,27 +281,20 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
                     int groups, const uint16_t *x, const uint16_t *w, const float *bias, float *y,
                     int relu, void *stream)
 {
-    ConvProblem p;
-    int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, sizeof(uint16_t), &p);
-    if (rc != MICONV_OK) return rc;
-    if ((rc = check_bias(bias)) != MICONV_OK) return rc;
-    p.relu = relu ? 1 : 0;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    return finish(launch_conv_direct_bf16(p, x, w, bias, y, st));
+    Resolved r;
+    int rc = resolve(OP_DENSE_BF16, MICONV_ALGO_AUTO, N, C, H, W, K, R, S, stride, pad, groups, x,
+                     w, bias, y, relu, &r);
+    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
 }
 
 int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
                  const float *x, const float *w, const float *bias, float *y, int relu,
                  void *stream)
 {
-    ConvProblem p;
-    int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, sizeof(float), &p);
-    if (rc != MICONV_OK) return rc;
-    if ((rc = check_bias(bias)) != MICONV_OK) return rc;
-    if (groups != C || K != C) return MICONV_ERR_GROUPS;
-    if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
-    p.relu = relu ? 1 : 0;
-    return finish(launch_dwconv_f32(p, x, w, bias, y, static_cast<hipStream_t>(stream)));
+    Resolved r;
+    int rc = resolve(OP_DW_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S, stride, pad, groups, x, w,
+                     bias, y, relu, &r);
+    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
 }
 
 int maxpool2d_fwd(int N, int C, int H, int W, int R, int S, int stride, int pad, const float *x,
@@ -292,30 +333,13 @@ int conv2d_describe(int N, int C, int H, int W, int K, int R, int S, int stride,
 {
     if (!buf || buflen <= 0 || !launches) return MICONV_ERR_NULL;
     buf[0] = 0;
-    static const float dummy[4] = {0, 0, 0, 0};
-    ConvProblem p;
-    int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, dummy, dummy, dummy,
-                      dtype == 1 ? sizeof(uint16_t) : sizeof(float), &p);
-    if (rc != MICONV_OK) return rc;
     if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
-    if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_IGEMM) return MICONV_ERR_UNSUPPORTED;
-    if (dtype == 1) {
-        describe_direct(1, buf, buflen, launches);
-        return MICONV_OK;
-    }
-    const bool depthwise = groups > 1 && groups == C && K == C;
-    if (algo == MICONV_ALGO_AUTO) {
-        if (depthwise && R <= 7 && S <= 7) {
-            describe_dwconv(p, buf, buflen, launches);
-            return MICONV_OK;
-        }
-        algo = (groups == 1 || p.Cg >= 8) ? MICONV_ALGO_IGEMM : MICONV_ALGO_DIRECT;
-    }
-    if (algo == MICONV_ALGO_DIRECT) {
-        describe_direct(0, buf, buflen, launches);
-        return MICONV_OK;
-    }
-    describe_igemm_f32(p, plan_igemm_f32(p, cu_count()), buf, buflen, launches);
+    alignas(256) static const float dummy[64] = {};
+    Resolved r;
+    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride,
+                     pad, groups, dummy, dummy, nullptr, const_cast<float *>(dummy), 0, &r);
+    if (rc != MICONV_OK) return rc;
+    describe(r, buf, buflen, launches);
     return MICONV_OK;
 }
 

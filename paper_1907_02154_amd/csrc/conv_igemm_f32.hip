@@ -22,10 +22,11 @@
 // one channel: 128-byte contiguous NCHW segments.
 //
 // Small layers (batch 1, late stages) do not fill 256 CUs with output tiles;
-// there the reduction is split over grid.z.  The work-groups of one output
-// tile leave fp32 partials in a workspace and the last to finish sums them
-// in split order inside the same launch, so results are run-to-run
-// deterministic and every conv is a single kernel launch.
+// there the reduction is split over grid.z, every split writes fp32 partials
+// to a workspace, and a second kernel sums them in split order, so results
+// are run-to-run deterministic.  (An in-kernel "last work-group reduces"
+// scheme needs device-scope fences, which on a multi-XCD part write back and
+// invalidate whole L2s and cost far more than a second launch.)
 #include "internal.h"
 
 #include <cstdio>
@@ -157,37 +158,8 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
         __syncthreads();
     }
 
-    // Epilogue.  Without a split: bias + activation and the NCHW store.
-    // With a split: every work-group of a tile stores its fp32 partials, and
-    // the last one to arrive (per-tile arrival counter) sums all partials in
-    // split order, so the result does not depend on arrival order.
-    if (a.splits > 1) {
-#pragma unroll
-        for (int bj = 0; bj < BJ; ++bj) {
-            const int m = m0 + wp * WTP + bj * 32 + ll;
-            if (m >= a.M) continue;
-#pragma unroll
-            for (int bi = 0; bi < BI; ++bi)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int k = k0 + wk * WTK + bi * 32 + 8 * (v >> 2) + 4 * hl + (v & 3);
-                    if (k < a.Kg)
-                        a.ws[((long)split * a.K + g * a.Kg + k) * a.M + m] = acc[bi][bj][v];
-                }
-        }
-        __threadfence();
-        __syncthreads();
-        __shared__ int s_last;
-        if (tid == 0) {
-            const int tile = (g * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
-            const int prev = atomicAdd(&a.counters[tile], 1);
-            s_last = prev == a.splits - 1;
-            if (s_last) atomicExch(&a.counters[tile], 0);   // ready for the next call
-        }
-        __syncthreads();
-        if (!s_last) return;
-        __threadfence();
-    }
+    // Epilogue: bias + activation and the NCHW store, or (split reduction)
+    // this split's raw fp32 partials, summed later by splitk_reduce_kernel.
 #pragma unroll
     for (int bj = 0; bj < BJ; ++bj) {
         const int m = m0 + wp * WTP + bj * 32 + ll;
@@ -202,17 +174,62 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
                 const int k = k0 + wk * WTK + bi * 32 + 8 * (v >> 2) + 4 * hl + (v & 3);
                 if (k >= a.Kg) continue;
                 const int kg = g * a.Kg + k;
-                float val = acc[bi][bj][v];
                 if (a.splits > 1) {
-                    val = 0.f;
-                    for (int sp = 0; sp < a.splits; ++sp)
-                        val += sp == split ? acc[bi][bj][v] : a.ws[((long)sp * a.K + kg) * a.M + m];
+                    a.ws[((long)split * a.K + kg) * a.M + m] = acc[bi][bj][v];
+                } else {
+                    float val = acc[bi][bj][v] + (a.bias ? a.bias[kg] : 0.f);
+                    if (a.relu) val = fmaxf(val, 0.f);
+                    a.y[ybase + (long)kg * a.PQ] = val;
                 }
-                val += a.bias ? a.bias[kg] : 0.f;
-                if (a.relu) val = fmaxf(val, 0.f);
-                a.y[ybase + (long)kg * a.PQ] = val;
             }
         }
+    }
+}
+
+// Sum the split partials in split order (deterministic), add bias, apply the
+// activation and store NCHW.  Lanes walk m, so reads and writes are contiguous.
+// With one image the partials' [K][M] order is y's own order, so (when the
+// sizes and pointers allow) lanes take four consecutive elements with
+// 16-byte accesses.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
+{
+    const long total = (long)a.K * a.M;
+    long start = 0;
+    if (a.vec4) {
+        const long n4 = total / 4;
+        const float4 *ws4 = reinterpret_cast<const float4 *>(a.ws);
+        for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+             i += (long)gridDim.x * blockDim.x) {
+            float4 s = ws4[i];
+            for (int sp = 1; sp < a.splits; ++sp) {
+                const float4 v = ws4[(long)sp * n4 + i];
+                s.x += v.x;
+                s.y += v.y;
+                s.z += v.z;
+                s.w += v.w;
+            }
+            float o[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int k = (int)((4 * i + e) / a.M);
+                o[e] += a.bias ? a.bias[k] : 0.f;
+                if (a.relu) o[e] = fmaxf(o[e], 0.f);
+            }
+            reinterpret_cast<float4 *>(a.y)[i] = make_float4(o[0], o[1], o[2], o[3]);
+        }
+        start = 4 * n4;
+    }
+    for (long i = start + (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const int k = (int)(i / a.M);
+        const int m = (int)(i - (long)k * a.M);
+        float s = a.ws[i];
+        for (int sp = 1; sp < a.splits; ++sp) s += a.ws[(long)sp * total + i];
+        s += a.bias ? a.bias[k] : 0.f;
+        if (a.relu) s = fmaxf(s, 0.f);
+        const int n = m / a.PQ;
+        const int pq = m - n * a.PQ;
+        a.y[((long)n * a.K + k) * a.PQ + pq] = s;
     }
 }
 
@@ -220,7 +237,11 @@ struct TileInfo {
     int bkc, bpx, wk, wp, krc;
 };
 // Tile table: 0 = 128x128 (large layers), 1 = 64x64, 2 = 32 channels x 64 pixels.
-const TileInfo kTiles[] = {{128, 128, 2, 2, 16}, {64, 64, 2, 2, 16}, {32, 64, 1, 2, 16}};
+// Bigger reduction chunks for the smaller tiles: small layers are bound by
+// the latency of a global-load round trip per chunk, so fewer, larger chunks
+// (more loads in flight per round trip) matter more there than occupancy.
+const TileInfo kTiles[] = {{128, 128, 2, 2, 16}, {64, 64, 2, 2, 32}, {32, 64, 1, 2, 64}};
+constexpr int kNumTiles = 3;
 
 int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 
@@ -232,10 +253,10 @@ hipError_t launch_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
         hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 128, 128, 2, 2, 16>), grid, dim3(256), 0, st, a);
         break;
     case 1:
-        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 64, 64, 2, 2, 16>), grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 64, 64, 2, 2, 32>), grid, dim3(256), 0, st, a);
         break;
     default:
-        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 32, 64, 1, 2, 16>), grid, dim3(128), 0, st, a);
+        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 32, 64, 1, 2, 64>), grid, dim3(128), 0, st, a);
         break;
     }
     return hipGetLastError();
@@ -244,34 +265,27 @@ hipError_t launch_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 }  // namespace
 
 // Pick the tile and the reduction split: the biggest tile that still gives
-// about two work-groups per CU, else the smallest tile plus a split of the
-// reduction (chunks of 16 taps, at least 4 chunks per split).
+// about two work-groups per CU; otherwise the smallest tile, with the
+// reduction split until there are about two work-groups per CU (each split
+// keeps at least one whole chunk).
 IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus)
 {
-    IgemmPlan plan{2, 1, 0, 0};
+    IgemmPlan plan{kNumTiles - 1, 1, p.Kred, 0};
     const long target = 2L * num_cus;
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t < kNumTiles; ++t) {
         const long tiles = (long)ceil_div(p.M, kTiles[t].bpx) * ceil_div(p.Kg, kTiles[t].bkc) * p.groups;
-        if (tiles >= target || t == 2) {
-            plan.tile = t;
-            const int krc = kTiles[t].krc;
-            const int chunks = ceil_div(p.Kred, krc);
-            int splits = 1;
-            if (tiles < target) {
-                splits = (int)((target + tiles - 1) / tiles);
-                const int max_splits = chunks / 4;
-                if (splits > max_splits) splits = max_splits;
-                if (splits < 1) splits = 1;
-            }
-            const int chunks_per = ceil_div(chunks, splits);
-            splits = ceil_div(chunks, chunks_per);   // no empty splits
-            plan.splits = splits;
-            plan.kr_per_split = chunks_per * krc;
-            const size_t tiles_total = (size_t)tiles;
-            plan.counters = splits > 1 ? (int)tiles_total : 0;
-            plan.ws_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
-            break;
-        }
+        if (tiles < target && t < kNumTiles - 1) continue;
+        plan.tile = t;
+        const int krc = kTiles[t].krc;
+        const int chunks = ceil_div(p.Kred, krc);
+        int splits = tiles < target ? (int)((target + tiles - 1) / tiles) : 1;
+        if (splits > chunks) splits = chunks;
+        const int chunks_per = ceil_div(chunks, splits);
+        splits = ceil_div(chunks, chunks_per);   // no empty splits
+        plan.splits = splits;
+        plan.kr_per_split = chunks_per * krc;
+        plan.ws_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
+        break;
     }
     return plan;
 }
@@ -282,14 +296,14 @@ void describe_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, char *buf, 
     const TileInfo &t = kTiles[plan.tile];
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R == 0 || S == 0 || R != S) R = S = 0;
-    snprintf(buf, len, "igemm_f32_kernel<%d, %d, %d, %d, %d, %d, %d>", R, S, t.bkc, t.bpx, t.wk,
-             t.wp, t.krc);
-    *launches = 1;
+    snprintf(buf, len, "igemm_f32_kernel<%d, %d, %d, %d, %d, %d, %d>%s", R, S, t.bkc, t.bpx, t.wk,
+             t.wp, t.krc, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    *launches = plan.splits > 1 ? 2 : 1;
 }
 
 hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const float *x,
-                            const float *w, const float *bias, float *y, float *ws, int *counters,
-                            hipStream_t st)
+                            const float *w, const float *bias, float *y, float *ws,
+                            hipStream_t st, const LaunchHook *hook)
 {
     ConvArgs a = make_args(p);
     a.x = x;
@@ -297,12 +311,12 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
     a.bias = bias;
     a.y = y;
     a.ws = plan.splits > 1 ? ws : nullptr;
-    a.counters = plan.splits > 1 ? counters : nullptr;
     a.splits = plan.splits;
     a.kr_per_split = plan.kr_per_split;
     const TileInfo &ti = kTiles[plan.tile];
     dim3 grid(ceil_div(p.M, ti.bpx), ceil_div(p.Kg, ti.bkc), p.groups * plan.splits);
-    hipError_t e;
+    hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
+    if (e != hipSuccess) return e;
     if (p.R == 1 && p.S == 1)
         e = launch_rs<1, 1>(a, plan.tile, grid, st);
     else if (p.R == 3 && p.S == 3)
@@ -311,7 +325,14 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
         e = launch_rs<7, 7>(a, plan.tile, grid, st);
     else
         e = launch_rs<0, 0>(a, plan.tile, grid, st);
-    return e;
+    if (e != hipSuccess || plan.splits == 1) return e;
+    if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+    const long total = (long)p.K * p.M;
+    a.vec4 = p.N == 1 && total % 4 == 0 && (uintptr_t)y % 16 == 0 && (uintptr_t)ws % 16 == 0;
+    long blocks = (total + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
 }
 
 }  // namespace miconv

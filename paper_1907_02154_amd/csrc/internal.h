@@ -24,15 +24,22 @@ struct ConvArgs {
     const float *bias;    // [K] or nullptr
     float *y;             // [N][K][P][Q]
     float *ws;            // split-K partials [splits][K][M] (nullptr when splits == 1)
-    int *counters;        // split-K arrival counter per output tile, zero between calls
     int N, C, H, W, K, R, S, stride, pad, groups;
     int P, Q, Cg, Kg, Kred, M, PQ, HW;
     int splits;           // reduction split count (grid.z = groups * splits)
     int kr_per_split;     // reduction length per split, a multiple of the chunk size
     int relu;
+    int vec4;             // split-K reduce may use 16-byte accesses (one image, aligned)
 };
 
 ConvArgs make_args(const ConvProblem &p);
+
+// Called before every kernel launch of one conv (the stack executor records
+// a timing event there).
+struct LaunchHook {
+    hipError_t (*before_launch)(void *ctx, hipStream_t st);
+    void *ctx;
+};
 
 // Launchers.  Each returns hipSuccess or the launch error.
 hipError_t launch_conv_direct_f32(const ConvProblem &p, const float *x, const float *w,
@@ -49,13 +56,12 @@ struct IgemmPlan {
     int tile;           // index into the tile table of the kernel family
     int splits;
     int kr_per_split;
-    int counters;       // output tiles needing an arrival counter (0 without a split)
     size_t ws_bytes;    // bytes of fp32 partials (0 without a split)
 };
 IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus);
 hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const float *x,
-                            const float *w, const float *bias, float *y, float *ws, int *counters,
-                            hipStream_t st);
+                            const float *w, const float *bias, float *y, float *ws,
+                            hipStream_t st, const LaunchHook *hook = nullptr);
 // Kernel names (as a profiler prints them, without namespace) and launch counts.
 void describe_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, char *buf, int len,
                         int *launches);
@@ -67,6 +73,26 @@ hipError_t launch_maxpool_f32(int N, int C, int H, int W, int R, int S, int stri
 hipError_t launch_add_act_f32(long count, const float *a, const float *b, float *y, int relu,
                               hipStream_t st);
 hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t st);
+
+// A validated conv call with its kernel fixed (what the ABI entry points and
+// the stack executor enqueue).
+enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2 };
+enum Impl { IMPL_DIRECT = 0, IMPL_IGEMM = 1, IMPL_DW = 2 };
+struct Resolved {
+    ConvProblem p;
+    int kind;
+    int impl;
+    IgemmPlan plan;     // IMPL_IGEMM only
+    const void *x, *w;
+    const float *bias;
+    float *y;
+};
+int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S, int stride,
+            int pad, int groups, const void *x, const void *w, const float *bias, float *y,
+            int relu, Resolved *out);
+hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
+void describe(const Resolved &r, char *buf, int len, int *launches);
+int set_hip_error(hipError_t e);   // records e for miconv_last_hip_error, returns MICONV_ERR_HIP
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 

@@ -1,0 +1,291 @@
+// Stack executor: a network's conv layers validated and planned once, then
+// enqueued back to back, or captured into one HIP graph and replayed.
+//
+// Batch-1 inference (the setting of the paper's latency tables, Sec. 4.2)
+// runs layers of a few microseconds each, so per-call host work and launch
+// gaps matter as much as the kernels.  The executor resolves every layer's
+// kernel and split-K plan up front, owns one split-K workspace sized for the
+// largest layer (layers run in stream order, so they can share it), and can
+// record the whole pass -- optionally repeated `steps` times, with an event
+// before every kernel launch -- as a graph that replays with a single launch.
+#include "../../include/miconv.h"
+#include "internal.h"
+
+#include <cstdio>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+struct miconv_stack {
+    int device = 0;
+    std::vector<miconv::Resolved> layers;
+    std::vector<int> launch_layer;          // layer of every kernel launch of one pass
+    std::vector<std::string> launch_name;   // its kernel name
+    float *partials = nullptr;              // split-K workspace shared by all layers
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    std::vector<hipEvent_t> events;         // steps * launches + 1 when timed
+    int steps = 0;
+};
+
+using namespace miconv;
+
+namespace {
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+void drop_graph(miconv_stack *s)
+{
+    if (s->exec) hipGraphExecDestroy(s->exec);
+    if (s->graph) hipGraphDestroy(s->graph);
+    for (hipEvent_t e : s->events) hipEventDestroy(e);
+    s->exec = nullptr;
+    s->graph = nullptr;
+    s->events.clear();
+    s->steps = 0;
+}
+
+// Record an event.  Under capture a plain record only marks a capture
+// dependency, so an event-record node is added to the graph by hand, after
+// the nodes the stream currently depends on, and becomes the new dependency.
+hipError_t record(hipEvent_t ev, hipStream_t st)
+{
+    hipStreamCaptureStatus status = hipStreamCaptureStatusNone;
+    unsigned long long id = 0;
+    hipGraph_t g = nullptr;
+    const hipGraphNode_t *deps = nullptr;
+    size_t ndeps = 0;
+    hipError_t e = hipStreamGetCaptureInfo_v2(st, &status, &id, &g, &deps, &ndeps);
+    if (e != hipSuccess) return e;
+    if (status != hipStreamCaptureStatusActive) return hipEventRecord(ev, st);
+    hipGraphNode_t node = nullptr;
+    e = hipGraphAddEventRecordNode(&node, g, deps, ndeps, ev);
+    if (e != hipSuccess) return e;
+    return hipStreamUpdateCaptureDependencies(st, &node, 1, hipStreamSetCaptureDependencies);
+}
+
+struct EventCursor {
+    hipEvent_t *next;
+};
+
+hipError_t record_next(void *ctx, hipStream_t st)
+{
+    EventCursor *c = static_cast<EventCursor *>(ctx);
+    return record(*c->next++, st);
+}
+
+// One pass over every layer; with `ev`, an event before every kernel launch.
+hipError_t enqueue_all(miconv_stack *s, hipStream_t st, hipEvent_t *ev)
+{
+    EventCursor cur{ev};
+    LaunchHook hook{record_next, &cur};
+    for (size_t i = 0; i < s->layers.size(); ++i) {
+        hipError_t e = enqueue(s->layers[i], s->partials, st, ev ? &hook : nullptr);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+int make_events(miconv_stack *s, int steps)
+{
+    s->events.resize((size_t)steps * s->launch_layer.size() + 1, nullptr);
+    for (auto &ev : s->events) {
+        hipError_t e = hipEventCreate(&ev);
+        if (e != hipSuccess) {
+            ev = nullptr;
+            drop_graph(s);
+            return set_hip_error(e);
+        }
+    }
+    return MICONV_OK;
+}
+
+int capture_on(miconv_stack *s, int steps, int timed, hipStream_t st)
+{
+    drop_graph(s);
+    const size_t n = s->launch_layer.size();
+    if (timed) {
+        int rc = make_events(s, steps);
+        if (rc != MICONV_OK) return rc;
+    }
+    hipError_t e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+        drop_graph(s);
+        return set_hip_error(e);
+    }
+    for (int k = 0; k < steps && e == hipSuccess; ++k)
+        e = enqueue_all(s, st, timed ? &s->events[(size_t)k * n] : nullptr);
+    if (e == hipSuccess && timed) e = record(s->events.back(), st);
+    hipGraph_t g = nullptr;
+    hipError_t e2 = hipStreamEndCapture(st, &g);
+    s->graph = g;
+    if (e == hipSuccess) e = e2;
+    if (e == hipSuccess) e = hipGraphInstantiate(&s->exec, s->graph, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        drop_graph(s);
+        return set_hip_error(e);
+    }
+    s->steps = steps;
+    return MICONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **out)
+{
+    if (!out) return MICONV_ERR_NULL;
+    *out = nullptr;
+    if (n <= 0) return MICONV_ERR_SHAPE;
+    if (!layers) return MICONV_ERR_NULL;
+    miconv_stack *s = new (std::nothrow) miconv_stack;
+    if (!s) return MICONV_ERR_HIP;
+    hipError_t e = hipGetDevice(&s->device);
+    if (e != hipSuccess) {
+        delete s;
+        return set_hip_error(e);
+    }
+    size_t need_p = 0;
+    for (int i = 0; i < n; ++i) {
+        const miconv_conv_desc &d = layers[i];
+        Resolved r;
+        int rc = resolve(d.op, MICONV_ALGO_AUTO, d.N, d.C, d.H, d.W, d.K, d.R, d.S, d.stride,
+                         d.pad, d.groups, d.x, d.w, d.bias, d.y, d.relu, &r);
+        if (rc != MICONV_OK) {
+            delete s;
+            return rc;
+        }
+        if (r.impl == IMPL_IGEMM && r.plan.splits > 1)
+            need_p = std::max(need_p, round_up(r.plan.ws_bytes, 256));
+        s->layers.push_back(r);
+        char buf[512];
+        int launches = 0;
+        describe(r, buf, sizeof buf, &launches);
+        std::string names(buf);
+        for (int j = 0; j < launches; ++j) {
+            const size_t cut = names.find(" + ");
+            s->launch_layer.push_back(i);
+            s->launch_name.push_back(names.substr(0, cut));
+            names = cut == std::string::npos ? std::string() : names.substr(cut + 3);
+        }
+    }
+    if (need_p) {
+        void *ptr = nullptr;
+        e = hipMalloc(&ptr, need_p);
+        if (e != hipSuccess) {
+            delete s;
+            return set_hip_error(e);
+        }
+        s->partials = static_cast<float *>(ptr);
+    }
+    *out = s;
+    return MICONV_OK;
+}
+
+int miconv_stack_size(const miconv_stack *s)
+{
+    return s ? (int)s->layers.size() : MICONV_ERR_NULL;
+}
+
+int miconv_stack_describe(const miconv_stack *s, int layer, char *buf, int buflen)
+{
+    if (!s || !buf || buflen <= 0) return MICONV_ERR_NULL;
+    if (layer < 0 || layer >= (int)s->layers.size()) return MICONV_ERR_SHAPE;
+    int launches = 0;
+    describe(s->layers[layer], buf, buflen, &launches);
+    return launches;
+}
+
+int miconv_stack_launches(const miconv_stack *s)
+{
+    return s ? (int)s->launch_layer.size() : MICONV_ERR_NULL;
+}
+
+int miconv_stack_launch_info(const miconv_stack *s, int launch, char *buf, int buflen)
+{
+    if (!s || !buf || buflen <= 0) return MICONV_ERR_NULL;
+    if (launch < 0 || launch >= (int)s->launch_layer.size()) return MICONV_ERR_SHAPE;
+    snprintf(buf, buflen, "%s", s->launch_name[launch].c_str());
+    return s->launch_layer[launch];
+}
+
+int miconv_stack_launch(miconv_stack *s, void *stream)
+{
+    if (!s) return MICONV_ERR_NULL;
+    hipError_t e = enqueue_all(s, static_cast<hipStream_t>(stream), nullptr);
+    return e == hipSuccess ? MICONV_OK : set_hip_error(e);
+}
+
+int miconv_stack_launch_timed(miconv_stack *s, int steps, void *stream)
+{
+    if (!s) return MICONV_ERR_NULL;
+    if (steps < 1) return MICONV_ERR_SHAPE;
+    drop_graph(s);
+    const size_t n = s->launch_layer.size();
+    int rc = make_events(s, steps);
+    if (rc != MICONV_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < steps && e == hipSuccess; ++k)
+        e = enqueue_all(s, st, &s->events[(size_t)k * n]);
+    if (e == hipSuccess) e = hipEventRecord(s->events.back(), st);
+    if (e != hipSuccess) {
+        drop_graph(s);
+        return set_hip_error(e);
+    }
+    s->steps = steps;
+    return MICONV_OK;
+}
+
+int miconv_stack_capture(miconv_stack *s, int steps, int timed, void *stream)
+{
+    if (!s) return MICONV_ERR_NULL;
+    if (steps < 1) return MICONV_ERR_SHAPE;
+    // The legacy default stream cannot be captured; record on a private stream
+    // instead (the graph can still be launched on any stream).
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipStream_t tmp = nullptr;
+    if (!st) {
+        hipError_t e = hipStreamCreateWithFlags(&tmp, hipStreamNonBlocking);
+        if (e != hipSuccess) return set_hip_error(e);
+        st = tmp;
+    }
+    const int rc = capture_on(s, steps, timed, st);
+    if (tmp) hipStreamDestroy(tmp);
+    return rc;
+}
+
+int miconv_stack_replay(miconv_stack *s, void *stream)
+{
+    if (!s) return MICONV_ERR_NULL;
+    if (!s->exec) return MICONV_ERR_UNSUPPORTED;
+    hipError_t e = hipGraphLaunch(s->exec, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? MICONV_OK : set_hip_error(e);
+}
+
+int miconv_stack_times(const miconv_stack *s, float *ms, long capacity)
+{
+    if (!s || !ms) return MICONV_ERR_NULL;
+    if (s->events.empty()) return MICONV_ERR_UNSUPPORTED;
+    const size_t total = s->events.size() - 1;
+    if ((size_t)capacity < total) return MICONV_ERR_SHAPE;
+    for (size_t i = 0; i < total; ++i) {
+        hipError_t e = hipEventElapsedTime(&ms[i], s->events[i], s->events[i + 1]);
+        if (e != hipSuccess) return set_hip_error(e);
+    }
+    return MICONV_OK;
+}
+
+int miconv_stack_destroy(miconv_stack *s)
+{
+    if (!s) return MICONV_OK;
+    drop_graph(s);
+    if (s->partials) hipFree(s->partials);
+    delete s;
+    return MICONV_OK;
+}
+
+}  // extern "C"

@@ -29,7 +29,10 @@ _lib = None
 class MiconvError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
-        super().__init__(f"{what}: {strerror(status)} ({status})")
+        extra = ""
+        if status == ERR_HIP:
+            extra = f", hipError {lib().miconv_last_hip_error()}"
+        super().__init__(f"{what}: {strerror(status)} ({status}{extra})")
 
 
 def lib() -> ctypes.CDLL:
@@ -51,6 +54,22 @@ def lib() -> ctypes.CDLL:
         L.cast_f32_to_bf16.argtypes = [l, p, p, p]
         L.conv2d_describe.argtypes = [i] * 12 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
         L.conv2d_describe.restype = i
+        L.miconv_stack_create.argtypes = [p, i, ctypes.POINTER(p)]
+        L.miconv_stack_size.argtypes = [p]
+        L.miconv_stack_describe.argtypes = [p, i, ctypes.c_char_p, i]
+        L.miconv_stack_launch.argtypes = [p, p]
+        L.miconv_stack_launches.argtypes = [p]
+        L.miconv_stack_launch_info.argtypes = [p, i, ctypes.c_char_p, i]
+        L.miconv_stack_capture.argtypes = [p, i, i, p]
+        L.miconv_stack_launch_timed.argtypes = [p, i, p]
+        L.miconv_stack_replay.argtypes = [p, p]
+        L.miconv_stack_times.argtypes = [p, p, l]
+        L.miconv_stack_destroy.argtypes = [p]
+        for f in ("miconv_stack_create", "miconv_stack_size", "miconv_stack_describe",
+                  "miconv_stack_launches", "miconv_stack_launch_info",
+                  "miconv_stack_launch", "miconv_stack_launch_timed", "miconv_stack_capture", "miconv_stack_replay",
+                  "miconv_stack_times", "miconv_stack_destroy"):
+            getattr(L, f).restype = i
         L.miconv_strerror.argtypes = [i]
         L.miconv_strerror.restype = ctypes.c_char_p
         L.miconv_last_hip_error.argtypes = []
@@ -200,6 +219,97 @@ def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", alg
                                1 if dtype == "bf16" else 0, int(algo), buf, 256, ctypes.byref(n))
     _check(rc, "conv2d_describe")
     return buf.value.decode(), n.value
+
+
+OP_CONV_F32, OP_CONV_BF16, OP_DWCONV_F32 = 0, 1, 2
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int)] + [(n, ctypes.c_int) for n in
+                                         ("N", "C", "H", "W", "K", "R", "S", "stride", "pad",
+                                          "groups", "relu")] + \
+               [("x", ctypes.c_void_p), ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("y", ctypes.c_void_p)]
+
+
+class Stack:
+    """A list of conv layers planned once by the library's stack executor.
+
+    ``layers`` holds tuples ``(op, x, w, bias, y, stride, pad, groups, relu)``
+    of device tensors (bias may be None).  The tensors are kept referenced
+    for the executor's lifetime.
+    """
+
+    def __init__(self, layers):
+        self._keep = []
+        descs = (ConvDesc * len(layers))()
+        for d, (op, x, w, bias, y, stride, pad, groups, relu) in zip(descs, layers):
+            xdt = torch.bfloat16 if op == OP_CONV_BF16 else torch.float32
+            _dev(x, xdt, "x", 4)
+            _dev(w, xdt, "w", 4)
+            _dev(y, torch.float32, "y", 4)
+            if bias is not None:
+                _dev(bias, torch.float32, "bias", 1)
+            N, C, H, W = x.shape
+            K, _, R, S = w.shape
+            d.op, d.N, d.C, d.H, d.W, d.K, d.R, d.S = op, N, C, H, W, K, R, S
+            d.stride, d.pad, d.groups, d.relu = stride, pad, groups, 1 if relu else 0
+            d.x, d.w, d.bias, d.y = x.data_ptr(), w.data_ptr(), _ptr(bias), y.data_ptr()
+            self._keep.append((x, w, bias, y))
+        self.n = len(layers)
+        self.steps = 0
+        h = ctypes.c_void_p()
+        _check(lib().miconv_stack_create(descs, self.n, ctypes.byref(h)), "miconv_stack_create")
+        self._h = h
+        self.launches = lib().miconv_stack_launches(h)
+
+    def launch_info(self, j: int):
+        """(layer index, kernel name) of kernel launch j of a pass."""
+        buf = ctypes.create_string_buffer(256)
+        layer = lib().miconv_stack_launch_info(self._h, j, buf, 256)
+        if layer < 0:
+            _check(layer, "miconv_stack_launch_info")
+        return layer, buf.value.decode()
+
+    def describe(self, i: int) -> str:
+        buf = ctypes.create_string_buffer(256)
+        rc = lib().miconv_stack_describe(self._h, i, buf, 256)
+        if rc < 0:
+            _check(rc, "miconv_stack_describe")
+        return buf.value.decode()
+
+    def launch(self, stream=None):
+        _check(lib().miconv_stack_launch(self._h, _stream(stream)), "miconv_stack_launch")
+
+    def launch_timed(self, steps: int, stream=None):
+        _check(lib().miconv_stack_launch_timed(self._h, steps, _stream(stream)),
+               "miconv_stack_launch_timed")
+        self.steps = steps
+
+    def capture(self, steps: int, timed: bool, stream=None):
+        _check(lib().miconv_stack_capture(self._h, steps, 1 if timed else 0, _stream(stream)),
+               "miconv_stack_capture")
+        self.steps = steps
+
+    def replay(self, stream=None):
+        _check(lib().miconv_stack_replay(self._h, _stream(stream)), "miconv_stack_replay")
+
+    def times(self):
+        import numpy as np
+        out = np.empty(self.steps * self.launches, np.float32)
+        _check(lib().miconv_stack_times(self._h, out.ctypes.data, out.size), "miconv_stack_times")
+        return out.reshape(self.steps, self.launches)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().miconv_stack_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # Allocating conveniences (output buffers come from torch's caching allocator).

@@ -1,0 +1,114 @@
+"""GPU: the stack executor (eager and HIP-graph replay) against single calls.
+
+Every layer of a stack must produce, bit for bit, what the same entry point
+produces when called on its own; a captured graph replayed several times,
+with eager work and synchronisations in between, must give the same bits on
+every replay.  The oracle ties the single calls to the definition elsewhere
+(test_gpu_parity); here a small-integer stack is also checked against it.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1907_02154_amd import miconv
+from paper_1907_02154_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    miconv.lib()
+
+
+def _mobilenet_stack(ints: bool):
+    ops, ref_inputs = [], []
+    for i, l in enumerate(wl.workload(3).layers[:9]):
+        x, w, b = wl.layer_tensors(3, i, l)
+        if ints:
+            x = wl.small_ints(x.shape, -3, 3, 500 + i)
+            w = wl.small_ints(w.shape, -3, 3, 600 + i)
+            b = wl.small_ints(b.shape, -8, 8, 700 + i)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        tx, tw, tb = (torch.from_numpy(a).cuda() for a in (x, w, b))
+        ty = torch.full((l.N, l.K, P, Q), float("nan"), device="cuda")
+        op = miconv.OP_DWCONV_F32 if l.kind == "dw" else miconv.OP_CONV_F32
+        ops.append((op, tx, tw, tb, ty, l.stride, l.pad, l.groups, l.relu))
+        ref_inputs.append((l, x, w, b))
+    return ops, ref_inputs
+
+
+def _single_calls(ops):
+    outs = []
+    for op, x, w, b, y, st, pad, g, relu in ops:
+        y2 = torch.empty_like(y)
+        if op == miconv.OP_DWCONV_F32:
+            miconv.dwconv2d_fwd(x, w, b, y2, st, pad, relu)
+        else:
+            miconv.conv2d_fwd(x, w, b, y2, st, pad, g, relu)
+        outs.append(y2)
+    torch.cuda.synchronize()
+    return outs
+
+
+def test_stack_eager_and_graph_match_single_calls():
+    ops, _ = _mobilenet_stack(ints=False)
+    ref = _single_calls(ops)
+    s = miconv.Stack(ops)
+    s.launch()
+    torch.cuda.synchronize()
+    for o, r in zip(ops, ref):
+        assert torch.equal(o[4], r)
+    for o in ops:
+        o[4].fill_(float("nan"))
+    s.capture(3, timed=True)
+    for rep in range(3):
+        for o in ops:
+            o[4].fill_(float("nan"))          # eager work between replays
+        torch.cuda.synchronize()
+        s.replay()
+        torch.cuda.synchronize()
+        for i, (o, r) in enumerate(zip(ops, ref)):
+            assert torch.equal(o[4], r), f"replay {rep} layer {i}"
+    t = s.times()
+    assert t.shape == (3, s.launches) and s.launches >= len(ops) and np.all(t > 0)
+    assert [s.launch_info(j)[0] for j in range(s.launches)] == sorted(s.launch_info(j)[0] for j in range(s.launches))
+    s.close()
+
+
+def test_stack_small_ints_against_oracle(oracle_lib):
+    ops, refs = _mobilenet_stack(ints=True)
+    s = miconv.Stack(ops)
+    s.capture(1, timed=False)
+    s.replay()
+    torch.cuda.synchronize()
+    for o, (l, x, w, b) in zip(ops, refs):
+        if l.kind == "dw":
+            want = oracle_lib.dwconv2d(x, w, b, l.stride, l.pad, l.relu)
+        else:
+            want = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        np.testing.assert_array_equal(o[4].cpu().numpy(), want, err_msg=l.name)
+    s.close()
+
+
+def test_stack_rejects_bad_layer():
+    x = torch.zeros((1, 4, 8, 8), device="cuda")
+    w = torch.zeros((4, 4, 3, 3), device="cuda")
+    y = torch.zeros((1, 4, 8, 8), device="cuda")
+    with pytest.raises(miconv.MiconvError):
+        miconv.Stack([(miconv.OP_DWCONV_F32, x, w, None, y, 1, 1, 1, False)])
+
+
+def test_stack_eager_timed_matches():
+    ops, _ = _mobilenet_stack(ints=False)
+    ref = _single_calls(ops)
+    s = miconv.Stack(ops)
+    s.launch_timed(2)
+    torch.cuda.synchronize()
+    for o, r in zip(ops, ref):
+        assert torch.equal(o[4], r)
+    t = s.times()
+    assert t.shape == (2, s.launches) and np.all(t > 0)
+    s.close()
