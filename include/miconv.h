@@ -62,7 +62,9 @@ enum miconv_status {
 enum miconv_algo {
     MICONV_ALGO_AUTO = 0,   /* shape-based choice, what conv2d_fwd does */
     MICONV_ALGO_DIRECT = 1, /* one output per lane, plain FMA loop: any shape and groups */
-    MICONV_ALGO_IGEMM = 2   /* implicit GEMM on MFMA with LDS-staged tiles (+ split-K when small) */
+    MICONV_ALGO_IGEMM = 2,  /* implicit GEMM on MFMA with LDS-staged tiles (+ split-K when small) */
+    MICONV_ALGO_WAVE = 3    /* implicit GEMM on MFMA fed straight from global memory by each
+                               wavefront, reduction split across wavefronts (small layers) */
 };
 
 /* Output extent: floor((H + 2*pad - R)/stride) + 1 and likewise for W.

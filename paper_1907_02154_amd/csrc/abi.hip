@@ -173,7 +173,7 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
     int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, elem, &r.p);
     if (rc != MICONV_OK) return rc;
     if ((rc = check_bias(bias)) != MICONV_OK) return rc;
-    if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_IGEMM) return MICONV_ERR_UNSUPPORTED;
+    if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_WAVE) return MICONV_ERR_UNSUPPORTED;
     r.p.relu = relu ? 1 : 0;
     r.kind = kind;
     r.x = x;
@@ -186,7 +186,8 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
         r.impl = IMPL_DW;
     } else if (kind == OP_DENSE_BF16) {
-        r.impl = IMPL_DIRECT;
+        r.impl = (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8)) ? IMPL_DIRECT
+                                                                         : IMPL_IGEMM_BF16;
     } else if (kind == OP_DENSE_F32) {
         if (algo == MICONV_ALGO_AUTO) {
             if (depthwise && R <= 7 && S <= 7)
@@ -194,20 +195,83 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
             else
                 r.impl = (groups == 1 || r.p.Cg >= 8) ? IMPL_IGEMM : IMPL_DIRECT;
         } else {
-            r.impl = algo == MICONV_ALGO_DIRECT ? IMPL_DIRECT : IMPL_IGEMM;
+            r.impl = algo == MICONV_ALGO_DIRECT ? IMPL_DIRECT
+                     : algo == MICONV_ALGO_WAVE ? IMPL_WAVE : IMPL_IGEMM;
         }
     } else {
         return MICONV_ERR_UNSUPPORTED;
     }
-    if (r.impl == IMPL_IGEMM) r.plan = plan_igemm_f32(r.p, cu_count());
+    if (r.impl == IMPL_IGEMM) {
+        // Small GEMM extents (too few 128x128 output tiles to fill the chip) go
+        // to the wave-direct kernel, unless the caller forced the tiled one.
+        const int cus = cu_count();
+        const long big_tiles = (long)ceil_div(r.p.M, 128) * ceil_div(r.p.Kg, 128) * r.p.groups;
+        if (algo != MICONV_ALGO_IGEMM && big_tiles < 2L * cus) {
+            r.impl = IMPL_WAVE;
+            r.wplan = plan_wave_f32(r.p, cus, (uintptr_t)w % 16 == 0);
+        } else {
+            r.plan = plan_igemm_f32(r.p, cus);
+        }
+    } else if (r.impl == IMPL_WAVE) {
+        r.wplan = plan_wave_f32(r.p, cu_count(), (uintptr_t)w % 16 == 0);
+    } else if (r.impl == IMPL_IGEMM_BF16) {
+        r.plan = plan_igemm_bf16(r.p, cu_count());
+        r.bfast = bf16_fast_1x1(r.p, x);
+        r.bva = r.p.Kred % 8 == 0 && (uintptr_t)w % 16 == 0;
+        // At the batch sizes the bf16 path serves, packing the filters on every
+        // call costs far less than per-tap index decoding in the gather.
+        if (krsc_eligible(r)) {
+            r.plan.krsc = true;
+            r.pack_per_call = true;
+        }
+    }
     *out = r;
     return MICONV_OK;
 }
 
-hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook)
+bool krsc_eligible(const Resolved &r)
 {
-    const float *xf = static_cast<const float *>(r.x), *wf = static_cast<const float *>(r.w);
+    return (r.impl == IMPL_WAVE || r.impl == IMPL_IGEMM_BF16) && r.p.R * r.p.S > 1 &&
+           r.p.Cg % 8 == 0;
+}
+
+size_t packed_bytes(const Resolved &r)
+{
+    const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
+    return (size_t)r.p.K * r.p.Cg * r.p.R * r.p.S * elem;
+}
+
+void set_krsc(Resolved &r, const void *packed)
+{
+    r.wk = packed;
+    r.pack_per_call = false;
+    if (r.impl == IMPL_WAVE) r.wplan.krsc = true;
+    if (r.impl == IMPL_IGEMM_BF16) r.plan.krsc = true;
+}
+
+static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
+
+hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHook *hook)
+{
+    Resolved r = r0;
+    if (r.pack_per_call) {
+        if (hook) {
+            hipError_t e = hook->before_launch(hook->ctx, st);
+            if (e != hipSuccess) return e;
+        }
+        const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
+        hipError_t e = launch_pack_krsc(r.p, r.w, ws, elem, st);
+        if (e != hipSuccess) return e;
+        r.wk = ws;
+        ws = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + round256(packed_bytes(r)));
+    }
+    const void *wkern = r.wk ? r.wk : r.w;
+    const float *xf = static_cast<const float *>(r.x), *wf = static_cast<const float *>(wkern);
     if (r.impl == IMPL_IGEMM) return launch_igemm_f32(r.p, r.plan, xf, wf, r.bias, r.y, ws, st, hook);
+    if (r.impl == IMPL_WAVE) return launch_wave_f32(r.p, r.wplan, xf, wf, r.bias, r.y, ws, st, hook);
+    if (r.impl == IMPL_IGEMM_BF16)
+        return launch_igemm_bf16(r.p, r.plan, r.bfast, r.bva, static_cast<const uint16_t *>(r.x),
+                                 static_cast<const uint16_t *>(wkern), r.bias, r.y, ws, st, hook);
     if (hook) {
         hipError_t e = hook->before_launch(hook->ctx, st);
         if (e != hipSuccess) return e;
@@ -222,11 +286,38 @@ hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHoo
     }
 }
 
+void describe_kernel(const Resolved &r, char *buf, int len, int *launches);
+
+size_t workspace_bytes(const Resolved &r)
+{
+    size_t b = 0;
+    if (r.impl == IMPL_IGEMM || r.impl == IMPL_IGEMM_BF16) b = r.plan.ws_bytes;
+    if (r.impl == IMPL_WAVE) b = r.wplan.ws_bytes;
+    if (r.pack_per_call) b = round256(b) + round256(packed_bytes(r));
+    return b;
+}
+
 void describe(const Resolved &r, char *buf, int len, int *launches)
+{
+    if (r.pack_per_call) {
+        const int n = snprintf(buf, len, "pack_krsc_kernel<%s> + ",
+                               r.kind == OP_DENSE_BF16 ? "unsigned short" : "float");
+        if (n > 0 && n < len) {
+            describe_kernel(r, buf + n, len - n, launches);
+            *launches += 1;
+            return;
+        }
+    }
+    describe_kernel(r, buf, len, launches);
+}
+
+void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
 {
     switch (r.impl) {
     case IMPL_DW: describe_dwconv(r.p, buf, len, launches); break;
     case IMPL_IGEMM: describe_igemm_f32(r.p, r.plan, buf, len, launches); break;
+    case IMPL_WAVE: describe_wave_f32(r.p, r.wplan, buf, len, launches); break;
+    case IMPL_IGEMM_BF16: describe_igemm_bf16(r.p, r.plan, r.bfast, r.bva, buf, len, launches); break;
     default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;
     }
 }
@@ -236,8 +327,9 @@ namespace {
 int run(const Resolved &r, hipStream_t st)
 {
     float *ws = nullptr;
-    if (r.impl == IMPL_IGEMM) {
-        int rc = get_workspace(st, r.plan.ws_bytes, &ws);
+    const size_t need = workspace_bytes(r);
+    if (need) {
+        int rc = get_workspace(st, need, &ws);
         if (rc != MICONV_OK) return rc;
     }
     return finish(enqueue(r, ws, st));

@@ -327,9 +327,14 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
         e = launch_rs<0, 0>(a, plan.tile, grid, st);
     if (e != hipSuccess || plan.splits == 1) return e;
     if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
-    const long total = (long)p.K * p.M;
-    a.vec4 = p.N == 1 && total % 4 == 0 && (uintptr_t)y % 16 == 0 && (uintptr_t)ws % 16 == 0;
-    long blocks = (total + 255) / 256;
+    return launch_splitk_reduce(a, st);
+}
+
+hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
+{
+    const long total = (long)a.K * a.M;
+    a.vec4 = a.N == 1 && total % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0;
+    long blocks = (a.vec4 ? total / 4 : total + 255) / 256 + 1;
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);
     return hipGetLastError();

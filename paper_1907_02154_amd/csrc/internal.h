@@ -57,11 +57,41 @@ struct IgemmPlan {
     int splits;
     int kr_per_split;
     size_t ws_bytes;    // bytes of fp32 partials (0 without a split)
+    bool krsc;          // filters pre-packed [K][R][S][C/groups] (reduction order r, s, c)
 };
 IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus);
 hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const float *x,
                             const float *w, const float *bias, float *y, float *ws,
                             hipStream_t st, const LaunchHook *hook = nullptr);
+// Small-extent dense path (batch-1 layers): wavefronts feed the MFMAs from
+// global memory and split the reduction among themselves.
+struct WavePlan {
+    int bj;             // 32-pixel blocks per work-group tile (1 or 2)
+    int waves;          // wavefronts per work-group splitting the reduction (4 or 8)
+    bool va;            // 16-byte filter loads
+    int splits;         // reduction splits across work-groups
+    int kr_per_split;
+    size_t ws_bytes;
+    bool krsc;          // filters pre-packed [K][R][S][C/groups]
+};
+WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, bool w_aligned16);
+hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const float *x,
+                           const float *w, const float *bias, float *y, float *ws,
+                           hipStream_t st, const LaunchHook *hook = nullptr);
+void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, int len,
+                       int *launches);
+// bf16 inputs, fp32 accumulation (v_mfma_f32_32x32x16_bf16).
+IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus);
+bool bf16_fast_1x1(const ConvProblem &p, const void *x);
+hipError_t launch_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast, bool va,
+                             const uint16_t *x, const uint16_t *w, const float *bias, float *y,
+                             float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
+void describe_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast, bool va,
+                         char *buf, int len, int *launches);
+
+// Sums split partials [splits][K][M] in split order into y (+ bias, activation).
+hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st);
+
 // Kernel names (as a profiler prints them, without namespace) and launch counts.
 void describe_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, char *buf, int len,
                         int *launches);
@@ -77,12 +107,16 @@ hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t
 // A validated conv call with its kernel fixed (what the ABI entry points and
 // the stack executor enqueue).
 enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2 };
-enum Impl { IMPL_DIRECT = 0, IMPL_IGEMM = 1, IMPL_DW = 2 };
+enum Impl { IMPL_DIRECT = 0, IMPL_IGEMM = 1, IMPL_DW = 2, IMPL_WAVE = 3, IMPL_IGEMM_BF16 = 4 };
 struct Resolved {
     ConvProblem p;
     int kind;
     int impl;
     IgemmPlan plan;     // IMPL_IGEMM only
+    WavePlan wplan;     // IMPL_WAVE only
+    bool bfast, bva;    // IMPL_IGEMM_BF16: vectorised 1x1 loader, 16-byte filter loads
+    bool pack_per_call; // enqueue packs the filters (KRSC) into the workspace first
+    const void *wk;     // filters the conv kernel reads when they were packed ahead (else w)
     const void *x, *w;
     const float *bias;
     float *y;
@@ -92,6 +126,12 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
             int relu, Resolved *out);
 hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
 void describe(const Resolved &r, char *buf, int len, int *launches);
+size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + split partials
+bool krsc_eligible(const Resolved &r);       // the kernel can read KRSC-packed filters
+size_t packed_bytes(const Resolved &r);      // bytes of the KRSC copy of the filters
+void set_krsc(Resolved &r, const void *packed);  // read filters pre-packed at `packed`
+hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
+                            hipStream_t st);
 int set_hip_error(hipError_t e);   // records e for miconv_last_hip_error, returns MICONV_ERR_HIP
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }

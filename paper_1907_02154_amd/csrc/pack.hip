@@ -1,0 +1,47 @@
+// Weight pre-packing ("pre-computing" at graph level, Sec. 3.2.3): KCRS
+// filters -> KRSC, i.e. w_p[k][(r*S + s)*Cg + c] = w[k][c][r][s].
+//
+// With the reduction ordered (r, s, c), c innermost, any 8 consecutive
+// reduction indices (Cg % 8 == 0) are 8 channels at one filter tap: a conv
+// kernel checks the padding and forms the input address once per 8 taps
+// instead of once per tap.  Lanes walk the destination, so stores are
+// contiguous; the reads gather within one filter's Cg*R*S block (L2-resident).
+#include "internal.h"
+
+namespace miconv {
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void pack_krsc_kernel(const T *__restrict__ src, T *__restrict__ dst,
+                                                        int K, int Cg, int RS, long total)
+{
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const long k = i / ((long)Cg * RS);
+        const int rem = (int)(i - k * Cg * RS);   // (rs, c) with c fastest
+        const int rs = rem / Cg;
+        const int c = rem - rs * Cg;
+        dst[i] = src[(k * Cg + c) * RS + rs];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
+                            hipStream_t st)
+{
+    const long total = (long)p.K * p.Cg * p.R * p.S;
+    long blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    if (elem == sizeof(float))
+        hipLaunchKernelGGL(pack_krsc_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
+                           static_cast<const float *>(w), static_cast<float *>(packed), p.K, p.Cg,
+                           p.R * p.S, total);
+    else
+        hipLaunchKernelGGL(pack_krsc_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
+                           static_cast<const uint16_t *>(w), static_cast<uint16_t *>(packed), p.K,
+                           p.Cg, p.R * p.S, total);
+    return hipGetLastError();
+}
+
+}  // namespace miconv

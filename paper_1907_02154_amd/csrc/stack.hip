@@ -24,6 +24,7 @@ struct miconv_stack {
     std::vector<int> launch_layer;          // layer of every kernel launch of one pass
     std::vector<std::string> launch_name;   // its kernel name
     float *partials = nullptr;              // split-K workspace shared by all layers
+    std::vector<void *> packed;             // KRSC copies of filters, packed at create
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
     std::vector<hipEvent_t> events;         // steps * launches + 1 when timed
@@ -155,11 +156,23 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
         int rc = resolve(d.op, MICONV_ALGO_AUTO, d.N, d.C, d.H, d.W, d.K, d.R, d.S, d.stride,
                          d.pad, d.groups, d.x, d.w, d.bias, d.y, d.relu, &r);
         if (rc != MICONV_OK) {
-            delete s;
+            miconv_stack_destroy(s);
             return rc;
         }
-        if (r.impl == IMPL_IGEMM && r.plan.splits > 1)
-            need_p = std::max(need_p, round_up(r.plan.ws_bytes, 256));
+        if (krsc_eligible(r)) {
+            // Pre-computing: pack the filters once, KRSC, for every replay.
+            void *pk = nullptr;
+            const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
+            e = hipMalloc(&pk, packed_bytes(r));
+            if (e == hipSuccess) s->packed.push_back(pk);
+            if (e == hipSuccess) e = launch_pack_krsc(r.p, r.w, pk, elem, nullptr);
+            if (e != hipSuccess) {
+                miconv_stack_destroy(s);
+                return set_hip_error(e);
+            }
+            set_krsc(r, pk);
+        }
+        need_p = std::max(need_p, round_up(workspace_bytes(r), 256));
         s->layers.push_back(r);
         char buf[512];
         int launches = 0;
@@ -176,10 +189,17 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
         void *ptr = nullptr;
         e = hipMalloc(&ptr, need_p);
         if (e != hipSuccess) {
-            delete s;
+            miconv_stack_destroy(s);
             return set_hip_error(e);
         }
         s->partials = static_cast<float *>(ptr);
+    }
+    if (!s->packed.empty()) {
+        e = hipStreamSynchronize(nullptr);   // packs run on the default stream
+        if (e != hipSuccess) {
+            miconv_stack_destroy(s);
+            return set_hip_error(e);
+        }
     }
     *out = s;
     return MICONV_OK;
@@ -284,6 +304,7 @@ int miconv_stack_destroy(miconv_stack *s)
     if (!s) return MICONV_OK;
     drop_graph(s);
     if (s->partials) hipFree(s->partials);
+    for (void *p : s->packed) hipFree(p);
     delete s;
     return MICONV_OK;
 }

@@ -21,7 +21,7 @@ HEADER = os.path.join(os.path.dirname(_PKG), "include", "miconv.h")
 
 OK = 0
 ERR_NULL, ERR_SHAPE, ERR_GROUPS, ERR_UNSUPPORTED, ERR_TOO_LARGE, ERR_ALIGN, ERR_HIP = range(-1, -8, -1)
-ALGO_AUTO, ALGO_DIRECT, ALGO_IGEMM = 0, 1, 2
+ALGO_AUTO, ALGO_DIRECT, ALGO_IGEMM, ALGO_WAVE = 0, 1, 2, 3
 
 _lib = None
 
@@ -160,7 +160,7 @@ def conv2d_fwd(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, stream=None
 
 def conv2d_fwd_algo(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO,
                     stream=None):
-    """conv2d_fwd with an explicit algorithm (ALGO_AUTO / ALGO_DIRECT / ALGO_IGEMM)."""
+    """conv2d_fwd with an explicit algorithm (ALGO_AUTO / ALGO_DIRECT / ALGO_IGEMM / ALGO_WAVE)."""
     f = lib().conv2d_fwd_algo
     _dev(x, torch.float32, "x", 4)
     return _conv_common(f, x, w, bias, y, stride, pad, groups, relu, stream, torch.float32,

@@ -74,11 +74,15 @@ DENSE_CASES = [
     (2, 32, 8, 8, 64, 3, 3, 1, 1, 2),        # grouped with Cg >= 8
     (1, 8, 6, 6, 4, 3, 3, 1, 4, 1),          # padding wider than the filter
     (1, 130, 130, 1, 3, 1, 1, 1, 0, 1),      # W = 1
+    (1, 1024, 7, 7, 40, 3, 3, 1, 1, 1),      # Kred 9216: wave split + work-group split
+    (2, 250, 9, 9, 33, 1, 1, 1, 0, 1),       # Kred not a multiple of 4
+    (1, 64, 60, 60, 64, 3, 3, 1, 1, 1),      # M >= 2048: two pixel blocks per tile
 ]
 
 
 @pytest.mark.parametrize("case", DENSE_CASES, ids=lambda c: "x".join(map(str, c)))
-@pytest.mark.parametrize("algo", [miconv.ALGO_DIRECT, miconv.ALGO_IGEMM, miconv.ALGO_AUTO])
+@pytest.mark.parametrize("algo", [miconv.ALGO_DIRECT, miconv.ALGO_IGEMM, miconv.ALGO_WAVE,
+                                  miconv.ALGO_AUTO])
 def test_dense_small_int_bitwise(oracle_lib, case, algo):
     N, C, H, W, K, R, S, st, pad, g = case
     seed = 1000 + sum(case)

@@ -112,3 +112,71 @@ def test_stack_eager_timed_matches():
     t = s.times()
     assert t.shape == (2, s.launches) and np.all(t > 0)
     s.close()
+
+
+def _resnet_stack_ints(config, idxs):
+    ops, refs = [], []
+    for i in idxs:
+        l = wl.workload(config).layers[i]
+        x = wl.small_ints((l.N, l.C, l.H, l.W), -3, 3, 800 + i)
+        w = wl.small_ints((l.K, l.C // l.groups, l.R, l.S), -3, 3, 900 + i)
+        b = wl.small_ints((l.K,), -8, 8, 1000 + i)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        y = torch.full((l.N, l.K, P, Q), float("nan"), device="cuda")
+        if wl.workload(config).dtype == "bf16":
+            bx, bw = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+            tx = torch.from_numpy(bx.view(np.int16)).cuda().view(torch.bfloat16)
+            tw = torch.from_numpy(bw.view(np.int16)).cuda().view(torch.bfloat16)
+            ops.append((miconv.OP_CONV_BF16, tx, tw, torch.from_numpy(b).cuda(), y, l.stride, l.pad,
+                        l.groups, l.relu))
+        else:
+            ops.append((miconv.OP_CONV_F32, torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(),
+                        torch.from_numpy(b).cuda(), y, l.stride, l.pad, l.groups, l.relu))
+        refs.append((l, x, w, b))
+    return ops, refs
+
+
+@pytest.mark.parametrize("config,idxs", [(2, [0, 2, 12, 25, 44, 48]), (5, [0, 2, 16, 29, 44])])
+def test_stack_packed_filters_small_ints(oracle_lib, config, idxs):
+    """3x3 layers in a stack read KRSC-packed filters (packed once at create):
+    exact against the oracle on small integers, eager and replayed."""
+    ops, refs = _resnet_stack_ints(config, idxs)
+    s = miconv.Stack(ops)
+    names = [s.describe(j) for j in range(len(ops))]
+    assert any(", true>" in n for n in names), names      # some layer reads packed filters
+    s.launch()
+    torch.cuda.synchronize()
+    for o, (l, x, w, b) in zip(ops, refs):
+        want = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        np.testing.assert_array_equal(o[4].cpu().numpy(), want, err_msg=l.name)
+        o[4].fill_(float("nan"))
+    s.capture(2, timed=False)
+    s.replay()
+    torch.cuda.synchronize()
+    for o, (l, x, w, b) in zip(ops, refs):
+        want = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        np.testing.assert_array_equal(o[4].cpu().numpy(), want, err_msg=l.name)
+    s.close()
+
+
+def test_stack_resnet_b1_random_within_gate(oracle_lib):
+    """The ResNet-50 batch-1 stack (packed 3x3 filters, split reductions) on
+    its seeded random layers: e = max|y - y_ref| / max|y_ref| <= 1e-4."""
+    ops, refs = [], []
+    for i, l in enumerate(wl.workload(2).layers):
+        x, w, b = wl.layer_tensors(2, i, l)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        y = torch.empty((l.N, l.K, P, Q), device="cuda")
+        ops.append((miconv.OP_CONV_F32, torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(),
+                    torch.from_numpy(b).cuda(), y, l.stride, l.pad, l.groups, l.relu))
+        refs.append((l, x, w, b))
+    s = miconv.Stack(ops)
+    s.capture(1, timed=False)
+    s.replay()
+    torch.cuda.synchronize()
+    for o, (l, x, w, b) in zip(ops, refs):
+        want = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        got = o[4].cpu().numpy()
+        e = np.max(np.abs(got.astype(np.float64) - want)) / np.max(np.abs(want))
+        assert e <= 1e-4, (l.name, e)
+    s.close()
