@@ -44,7 +44,66 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget for the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--layers", action="store_true", help="also print a per-layer table to stderr")
+    ap.add_argument("--dw-sweep", type=int, default=0, metavar="N",
+                    help="instead: HBM bandwidth of the depthwise kernel on the 13 MobileNet "
+                         "depthwise shapes at batch N (e.g. 256)")
     return ap.parse_args()
+
+
+def dw_sweep(args):
+    """Depthwise bandwidth sweep: the 13 MobileNet-v1 depthwise layer shapes at
+    batch N, each timed with events over `steps` launches that rotate through
+    enough (x, y) buffer pairs to exceed the 256 MB last-level cache, so every
+    launch streams from HBM.  Inputs are seeded on the device (uniform [0,1));
+    values do not affect the timing, and parity at these shapes is tested
+    separately on sampled images."""
+    import torch
+    from paper_1907_02154_amd import miconv
+    from paper_1907_02154_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(wl.SEED_BASE + 777)
+    rows, tot_bytes, tot_ms = [], 0, 0.0
+    stream = torch.cuda.current_stream()
+    for l in [l for l in wl.workload(3).layers if l.kind == "dw"]:
+        l = l.with_batch(args.dw_sweep)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        nbytes = 4 * (l.N * l.C * l.H * l.W + l.N * l.C * P * Q + 10 * l.C)
+        sets = max(2, -(-(768 << 20) // nbytes))            # > 3x the 256 MB cache
+        xs = [torch.rand((l.N, l.C, l.H, l.W), device="cuda", generator=gen) for _ in range(sets)]
+        ys = [torch.empty((l.N, l.C, P, Q), device="cuda") for _ in range(sets)]
+        w = torch.randn((l.C, 1, 3, 3), device="cuda", generator=gen) * l.he_std
+        b = torch.randn((l.C,), device="cuda", generator=gen) * 0.01
+        for i in range(args.warmup):
+            miconv.dwconv2d_fwd(xs[i % sets], w, b, ys[i % sets], l.stride, l.pad, l.relu)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(args.steps):
+            miconv.dwconv2d_fwd(xs[i % sets], w, b, ys[i % sets], l.stride, l.pad, l.relu)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        rows.append(dict(layer=l.name, C=l.C, H=l.H, stride=l.stride, MB=round(nbytes / 1e6, 1),
+                         us=round(ms * 1e3, 2), GBs=round(nbytes / ms / 1e6, 1), buffers=sets,
+                         kernel=miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride,
+                                                       l.pad, l.groups)[0]))
+        tot_bytes += nbytes
+        tot_ms += ms
+        del xs, ys
+        torch.cuda.empty_cache()
+    gbs = tot_bytes / tot_ms / 1e6
+    out = {"metric": "depthwise conv HBM bandwidth (MobileNet-v1 dw shapes)", "value": round(gbs, 1),
+           "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(tot_ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic (device-seeded uniform)",
+           "config": {"workload": f"MobileNet-v1 depthwise layers, batch {args.dw_sweep}",
+                      "algorithmic_bytes": tot_bytes},
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
+           "layers": rows}
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -53,6 +112,9 @@ def main():
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
+    if args.dw_sweep:
+        dw_sweep(args)
+        return
 
     import torch
     from paper_1907_02154_amd import miconv
@@ -140,10 +202,10 @@ def main():
     step_flops = sum(d["flops"] for d in layers)
     tflops = step_flops / (ms_per_step * 1e-3) / 1e12
 
-    # Dominant kernel: the kernel name with the largest summed time.  Its
-    # algorithmic work is that of the layers whose main kernel it is (a split
-    # reduction's own launches are attributed to splitk_reduce_kernel, which
-    # then carries the layers' output bytes but no FLOPs).
+    # Dominant kernel: the kernel name with the largest summed time.  A conv
+    # kernel carries its layers' FLOPs and algorithmic bytes; the helper
+    # launches of a layer (split-K reduction, channel-last copy of x, filter
+    # packing) carry the bytes they move but no FLOPs.
     groups = {}
     for j in range(n_launch):
         li, name = launch_info[j]
@@ -151,13 +213,18 @@ def main():
         g = groups.setdefault(name, dict(ms=0.0, flops=0, bytes=0, launches=0, layers=[]))
         g["ms"] += float(launch_ms[j])
         g["launches"] += 1
-        main = j == 0 or launch_info[j - 1][0] != li
+        main = not name.startswith(("nchw_to_nhwc", "pack_krsc", "splitk_reduce"))
         if main:
             g["flops"] += d["flops"]
             g["bytes"] += d["bytes"]
         else:
             l = d["layer"]
-            g["bytes"] += l.N * l.K * d["P"] * d["Q"] * 4
+            if name.startswith("splitk_reduce"):
+                g["bytes"] += l.N * l.K * d["P"] * d["Q"] * 4
+            elif name.startswith("nchw_to_nhwc"):
+                g["bytes"] += 2 * l.N * l.C * l.H * l.W * (2 if bf16 else 4)
+            else:
+                g["bytes"] += 2 * l.K * (l.C // l.groups) * l.R * l.S * (2 if bf16 else 4)
         g["layers"].append(d["layer"].name)
     dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
     avg_launch_us = dom["ms"] / dom["launches"] * 1e3

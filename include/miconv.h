@@ -90,6 +90,13 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
                     int groups, const uint16_t *x, const uint16_t *w, const float *bias,
                     float *y, int relu, void *stream);
 
+/* conv2d_fwd_bf16 with an explicit algorithm: MICONV_ALGO_AUTO (channel-last
+ * internal copy of x when C/groups % 32 == 0, else the NCHW-gather MFMA
+ * kernel), MICONV_ALGO_IGEMM (the NCHW-gather MFMA kernel), MICONV_ALGO_DIRECT. */
+int conv2d_fwd_bf16_algo(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                         int groups, const uint16_t *x, const uint16_t *w, const float *bias,
+                         float *y, int relu, int algo, void *stream);
+
 /* Depthwise conv2d forward in fp32 (MobileNet's per-channel filter, Sec. 4.2
  * discusses its cost): requires groups == C == K; w fp32 [C][1][R][S] with
  * R, S <= 7; otherwise the same conventions as conv2d_fwd. */

@@ -186,8 +186,12 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
         r.impl = IMPL_DW;
     } else if (kind == OP_DENSE_BF16) {
-        r.impl = (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8)) ? IMPL_DIRECT
-                                                                         : IMPL_IGEMM_BF16;
+        if (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8))
+            r.impl = IMPL_DIRECT;
+        else if (algo != MICONV_ALGO_IGEMM && nhwc_bf16_eligible(r.p))
+            r.impl = IMPL_NHWC_BF16;
+        else
+            r.impl = IMPL_IGEMM_BF16;
     } else if (kind == OP_DENSE_F32) {
         if (algo == MICONV_ALGO_AUTO) {
             if (depthwise && R <= 7 && S <= 7)
@@ -224,6 +228,9 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
             r.plan.krsc = true;
             r.pack_per_call = true;
         }
+    } else if (r.impl == IMPL_NHWC_BF16) {
+        r.nplan = plan_nhwc_bf16(r.p, cu_count());
+        r.pack_per_call = krsc_eligible(r);   // 1x1 filters are already in KRSC order
     }
     *out = r;
     return MICONV_OK;
@@ -231,8 +238,8 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
 
 bool krsc_eligible(const Resolved &r)
 {
-    return (r.impl == IMPL_WAVE || r.impl == IMPL_IGEMM_BF16) && r.p.R * r.p.S > 1 &&
-           r.p.Cg % 8 == 0;
+    return (r.impl == IMPL_WAVE || r.impl == IMPL_IGEMM_BF16 || r.impl == IMPL_NHWC_BF16) &&
+           r.p.R * r.p.S > 1 && r.p.Cg % 8 == 0;
 }
 
 size_t packed_bytes(const Resolved &r)
@@ -254,18 +261,29 @@ static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHook *hook)
 {
     Resolved r = r0;
+    // workspace layout: [packed filters (per-call packing)][channel-last x][split partials]
+    char *cursor = reinterpret_cast<char *>(ws);
     if (r.pack_per_call) {
         if (hook) {
             hipError_t e = hook->before_launch(hook->ctx, st);
             if (e != hipSuccess) return e;
         }
         const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
-        hipError_t e = launch_pack_krsc(r.p, r.w, ws, elem, st);
+        hipError_t e = launch_pack_krsc(r.p, r.w, cursor, elem, st);
         if (e != hipSuccess) return e;
-        r.wk = ws;
-        ws = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + round256(packed_bytes(r)));
+        r.wk = cursor;
+        cursor += round256(packed_bytes(r));
     }
+    uint16_t *xcl = nullptr;
+    if (r.impl == IMPL_NHWC_BF16) {
+        xcl = reinterpret_cast<uint16_t *>(cursor);
+        cursor += round256(r.nplan.xcl_bytes);
+    }
+    ws = reinterpret_cast<float *>(cursor);
     const void *wkern = r.wk ? r.wk : r.w;
+    if (r.impl == IMPL_NHWC_BF16)
+        return launch_nhwc_bf16(r.p, r.nplan, static_cast<const uint16_t *>(r.x),
+                                static_cast<const uint16_t *>(wkern), r.bias, r.y, xcl, ws, st, hook);
     const float *xf = static_cast<const float *>(r.x), *wf = static_cast<const float *>(wkern);
     if (r.impl == IMPL_IGEMM) return launch_igemm_f32(r.p, r.plan, xf, wf, r.bias, r.y, ws, st, hook);
     if (r.impl == IMPL_WAVE) return launch_wave_f32(r.p, r.wplan, xf, wf, r.bias, r.y, ws, st, hook);
@@ -293,6 +311,7 @@ size_t workspace_bytes(const Resolved &r)
     size_t b = 0;
     if (r.impl == IMPL_IGEMM || r.impl == IMPL_IGEMM_BF16) b = r.plan.ws_bytes;
     if (r.impl == IMPL_WAVE) b = r.wplan.ws_bytes;
+    if (r.impl == IMPL_NHWC_BF16) b = round256(r.nplan.xcl_bytes) + r.nplan.partial_bytes;
     if (r.pack_per_call) b = round256(b) + round256(packed_bytes(r));
     return b;
 }
@@ -318,6 +337,7 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     case IMPL_IGEMM: describe_igemm_f32(r.p, r.plan, buf, len, launches); break;
     case IMPL_WAVE: describe_wave_f32(r.p, r.wplan, buf, len, launches); break;
     case IMPL_IGEMM_BF16: describe_igemm_bf16(r.p, r.plan, r.bfast, r.bva, buf, len, launches); break;
+    case IMPL_NHWC_BF16: describe_nhwc_bf16(r.p, r.nplan, buf, len, launches); break;
     default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;
     }
 }
@@ -369,14 +389,22 @@ int conv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int 
                            MICONV_ALGO_AUTO, stream);
 }
 
+int conv2d_fwd_bf16_algo(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                         int groups, const uint16_t *x, const uint16_t *w, const float *bias,
+                         float *y, int relu, int algo, void *stream)
+{
+    Resolved r;
+    int rc = resolve(OP_DENSE_BF16, algo, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y,
+                     relu, &r);
+    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+}
+
 int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                     int groups, const uint16_t *x, const uint16_t *w, const float *bias, float *y,
                     int relu, void *stream)
 {
-    Resolved r;
-    int rc = resolve(OP_DENSE_BF16, MICONV_ALGO_AUTO, N, C, H, W, K, R, S, stride, pad, groups, x,
-                     w, bias, y, relu, &r);
-    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+    return conv2d_fwd_bf16_algo(N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y, relu,
+                                MICONV_ALGO_AUTO, stream);
 }
 
 int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,

@@ -1,0 +1,398 @@
+// bf16 conv2d through an internal channel-last layout.
+//
+// The bf16 MFMA (v_mfma_f32_32x32x16_bf16) wants 8 consecutive reduction
+// elements per lane.  With the reduction ordered (r, s, c), c innermost, and
+// the activations channel-last, those 8 elements are 8 adjacent channels of
+// one input pixel: one aligned 16-byte load, one padding check.  So a call
+//  1. transposes x from NCHW to an internal NHWC copy (x_cl, one HBM pass,
+//     through LDS so both the reads and the writes are contiguous),
+//  2. reads filters packed KRSC (w_p[k][(r*S+s)*Cg + c], packed once by the
+//     stack executor or per call),
+//  3. runs the implicit GEMM D[k][m] = sum_kr W[k][kr] X[kr][m] with both
+//     operand tiles staged reduction-contiguous in LDS (rows padded by 16
+//     bytes: conflict-free 16-byte reads), double-buffered, MFMA 32x32x16,
+//     and stores y in NCHW fp32 with bias + activation.
+// Requirements: C/groups % KRC == 0 (every reduction chunk of KRC elements
+// is KRC channels at one filter position), so the chunk's (r, s) is uniform.
+#include "internal.h"
+
+#include <cstdio>
+
+namespace miconv {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// x [N][C][HW] -> x_cl [N][HW][C] in 64 x 64 tiles (channels x pixels).
+// With HW % 8 == 0 and C % 8 == 0 every lane moves 16 bytes per global access:
+// it reads 8 pixels of one channel and, after the LDS exchange, writes 8
+// channels of one pixel.
+template <bool VEC>
+__global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *__restrict__ x,
+                                                                uint16_t *__restrict__ xt, int C,
+                                                                int HW, int tiles_hw, int tiles_c)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];   // [channel][pixel]
+    const int t = threadIdx.x;
+    const int b = blockIdx.x;
+    const int th = b % tiles_hw;
+    const int tc = (b / tiles_hw) % tiles_c;
+    const long n = b / ((long)tiles_hw * tiles_c);
+    const int c0 = tc * 64, p0 = th * 64;
+    const uint16_t *src = x + n * (long)C * HW;
+    uint16_t *dst = xt + n * (long)C * HW;
+    if constexpr (VEC) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {   // 64 channels x 8 pixel octets = 512 lanes' worth
+            const int id = t + 256 * i;
+            const int c = id >> 3, o = id & 7;
+            const bool ok = c0 + c < C && p0 + 8 * o < HW;
+            const uint4 v = ok ? *reinterpret_cast<const uint4 *>(src + (long)(c0 + c) * HW + p0 + 8 * o)
+                               : make_uint4(0, 0, 0, 0);
+            *reinterpret_cast<uint4 *>(&tile[c][8 * o]) = v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {   // 64 pixels x 8 channel octets
+            const int id = t + 256 * i;
+            const int px = id >> 3, o = id & 7;
+            if (c0 + 8 * o < C && p0 + px < HW) {
+                uint32_t d[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    d[e] = (uint32_t)tile[8 * o + 2 * e][px] | ((uint32_t)tile[8 * o + 2 * e + 1][px] << 16);
+                *reinterpret_cast<uint4 *>(dst + (long)(p0 + px) * C + c0 + 8 * o) =
+                    make_uint4(d[0], d[1], d[2], d[3]);
+            }
+        }
+    } else {
+        const int px = t & 63;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int c = (t >> 6) + 4 * i;
+            const bool ok = c0 + c < C && p0 + px < HW;
+            tile[c][px] = ok ? src[(long)(c0 + c) * HW + p0 + px] : 0;
+        }
+        __syncthreads();
+        const int cc = t & 63;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int p = (t >> 6) + 4 * i;
+            if (c0 + cc < C && p0 + p < HW) dst[(long)(p0 + p) * C + c0 + cc] = tile[cc][p];
+        }
+    }
+}
+
+// MFMA roles: the pixel tile is the MFMA's A operand (rows i) and the filter
+// tile its B operand (columns j), so accumulator register v of lane l holds
+// pixel 8*(v/4) + 4*(l/32) + v%4 of column (channel) l%32: four consecutive
+// output pixels of one channel per group of 4 registers, stored as one
+// 16-byte write when the plane size allows.
+//
+// Pipeline: two LDS stages plus two chunks of global loads held in
+// registers, so while the wavefronts multiply chunk t, chunks t+1 and t+2
+// are in flight.
+template <int R_, int S_, int BKC, int BPX, int KRC>
+__global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
+{
+    constexpr int NT = 256;
+    constexpr int WTK = BKC / 2, WTP = BPX / 2;      // 2 x 2 wavefronts
+    constexpr int BI = WTK / 32, BJ = WTP / 32;      // channel blocks, pixel blocks
+    constexpr int LDR = KRC + 8;                     // row stride in bf16 (16-byte pad)
+    constexpr int G8 = KRC / 8;                      // 8-element groups per row chunk
+    constexpr int A_PER = BKC * G8 / NT;             // groups per lane
+    constexpr int B_PER = BPX * G8 / NT;
+    static_assert(BI >= 1 && BJ >= 1 && A_PER >= 1 && B_PER >= 1, "tile shape");
+    static_assert((BKC * G8) % NT == 0 && (BPX * G8) % NT == 0 && NT % G8 == 0, "loader shape");
+
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BKC][LDR];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BPX][LDR];
+
+    const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
+    const uint16_t *__restrict__ wp = static_cast<const uint16_t *>(a.w);    // [K][R][S][Cg]
+    const int S = S_ ? S_ : a.S;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wk = wid >> 1, wq = wid & 1;
+    const int h = lane >> 5, ll = lane & 31;
+    const int g = blockIdx.z % a.groups;
+    const int split = blockIdx.z / a.groups;
+    const int m0 = blockIdx.x * BPX;
+    const int k0 = blockIdx.y * BKC;
+    const int kr_begin = split * a.kr_per_split;
+    const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
+
+    // Loader lanes: group column j8 = tid % G8 (8 channels), row = tid / G8 + i * RSTEP.
+    const int j8 = tid % G8;
+    const int row0 = tid / G8;
+    constexpr int RSTEP = NT / G8;
+
+    const uint16_t *arow[A_PER];
+    bool aok[A_PER];
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+        const int k = k0 + row0 + i * RSTEP;
+        aok[i] = k < a.Kg;
+        arow[i] = wp + ((long)g * a.Kg + (aok[i] ? k : 0)) * a.Kred + j8 * 8;
+    }
+    int bih[B_PER], biw[B_PER];
+    long bbase[B_PER];
+    bool bok[B_PER];
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i) {
+        const int m = m0 + row0 + i * RSTEP;
+        bok[i] = m < a.M;
+        const int mm = bok[i] ? m : 0;
+        const int n = mm / a.PQ;
+        const int pq = mm - n * a.PQ;
+        const int p = pq / a.Q;
+        const int q = pq - p * a.Q;
+        bih[i] = p * a.stride - a.pad;
+        biw[i] = q * a.stride - a.pad;
+        bbase[i] = (long)n * a.H * a.W * a.C + (long)g * a.Cg + j8 * 8;
+    }
+
+    struct Regs {
+        uint4 a[A_PER], b[B_PER];
+    };
+    auto gload = [&](Regs &rg, int t) {
+        const int kr0 = kr_begin + t * KRC;
+        // the chunk [kr0, kr0 + KRC) is KRC channels at filter position rs
+        const int rs = kr0 / a.Cg;
+        const int c0 = kr0 - rs * a.Cg;
+        const int r = rs / S;
+        const int s = rs - r * S;
+        const bool live = kr0 < kr_end;
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i)
+            rg.a[i] = (live && aok[i]) ? *reinterpret_cast<const uint4 *>(arow[i] + kr0)
+                                       : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < B_PER; ++i) {
+            const int ih = bih[i] + r, iw = biw[i] + s;
+            const bool ok = live && bok[i] && (unsigned)ih < (unsigned)a.H &&
+                            (unsigned)iw < (unsigned)a.W;
+            rg.b[i] = ok ? *reinterpret_cast<const uint4 *>(xcl + bbase[i] +
+                                                            ((long)ih * a.W + iw) * a.C + c0)
+                         : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto sstore = [&](const Regs &rg, int buf) {
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i)
+            *reinterpret_cast<uint4 *>(&As[buf][row0 + i * RSTEP][j8 * 8]) = rg.a[i];
+#pragma unroll
+        for (int i = 0; i < B_PER; ++i)
+            *reinterpret_cast<uint4 *>(&Bs[buf][row0 + i * RSTEP][j8 * 8]) = rg.b[i];
+    };
+
+    // acc[bj][bi]: rows = pixel block bj, columns = channel block bi
+    floatx16 acc[BJ][BI];
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+        for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[bj][bi][v] = 0.f;
+
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int ks = 0; ks < KRC; ks += 16) {
+            bf16x8 wv[BI], xv[BJ];
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi)
+                wv[bi] = *reinterpret_cast<const bf16x8 *>(&As[buf][wk * WTK + bi * 32 + ll][ks + 8 * h]);
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj)
+                xv[bj] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][wq * WTP + bj * 32 + ll][ks + 8 * h]);
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+                for (int bi = 0; bi < BI; ++bi)
+                    acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[bj], wv[bi], acc[bj][bi],
+                                                                         0, 0, 0);
+        }
+    };
+
+    const int nchunks = kr_end > kr_begin ? (kr_end - kr_begin) / KRC : 0;
+    Regs r0, r1;
+    if (nchunks > 0) {
+        gload(r0, 0);
+        gload(r1, 1);          // beyond the last chunk the loads are masked to zero
+        sstore(r0, 0);
+        gload(r0, 2);
+    }
+    __syncthreads();
+    // Step t: the register set holding chunk t+1 goes to LDS stage (t+1)&1 and
+    // is refilled with chunk t+3, then stage t&1 is multiplied.  The loop is
+    // unrolled by two so that each register set has a fixed role (a runtime
+    // choice between them would push both into scratch memory).
+    auto step = [&](int t, Regs &nx) {
+        if (t + 1 < nchunks) sstore(nx, (t + 1) & 1);
+        if (t + 3 < nchunks) gload(nx, t + 3);
+        compute(t & 1);
+        __syncthreads();
+    };
+    for (int t = 0; t < nchunks; t += 2) {
+        step(t, r1);
+        if (t + 1 < nchunks) step(t + 1, r0);
+    }
+
+    // Epilogue: lane l holds channel column l%32 and, per group of 4
+    // registers, 4 consecutive pixels.
+    const bool vec = a.splits == 1 && (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+    const long cstride = a.splits > 1 ? (long)a.M : (long)a.PQ;
+    float *out = a.splits > 1 ? a.ws + (long)split * a.K * a.M : a.y;
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) {
+        const int k = k0 + wk * WTK + bi * 32 + ll;
+        if (k >= a.Kg) continue;
+        const int kg = g * a.Kg + k;
+        const float bv = (a.splits == 1 && a.bias) ? a.bias[kg] : 0.f;
+        const long coff = (long)kg * cstride;
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj) {
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int mb = m0 + wq * WTP + bj * 32 + 8 * q4 + 4 * h;   // first of 4 pixels
+                float v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float val = acc[bj][bi][4 * q4 + e];
+                    if (a.splits == 1) {
+                        val += bv;
+                        if (a.relu) val = fmaxf(val, 0.f);
+                    }
+                    v4[e] = val;
+                }
+                if (vec && mb + 3 < a.M) {
+                    const int n = mb / a.PQ;
+                    const long off = (long)n * a.K * a.PQ + (mb - n * a.PQ) + coff;
+                    *reinterpret_cast<float4 *>(out + off) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int m = mb + e;
+                        if (m >= a.M) continue;
+                        const int n = m / a.PQ;
+                        const long off = a.splits > 1 ? (long)m + coff
+                                                      : (long)n * a.K * a.PQ + (m - n * a.PQ) + coff;
+                        out[off] = v4[e];
+                    }
+                }
+            }
+        }
+    }
+}
+
+struct TileN {
+    int bkc, bpx;
+};
+const TileN kTilesN[] = {{128, 128}, {64, 64}};
+
+template <int R_, int S_, int KRC>
+void launch_tile(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    if (tile == 0)
+        hipLaunchKernelGGL((igemm_bf16_nhwc_kernel<R_, S_, 128, 128, KRC>), grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((igemm_bf16_nhwc_kernel<R_, S_, 64, 64, KRC>), grid, dim3(256), 0, st, a);
+}
+
+template <int KRC>
+void launch_krc(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    if (a.R == 1 && a.S == 1)
+        launch_tile<1, 1, KRC>(a, tile, grid, st);
+    else if (a.R == 3 && a.S == 3)
+        launch_tile<3, 3, KRC>(a, tile, grid, st);
+    else
+        launch_tile<0, 0, KRC>(a, tile, grid, st);
+}
+
+int rs_template(int v) { return (v == 1 || v == 3) ? v : 0; }
+
+}  // namespace
+
+bool nhwc_bf16_eligible(const ConvProblem &p) { return p.Cg % 32 == 0; }
+
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus)
+{
+    NhwcPlan plan{};
+    plan.krc = p.Cg % 64 == 0 ? 64 : 32;
+    plan.tile = 1;
+    const long target = num_cus;
+    for (int t = 0; t < 2; ++t) {
+        const long tiles = (long)ceil_div(p.M, kTilesN[t].bpx) * ceil_div(p.Kg, kTilesN[t].bkc) * p.groups;
+        if (tiles < target && t == 0) continue;
+        plan.tile = t;
+        const int chunks = p.Kred / plan.krc;
+        int splits = tiles < target ? (int)((target + tiles - 1) / tiles) : 1;
+        const int max_splits = chunks / 2;
+        if (splits > max_splits) splits = max_splits;
+        if (splits < 1) splits = 1;
+        const int per = ceil_div(chunks, splits);
+        splits = ceil_div(chunks, per);
+        plan.splits = splits;
+        plan.kr_per_split = per * plan.krc;
+        plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
+        break;
+    }
+    plan.xcl_bytes = (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
+    return plan;
+}
+
+void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, int len,
+                        int *launches)
+{
+    const TileN &t = kTilesN[plan.tile];
+    int R = rs_template(p.R), S = rs_template(p.S);
+    if (R != S) R = S = 0;
+    const bool vec = (p.H * p.W) % 8 == 0 && p.C % 8 == 0;
+    snprintf(buf, len, "nchw_to_nhwc_bf16_kernel<%s> + igemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s",
+             vec ? "true" : "false", R, S,
+             t.bkc, t.bpx, plan.krc, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    *launches = plan.splits > 1 ? 3 : 2;
+}
+
+hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const uint16_t *x,
+                            const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
+                            float *partials, hipStream_t st, const LaunchHook *hook)
+{
+    hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
+    if (e != hipSuccess) return e;
+    const int HW = p.H * p.W;
+    const int th = ceil_div(HW, 64), tc = ceil_div(p.C, 64);
+    const bool vec = HW % 8 == 0 && p.C % 8 == 0 && ((uintptr_t)x & 15) == 0;
+    if (vec)
+        hipLaunchKernelGGL(nchw_to_nhwc_bf16_kernel<true>, dim3((unsigned)((long)th * tc * p.N)),
+                           dim3(256), 0, st, x, xcl, p.C, HW, th, tc);
+    else
+        hipLaunchKernelGGL(nchw_to_nhwc_bf16_kernel<false>, dim3((unsigned)((long)th * tc * p.N)),
+                           dim3(256), 0, st, x, xcl, p.C, HW, th, tc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    ConvArgs a = make_args(p);
+    a.x = xcl;
+    a.w = w_krsc;
+    a.bias = bias;
+    a.y = y;
+    a.ws = plan.splits > 1 ? partials : nullptr;
+    a.splits = plan.splits;
+    a.kr_per_split = plan.kr_per_split;
+    const TileN &t = kTilesN[plan.tile];
+    dim3 grid(ceil_div(p.M, t.bpx), ceil_div(p.Kg, t.bkc), p.groups * plan.splits);
+    if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+    if (plan.krc == 64)
+        launch_krc<64>(a, plan.tile, grid, st);
+    else
+        launch_krc<32>(a, plan.tile, grid, st);
+    if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
+    if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+    return launch_splitk_reduce(a, st);
+}
+
+}  // namespace miconv

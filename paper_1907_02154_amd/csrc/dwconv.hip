@@ -15,8 +15,10 @@
 //    registers while the group walks down its strip: stride 1 loads one new
 //    input row per output row, stride 2 loads two.
 //
-// Other depthwise shapes (filters up to 7x7, any stride and pad) use a plain
-// one-output-per-lane kernel.
+// Planes small enough for LDS (every MobileNet depthwise layer) use the
+// LDS-run kernel below instead, which reads and writes whole contiguous runs
+// of planes; other depthwise shapes (filters up to 7x7, any stride and pad)
+// use a plain one-output-per-lane kernel.
 #include "internal.h"
 
 #include <cstdio>
@@ -180,6 +182,133 @@ __global__ __launch_bounds__(256) void dw3x3_kernel(DwArgs a)
     }
 }
 
+// Small planes: a work-group takes runs of PB consecutive (n, c) planes --
+// each run one contiguous stretch of PB*H*W inputs in NCHW -- and streams
+// them through two LDS buffers: while the lanes compute run i from LDS, the
+// 16-byte loads of run i+1 are in flight in registers.  Every lane produces
+// 4 consecutive outputs of the run's contiguous output stretch (flattened
+// over planes, rows and columns) and writes them with one 16-byte store, so
+// HBM sees one contiguous read of x and one contiguous write of y.  The
+// filter taps and biases of a run travel with it into LDS.
+struct DwLdsArgs {
+    const float *x, *w, *bias;
+    float *y;
+    int C, H, W, P, Q, stride, pad;
+    int HW, PQ;
+    long planes;
+    int PB;          // planes per run (PB*HW <= kRunFloats, PB*HW and PB*PQ multiples of 4)
+    long runs;
+    int relu;
+};
+
+constexpr int kRunFloats = 6144;                   // per LDS buffer (24 KB)
+constexpr int kRun4 = kRunFloats / 4 / 256;        // float4 per lane per run
+
+__global__ __launch_bounds__(256) void dw_lds_kernel(DwLdsArgs a)
+{
+    __shared__ __attribute__((aligned(16))) float xs[2][kRunFloats];
+    __shared__ float wb[2][64 * 10];        // per plane of the run: 9 taps, then the bias
+    const int tid = threadIdx.x;
+    float4 stage[kRun4];
+    float tail;          // the last partial run's inputs beyond its last whole float4
+    int tail_at;
+    float wstage[3];
+
+    auto load = [&](long run) {
+        const long plane0 = run * a.PB;
+        const int np = run < a.runs ? (int)min((long)a.PB, a.planes - plane0) : 0;
+        const int cnt = np * a.HW;
+        const int c4 = cnt / 4;
+        const float4 *src = reinterpret_cast<const float4 *>(a.x + plane0 * a.HW);
+        tail_at = 4 * c4 + tid;
+        tail = tail_at < cnt ? a.x[plane0 * a.HW + tail_at] : 0.f;
+        if (tail_at >= cnt) tail_at = -1;
+#pragma unroll
+        for (int i = 0; i < kRun4; ++i) {
+            const int j = tid + i * 256;
+            stage[i] = j < c4 ? src[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            const int j = tid + i * 256;          // j = plane * 10 + tap (tap 9 = bias)
+            const int pl = j / 10, t = j - pl * 10;
+            float v = 0.f;
+            if (pl < np) {
+                const int c = (int)((plane0 + pl) % a.C);
+                v = t < 9 ? a.w[c * 9 + t] : (a.bias ? a.bias[c] : 0.f);
+            }
+            wstage[i] = v;
+        }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < kRun4; ++i)
+            reinterpret_cast<float4 *>(xs[buf])[tid + i * 256] = stage[i];
+        if (tail_at >= 0) xs[buf][tail_at] = tail;
+#pragma unroll
+        for (int i = 0; i < 3; ++i)
+            if (tid + i * 256 < 64 * 10) wb[buf][tid + i * 256] = wstage[i];
+    };
+
+    long run = blockIdx.x;
+    int buf = 0;
+    load(run);
+    store(0);
+    load(run + gridDim.x);
+    __syncthreads();
+    for (; run < a.runs; run += gridDim.x) {
+        const long plane0 = run * a.PB;
+        const int np = (int)min((long)a.PB, a.planes - plane0);
+        const float *xr = xs[buf];
+        float *dst = a.y + plane0 * a.PQ;
+        const int ocnt = np * a.PQ;
+        for (int o = tid * 4; o < ocnt; o += 256 * 4) {
+            int pl = o / a.PQ;
+            int pq = o - pl * a.PQ;
+            int p = pq / a.Q;
+            int q = pq - p * a.Q;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float *wp = wb[buf] + pl * 10;
+                const float *xp = xr + pl * a.HW;
+                float acc = wp[9];
+                const int h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+#pragma unroll
+                for (int r = 0; r < 3; ++r) {
+                    const int hh = h0 + r;
+                    const bool hv = (unsigned)hh < (unsigned)a.H;
+#pragma unroll
+                    for (int ss = 0; ss < 3; ++ss) {
+                        const int ww = w0 + ss;
+                        const bool ok = hv && (unsigned)ww < (unsigned)a.W;
+                        acc = fmaf(ok ? xp[hh * a.W + ww] : 0.f, wp[r * 3 + ss], acc);
+                    }
+                }
+                v[e] = a.relu ? fmaxf(acc, 0.f) : acc;
+                if (++q == a.Q) {
+                    q = 0;
+                    if (++p == a.P) {
+                        p = 0;
+                        ++pl;
+                    }
+                }
+            }
+            if (o + 3 < ocnt) {
+                *reinterpret_cast<float4 *>(dst + o) = make_float4(v[0], v[1], v[2], v[3]);
+            } else {
+                for (int e = 0; e < 4; ++e)
+                    if (o + e < ocnt) dst[o + e] = v[e];
+            }
+        }
+        // run + gridDim.x is in registers: publish it, start the one after
+        buf ^= 1;
+        store(buf);
+        load(run + 2L * gridDim.x);
+        __syncthreads();
+    }
+}
+
 // Any depthwise shape: one output per lane, taps read through the caches.
 __global__ __launch_bounds__(256) void dw_generic_kernel(const float *__restrict__ x,
                                                          const float *__restrict__ w,
@@ -240,10 +369,25 @@ int dw_vector_width(const ConvProblem &p, const void *x, const void *y)
     return 0;
 }
 
+// Planes per LDS run for the small-plane kernel (0: use the lane-group kernel).
+// 3x3 filters on planes narrower than 56 columns; runs keep 16-byte alignment.
+int dw_lds_planes(const ConvProblem &p, const void *x, const void *y)
+{
+    if (p.R != 3 || p.S != 3 || p.W >= 56) return 0;
+    const long hw = (long)p.H * p.W, pq = (long)p.P * p.Q;
+    long pb = kRunFloats / hw;
+    if (pb > 64) pb = 64;
+    while (pb > 0 && ((pb * hw) % 4 || (pb * pq) % 4)) --pb;
+    if (pb <= 0 || !aligned(x, 16) || !aligned(y, 16)) return 0;
+    return (int)pb;
+}
+
 void describe_dwconv(const ConvProblem &p, char *buf, int len, int *launches)
 {
     const int V = dw_vector_width(p, nullptr, nullptr);
-    if (V)
+    if (dw_lds_planes(p, nullptr, nullptr) > 0)
+        snprintf(buf, len, "dw_lds_kernel");
+    else if (V)
         snprintf(buf, len, "dw3x3_kernel<%d, %d>", p.stride, V);
     else
         snprintf(buf, len, "dw_generic_kernel");
@@ -254,9 +398,33 @@ hipError_t launch_dwconv_f32(const ConvProblem &p, const float *x, const float *
                              const float *bias, float *y, hipStream_t st)
 {
     const long planes = (long)p.N * p.C;
+    const int PB = dw_lds_planes(p, x, y);
+    if (PB > 0) {
+        DwLdsArgs a{};
+        a.x = x;
+        a.w = w;
+        a.bias = bias;
+        a.y = y;
+        a.C = p.C;
+        a.H = p.H;
+        a.W = p.W;
+        a.P = p.P;
+        a.Q = p.Q;
+        a.stride = p.stride;
+        a.pad = p.pad;
+        a.HW = p.H * p.W;
+        a.PQ = p.P * p.Q;
+        a.planes = planes;
+        a.PB = PB;
+        a.runs = (planes + PB - 1) / PB;
+        a.relu = p.relu;
+        long grid = a.runs < 2048 ? a.runs : 2048;   // about eight work-groups per CU
+        hipLaunchKernelGGL(dw_lds_kernel, dim3((unsigned)grid), dim3(256), 0, st, a);
+        return hipGetLastError();
+    }
     const int V = dw_vector_width(p, x, y);
     if (V) {
-        DwArgs a;
+        DwArgs a{};
         a.x = x;
         a.w = w;
         a.bias = bias;

@@ -89,6 +89,23 @@ hipError_t launch_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool f
 void describe_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast, bool va,
                          char *buf, int len, int *launches);
 
+// bf16 through an internal channel-last copy of x (C/groups % 32 == 0).
+struct NhwcPlan {
+    int tile;             // 0: 128 x 128, 1: 64 x 64
+    int krc;              // reduction chunk (64 or 32 channels at one filter position)
+    int splits;
+    int kr_per_split;
+    size_t partial_bytes; // split-K partials
+    size_t xcl_bytes;     // the channel-last copy of x
+};
+bool nhwc_bf16_eligible(const ConvProblem &p);
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus);
+hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const uint16_t *x,
+                            const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
+                            float *partials, hipStream_t st, const LaunchHook *hook = nullptr);
+void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, int len,
+                        int *launches);
+
 // Sums split partials [splits][K][M] in split order into y (+ bias, activation).
 hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st);
 
@@ -107,7 +124,14 @@ hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t
 // A validated conv call with its kernel fixed (what the ABI entry points and
 // the stack executor enqueue).
 enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2 };
-enum Impl { IMPL_DIRECT = 0, IMPL_IGEMM = 1, IMPL_DW = 2, IMPL_WAVE = 3, IMPL_IGEMM_BF16 = 4 };
+enum Impl {
+    IMPL_DIRECT = 0,
+    IMPL_IGEMM = 1,
+    IMPL_DW = 2,
+    IMPL_WAVE = 3,
+    IMPL_IGEMM_BF16 = 4,
+    IMPL_NHWC_BF16 = 5
+};
 struct Resolved {
     ConvProblem p;
     int kind;
@@ -115,6 +139,7 @@ struct Resolved {
     IgemmPlan plan;     // IMPL_IGEMM only
     WavePlan wplan;     // IMPL_WAVE only
     bool bfast, bva;    // IMPL_IGEMM_BF16: vectorised 1x1 loader, 16-byte filter loads
+    NhwcPlan nplan;     // IMPL_NHWC_BF16 only
     bool pack_per_call; // enqueue packs the filters (KRSC) into the workspace first
     const void *wk;     // filters the conv kernel reads when they were packed ahead (else w)
     const void *x, *w;

@@ -48,6 +48,7 @@ def lib() -> ctypes.CDLL:
         L.conv2d_fwd_bf16.argtypes = conv
         L.dwconv2d_fwd.argtypes = conv
         L.conv2d_fwd_algo.argtypes = [i] * 10 + [p, p, p, p, i, i, p]
+        L.conv2d_fwd_bf16_algo.argtypes = [i] * 10 + [p, p, p, p, i, i, p]
         L.miconv_out_dims.argtypes = [i] * 6 + [ctypes.POINTER(i)] * 2
         L.maxpool2d_fwd.argtypes = [i] * 8 + [p, p, p]
         L.add_act_fwd.argtypes = [l, p, p, p, i, p]
@@ -75,6 +76,7 @@ def lib() -> ctypes.CDLL:
         L.miconv_last_hip_error.argtypes = []
         L.miconv_version.argtypes = []
         for f in ("conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd", "conv2d_fwd_algo",
+                  "conv2d_fwd_bf16_algo",
                   "miconv_out_dims", "maxpool2d_fwd", "add_act_fwd", "cast_f32_to_bf16",
                   "miconv_last_hip_error", "miconv_version"):
             getattr(L, f).restype = i
@@ -171,6 +173,13 @@ def conv2d_fwd_bf16(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, stream
     """bf16 x and w (torch.bfloat16), fp32 bias and y."""
     return _conv_common(lib().conv2d_fwd_bf16, x, w, bias, y, stride, pad, groups, relu, stream,
                         torch.bfloat16)
+
+
+def conv2d_fwd_bf16_algo(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO,
+                         stream=None):
+    """conv2d_fwd_bf16 with an explicit algorithm (ALGO_AUTO / ALGO_IGEMM / ALGO_DIRECT)."""
+    return _conv_common(lib().conv2d_fwd_bf16_algo, x, w, bias, y, stride, pad, groups, relu, stream,
+                        torch.bfloat16, extra=(int(algo),))
 
 
 def dwconv2d_fwd(x, w, bias, y, stride=1, pad=1, relu=False, stream=None):
@@ -320,7 +329,9 @@ def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUT
     P, Q = out_dims(H, W, R, S, stride, pad)
     y = torch.empty((N, K, P, Q), device=x.device, dtype=torch.float32)
     if x.dtype == torch.bfloat16:
-        return conv2d_fwd_bf16(x, w, bias, y, stride, pad, groups, relu, stream)
+        if algo == ALGO_AUTO:
+            return conv2d_fwd_bf16(x, w, bias, y, stride, pad, groups, relu, stream)
+        return conv2d_fwd_bf16_algo(x, w, bias, y, stride, pad, groups, relu, algo, stream)
     if algo == ALGO_AUTO:
         return conv2d_fwd(x, w, bias, y, stride, pad, groups, relu, stream)
     return conv2d_fwd_algo(x, w, bias, y, stride, pad, groups, relu, algo, stream)

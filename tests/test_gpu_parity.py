@@ -123,15 +123,24 @@ def test_depthwise_small_int_bitwise(oracle_lib, case):
         np.testing.assert_array_equal(y2, ref)
 
 
-@pytest.mark.parametrize("case", DENSE_CASES[:9], ids=lambda c: "x".join(map(str, c)))
-def test_bf16_small_int_bitwise(oracle_lib, case):
+BF16_CASES = DENSE_CASES[:9] + [
+    (2, 64, 15, 15, 70, 3, 3, 2, 1, 1),      # channel-last path, 3x3 stride 2, ragged tiles
+    (1, 64, 9, 9, 48, 3, 3, 1, 1, 2),        # channel-last path, grouped (C/groups = 32)
+    (3, 96, 13, 11, 130, 1, 1, 1, 0, 1),     # channel-last 1x1, chunk of 32 channels
+    (1, 256, 7, 7, 520, 3, 3, 1, 1, 1),      # long reduction: split across work-groups
+]
+
+
+@pytest.mark.parametrize("case", BF16_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("algo", [miconv.ALGO_AUTO, miconv.ALGO_IGEMM, miconv.ALGO_DIRECT])
+def test_bf16_small_int_bitwise(oracle_lib, case, algo):
     N, C, H, W, K, R, S, st, pad, g = case
     seed = 3000 + sum(case)
     x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
     w = wl.to_bf16_bits(ints((K, C // g, R, S), -4, 4, seed + 1))
     b = ints((K,), -8, 8, seed + 2)
     ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
-    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True)
+    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True, algo=algo)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), ref)
 
@@ -246,3 +255,20 @@ def test_rejects_wrong_shapes_from_python():
         miconv.conv2d_fwd(x, w, None, torch.zeros((1, 4, 7, 7), device="cuda"), 1, 1)
     with pytest.raises(TypeError):
         miconv.conv2d_fwd(x.double(), w, None, torch.zeros((1, 4, 8, 8), device="cuda"), 1, 1)
+
+
+def test_depthwise_batch64_sampled(oracle_lib):
+    """Depthwise at the bandwidth-sweep batch (64 images): images 0 and 63 of
+    every MobileNet depthwise shape against the oracle."""
+    for i, l in _layers(3):
+        if l.kind != "dw":
+            continue
+        l = l.with_batch(64)
+        x, w, b = wl.layer_tensors(3, i, l)
+        y = miconv.dwconv2d(dev(x), dev(w), dev(b), l.stride, l.pad, l.relu)
+        torch.cuda.synchronize()
+        y = y.cpu().numpy()
+        for n in (0, 63):
+            ref = oracle_lib.dwconv2d(x[n:n + 1], w, b, l.stride, l.pad, l.relu)
+            e = err_inf(y[n:n + 1], ref)
+            assert e <= TOL_F32, (l.name, n, e)
