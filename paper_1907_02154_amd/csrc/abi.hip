@@ -103,21 +103,6 @@ int check_bias(const float *bias)
     return (bias && (uintptr_t)bias % sizeof(float)) ? MICONV_ERR_ALIGN : MICONV_OK;
 }
 
-int cu_count()
-{
-    static std::mutex mu;
-    static std::map<int, int> cache;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 256;
-    std::lock_guard<std::mutex> lk(mu);
-    auto it = cache.find(dev);
-    if (it != cache.end()) return it->second;
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-        n = 256;
-    cache[dev] = n;
-    return n;
-}
 
 // Split-K workspace (fp32 partials), one per (device, stream).
 struct Workspace {
@@ -160,6 +145,22 @@ int get_workspace(hipStream_t st, size_t need, float **out)
 int finish(hipError_t e) { return e == hipSuccess ? MICONV_OK : hip_fail(e); }
 
 }  // namespace
+
+int cu_count()
+{
+    static std::mutex mu;
+    static std::map<int, int> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = cache.find(dev);
+    if (it != cache.end()) return it->second;
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        n = 256;
+    cache[dev] = n;
+    return n;
+}
 
 int set_hip_error(hipError_t e) { return hip_fail(e); }
 

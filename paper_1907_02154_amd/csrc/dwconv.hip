@@ -15,10 +15,10 @@
 //    registers while the group walks down its strip: stride 1 loads one new
 //    input row per output row, stride 2 loads two.
 //
-// Planes small enough for LDS (every MobileNet depthwise layer) use the
-// LDS-run kernel below instead, which reads and writes whole contiguous runs
-// of planes; other depthwise shapes (filters up to 7x7, any stride and pad)
-// use a plain one-output-per-lane kernel.
+// Square planes up to 56x56 use the whole-plane run kernel below instead,
+// which streams contiguous runs of planes through LDS; other depthwise shapes
+// (filters up to 7x7, any stride and pad) use a plain one-output-per-lane
+// kernel.
 #include "internal.h"
 
 #include <cstdio>
@@ -182,130 +182,322 @@ __global__ __launch_bounds__(256) void dw3x3_kernel(DwArgs a)
     }
 }
 
-// Small planes: a work-group takes runs of PB consecutive (n, c) planes --
-// each run one contiguous stretch of PB*H*W inputs in NCHW -- and streams
-// them through two LDS buffers: while the lanes compute run i from LDS, the
-// 16-byte loads of run i+1 are in flight in registers.  Every lane produces
-// 4 consecutive outputs of the run's contiguous output stretch (flattened
-// over planes, rows and columns) and writes them with one 16-byte store, so
-// HBM sees one contiguous read of x and one contiguous write of y.  The
-// filter taps and biases of a run travel with it into LDS.
-struct DwLdsArgs {
+// Planes up to 56x56 (3x3, pad 1): a work-group takes runs of PB whole
+// consecutive (n, c) planes -- in NCHW one contiguous stretch of PB*H*W
+// inputs -- and reads each run from HBM once with 16-byte loads.  The run is
+// laid out in LDS with a zero gap of at least W+1 floats before and after
+// every plane, so taps above the first row and below the last row read zeros
+// without a test; only the left and right image borders need a mask.  The
+// plane extents are compile-time constants, so the lanes' index arithmetic
+// is multiplies and shifts.  A lane computes a column of several output rows
+// at one position, reading each input row once for all of them; neighbouring
+// lanes take neighbouring columns, so LDS reads are conflict-free (stride 1)
+// and each output store of a wavefront covers whole row segments.  While the
+// lanes compute run i from LDS, the loads of the work-group's next run are
+// already in flight into registers.
+struct DwRunArgs {
     const float *x, *w, *bias;
     float *y;
-    int C, H, W, P, Q, stride, pad;
-    int HW, PQ;
+    int C;
     long planes;
-    int PB;          // planes per run (PB*HW <= kRunFloats, PB*HW and PB*PQ multiples of 4)
+    int PB;          // planes per run
     long runs;
     int relu;
 };
 
-constexpr int kRunFloats = 6144;                   // per LDS buffer (24 KB)
-constexpr int kRun4 = kRunFloats / 4 / 256;        // float4 per lane per run
+constexpr int kRunLds = 9728;                       // floats of LDS per work-group (38 KB)
+constexpr int kTapStride = 12;                      // per plane in LDS: 9 taps, bias, 2 unused
 
-__global__ __launch_bounds__(256) void dw_lds_kernel(DwLdsArgs a)
+template <int H_, int W_, int ST>
+struct DwRunShape {
+    static constexpr int P = (H_ - 1) / ST + 1;     // 3x3, pad 1
+    static constexpr int Q = (W_ - 1) / ST + 1;
+    static constexpr int HW = H_ * W_;
+    static constexpr int PQ = P * Q;
+    static constexpr int G0 = (W_ + 1 + 3) / 4 * 4;                     // gap before plane 0
+    static constexpr int PP = (HW + W_ + 1 + 3) / 4 * 4;               // plane pitch (plane + gap)
+    static constexpr bool RIGHT_MASK = (Q - 1) * ST + 1 >= W_;         // a right tap can leave the image
+    // float4 per lane staged per run (odd planes scatter element-wise and
+    // take more registers, so they stage less)
+    static constexpr int STAGE4 = HW % 4 == 0 ? 7 : 5;
+    static constexpr int STAGE_FLOATS = STAGE4 * 4 * 256;
+    static constexpr int MAX_PB_LDS = (kRunLds - G0) / (PP + kTapStride);
+    static constexpr int MAX_PB = STAGE_FLOATS / HW < MAX_PB_LDS ? STAGE_FLOATS / HW : MAX_PB_LDS;
+    static constexpr int NW = (MAX_PB * kTapStride + 255) / 256;       // tap words staged per lane
+    // A lane's work item is a column of RG output rows of one plane: the
+    // (RG-1)*ST+3 input rows it reads feed all RG outputs, so each input
+    // element is read from LDS about once per item instead of 9 times.
+    static constexpr int RG = P % 7 == 0 ? 7 : P;
+    static constexpr int NG = P / RG;                                  // row groups per plane
+    static constexpr int IPP = NG * Q;                                 // items per plane
+    static_assert(P % RG == 0, "row groups tile the plane");
+};
+
+// Planes per run for a shape.  Runs are as large as the register stage and
+// LDS allow, then evened out so that the run count is a whole multiple of the
+// grid (`grid` work-groups, one run each per round): no round ends with part
+// of the chip idle.  0 if one plane does not fit.
+template <int H_, int W_, int ST>
+int dw_run_planes_for(long planes, long grid)
 {
-    __shared__ __attribute__((aligned(16))) float xs[2][kRunFloats];
-    __shared__ float wb[2][64 * 10];        // per plane of the run: 9 taps, then the bias
+    using S = DwRunShape<H_, W_, ST>;
+    const int align = S::HW % 4 == 0 ? 1 : (S::HW % 2 == 0 ? 2 : 4);  // PB*HW % 4 == 0
+    long pbmax = S::MAX_PB;
+    pbmax = pbmax / align * align;
+    if (pbmax < align) return 0;
+    long rounds = (planes + pbmax * grid - 1) / (pbmax * grid);
+    long pb;
+    for (;; ++rounds) {
+        pb = (planes + rounds * grid - 1) / (rounds * grid);
+        pb = (pb + align - 1) / align * align;
+        if (pb <= pbmax) break;
+    }
+    return (int)pb;
+}
+
+template <int H_, int W_, int ST>
+__global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
+{
+    using S = DwRunShape<H_, W_, ST>;
+    __shared__ __attribute__((aligned(16))) float lds[kRunLds];
     const int tid = threadIdx.x;
-    float4 stage[kRun4];
-    float tail;          // the last partial run's inputs beyond its last whole float4
-    int tail_at;
-    float wstage[3];
+    float *taps = lds + S::G0 + a.PB * S::PP;      // 16-byte aligned: G0 and PP are multiples of 4
+
+    // The gaps are written here once and never again: runs only write plane slots.
+    for (int i = tid; i < kRunLds / 4; i += 256)
+        reinterpret_cast<float4 *>(lds)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+
+    float4 stage[S::STAGE4];
+    constexpr int kW = S::NW;
+    float wstage[kW];
+    float tail = 0.f;
+    int c4 = 0, cnt = 0, wcnt = 0;
+    long sp0 = 0;          // first plane of the staged run
 
     auto load = [&](long run) {
-        const long plane0 = run * a.PB;
-        const int np = run < a.runs ? (int)min((long)a.PB, a.planes - plane0) : 0;
-        const int cnt = np * a.HW;
-        const int c4 = cnt / 4;
-        const float4 *src = reinterpret_cast<const float4 *>(a.x + plane0 * a.HW);
-        tail_at = 4 * c4 + tid;
-        tail = tail_at < cnt ? a.x[plane0 * a.HW + tail_at] : 0.f;
-        if (tail_at >= cnt) tail_at = -1;
+        sp0 = run * a.PB;
+        const int np = run < a.runs ? (int)min((long)a.PB, a.planes - sp0) : 0;
+        cnt = np * S::HW;
+        c4 = cnt / 4;
+        wcnt = np * kTapStride;
+        const float4 *src = reinterpret_cast<const float4 *>(a.x + sp0 * S::HW);
+        const int c0 = (int)(sp0 % a.C);            // channel of the run's first plane (uniform)
 #pragma unroll
-        for (int i = 0; i < kRun4; ++i) {
+        for (int i = 0; i < S::STAGE4; ++i) {
             const int j = tid + i * 256;
             stage[i] = j < c4 ? src[j] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
+        // The last run of an odd-sized tensor ends inside a float4: at most 3 lanes.
+        const int tj = 4 * c4 + tid;
+        tail = tj < cnt ? a.x[sp0 * S::HW + tj] : 0.f;
 #pragma unroll
-        for (int i = 0; i < 3; ++i) {
-            const int j = tid + i * 256;          // j = plane * 10 + tap (tap 9 = bias)
-            const int pl = j / 10, t = j - pl * 10;
+        for (int i = 0; i < kW; ++i) {
+            const int j = tid + i * 256;             // j = plane * kTapStride + tap
+            const int pl = j / kTapStride, t = j - pl * kTapStride;
             float v = 0.f;
-            if (pl < np) {
-                const int c = (int)((plane0 + pl) % a.C);
-                v = t < 9 ? a.w[c * 9 + t] : (a.bias ? a.bias[c] : 0.f);
+            if (j < wcnt) {
+                const int c = (c0 + pl) % a.C;
+                v = t < 9 ? a.w[c * 9 + t] : (t == 9 && a.bias ? a.bias[c] : 0.f);
             }
             wstage[i] = v;
         }
     };
-    auto store = [&](int buf) {
+    // Staged inputs -> their plane slots in LDS.
+    auto put = [&]() {
 #pragma unroll
-        for (int i = 0; i < kRun4; ++i)
-            reinterpret_cast<float4 *>(xs[buf])[tid + i * 256] = stage[i];
-        if (tail_at >= 0) xs[buf][tail_at] = tail;
+        for (int i = 0; i < S::STAGE4; ++i) {
+            const int j4 = tid + i * 256;
+            if (j4 < c4) {
+                const int j = 4 * j4;
+                if constexpr (S::HW % 4 == 0) {
+                    const int pl = j / S::HW;
+                    *reinterpret_cast<float4 *>(lds + S::G0 + pl * S::PP + (j - pl * S::HW)) =
+                        stage[i];
+                } else {
+                    // a vector may cross into the next plane (at most once: HW >= 4)
+                    const float e[4] = {stage[i].x, stage[i].y, stage[i].z, stage[i].w};
+                    const int pl = j / S::HW;
+                    const int off = j - pl * S::HW;
+                    float *d = lds + S::G0 + pl * S::PP + off;
 #pragma unroll
-        for (int i = 0; i < 3; ++i)
-            if (tid + i * 256 < 64 * 10) wb[buf][tid + i * 256] = wstage[i];
+                    for (int k = 0; k < 4; ++k) d[k + (off + k >= S::HW ? S::PP - S::HW : 0)] = e[k];
+                }
+            }
+        }
+        const int tj = 4 * c4 + tid;
+        if (tj < cnt) {
+            const int pl = tj / S::HW;
+            lds[S::G0 + pl * S::PP + (tj - pl * S::HW)] = tail;
+        }
+#pragma unroll
+        for (int i = 0; i < kW; ++i)
+            if (tid + i * 256 < wcnt) taps[tid + i * 256] = wstage[i];
     };
 
     long run = blockIdx.x;
-    int buf = 0;
-    load(run);
-    store(0);
-    load(run + gridDim.x);
     __syncthreads();
+    load(run);
+    put();
     for (; run < a.runs; run += gridDim.x) {
-        const long plane0 = run * a.PB;
-        const int np = (int)min((long)a.PB, a.planes - plane0);
-        const float *xr = xs[buf];
-        float *dst = a.y + plane0 * a.PQ;
-        const int ocnt = np * a.PQ;
-        for (int o = tid * 4; o < ocnt; o += 256 * 4) {
-            int pl = o / a.PQ;
-            int pq = o - pl * a.PQ;
-            int p = pq / a.Q;
-            int q = pq - p * a.Q;
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float *wp = wb[buf] + pl * 10;
-                const float *xp = xr + pl * a.HW;
-                float acc = wp[9];
-                const int h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
-#pragma unroll
-                for (int r = 0; r < 3; ++r) {
-                    const int hh = h0 + r;
-                    const bool hv = (unsigned)hh < (unsigned)a.H;
-#pragma unroll
-                    for (int ss = 0; ss < 3; ++ss) {
-                        const int ww = w0 + ss;
-                        const bool ok = hv && (unsigned)ww < (unsigned)a.W;
-                        acc = fmaf(ok ? xp[hh * a.W + ww] : 0.f, wp[r * 3 + ss], acc);
-                    }
-                }
-                v[e] = a.relu ? fmaxf(acc, 0.f) : acc;
-                if (++q == a.Q) {
-                    q = 0;
-                    if (++p == a.P) {
-                        p = 0;
-                        ++pl;
-                    }
-                }
-            }
-            if (o + 3 < ocnt) {
-                *reinterpret_cast<float4 *>(dst + o) = make_float4(v[0], v[1], v[2], v[3]);
-            } else {
-                for (int e = 0; e < 4; ++e)
-                    if (o + e < ocnt) dst[o + e] = v[e];
-            }
-        }
-        // run + gridDim.x is in registers: publish it, start the one after
-        buf ^= 1;
-        store(buf);
-        load(run + 2L * gridDim.x);
+        const long plane0 = sp0;
+        load(run + gridDim.x);                      // in flight while this run computes
         __syncthreads();
+        const int np = (int)min((long)a.PB, a.planes - plane0);
+        const int icnt = np * S::IPP;
+        float *dst = a.y + plane0 * S::PQ;
+        constexpr int NR = (S::RG - 1) * ST + 3;   // input rows an item reads
+        for (int it = tid; it < icnt; it += 256) {
+            const int pl = it / S::IPP;
+            const int rem = it - pl * S::IPP;
+            const int g = rem / S::Q;
+            const int q = rem - g * S::Q;
+            const int p0 = g * S::RG;
+            // input row p0*ST - 1 (a zero gap row for the first group), column q*ST
+            const float *xb = lds + S::G0 + pl * S::PP + (p0 * ST - 1) * W_ + q * ST;
+            const float4 *tq = reinterpret_cast<const float4 *>(taps + pl * kTapStride);
+            const float4 t0 = tq[0], t1 = tq[1], t2 = tq[2];
+            const float wt[9] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w, t2.x};
+            const bool lok = q != 0;
+            const bool rok = !S::RIGHT_MASK || q * ST + 1 < W_;
+            float acc[S::RG];
+#pragma unroll
+            for (int j = 0; j < S::RG; ++j) acc[j] = t2.y;
+#pragma unroll
+            for (int rr = 0; rr < NR; ++rr) {
+                const float *row = xb + rr * W_;
+                const float v0 = lok ? row[-1] : 0.f;
+                const float v1 = row[0];
+                const float v2 = rok ? row[1] : 0.f;
+                // input row rr meets output row j through filter row rr - j*ST
+#pragma unroll
+                for (int j = 0; j < S::RG; ++j) {
+                    const int r = rr - j * ST;
+                    if (r >= 0 && r < 3) {
+                        acc[j] = fmaf(v0, wt[r * 3 + 0], acc[j]);
+                        acc[j] = fmaf(v1, wt[r * 3 + 1], acc[j]);
+                        acc[j] = fmaf(v2, wt[r * 3 + 2], acc[j]);
+                    }
+                }
+            }
+            float *yo = dst + pl * S::PQ + p0 * S::Q + q;
+#pragma unroll
+            for (int j = 0; j < S::RG; ++j) yo[j * S::Q] = a.relu ? fmaxf(acc[j], 0.f) : acc[j];
+        }
+        __syncthreads();                            // LDS free for the next run
+        put();
+    }
+}
+
+// Planes too large for one run (112x112): a run is a band of BR output rows
+// of one plane.  Its input rows, halo rows included, are one contiguous
+// stretch of the plane, staged into LDS as in the whole-plane kernel; halo
+// rows outside the image are staged as zeros.  Neighbouring bands share two
+// (stride 1) or one (stride 2) input rows, so the input is read 1 + 2/BR
+// (1 + 1/(2*BR)) times.
+template <int H_, int W_, int ST, int BR>
+struct DwBandShape {
+    static constexpr int P = (H_ - 1) / ST + 1;
+    static constexpr int Q = (W_ - 1) / ST + 1;
+    static constexpr int NB = P / BR;                                  // bands per plane
+    static constexpr int NRB = (BR - 1) * ST + 3;                      // input rows of a band
+    static constexpr int ROW0 = 4;                                     // LDS offset of the band's first row
+    static constexpr int STAGE4 = (NRB * W_ / 4 + 255) / 256;
+    static constexpr int RG = 7;
+    static constexpr int IPB = BR / RG * Q;                            // items per band
+    static constexpr bool RIGHT_MASK = (Q - 1) * ST + 1 >= W_;
+    static_assert(P % BR == 0 && BR % RG == 0 && W_ % 4 == 0, "band tiling");
+    static_assert(ROW0 + NRB * W_ + 4 + kTapStride <= kRunLds, "band fits in LDS");
+};
+
+template <int H_, int W_, int ST, int BR>
+__global__ __launch_bounds__(256, 4) void dw_band_kernel(DwRunArgs a)
+{
+    using S = DwBandShape<H_, W_, ST, BR>;
+    __shared__ __attribute__((aligned(16))) float lds[kRunLds];
+    float *taps = lds + kRunLds - kTapStride;      // 16-byte aligned
+    const int tid = threadIdx.x;
+    constexpr int NF4 = S::NRB * W_ / 4;           // float4 of a band
+    float4 stage[S::STAGE4];
+    float wst = 0.f;
+    long splane = 0;
+    int sband = 0;
+    bool slive = false;
+
+    auto load = [&](long run) {
+        slive = run < a.runs;
+        splane = run / S::NB;
+        sband = (int)(run - splane * S::NB);
+        const int h0 = sband * BR * ST - 1;        // first input row of the band
+        const float *xp = a.x + splane * (H_ * W_);
+#pragma unroll
+        for (int i = 0; i < S::STAGE4; ++i) {
+            const int j = tid + i * 256;
+            const int h = h0 + (4 * j) / W_;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (slive && j < NF4 && h >= 0 && h < H_)
+                v = *reinterpret_cast<const float4 *>(xp + (long)h0 * W_ + 4 * j);
+            stage[i] = v;
+        }
+        if (slive && tid < kTapStride) {
+            const int c = (int)(splane % a.C);
+            wst = tid < 9 ? a.w[c * 9 + tid] : (tid == 9 && a.bias ? a.bias[c] : 0.f);
+        }
+    };
+    auto put = [&]() {
+#pragma unroll
+        for (int i = 0; i < S::STAGE4; ++i) {
+            const int j = tid + i * 256;
+            if (j < NF4) *reinterpret_cast<float4 *>(lds + S::ROW0 + 4 * j) = stage[i];
+        }
+        if (tid < kTapStride) taps[tid] = wst;
+    };
+
+    long run = blockIdx.x;
+    load(run);
+    put();
+    for (; run < a.runs; run += gridDim.x) {
+        const long plane = splane;
+        const int band = sband;
+        load(run + gridDim.x);                      // in flight while this band computes
+        __syncthreads();
+        const float4 t0 = reinterpret_cast<const float4 *>(taps)[0];
+        const float4 t1 = reinterpret_cast<const float4 *>(taps)[1];
+        const float4 t2 = reinterpret_cast<const float4 *>(taps)[2];
+        const float wt[9] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w, t2.x};
+        float *dst = a.y + plane * (S::P * S::Q) + (long)band * BR * S::Q;
+        constexpr int NR = (S::RG - 1) * ST + 3;
+        for (int it = tid; it < S::IPB; it += 256) {
+            const int g = it / S::Q;
+            const int q = it - g * S::Q;
+            const int p0 = g * S::RG;                       // output row within the band
+            const float *xb = lds + S::ROW0 + p0 * ST * W_ + q * ST;
+            const bool lok = q != 0;
+            const bool rok = !S::RIGHT_MASK || q * ST + 1 < W_;
+            float acc[S::RG];
+#pragma unroll
+            for (int j = 0; j < S::RG; ++j) acc[j] = t2.y;
+#pragma unroll
+            for (int rr = 0; rr < NR; ++rr) {
+                const float *row = xb + rr * W_;
+                const float v0 = lok ? row[-1] : 0.f;
+                const float v1 = row[0];
+                const float v2 = rok ? row[1] : 0.f;
+#pragma unroll
+                for (int j = 0; j < S::RG; ++j) {
+                    const int r = rr - j * ST;
+                    if (r >= 0 && r < 3) {
+                        acc[j] = fmaf(v0, wt[r * 3 + 0], acc[j]);
+                        acc[j] = fmaf(v1, wt[r * 3 + 1], acc[j]);
+                        acc[j] = fmaf(v2, wt[r * 3 + 2], acc[j]);
+                    }
+                }
+            }
+            float *yo = dst + p0 * S::Q + q;
+#pragma unroll
+            for (int j = 0; j < S::RG; ++j) yo[j * S::Q] = a.relu ? fmaxf(acc[j], 0.f) : acc[j];
+        }
+        __syncthreads();
+        put();
     }
 }
 
@@ -369,24 +561,48 @@ int dw_vector_width(const ConvProblem &p, const void *x, const void *y)
     return 0;
 }
 
-// Planes per LDS run for the small-plane kernel (0: use the lane-group kernel).
-// 3x3 filters on planes narrower than 56 columns; runs keep 16-byte alignment.
-int dw_lds_planes(const ConvProblem &p, const void *x, const void *y)
+// Planes per run for the whole-plane kernel (0: not eligible): 3x3 pad 1
+// filters, stride 1 or 2, on the square plane sizes it is built for, with a
+// 16-byte aligned input.  The grid is four work-groups per compute unit.
+int dw_run_planes(const ConvProblem &p, const void *x, int cus)
 {
-    if (p.R != 3 || p.S != 3 || p.W >= 56) return 0;
-    const long hw = (long)p.H * p.W, pq = (long)p.P * p.Q;
-    long pb = kRunFloats / hw;
-    if (pb > 64) pb = 64;
-    while (pb > 0 && ((pb * hw) % 4 || (pb * pq) % 4)) --pb;
-    if (pb <= 0 || !aligned(x, 16) || !aligned(y, 16)) return 0;
-    return (int)pb;
+    if (p.R != 3 || p.S != 3 || p.pad != 1 || (p.stride != 1 && p.stride != 2) || p.H != p.W) return 0;
+    if (x && !aligned(x, 16)) return 0;
+    const long planes = (long)p.N * p.C;
+    const long grid = 4L * cus;
+    const bool s1 = p.stride == 1;
+    switch (p.H) {
+    case 7: return s1 ? dw_run_planes_for<7, 7, 1>(planes, grid) : dw_run_planes_for<7, 7, 2>(planes, grid);
+    case 14: return s1 ? dw_run_planes_for<14, 14, 1>(planes, grid) : dw_run_planes_for<14, 14, 2>(planes, grid);
+    case 28: return s1 ? dw_run_planes_for<28, 28, 1>(planes, grid) : dw_run_planes_for<28, 28, 2>(planes, grid);
+    case 56: return s1 ? dw_run_planes_for<56, 56, 1>(planes, grid) : dw_run_planes_for<56, 56, 2>(planes, grid);
+    default: return 0;
+    }
+}
+
+// Bands per launch for the 112x112 band kernel (0: not eligible).  Used
+// when there are at least as many bands as the grid has work-groups; fewer
+// (small batches) go to the lane-group kernel.
+constexpr int kBandRows1 = 56, kBandRows2 = 28;      // output rows per band, stride 1 / 2
+
+long dw_band_runs(const ConvProblem &p, const void *x, int cus)
+{
+    if (p.R != 3 || p.S != 3 || p.pad != 1 || (p.stride != 1 && p.stride != 2) || p.H != 112 ||
+        p.W != 112)
+        return 0;
+    if (x && !aligned(x, 16)) return 0;
+    const long runs = (long)p.N * p.C * (p.P / (p.stride == 1 ? kBandRows1 : kBandRows2));
+    return runs >= 4L * cus ? runs : 0;
 }
 
 void describe_dwconv(const ConvProblem &p, char *buf, int len, int *launches)
 {
     const int V = dw_vector_width(p, nullptr, nullptr);
-    if (dw_lds_planes(p, nullptr, nullptr) > 0)
-        snprintf(buf, len, "dw_lds_kernel");
+    if (dw_run_planes(p, nullptr, 256) > 0)
+        snprintf(buf, len, "dw_run_kernel<%d, %d, %d>", p.H, p.W, p.stride);
+    else if (dw_band_runs(p, nullptr, 256) > 0)
+        snprintf(buf, len, "dw_band_kernel<%d, %d, %d, %d>", p.H, p.W, p.stride,
+                 p.stride == 1 ? kBandRows1 : kBandRows2);
     else if (V)
         snprintf(buf, len, "dw3x3_kernel<%d, %d>", p.stride, V);
     else
@@ -398,28 +614,48 @@ hipError_t launch_dwconv_f32(const ConvProblem &p, const float *x, const float *
                              const float *bias, float *y, hipStream_t st)
 {
     const long planes = (long)p.N * p.C;
-    const int PB = dw_lds_planes(p, x, y);
+    const int cus = cu_count();
+    const int PB = dw_run_planes(p, x, cus);
     if (PB > 0) {
-        DwLdsArgs a{};
+        DwRunArgs a{};
         a.x = x;
         a.w = w;
         a.bias = bias;
         a.y = y;
         a.C = p.C;
-        a.H = p.H;
-        a.W = p.W;
-        a.P = p.P;
-        a.Q = p.Q;
-        a.stride = p.stride;
-        a.pad = p.pad;
-        a.HW = p.H * p.W;
-        a.PQ = p.P * p.Q;
         a.planes = planes;
         a.PB = PB;
         a.runs = (planes + PB - 1) / PB;
         a.relu = p.relu;
-        long grid = a.runs < 2048 ? a.runs : 2048;   // about eight work-groups per CU
-        hipLaunchKernelGGL(dw_lds_kernel, dim3((unsigned)grid), dim3(256), 0, st, a);
+        const long grid = a.runs < 4L * cus ? a.runs : 4L * cus;   // four 38 KB work-groups per CU
+        const dim3 g((unsigned)grid), b(256);
+#define MICONV_DW_RUN(HH, ST)                                                         \
+    if (p.H == HH && p.stride == ST) {                                               \
+        hipLaunchKernelGGL((dw_run_kernel<HH, HH, ST>), g, b, 0, st, a);             \
+        return hipGetLastError();                                                    \
+    }
+        MICONV_DW_RUN(7, 1) MICONV_DW_RUN(7, 2) MICONV_DW_RUN(14, 1) MICONV_DW_RUN(14, 2)
+        MICONV_DW_RUN(28, 1) MICONV_DW_RUN(28, 2) MICONV_DW_RUN(56, 1) MICONV_DW_RUN(56, 2)
+#undef MICONV_DW_RUN
+        return hipErrorInvalidValue;
+    }
+    const long band_runs = dw_band_runs(p, x, cus);
+    if (band_runs > 0) {
+        DwRunArgs a{};
+        a.x = x;
+        a.w = w;
+        a.bias = bias;
+        a.y = y;
+        a.C = p.C;
+        a.planes = planes;
+        a.PB = 1;
+        a.runs = band_runs;
+        a.relu = p.relu;
+        const dim3 g((unsigned)(4L * cus)), b(256);
+        if (p.stride == 1)
+            hipLaunchKernelGGL((dw_band_kernel<112, 112, 1, kBandRows1>), g, b, 0, st, a);
+        else
+            hipLaunchKernelGGL((dw_band_kernel<112, 112, 2, kBandRows2>), g, b, 0, st, a);
         return hipGetLastError();
     }
     const int V = dw_vector_width(p, x, y);

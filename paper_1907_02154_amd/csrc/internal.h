@@ -34,6 +34,9 @@ struct ConvArgs {
 
 ConvArgs make_args(const ConvProblem &p);
 
+// Compute units of the current device (cached per device).
+int cu_count();
+
 // Called before every kernel launch of one conv (the stack executor records
 // a timing event there).
 struct LaunchHook {

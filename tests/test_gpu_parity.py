@@ -103,6 +103,16 @@ DW_CASES = [  # (N, C, H, W, R, stride, pad)
     (1, 4, 130, 130, 3, 1, 1),          # row wider than one lane group: several segments
     (1, 4, 9, 13, 3, 1, 1), (2, 3, 11, 10, 3, 2, 1),   # odd sizes
     (1, 6, 12, 12, 5, 3, 2), (1, 2, 8, 8, 7, 1, 3), (1, 3, 6, 6, 1, 1, 0), (1, 2, 5, 5, 3, 1, 0),
+    # whole-plane run kernel: every plane size and stride it is built for, with
+    # a partial last run (and, for 7x7, runs that end inside a 16-byte vector)
+    (3, 37, 7, 7, 3, 1, 1), (2, 41, 7, 7, 3, 2, 1), (5, 61, 14, 14, 3, 1, 1),
+    (3, 53, 14, 14, 3, 2, 1), (2, 23, 28, 28, 3, 1, 1), (1, 19, 28, 28, 3, 2, 1),
+    (1, 9, 56, 56, 3, 1, 1), (1, 7, 56, 56, 3, 2, 1),
+    # ... and with more runs than work-groups, so work-groups loop over runs
+    (133, 1024, 7, 7, 3, 1, 1), (37, 1024, 14, 14, 3, 1, 1), (10, 1000, 28, 28, 3, 2, 1),
+    (9, 250, 56, 56, 3, 1, 1),
+    # 112x112 band kernel (enough bands to fill the grid; a few work-groups take two)
+    (4, 130, 112, 112, 3, 1, 1), (2, 260, 112, 112, 3, 2, 1),
 ]
 
 
