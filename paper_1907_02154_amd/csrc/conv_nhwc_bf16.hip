@@ -24,11 +24,12 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// x [N][C][HW] -> x_cl [N][HW][C] in 64 x 64 tiles (channels x pixels).
-// With HW % 8 == 0 and C % 8 == 0 every lane moves 16 bytes per global access:
-// it reads 8 pixels of one channel and, after the LDS exchange, writes 8
-// channels of one pixel.
-template <bool VEC>
+// x [N][C][HW] -> x_cl [N][HW][C] in 64 x 64 tiles (channels x pixels),
+// exchanged through LDS so that both sides of the copy are contiguous.  A
+// lane reads RV consecutive pixels of one channel per global load (RV = 8, 4
+// or 1: the widest that HW's alignment allows) and, with C % 8 == 0 (WV),
+// writes 8 channels of one pixel per 16-byte store.
+template <int RV, bool WV>
 __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *__restrict__ x,
                                                                 uint16_t *__restrict__ xt, int C,
                                                                 int HW, int tiles_hw, int tiles_c)
@@ -42,9 +43,9 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *
     const int c0 = tc * 64, p0 = th * 64;
     const uint16_t *src = x + n * (long)C * HW;
     uint16_t *dst = xt + n * (long)C * HW;
-    if constexpr (VEC) {
+    if constexpr (RV == 8) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {   // 64 channels x 8 pixel octets = 512 lanes' worth
+        for (int i = 0; i < 2; ++i) {   // 64 channels x 8 pixel octets
             const int id = t + 256 * i;
             const int c = id >> 3, o = id & 7;
             const bool ok = c0 + c < C && p0 + 8 * o < HW;
@@ -52,7 +53,27 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *
                                : make_uint4(0, 0, 0, 0);
             *reinterpret_cast<uint4 *>(&tile[c][8 * o]) = v;
         }
-        __syncthreads();
+    } else if constexpr (RV == 4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {   // 64 channels x 16 pixel quads
+            const int id = t + 256 * i;
+            const int c = id >> 4, o = id & 15;
+            const bool ok = c0 + c < C && p0 + 4 * o < HW;
+            const uint2 v = ok ? *reinterpret_cast<const uint2 *>(src + (long)(c0 + c) * HW + p0 + 4 * o)
+                               : make_uint2(0, 0);
+            *reinterpret_cast<uint2 *>(&tile[c][4 * o]) = v;
+        }
+    } else {
+        const int px = t & 63;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int c = (t >> 6) + 4 * i;
+            const bool ok = c0 + c < C && p0 + px < HW;
+            tile[c][px] = ok ? src[(long)(c0 + c) * HW + p0 + px] : 0;
+        }
+    }
+    __syncthreads();
+    if constexpr (WV) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {   // 64 pixels x 8 channel octets
             const int id = t + 256 * i;
@@ -67,14 +88,6 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *
             }
         }
     } else {
-        const int px = t & 63;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int c = (t >> 6) + 4 * i;
-            const bool ok = c0 + c < C && p0 + px < HW;
-            tile[c][px] = ok ? src[(long)(c0 + c) * HW + p0 + px] : 0;
-        }
-        __syncthreads();
         const int cc = t & 63;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -288,6 +301,245 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
     }
 }
 
+// Direct-to-LDS variant (64-channel reduction chunks).  Every lane's
+// global_load_lds_dwordx4 writes its 16 bytes straight into LDS, at the
+// wavefront's base plus 16 bytes per lane, so operand tiles never pass through
+// registers: the pipeline can run NST chunks deep with few VGPRs.  A chunk
+// row (one pixel or one filter, 64 channels = 128 bytes = 8 units of 16 bytes)
+// is stored with its units permuted, unit kg at slot kg ^ f(row), with
+// f(row) = (row & 7) ^ ((row >> 3) & 1): the MFMA operand reads (16
+// consecutive rows, one unit each) then hit 16 distinct 16-byte bank groups,
+// and each load instruction still fills 1 KB of LDS contiguously.
+__device__ inline int unit_swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+template <int N>
+__device__ inline void wait_vmcnt()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
+{
+    constexpr int NT = 64 * WPX * WCH;
+    constexpr int KRC = 64;
+    constexpr int TPX = BPX / WPX, TCH = BKC / WCH;     // one wavefront's tile
+    constexpr int BJ = TPX / 32, BI = TCH / 32;         // pixel blocks, channel blocks
+    constexpr int UA = BKC * 8, UB = BPX * 8;           // 16-byte units per stage
+    constexpr int LA = UA / NT, LB = UB / NT;           // load instructions per lane per chunk
+    constexpr int LOADS = LA + LB;
+    static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UB % NT == 0, "tile shape");
+    static_assert(NST >= 2 && NST <= 4, "pipeline depth");
+
+    __shared__ __attribute__((aligned(16))) uint4 smem[NST * (UA + UB)];
+
+    const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
+    const uint16_t *__restrict__ wp = static_cast<const uint16_t *>(a.w);    // [K][R][S][Cg]
+    const int S = S_ ? S_ : a.S;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wpx = wid % WPX, wch = wid / WPX;
+    const int h = lane >> 5, ll = lane & 31;
+    // XCD-aware tile order: the hardware deals work-groups to the 8 XCDs
+    // round-robin, so work-group w runs on XCD w % 8.  Logical tiles are
+    // renumbered so that each XCD gets one contiguous range of them, with the
+    // channel tiles of one pixel tile adjacent: tiles that read the same
+    // input pixels share that XCD's L2.
+    const int T = gridDim.x;
+    const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+    const int L = xcd * (T / 8) + min(xcd, T % 8) + j;
+    const int ktiles = (a.Kg + BKC - 1) / BKC;
+    const int mtiles = (a.M + BPX - 1) / BPX;
+    const int ky = L % ktiles;
+    const int mx = (L / ktiles) % mtiles;
+    const int z = L / (ktiles * mtiles);
+    const int g = z % a.groups;
+    const int split = z / a.groups;
+    const int m0 = mx * BPX;
+    const int k0 = ky * BKC;
+    const int kr_begin = split * a.kr_per_split;
+    const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
+
+    // Operands are read through buffer resources: an offset past the end
+    // (kOutside) makes the hardware range check return zeros, which is how
+    // padding taps, pixels past M and filters past K are loaded.
+    constexpr unsigned kOutside = 0xffffffffu;
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(wp), (short)0, (int)((long)a.K * a.Kred * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(xcl), (short)0, (int)((long)a.N * a.H * a.W * a.C * 2), 0x00020000);
+
+    // Loader: load i of lane tid fills unit u = i*NT + tid of its operand.
+    // Byte offsets of the lane's row at reduction index 0 / tap (0, 0).
+    unsigned aoffs[LA];
+    bool aok[LA];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int u = i * NT + tid;
+        const int row = u >> 3;
+        const int kg = (u & 7) ^ unit_swz(row);
+        const int k = k0 + row;
+        aok[i] = k < a.Kg;
+        aoffs[i] = (unsigned)((((long)g * a.Kg + (aok[i] ? k : 0)) * a.Kred + kg * 8) * 2);
+    }
+    int bih[LB], biw[LB], boffs[LB];
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int u = i * NT + tid;
+        const int row = u >> 3;
+        const int kg = (u & 7) ^ unit_swz(row);
+        const int m = m0 + row;
+        const bool ok = m < a.M;
+        const int mm = ok ? m : 0;
+        const int n = mm / a.PQ;
+        const int pq = mm - n * a.PQ;
+        const int p = pq / a.Q;
+        const int q = pq - p * a.Q;
+        bih[i] = ok ? p * a.stride - a.pad : -(1 << 28);      // never inside the image
+        biw[i] = q * a.stride - a.pad;
+        // element offset of (n, bih, biw, g*Cg + kg*8); negative for a top/left
+        // padding origin, but every tap that passes the bounds test is >= 0
+        boffs[i] = (int)((long)n * a.H * a.W * a.C + ((long)bih[i] * a.W + biw[i]) * a.C +
+                         (long)g * a.Cg + kg * 8);
+    }
+
+    auto issue = [&](int t) {
+        // chunk parameters are uniform: keep them in scalar registers
+        const int kr0 = __builtin_amdgcn_readfirstlane(kr_begin + t * KRC);
+        const int rs = kr0 / a.Cg;                  // the chunk is 64 channels at tap rs
+        const int c0 = kr0 - rs * a.Cg;
+        const int r = rs / S;
+        const int s = rs - r * S;
+        const int delta = (r * a.W + s) * a.C + c0;    // element offset of the tap
+        const int stage = t % NST;
+        uint4 *st = smem + stage * (UA + UB);
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            const unsigned off = aok[i] ? aoffs[i] + 2u * kr0 : kOutside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_void_t *)(st + i * NT + wid * 64), 16,
+                                                     off, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < LB; ++i) {
+            const bool ok = (unsigned)(bih[i] + r) < (unsigned)a.H &&
+                            (unsigned)(biw[i] + s) < (unsigned)a.W;
+            const unsigned off = ok ? 2u * (unsigned)(boffs[i] + delta) : kOutside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_void_t *)(st + UA + i * NT + wid * 64),
+                                                     16, off, 0, 0, 0);
+        }
+    };
+
+    // Operand reads: row offsets (in units) and the permuted slot of unit
+    // 2*ks + h, per 16-wide reduction step ks.
+    const int fl = unit_swz(ll);
+    int aoff[BI], boff[BJ];
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) aoff[bi] = (wch * TCH + bi * 32 + ll) * 8;
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj) boff[bj] = UA + (wpx * TPX + bj * 32 + ll) * 8;
+
+    floatx16 acc[BJ][BI];
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+        for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[bj][bi][v] = 0.f;
+
+    // All operand reads of a chunk are issued before its first MFMA, so LDS
+    // latency overlaps the MFMAs of the earlier reduction steps.
+    auto compute = [&](int t) {
+        const uint4 *st = smem + (t % NST) * (UA + UB);
+        constexpr int KS = KRC / 16;
+        bf16x8 wv[KS][BI], xv[KS][BJ];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int slot = (2 * ks + h) ^ fl;
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi)
+                wv[ks][bi] = *reinterpret_cast<const bf16x8 *>(st + aoff[bi] + slot);
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj)
+                xv[ks][bj] = *reinterpret_cast<const bf16x8 *>(st + boff[bj] + slot);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+                for (int bi = 0; bi < BI; ++bi)
+                    acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
+                                                                         acc[bj][bi], 0, 0, 0);
+    };
+
+    const int nchunks = kr_end > kr_begin ? (kr_end - kr_begin) / KRC : 0;
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t)
+        if (t < nchunks) issue(t);
+    for (int t = 0; t < nchunks; ++t) {
+        // this lane's loads of chunk t are done once at most `ahead` later
+        // chunks' loads are outstanding
+        const int ahead = min(NST - 2, nchunks - 1 - t);
+        if (NST >= 4 && ahead == 2) wait_vmcnt<2 * LOADS>();
+        else if (NST >= 3 && ahead == 1) wait_vmcnt<LOADS>();
+        else wait_vmcnt<0>();
+        // every lane's chunk t is in LDS, and every wavefront is done with chunk t-1
+        asm volatile("s_barrier" ::: "memory");
+        if (t + NST - 1 < nchunks) issue(t + NST - 1);
+        compute(t);
+    }
+
+    // Epilogue: lane l holds channel column l%32 and, per group of 4
+    // registers, 4 consecutive pixels.
+    const bool vec = a.splits == 1 && (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+    const long cstride = a.splits > 1 ? (long)a.M : (long)a.PQ;
+    float *out = a.splits > 1 ? a.ws + (long)split * a.K * a.M : a.y;
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) {
+        const int k = k0 + wch * TCH + bi * 32 + ll;
+        if (k >= a.Kg) continue;
+        const int kg = g * a.Kg + k;
+        const float bv = (a.splits == 1 && a.bias) ? a.bias[kg] : 0.f;
+        const long coff = (long)kg * cstride;
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj) {
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int mb = m0 + wpx * TPX + bj * 32 + 8 * q4 + 4 * h;   // first of 4 pixels
+                float v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float val = acc[bj][bi][4 * q4 + e];
+                    if (a.splits == 1) {
+                        val += bv;
+                        if (a.relu) val = fmaxf(val, 0.f);
+                    }
+                    v4[e] = val;
+                }
+                if (vec && mb + 3 < a.M) {
+                    const int n = mb / a.PQ;
+                    const long off = (long)n * a.K * a.PQ + (mb - n * a.PQ) + coff;
+                    *reinterpret_cast<float4 *>(out + off) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int m = mb + e;
+                        if (m >= a.M) continue;
+                        const int n = m / a.PQ;
+                        const long off = a.splits > 1 ? (long)m + coff
+                                                      : (long)n * a.K * a.PQ + (m - n * a.PQ) + coff;
+                        out[off] = v4[e];
+                    }
+                }
+            }
+        }
+    }
+}
+
 struct TileN {
     int bkc, bpx;
 };
@@ -315,12 +567,91 @@ void launch_krc(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 
 int rs_template(int v) { return (v == 1 || v == 3) ? v : 0; }
 
+// Pixels per global read of the NCHW -> NHWC copy (x may be null: describe).
+int transpose_read_width(int HW, const void *x)
+{
+    const uintptr_t xa = (uintptr_t)x;
+    if (HW % 8 == 0 && xa % 16 == 0) return 8;
+    if (HW % 4 == 0 && xa % 8 == 0) return 4;
+    return 1;
+}
+// Direct-to-LDS tiles: pixels x channels, wavefronts along pixels x channels,
+// pipeline depth.  LDS per work-group = depth * (bpx + bkc) * 128 bytes.
+struct TileD {
+    int bpx, bkc, wpx, wch, nst;
+};
+const TileD kTilesD[] = {
+    {128, 128, 2, 2, 2},   // 64 KB: two work-groups per CU, wavefront tile 64 x 64
+    {128, 64, 2, 2, 2},    // 48 KB: three per CU, wavefront tile 64 x 32
+    {64, 64, 2, 2, 2},     // 32 KB: four per CU, wavefront tile 32 x 32
+};
+
+template <int R_, int S_>
+void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    switch (tile) {
+    case 0: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    }
+}
+
+void launch_dma(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    if (a.R == 1 && a.S == 1)
+        launch_dma_rs<1, 1>(a, tile, grid, st);
+    else if (a.R == 3 && a.S == 3)
+        launch_dma_rs<3, 3>(a, tile, grid, st);
+    else
+        launch_dma_rs<0, 0>(a, tile, grid, st);
+}
+
+
 }  // namespace
 
 bool nhwc_bf16_eligible(const ConvProblem &p) { return p.Cg % 32 == 0; }
 
+// Direct-to-LDS plan.  Measured on ResNet-50's bf16 layers at batch 64:
+// the 128 x 128 tile is fastest while it yields at least 1.5 work-groups per
+// CU; below that, 128 x 64 while it still covers every CU, then 64 x 64.
+// Filters of at most 64 channels take the 64-wide channel tiles.  A launch
+// with fewer than half as many 64 x 64 tiles as CUs splits the reduction.
+static NhwcPlan plan_dma(const ConvProblem &p, int num_cus)
+{
+    NhwcPlan plan{};
+    plan.dma = 1;
+    plan.krc = 64;
+    auto wgs = [&](int t) {
+        return (long)ceil_div(p.M, kTilesD[t].bpx) * ceil_div(p.Kg, kTilesD[t].bkc) * p.groups;
+    };
+    if (p.Kg > 64 && wgs(0) * 2 >= 3L * num_cus)
+        plan.tile = 0;
+    else if (wgs(1) >= num_cus)
+        plan.tile = 1;
+    else
+        plan.tile = 2;
+    const int chunks = p.Kred / 64;
+    int splits = 1;
+    const long tiles = wgs(plan.tile);
+    if (tiles * 2 < num_cus && chunks >= 8) {
+        splits = (int)((num_cus + tiles - 1) / tiles);
+        if (splits > chunks / 4) splits = chunks / 4;
+        const int per = ceil_div(chunks, splits);
+        splits = ceil_div(chunks, per);
+    }
+    plan.splits = splits;
+    plan.kr_per_split = ceil_div(chunks, splits) * 64;
+    plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
+    plan.xcl_bytes = (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
+    return plan;
+}
+
 NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus)
 {
+    // the direct-to-LDS kernel addresses x and w through 32-bit buffer offsets
+    const bool fits = (long)p.N * p.C * p.H * p.W * 2 < (1L << 31) &&
+                      (long)p.K * p.Cg * p.R * p.S * 2 < (1L << 31);
+    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus);
     NhwcPlan plan{};
     plan.krc = p.Cg % 64 == 0 ? 64 : 32;
     plan.tile = 1;
@@ -348,13 +679,22 @@ NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus)
 void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, int len,
                         int *launches)
 {
-    const TileN &t = kTilesN[plan.tile];
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R != S) R = S = 0;
-    const bool vec = (p.H * p.W) % 8 == 0 && p.C % 8 == 0;
-    snprintf(buf, len, "nchw_to_nhwc_bf16_kernel<%s> + igemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s",
-             vec ? "true" : "false", R, S,
-             t.bkc, t.bpx, plan.krc, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    char tname[64];
+    snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d, %s>", transpose_read_width(p.H * p.W, nullptr),
+             p.C % 8 == 0 ? "true" : "false");
+    if (plan.dma) {
+        const TileD &d = kTilesD[plan.tile];
+        snprintf(buf, len, "%s + igemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d>%s", tname, R, S, d.bpx,
+                 d.bkc, d.wpx, d.wch, d.nst,
+                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    } else {
+        const TileN &t = kTilesN[plan.tile];
+        snprintf(buf, len, "%s + igemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s", tname, R, S, t.bkc,
+                 t.bpx, plan.krc,
+                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    }
     *launches = plan.splits > 1 ? 3 : 2;
 }
 
@@ -366,13 +706,17 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     if (e != hipSuccess) return e;
     const int HW = p.H * p.W;
     const int th = ceil_div(HW, 64), tc = ceil_div(p.C, 64);
-    const bool vec = HW % 8 == 0 && p.C % 8 == 0 && ((uintptr_t)x & 15) == 0;
-    if (vec)
-        hipLaunchKernelGGL(nchw_to_nhwc_bf16_kernel<true>, dim3((unsigned)((long)th * tc * p.N)),
-                           dim3(256), 0, st, x, xcl, p.C, HW, th, tc);
+    const int rv = transpose_read_width(HW, x);
+    const bool wv = p.C % 8 == 0;
+    const dim3 tg((unsigned)((long)th * tc * p.N)), tb(256);
+    if (wv && rv == 8)
+        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<8, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+    else if (wv && rv == 4)
+        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<4, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+    else if (wv)
+        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<1, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     else
-        hipLaunchKernelGGL(nchw_to_nhwc_bf16_kernel<false>, dim3((unsigned)((long)th * tc * p.N)),
-                           dim3(256), 0, st, x, xcl, p.C, HW, th, tc);
+        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<1, false>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     ConvArgs a = make_args(p);
@@ -383,9 +727,17 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     a.ws = plan.splits > 1 ? partials : nullptr;
     a.splits = plan.splits;
     a.kr_per_split = plan.kr_per_split;
+    if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+    if (plan.dma) {
+        const TileD &d = kTilesD[plan.tile];
+        const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
+        launch_dma(a, plan.tile, dim3((unsigned)wgs), st);
+        if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
+        if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+        return launch_splitk_reduce(a, st);
+    }
     const TileN &t = kTilesN[plan.tile];
     dim3 grid(ceil_div(p.M, t.bpx), ceil_div(p.Kg, t.bkc), p.groups * plan.splits);
-    if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
     if (plan.krc == 64)
         launch_krc<64>(a, plan.tile, grid, st);
     else

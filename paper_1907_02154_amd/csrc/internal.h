@@ -94,7 +94,8 @@ void describe_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast,
 
 // bf16 through an internal channel-last copy of x (C/groups % 32 == 0).
 struct NhwcPlan {
-    int tile;             // 0: 128 x 128, 1: 64 x 64
+    int dma;              // direct-to-LDS kernel (64-channel chunks), else the register-staged one
+    int tile;             // index into the kernel family's tile table
     int krc;              // reduction chunk (64 or 32 channels at one filter position)
     int splits;
     int kr_per_split;
