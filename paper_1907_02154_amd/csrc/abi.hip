@@ -239,8 +239,8 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
 
 bool krsc_eligible(const Resolved &r)
 {
-    return (r.impl == IMPL_WAVE || r.impl == IMPL_IGEMM_BF16 || r.impl == IMPL_NHWC_BF16) &&
-           r.p.R * r.p.S > 1 && r.p.Cg % 8 == 0;
+    return (r.impl == IMPL_IGEMM_BF16 || r.impl == IMPL_NHWC_BF16) && r.p.R * r.p.S > 1 &&
+           r.p.Cg % 8 == 0;
 }
 
 size_t packed_bytes(const Resolved &r)
@@ -253,7 +253,6 @@ void set_krsc(Resolved &r, const void *packed)
 {
     r.wk = packed;
     r.pack_per_call = false;
-    if (r.impl == IMPL_WAVE) r.wplan.krsc = true;
     if (r.impl == IMPL_IGEMM_BF16) r.plan.krsc = true;
 }
 

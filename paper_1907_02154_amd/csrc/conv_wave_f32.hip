@@ -36,7 +36,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 // (reduction ordered r, s, c with C/groups % 8 == 0), so the 4 taps of a
 // half-block are 4 channels at one filter position: one padding check and
 // one address per half-block.
-template <int R_, int S_, int WAVES, int BJ, bool VA, bool KRSC>
+template <int R_, int S_, int WAVES, int BJ, bool VA, bool KRSC, bool PK>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
@@ -50,18 +50,32 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int h = lane >> 5, ll = lane & 31;
-    const int g = blockIdx.z % a.groups;
-    const int split = blockIdx.z / a.groups;
-    const int m0 = blockIdx.x * (32 * BJ);
-    const int k0 = blockIdx.y * 32;
+    // XCD-aware tile order: the hardware deals work-groups to the 8 XCDs
+    // round-robin (work-group b runs on XCD b % 8), so logical tiles are
+    // renumbered to give each XCD one contiguous range, pixel tiles fastest:
+    // the work-groups that read the same filter rows share an L2.
+    const int mtiles = ceil_div(a.M, 32 * BJ), ktiles = ceil_div(a.Kg, 32);
+    const int T = gridDim.x;
+    const int xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
+    const int L = xcd * (T / 8) + min(xcd, T % 8) + jx;
+    const int mx = L % mtiles;
+    const int ky = (L / mtiles) % ktiles;
+    const int z = L / (mtiles * ktiles);
+    const int g = z % a.groups;
+    const int split = z / a.groups;
+    const int m0 = mx * (32 * BJ);
+    const int k0 = ky * 32;
     const int kr_begin = split * a.kr_per_split;
     const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
     const int nblk = kr_end > kr_begin ? ceil_div(kr_end - kr_begin, 8) : 0;
 
-    // A: this lane's filter row.
+    // A: this lane's filter row, or (PK) its 16-byte slot of the packed
+    // filters: w_pk[g][k/32][kr/8][lane][4] holds W[k0 + l%32][8*blk + 4*h + e],
+    // zero past K and Kred, so a wavefront's A load is 1 KB contiguous.
     const int kA = k0 + ll;
     const bool kvalid = kA < a.Kg;
     const float *wrow = w + ((long)g * a.Kg + (kvalid ? kA : 0)) * a.Kred;
+    const float *wpk = w + (((long)(g * ktiles + ky) * ceil_div(a.Kred, 8) + kr_begin / 8) * 64 + lane) * 4;
 
     // B: this lane's output pixels, one per 32-pixel block.
     int ih0[BJ], iw0[BJ];
@@ -90,7 +104,14 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     auto load = [&](Frag &f, int blk) {
         const int kr0 = kr_begin + 8 * blk + 4 * h;
         const bool live = blk < nblk;
-        if (VA && live && kvalid && kr0 + 4 <= kr_end) {
+        if (PK) {
+            const float4 v = live ? *reinterpret_cast<const float4 *>(wpk + (long)blk * 256)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+            f.av[0] = v.x;
+            f.av[1] = v.y;
+            f.av[2] = v.z;
+            f.av[3] = v.w;
+        } else if (VA && live && kvalid && kr0 + 4 <= kr_end) {
             const float4 v = *reinterpret_cast<const float4 *>(wrow + kr0);
             f.av[0] = v.x;
             f.av[1] = v.y;
@@ -196,23 +217,25 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 }
 
 template <int R_, int S_, int WAVES, int BJ, bool KRSC>
-void launch_va(const ConvArgs &a, bool va, dim3 grid, hipStream_t st)
+void launch_va(const ConvArgs &a, bool va, bool pk, dim3 grid, hipStream_t st)
 {
-    if (va)
-        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC>), grid, dim3(64 * WAVES), 0, st, a);
+    if (pk)
+        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, true>), grid, dim3(64 * WAVES), 0, st, a);
+    else if (va)
+        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
     else
-        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, false, KRSC>), grid, dim3(64 * WAVES), 0, st, a);
+        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, false, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
 }
 
 template <int R_, int S_, bool KRSC>
-void launch_rs(const ConvArgs &a, int waves, int bj, bool va, dim3 grid, hipStream_t st)
+void launch_rs(const ConvArgs &a, int waves, int bj, bool va, bool pk, dim3 grid, hipStream_t st)
 {
     if (waves == 8) {
-        if (bj == 2) launch_va<R_, S_, 8, 2, KRSC>(a, va, grid, st);
-        else launch_va<R_, S_, 8, 1, KRSC>(a, va, grid, st);
+        if (bj == 2) launch_va<R_, S_, 8, 2, KRSC>(a, va, pk, grid, st);
+        else launch_va<R_, S_, 8, 1, KRSC>(a, va, pk, grid, st);
     } else {
-        if (bj == 2) launch_va<R_, S_, 4, 2, KRSC>(a, va, grid, st);
-        else launch_va<R_, S_, 4, 1, KRSC>(a, va, grid, st);
+        if (bj == 2) launch_va<R_, S_, 4, 2, KRSC>(a, va, pk, grid, st);
+        else launch_va<R_, S_, 4, 1, KRSC>(a, va, pk, grid, st);
     }
 }
 
@@ -267,8 +290,9 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R == 0 || S == 0 || R != S) R = S = 0;
     if (plan.krsc && R != 3) R = S = 0;
-    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %s, %s>%s", R, S, plan.waves, plan.bj,
-             plan.va ? "true" : "false", plan.krsc ? "true" : "false",
+    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %s, %s, %s>%s", R, S, plan.waves, plan.bj,
+             (plan.va || plan.pk) ? "true" : "false", plan.krsc ? "true" : "false",
+             plan.pk ? "true" : "false",
              plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     *launches = plan.splits > 1 ? 2 : 1;
 }
@@ -286,22 +310,23 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
     a.splits = plan.splits;
     a.kr_per_split = plan.kr_per_split;
     const bool va = plan.va && (uintptr_t)w % 16 == 0;
-    dim3 grid(ceil_div(p.M, 32 * plan.bj), ceil_div(p.Kg, 32), p.groups * plan.splits);
+    const dim3 grid((unsigned)((long)ceil_div(p.M, 32 * plan.bj) * ceil_div(p.Kg, 32) * p.groups *
+                               plan.splits));
     hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
     if (plan.krsc) {   // filters packed KRSC (R * S > 1)
         if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, true>(a, plan.waves, plan.bj, va, grid, st);
+            launch_rs<3, 3, true>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
         else
-            launch_rs<0, 0, true>(a, plan.waves, plan.bj, va, grid, st);
+            launch_rs<0, 0, true>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
     } else if (p.R == 1 && p.S == 1) {
-        launch_rs<1, 1, false>(a, plan.waves, plan.bj, va, grid, st);
+        launch_rs<1, 1, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
     } else if (p.R == 3 && p.S == 3) {
-        launch_rs<3, 3, false>(a, plan.waves, plan.bj, va, grid, st);
+        launch_rs<3, 3, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
     } else if (p.R == 7 && p.S == 7) {
-        launch_rs<7, 7, false>(a, plan.waves, plan.bj, va, grid, st);
+        launch_rs<7, 7, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
     } else {
-        launch_rs<0, 0, false>(a, plan.waves, plan.bj, va, grid, st);
+        launch_rs<0, 0, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
     }
     e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return e;

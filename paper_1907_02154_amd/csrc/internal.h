@@ -76,6 +76,7 @@ struct WavePlan {
     int kr_per_split;
     size_t ws_bytes;
     bool krsc;          // filters pre-packed [K][R][S][C/groups]
+    bool pk;            // filters pre-packed in the wavefront load order (launch_pack_wave)
 };
 WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, bool w_aligned16);
 hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const float *x,
@@ -159,6 +160,11 @@ size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing
 bool krsc_eligible(const Resolved &r);       // the kernel can read KRSC-packed filters
 size_t packed_bytes(const Resolved &r);      // bytes of the KRSC copy of the filters
 void set_krsc(Resolved &r, const void *packed);  // read filters pre-packed at `packed`
+// Filters in the wave kernel's A-operand order, w_pk[g][ceil(Kg/32)][ceil(Kred/8)][64][4]
+// (reduction order r, s, c when `krsc`, else c, r, s), zero-padded.
+size_t wave_packed_floats(const ConvProblem &p);
+hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, bool krsc,
+                            hipStream_t st);
 hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
                             hipStream_t st);
 int set_hip_error(hipError_t e);   // records e for miconv_last_hip_error, returns MICONV_ERR_HIP

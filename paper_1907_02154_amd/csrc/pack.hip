@@ -25,7 +25,57 @@ __global__ __launch_bounds__(256) void pack_krsc_kernel(const T *__restrict__ sr
     }
 }
 
+// Wave-kernel order: one slot per (group, 32-filter block kb, 8-tap block b,
+// lane l, element e) holding W[kb*32 + l%32][8*b + 4*(l/32) + e], where the
+// reduction index runs over (r, s, c) when `krsc`, else over (c, r, s);
+// zero past K/groups and past C/groups*R*S.
+__global__ __launch_bounds__(256) void pack_wave_kernel(const float *__restrict__ src,
+                                                        float *__restrict__ dst, int Kg, int Cg,
+                                                        int RS, int KB, int NB, int krsc, long total)
+{
+    const int Kred = Cg * RS;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const int e = (int)(i & 3);
+        const int l = (int)((i >> 2) & 63);
+        const long t = i >> 8;                 // (g * KB + kb) * NB + b
+        const int b = (int)(t % NB);
+        const long gk = t / NB;
+        const int kb = (int)(gk % KB);
+        const int g = (int)(gk / KB);
+        const int k = kb * 32 + (l & 31);
+        const int kr = 8 * b + 4 * (l >> 5) + e;
+        float v = 0.f;
+        if (k < Kg && kr < Kred) {
+            const long row = ((long)g * Kg + k) * Kred;
+            if (krsc) {
+                const int rs = kr / Cg, c = kr - rs * Cg;
+                v = src[row + (long)c * RS + rs];
+            } else {
+                v = src[row + kr];
+            }
+        }
+        dst[i] = v;
+    }
+}
+
 }  // namespace
+
+size_t wave_packed_floats(const ConvProblem &p)
+{
+    return (size_t)p.groups * ceil_div(p.Kg, 32) * ceil_div(p.Kred, 8) * 256;
+}
+
+hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, bool krsc,
+                            hipStream_t st)
+{
+    const long total = (long)wave_packed_floats(p);
+    long blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(pack_wave_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, packed, p.Kg,
+                       p.Cg, p.R * p.S, ceil_div(p.Kg, 32), ceil_div(p.Kred, 8), krsc ? 1 : 0, total);
+    return hipGetLastError();
+}
 
 hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
                             hipStream_t st)

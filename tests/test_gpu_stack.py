@@ -182,3 +182,49 @@ def test_stack_resnet_b1_random_within_gate(oracle_lib):
         e = np.max(np.abs(got.astype(np.float64) - want)) / np.max(np.abs(want))
         assert e <= 1e-4, (l.name, e)
     s.close()
+
+
+RAGGED = [  # (N, C, H, W, K, R, S, stride, pad, groups): small layers that take the wave kernel
+    (1, 24, 11, 11, 40, 3, 3, 1, 1, 1),    # K % 32 != 0, N*P*Q % 32 != 0
+    (1, 5, 9, 7, 7, 1, 1, 1, 0, 1),        # reduction of 5 taps (< one 8-tap block)
+    (1, 16, 13, 13, 33, 3, 3, 2, 1, 1),    # stride 2, K = 33
+    (1, 32, 10, 10, 48, 3, 3, 1, 1, 2),    # two groups of 16 -> 24
+    (2, 12, 8, 8, 20, 5, 5, 1, 2, 1),      # 5x5, two images, reduction 300
+    (1, 64, 7, 7, 96, 1, 1, 1, 0, 1),
+    (1, 512, 7, 7, 64, 3, 3, 1, 1, 1),     # long reduction: split across work-groups
+]
+
+
+def test_stack_wave_packed_filters_ragged(oracle_lib):
+    """Wave-kernel layers in a stack read filters packed once in the kernel's
+    operand order (zero-padded blocks of 32 filters x 8 taps): exact against
+    the oracle on small integers for ragged filter counts, reductions, groups
+    and strides, eager and replayed."""
+    ops, refs = [], []
+    for i, (N, C, H, W, K, R, S, st, pad, g) in enumerate(RAGGED):
+        x = wl.small_ints((N, C, H, W), -3, 3, 900 + i)
+        w = wl.small_ints((K, C // g, R, S), -3, 3, 950 + i)
+        b = wl.small_ints((K,), -8, 8, 990 + i)
+        P, Q = miconv.out_dims(H, W, R, S, st, pad)
+        y = torch.full((N, K, P, Q), float("nan"), device="cuda")
+        ops.append((miconv.OP_CONV_F32, torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(),
+                    torch.from_numpy(b).cuda(), y, st, pad, g, i % 2 == 0))
+        refs.append((x, w, b, st, pad, g, i % 2 == 0))
+    s = miconv.Stack(ops)
+    names = [s.describe(j) for j in range(len(ops))]
+    assert all(n.startswith("igemm_wave_f32_kernel") for n in names), names
+    assert all(n.split(" + ")[0].endswith(", true>") for n in names), names   # packed filters
+    assert any("splitk_reduce" in n for n in names), names
+    for replay in (False, True):
+        if replay:
+            for o in ops:
+                o[4].fill_(float("nan"))
+            s.capture(2, timed=False)
+            s.replay()
+        else:
+            s.launch()
+        torch.cuda.synchronize()
+        for o, (x, w, b, st, pad, g, relu), shape in zip(ops, refs, RAGGED):
+            want = oracle_lib.conv2d(x, w, b, st, pad, g, relu)
+            np.testing.assert_array_equal(o[4].cpu().numpy(), want, err_msg=f"{shape} replay={replay}")
+    s.close()
