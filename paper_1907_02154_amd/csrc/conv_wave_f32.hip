@@ -243,45 +243,46 @@ int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 
 }  // namespace
 
-// Work-group tile 32 channels x 32*BJ pixels; a work-group runs on one CU, so
-// the parallelism across CUs is the number of work-groups, and the
-// wavefronts of a work-group (4 or 8, splitting the tile's reduction) only
-// fill that CU's SIMDs and hide latency.  The reduction is also split across
-// work-groups when a simple cost model says the extra reduce launch (about
-// 4.5 us on this part) is repaid: MFMA-bound time per wavefront =
-// blocks * BJ * 4 MFMAs * 64 cycles, in rounds of ceil(work-groups / CUs).
+// Work-group tile 32 channels x 32*BJ pixels; a work-group runs on one CU,
+// so the parallelism across CUs is the number of work-groups, and its
+// wavefronts (4 or 8, splitting the tile's reduction) fill that CU's SIMDs.
+// The plan minimises a latency model fitted to batch-1 ResNet-50 layers on
+// this part: a fixed ~4.5 us per launch (dispatch, first loads, epilogue),
+// then per round of work-groups over the CUs, each wavefront's MFMA time
+// (blocks * BJ * 4 MFMAs * 64 cycles) plus ~1.2 us per dependent round of
+// loads (kDepth blocks in flight), plus ~2.5 us for a split-K reduce launch.
 WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, bool w_aligned16)
 {
-    WavePlan plan{};
-    plan.bj = p.M >= 2048 ? 2 : 1;
-    plan.va = p.Kred % 4 == 0 && w_aligned16;
-    const long tiles = (long)ceil_div(p.M, 32 * plan.bj) * ceil_div(p.Kg, 32) * p.groups;
+    WavePlan best{};
+    best.va = p.Kred % 4 == 0 && w_aligned16;
     const int blocks = ceil_div(p.Kred, 8);
-    plan.waves = blocks >= 64 ? 8 : 4;
-    const double us_per_block = plan.bj * 4 * 64 / 2400.0;   // one SIMD, 2.4 GHz
-    auto cost = [&](int splits) {
-        const long wgs = tiles * splits;
-        const long rounds = (wgs + num_cus - 1) / num_cus;
-        const double per_wg = (double)ceil_div(blocks, splits) * us_per_block;  // 4 SIMDs share it
-        return rounds * per_wg / 4.0 * (plan.waves >= 4 ? 1.0 : 4.0 / plan.waves) +
-               (splits > 1 ? 4.5 : 0.0);
-    };
-    int best = 1;
-    double best_cost = cost(1);
-    const int max_splits = blocks / (2 * plan.waves);   // at least 2 blocks per wavefront
-    for (int sp = 2; sp <= max_splits && tiles * sp <= 4L * num_cus; ++sp) {
-        const double c = cost(sp);
-        if (c < best_cost) {
-            best_cost = c;
-            best = sp;
+    double best_us = 1e30;
+    for (int bj = 1; bj <= 2; ++bj) {
+        if (bj == 2 && p.M < 64) continue;
+        const long tiles = (long)ceil_div(p.M, 32 * bj) * ceil_div(p.Kg, 32) * p.groups;
+        const int depth = bj == 2 ? 2 : 4;
+        for (int waves : {8, 4}) {
+            for (int sp = 1; sp <= 16; ++sp) {
+                const int per = ceil_div(blocks, sp);
+                if (sp > 1 && per < 2 * waves) break;           // at least 2 blocks per wavefront
+                if (ceil_div(blocks, per) != sp) continue;
+                const long wgs = tiles * sp;
+                const long rounds = (wgs + num_cus - 1) / num_cus;
+                const int bw = ceil_div(per, waves);             // blocks per wavefront
+                const double us = 4.5 + rounds * (bw * bj * 4 * 64 / 2400.0 + ceil_div(bw, depth) * 1.2) +
+                                  (sp > 1 ? 2.5 : 0.0);
+                if (us < best_us - 1e-9) {
+                    best_us = us;
+                    best.bj = bj;
+                    best.waves = waves;
+                    best.splits = sp;
+                    best.kr_per_split = per * 8;
+                }
+            }
         }
     }
-    const int per = ceil_div(blocks, best);
-    const int splits = ceil_div(blocks, per);
-    plan.splits = splits;
-    plan.kr_per_split = per * 8;
-    plan.ws_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
-    return plan;
+    best.ws_bytes = best.splits > 1 ? (size_t)best.splits * p.K * p.M * sizeof(float) : 0;
+    return best;
 }
 
 void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, int len,
