@@ -8,12 +8,15 @@ region holds only conv kernels.  The default workload is the ResNet-50 v1
 conv stack at batch 1 in fp32 (53 convs); --config picks another.
 
 The passes run through the library's stack executor: W eager passes, then
-one HIP graph holding exactly K passes (after one untimed replay of it).
+the timed region, one HIP graph holding exactly K passes (after one untimed
+replay of it), then K eager passes whose kernel launches carry start/end
+events that the runtime stamps with each kernel's execution interval.
 
-Prints one JSON line with the conv TFLOP/s of the step, ms per image, the
-roofline of the dominant kernel (the kernel with the largest summed time,
-timed live with HIP events around each of its launches on the launch
-stream) and the CPU oracle timed on a bounded sample of the same stack.
+Prints one JSON line with the conv TFLOP/s of the step (from the timed
+region), ms per image, the roofline of the dominant kernel (the kernel with
+the largest summed execution time; its traffic comes from the committed
+counter summary profiles/traffic.txt when that matches the kernel's source)
+and the CPU oracle timed on a bounded sample of the same stack.
 """
 from __future__ import annotations
 
@@ -34,6 +37,27 @@ PEAK_BF16_MFMA_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
 
 
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` (read + written, calibrated against a
+    plain copy) from the committed counter summary profiles/traffic.txt, or
+    None when it has no line for this kernel or the kernel's source changed
+    since the counters were taken."""
+    from paper_1907_02154_amd.traffic import source_sha
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            parts = line.rstrip("\n").split("\t")
+            if parts[0] == kernel and len(parts) >= 4:
+                if parts[1] != source_sha(kernel):
+                    return None
+                return int(parts[2]) + int(parts[3])
+    return None
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -44,6 +68,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget for the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--layers", action="store_true", help="also print a per-layer table to stderr")
+    ap.add_argument("--profile-passes", type=int, default=0, metavar="N",
+                    help="instead: run N eager passes of the stack and exit (for counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="instead: 4 device-to-device copies of 256 MiB (counter calibration)")
     ap.add_argument("--dw-sweep", type=int, default=0, metavar="N",
                     help="instead: HBM bandwidth of the depthwise kernel on the 13 MobileNet "
                          "depthwise shapes at batch N (e.g. 256)")
@@ -133,6 +161,16 @@ def main():
     if args.dw_sweep:
         dw_sweep(args)
         return
+    if args.copy_calibration:
+        import torch
+        torch.cuda.set_device(0)
+        src = torch.zeros(64 << 20, device="cuda")     # 256 MiB of fp32
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print("copy calibration: 4 copies of 268435456 bytes", flush=True)
+        return
 
     import torch
     from paper_1907_02154_amd import miconv
@@ -178,6 +216,12 @@ def main():
     launch_info = [stack.launch_info(j) for j in range(n_launch)]
 
     stream = torch.cuda.current_stream()
+    if args.profile_passes:
+        for _ in range(args.profile_passes):
+            stack.launch(stream)
+        torch.cuda.synchronize()
+        print(f"{args.profile_passes} eager passes of {wk.name}", flush=True)
+        return
     for _ in range(args.warmup):          # eager passes: planning, workspace, caches
         stack.launch(stream)
     torch.cuda.synchronize()
@@ -199,19 +243,11 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / K
 
-    # Per-kernel durations: the same K passes captured with an event before
-    # every kernel launch and after the last one (event nodes add a few
-    # microseconds per launch, so this replay is not the timed region).
-    stack.capture(K, timed=True, stream=stream)
-    stack.replay(stream)
+    # Per-kernel durations: K eager passes in which every kernel launch carries
+    # a start and an end event that the runtime stamps with the kernel's own
+    # execution interval (the figure a kernel-trace profiler reports).
+    stack.launch_timed(K, stream)
     torch.cuda.synchronize()
-    u0 = torch.cuda.Event(enable_timing=True)
-    u1 = torch.cuda.Event(enable_timing=True)
-    u0.record(stream)
-    stack.replay(stream)
-    u1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step_evented = u0.elapsed_time(u1) / K
     per_launch_ms = stack.times()
     stack.close()
 
@@ -257,7 +293,7 @@ def main():
         achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                     frac=round(achieved / peak, 4))
-    roof.update(traffic=None, kernel=dom_name, launches_per_step=dom["launches"],
+    roof.update(traffic=measured_traffic(dom_name), kernel=dom_name, launches_per_step=dom["launches"],
                 avg_launch_us=round(avg_launch_us, 3),
                 share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
 
@@ -312,9 +348,9 @@ def main():
         "config": {"workload": wk.name, "convs": len(layers), "batch": wk.layers[0].N,
                    "gflop_per_step": round(step_flops / 1e9, 4), "device": torch.cuda.get_device_name(0),
                    "wall_s_timed": round(wall, 4),
-                   "timing": "value: one HIP graph of K passes between two events; roofline: per-launch "
-                             "durations from a replay of the same passes with an event before every launch",
-                   "ms_per_step_with_launch_events": round(ms_per_step_evented, 5)},
+                   "timing": "value: one HIP graph of K passes between two events; roofline: kernel "
+                             "execution times stamped by the runtime on K eager passes",
+                   "kernel_ms_per_step": round(float(launch_ms.sum()), 5)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

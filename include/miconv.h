@@ -163,9 +163,10 @@ int miconv_stack_launch_info(const miconv_stack *s, int launch, char *buf, int b
 /* Enqueue every layer once, in order, on `stream`. */
 int miconv_stack_launch(miconv_stack *s, void *stream);
 
-/* Enqueue `steps` passes eagerly with an event before every kernel launch and
- * after the last one (read them with miconv_stack_times once the stream is done).
- * Drops any captured graph. */
+/* Enqueue `steps` passes eagerly, every kernel launch carrying a start and an
+ * end event that the runtime stamps with that kernel's own execution interval
+ * (read them with miconv_stack_times once the stream is done).  Drops any
+ * captured graph. */
 int miconv_stack_launch_timed(miconv_stack *s, int steps, void *stream);
 
 /* Capture `steps` consecutive passes into one HIP graph, replacing any
@@ -178,10 +179,10 @@ int miconv_stack_capture(miconv_stack *s, int steps, int timed, void *stream);
 /* Launch the captured graph on `stream` (MICONV_ERR_UNSUPPORTED if none). */
 int miconv_stack_replay(miconv_stack *s, void *stream);
 
-/* After a timed replay (or miconv_stack_launch_timed) has completed:
- * ms[k*L + j] = time from the event before launch j of pass k to the next
- * event (L = miconv_stack_launches).  capacity is the length of ms, at least
- * steps*L. */
+/* After a timed replay has completed: ms[k*L + j] = time from the event
+ * before launch j of pass k to the next event (L = miconv_stack_launches);
+ * after miconv_stack_launch_timed: the execution time of launch j of pass k.
+ * capacity is the length of ms, at least steps*L. */
 int miconv_stack_times(const miconv_stack *s, float *ms, long capacity);
 
 /* Free the graph, events, workspace and the executor (NULL is a no-op). */

@@ -18,6 +18,8 @@
 
 namespace miconv {
 
+thread_local hipEvent_t t_launch_start = nullptr, t_launch_stop = nullptr;
+
 ConvArgs make_args(const ConvProblem &p)
 {
     ConvArgs a{};

@@ -63,7 +63,7 @@ hipError_t launch_direct(const ConvProblem &p, const T *x, const T *w, const flo
     const long total = (long)p.N * p.K * p.P * p.Q;
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;  // grid-stride loop covers the rest
-    hipLaunchKernelGGL(conv_direct_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, a);
+    launch_kernel(conv_direct_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

@@ -314,9 +314,9 @@ template <int R_, int S_, bool F, bool VA, bool KRSC>
 void launch_tile(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     if (tile == 0)
-        hipLaunchKernelGGL((igemm_bf16_kernel<R_, S_, 128, 128, kKrcB, F, VA, KRSC>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_bf16_kernel<R_, S_, 128, 128, kKrcB, F, VA, KRSC>), grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL((igemm_bf16_kernel<R_, S_, 64, 64, kKrcB, F, VA, KRSC>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_bf16_kernel<R_, S_, 64, 64, kKrcB, F, VA, KRSC>), grid, dim3(256), 0, st, a);
 }
 
 template <int R_, int S_, bool KRSC>

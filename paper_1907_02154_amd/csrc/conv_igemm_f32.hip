@@ -250,13 +250,13 @@ hipError_t launch_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     switch (tile) {
     case 0:
-        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 128, 128, 2, 2, 16>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_f32_kernel<R_, S_, 128, 128, 2, 2, 16>), grid, dim3(256), 0, st, a);
         break;
     case 1:
-        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 64, 64, 2, 2, 32>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_f32_kernel<R_, S_, 64, 64, 2, 2, 32>), grid, dim3(256), 0, st, a);
         break;
     default:
-        hipLaunchKernelGGL((igemm_f32_kernel<R_, S_, 32, 64, 1, 2, 64>), grid, dim3(128), 0, st, a);
+        launch_kernel((igemm_f32_kernel<R_, S_, 32, 64, 1, 2, 64>), grid, dim3(128), 0, st, a);
         break;
     }
     return hipGetLastError();
@@ -336,7 +336,7 @@ hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
     a.vec4 = a.N == 1 && total % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0;
     long blocks = (a.vec4 ? total / 4 : total + 255) / 256 + 1;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);
+    launch_kernel(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

@@ -549,9 +549,9 @@ template <int R_, int S_, int KRC>
 void launch_tile(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     if (tile == 0)
-        hipLaunchKernelGGL((igemm_bf16_nhwc_kernel<R_, S_, 128, 128, KRC>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_bf16_nhwc_kernel<R_, S_, 128, 128, KRC>), grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL((igemm_bf16_nhwc_kernel<R_, S_, 64, 64, KRC>), grid, dim3(256), 0, st, a);
+        launch_kernel((igemm_bf16_nhwc_kernel<R_, S_, 64, 64, KRC>), grid, dim3(256), 0, st, a);
 }
 
 template <int KRC>
@@ -590,9 +590,9 @@ template <int R_, int S_>
 void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     switch (tile) {
-    case 0: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
-    case 1: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
     }
 }
 
@@ -710,13 +710,13 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     const bool wv = p.C % 8 == 0;
     const dim3 tg((unsigned)((long)th * tc * p.N)), tb(256);
     if (wv && rv == 8)
-        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<8, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+        launch_kernel((nchw_to_nhwc_bf16_kernel<8, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     else if (wv && rv == 4)
-        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<4, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+        launch_kernel((nchw_to_nhwc_bf16_kernel<4, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     else if (wv)
-        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<1, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+        launch_kernel((nchw_to_nhwc_bf16_kernel<1, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     else
-        hipLaunchKernelGGL((nchw_to_nhwc_bf16_kernel<1, false>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+        launch_kernel((nchw_to_nhwc_bf16_kernel<1, false>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     ConvArgs a = make_args(p);

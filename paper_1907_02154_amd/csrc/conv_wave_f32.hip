@@ -220,11 +220,11 @@ template <int R_, int S_, int WAVES, int BJ, bool KRSC>
 void launch_va(const ConvArgs &a, bool va, bool pk, dim3 grid, hipStream_t st)
 {
     if (pk)
-        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, true>), grid, dim3(64 * WAVES), 0, st, a);
+        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, true>), grid, dim3(64 * WAVES), 0, st, a);
     else if (va)
-        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
+        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
     else
-        hipLaunchKernelGGL((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, false, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
+        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, false, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
 }
 
 template <int R_, int S_, bool KRSC>

@@ -539,7 +539,7 @@ hipError_t launch_fast(DwArgs a, hipStream_t st)
     const long gpw = 64 / a.G;
     const long waves = (a.items + gpw - 1) / gpw;
     const long blocks = (waves + 3) / 4;
-    hipLaunchKernelGGL((dw3x3_kernel<ST, V>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+    launch_kernel((dw3x3_kernel<ST, V>), dim3((unsigned)blocks), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
@@ -631,7 +631,7 @@ hipError_t launch_dwconv_f32(const ConvProblem &p, const float *x, const float *
         const dim3 g((unsigned)grid), b(256);
 #define MICONV_DW_RUN(HH, ST)                                                         \
     if (p.H == HH && p.stride == ST) {                                               \
-        hipLaunchKernelGGL((dw_run_kernel<HH, HH, ST>), g, b, 0, st, a);             \
+        launch_kernel((dw_run_kernel<HH, HH, ST>), g, b, 0, st, a);             \
         return hipGetLastError();                                                    \
     }
         MICONV_DW_RUN(7, 1) MICONV_DW_RUN(7, 2) MICONV_DW_RUN(14, 1) MICONV_DW_RUN(14, 2)
@@ -653,9 +653,9 @@ hipError_t launch_dwconv_f32(const ConvProblem &p, const float *x, const float *
         a.relu = p.relu;
         const dim3 g((unsigned)(4L * cus)), b(256);
         if (p.stride == 1)
-            hipLaunchKernelGGL((dw_band_kernel<112, 112, 1, kBandRows1>), g, b, 0, st, a);
+            launch_kernel((dw_band_kernel<112, 112, 1, kBandRows1>), g, b, 0, st, a);
         else
-            hipLaunchKernelGGL((dw_band_kernel<112, 112, 2, kBandRows2>), g, b, 0, st, a);
+            launch_kernel((dw_band_kernel<112, 112, 2, kBandRows2>), g, b, 0, st, a);
         return hipGetLastError();
     }
     const int V = dw_vector_width(p, x, y);
@@ -698,7 +698,7 @@ hipError_t launch_dwconv_f32(const ConvProblem &p, const float *x, const float *
     const long total = planes * p.P * p.Q;
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(dw_generic_kernel, dim3((unsigned)blocks), dim3(256), 0, st, x, w, bias, y,
+    launch_kernel(dw_generic_kernel, dim3((unsigned)blocks), dim3(256), 0, st, x, w, bias, y,
                        p.C, p.H, p.W, p.R, p.S, p.stride, p.pad, p.P, p.Q, total, p.relu);
     return hipGetLastError();
 }

@@ -95,7 +95,7 @@ hipError_t launch_maxpool_f32(int N, int C, int H, int W, int R, int S, int stri
                               int P, int Q, const float *x, float *y, hipStream_t st)
 {
     const long total = (long)N * C * P * Q;
-    hipLaunchKernelGGL(maxpool_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, y, H, W, R, S,
+    launch_kernel(maxpool_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, y, H, W, R, S,
                        stride, pad, P, Q, total);
     return hipGetLastError();
 }
@@ -107,10 +107,10 @@ hipError_t launch_add_act_f32(long count, const float *a, const float *b, float 
     const bool vec = (count % 4 == 0) && ((uintptr_t)a % 16 == 0) && ((uintptr_t)b % 16 == 0) &&
                      ((uintptr_t)y % 16 == 0);
     if (vec) {
-        hipLaunchKernelGGL(add_act_vec4_kernel, dim3(grid_for(count / 4)), dim3(256), 0, st,
+        launch_kernel(add_act_vec4_kernel, dim3(grid_for(count / 4)), dim3(256), 0, st,
                            (const float4 *)a, (const float4 *)b, (float4 *)y, count / 4, relu);
     } else {
-        hipLaunchKernelGGL(add_act_kernel, dim3(grid_for(count)), dim3(256), 0, st, a, b, y, count,
+        launch_kernel(add_act_kernel, dim3(grid_for(count)), dim3(256), 0, st, a, b, y, count,
                            relu);
     }
     return hipGetLastError();
@@ -119,7 +119,7 @@ hipError_t launch_add_act_f32(long count, const float *a, const float *b, float 
 hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t st)
 {
     if (count == 0) return hipSuccess;
-    hipLaunchKernelGGL(cast_bf16_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, y, count);
+    launch_kernel(cast_bf16_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, y, count);
     return hipGetLastError();
 }
 

@@ -2,10 +2,28 @@
 // Nothing here is part of the public ABI (include/miconv.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace miconv {
+
+// Kernel timing: a caller that wants the execution time of the next kernel
+// launch on this thread sets these two events; launch_kernel hands them to
+// the runtime, which stamps them with the kernel's start and end, and clears
+// them.  Unset (the normal case), launch_kernel is a plain launch.
+extern thread_local hipEvent_t t_launch_start, t_launch_stop;
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t st, Args... args)
+{
+    hipEvent_t a = t_launch_start, b = t_launch_stop;
+    t_launch_start = t_launch_stop = nullptr;
+    if (a)
+        hipExtLaunchKernelGGL(kernel, grid, block, shm, st, a, b, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+}
 
 // One conv problem, already validated, with the derived extents filled in.
 struct ConvProblem {

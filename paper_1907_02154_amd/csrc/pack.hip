@@ -72,7 +72,7 @@ hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed,
     const long total = (long)wave_packed_floats(p);
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(pack_wave_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, packed, p.Kg,
+    launch_kernel(pack_wave_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, packed, p.Kg,
                        p.Cg, p.R * p.S, ceil_div(p.Kg, 32), ceil_div(p.Kred, 8), krsc ? 1 : 0, total);
     return hipGetLastError();
 }
@@ -84,11 +84,11 @@ hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, s
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     if (elem == sizeof(float))
-        hipLaunchKernelGGL(pack_krsc_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
+        launch_kernel(pack_krsc_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
                            static_cast<const float *>(w), static_cast<float *>(packed), p.K, p.Cg,
                            p.R * p.S, total);
     else
-        hipLaunchKernelGGL(pack_krsc_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
+        launch_kernel(pack_krsc_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
                            static_cast<const uint16_t *>(w), static_cast<uint16_t *>(packed), p.K,
                            p.Cg, p.R * p.S, total);
     return hipGetLastError();

@@ -24,7 +24,8 @@ struct miconv_stack {
     std::vector<int> launch_layer;          // layer of every kernel launch of one pass
     std::vector<std::string> launch_name;   // its kernel name
     float *partials = nullptr;              // split-K workspace shared by all layers
-    std::vector<void *> packed;             // KRSC copies of filters, packed at create
+    std::vector<void *> packed;             // packed copies of filters, made at create
+    bool stamps = false;                    // events are (start, end) pairs per launch
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
     std::vector<hipEvent_t> events;         // steps * launches + 1 when timed
@@ -45,6 +46,7 @@ void drop_graph(miconv_stack *s)
     s->exec = nullptr;
     s->graph = nullptr;
     s->events.clear();
+    s->stamps = false;
     s->steps = 0;
 }
 
@@ -77,11 +79,22 @@ hipError_t record_next(void *ctx, hipStream_t st)
     return record(*c->next++, st);
 }
 
-// One pass over every layer; with `ev`, an event before every kernel launch.
-hipError_t enqueue_all(miconv_stack *s, hipStream_t st, hipEvent_t *ev)
+// Eager kernel timing: the next launch gets the next two events as its
+// start/end stamps (the runtime writes the kernel's own execution interval).
+hipError_t arm_next(void *ctx, hipStream_t)
+{
+    EventCursor *c = static_cast<EventCursor *>(ctx);
+    t_launch_start = *c->next++;
+    t_launch_stop = *c->next++;
+    return hipSuccess;
+}
+
+// One pass over every layer; with `ev`, an event before every kernel launch
+// (or, `stamps`, a start and an end event stamped on every kernel launch).
+hipError_t enqueue_all(miconv_stack *s, hipStream_t st, hipEvent_t *ev, bool stamps = false)
 {
     EventCursor cur{ev};
-    LaunchHook hook{record_next, &cur};
+    LaunchHook hook{stamps ? arm_next : record_next, &cur};
     for (size_t i = 0; i < s->layers.size(); ++i) {
         hipError_t e = enqueue(s->layers[i], s->partials, st, ev ? &hook : nullptr);
         if (e != hipSuccess) return e;
@@ -89,9 +102,11 @@ hipError_t enqueue_all(miconv_stack *s, hipStream_t st, hipEvent_t *ev)
     return hipSuccess;
 }
 
-int make_events(miconv_stack *s, int steps)
+int make_events(miconv_stack *s, int steps, bool stamps = false)
 {
-    s->events.resize((size_t)steps * s->launch_layer.size() + 1, nullptr);
+    const size_t per = s->launch_layer.size();
+    s->events.resize(stamps ? 2 * (size_t)steps * per : (size_t)steps * per + 1, nullptr);
+    s->stamps = stamps;
     for (auto &ev : s->events) {
         hipError_t e = hipEventCreate(&ev);
         if (e != hipSuccess) {
@@ -262,13 +277,13 @@ int miconv_stack_launch_timed(miconv_stack *s, int steps, void *stream)
     if (steps < 1) return MICONV_ERR_SHAPE;
     drop_graph(s);
     const size_t n = s->launch_layer.size();
-    int rc = make_events(s, steps);
+    int rc = make_events(s, steps, true);
     if (rc != MICONV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e = hipSuccess;
     for (int k = 0; k < steps && e == hipSuccess; ++k)
-        e = enqueue_all(s, st, &s->events[(size_t)k * n]);
-    if (e == hipSuccess) e = hipEventRecord(s->events.back(), st);
+        e = enqueue_all(s, st, &s->events[2 * (size_t)k * n], true);
+    t_launch_start = t_launch_stop = nullptr;
     if (e != hipSuccess) {
         drop_graph(s);
         return set_hip_error(e);
@@ -307,10 +322,11 @@ int miconv_stack_times(const miconv_stack *s, float *ms, long capacity)
 {
     if (!s || !ms) return MICONV_ERR_NULL;
     if (s->events.empty()) return MICONV_ERR_UNSUPPORTED;
-    const size_t total = s->events.size() - 1;
+    const size_t total = s->stamps ? s->events.size() / 2 : s->events.size() - 1;
     if ((size_t)capacity < total) return MICONV_ERR_SHAPE;
     for (size_t i = 0; i < total; ++i) {
-        hipError_t e = hipEventElapsedTime(&ms[i], s->events[i], s->events[i + 1]);
+        hipError_t e = s->stamps ? hipEventElapsedTime(&ms[i], s->events[2 * i], s->events[2 * i + 1])
+                                 : hipEventElapsedTime(&ms[i], s->events[i], s->events[i + 1]);
         if (e != hipSuccess) return set_hip_error(e);
     }
     return MICONV_OK;
