@@ -293,7 +293,9 @@ def main():
         achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                     frac=round(achieved / peak, 4))
-    roof.update(traffic=measured_traffic(dom_name), kernel=dom_name, launches_per_step=dom["launches"],
+    roof.update(traffic=measured_traffic(dom_name),
+                algorithmic_bytes_per_launch=round(dom["bytes"] / dom["launches"]),
+                kernel=dom_name, launches_per_step=dom["launches"],
                 avg_launch_us=round(avg_launch_us, 3),
                 share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
 
