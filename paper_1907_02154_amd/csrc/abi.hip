@@ -191,6 +191,8 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
     } else if (kind == OP_DENSE_BF16) {
         if (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8))
             r.impl = IMPL_DIRECT;
+        else if (algo == MICONV_ALGO_AUTO && stem_bf16_eligible(r.p, y))
+            r.impl = IMPL_STEM_BF16;
         else if (algo != MICONV_ALGO_IGEMM && nhwc_bf16_eligible(r.p))
             r.impl = IMPL_NHWC_BF16;
         else
@@ -234,6 +236,8 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
     } else if (r.impl == IMPL_NHWC_BF16) {
         r.nplan = plan_nhwc_bf16(r.p, cu_count());
         r.pack_per_call = krsc_eligible(r);   // 1x1 filters are already in KRSC order
+    } else if (r.impl == IMPL_STEM_BF16) {
+        r.pack_per_call = true;               // filters in tap-pair order
     }
     *out = r;
     return MICONV_OK;
@@ -247,6 +251,7 @@ bool krsc_eligible(const Resolved &r)
 
 size_t packed_bytes(const Resolved &r)
 {
+    if (r.impl == IMPL_STEM_BF16) return stem_packed_bytes(r.p);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     return (size_t)r.p.K * r.p.Cg * r.p.R * r.p.S * elem;
 }
@@ -260,6 +265,16 @@ void set_krsc(Resolved &r, const void *packed)
 
 static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
+// The filter copy a layer's kernel reads: tap-pair order for the bf16 stem,
+// KRSC otherwise.
+hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
+{
+    if (r.impl == IMPL_STEM_BF16)
+        return launch_pack_stem(r.p, static_cast<const uint16_t *>(r.w), static_cast<uint16_t *>(dst), st);
+    const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
+    return launch_pack_krsc(r.p, r.w, dst, elem, st);
+}
+
 hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHook *hook)
 {
     Resolved r = r0;
@@ -270,8 +285,7 @@ hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHo
             hipError_t e = hook->before_launch(hook->ctx, st);
             if (e != hipSuccess) return e;
         }
-        const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
-        hipError_t e = launch_pack_krsc(r.p, r.w, cursor, elem, st);
+        hipError_t e = launch_pack(r, cursor, st);
         if (e != hipSuccess) return e;
         r.wk = cursor;
         cursor += round256(packed_bytes(r));
@@ -289,6 +303,14 @@ hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHo
     const float *xf = static_cast<const float *>(r.x), *wf = static_cast<const float *>(wkern);
     if (r.impl == IMPL_IGEMM) return launch_igemm_f32(r.p, r.plan, xf, wf, r.bias, r.y, ws, st, hook);
     if (r.impl == IMPL_WAVE) return launch_wave_f32(r.p, r.wplan, xf, wf, r.bias, r.y, ws, st, hook);
+    if (r.impl == IMPL_STEM_BF16) {
+        if (hook) {
+            hipError_t e = hook->before_launch(hook->ctx, st);
+            if (e != hipSuccess) return e;
+        }
+        return launch_stem_bf16(r.p, static_cast<const uint16_t *>(r.x),
+                                static_cast<const uint16_t *>(wkern), r.bias, r.y, st);
+    }
     if (r.impl == IMPL_IGEMM_BF16)
         return launch_igemm_bf16(r.p, r.plan, r.bfast, r.bva, static_cast<const uint16_t *>(r.x),
                                  static_cast<const uint16_t *>(wkern), r.bias, r.y, ws, st, hook);
@@ -321,8 +343,10 @@ size_t workspace_bytes(const Resolved &r)
 void describe(const Resolved &r, char *buf, int len, int *launches)
 {
     if (r.pack_per_call) {
-        const int n = snprintf(buf, len, "pack_krsc_kernel<%s> + ",
-                               r.kind == OP_DENSE_BF16 ? "unsigned short" : "float");
+        const int n = r.impl == IMPL_STEM_BF16
+                          ? snprintf(buf, len, "pack_stem_kernel + ")
+                          : snprintf(buf, len, "pack_krsc_kernel<%s> + ",
+                                     r.kind == OP_DENSE_BF16 ? "unsigned short" : "float");
         if (n > 0 && n < len) {
             describe_kernel(r, buf + n, len - n, launches);
             *launches += 1;
@@ -340,6 +364,7 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     case IMPL_WAVE: describe_wave_f32(r.p, r.wplan, buf, len, launches); break;
     case IMPL_IGEMM_BF16: describe_igemm_bf16(r.p, r.plan, r.bfast, r.bva, buf, len, launches); break;
     case IMPL_NHWC_BF16: describe_nhwc_bf16(r.p, r.nplan, buf, len, launches); break;
+    case IMPL_STEM_BF16: describe_stem_bf16(buf, len, launches); break;
     default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;
     }
 }

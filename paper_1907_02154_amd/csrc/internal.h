@@ -129,6 +129,15 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
 void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, int len,
                         int *launches);
 
+// bf16 7x7/2 stem on <= 4 channels with 112 output columns (filters packed by
+// launch_pack_stem into [K][28 tap pairs][8]).
+bool stem_bf16_eligible(const ConvProblem &p, const void *y);
+size_t stem_packed_bytes(const ConvProblem &p);
+hipError_t launch_pack_stem(const ConvProblem &p, const uint16_t *w, uint16_t *packed, hipStream_t st);
+hipError_t launch_stem_bf16(const ConvProblem &p, const uint16_t *x, const uint16_t *wpacked,
+                            const float *bias, float *y, hipStream_t st);
+void describe_stem_bf16(char *buf, int len, int *launches);
+
 // Sums split partials [splits][K][M] in split order into y (+ bias, activation).
 hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st);
 
@@ -153,7 +162,8 @@ enum Impl {
     IMPL_DW = 2,
     IMPL_WAVE = 3,
     IMPL_IGEMM_BF16 = 4,
-    IMPL_NHWC_BF16 = 5
+    IMPL_NHWC_BF16 = 5,
+    IMPL_STEM_BF16 = 6
 };
 struct Resolved {
     ConvProblem p;
@@ -176,6 +186,7 @@ hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHoo
 void describe(const Resolved &r, char *buf, int len, int *launches);
 size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + split partials
 bool krsc_eligible(const Resolved &r);       // the kernel can read KRSC-packed filters
+hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st);   // the copy its kernel reads
 size_t packed_bytes(const Resolved &r);      // bytes of the KRSC copy of the filters
 void set_krsc(Resolved &r, const void *packed);  // read filters pre-packed at `packed`
 // Filters in the wave kernel's A-operand order, w_pk[g][ceil(Kg/32)][ceil(Kred/8)][64][4]

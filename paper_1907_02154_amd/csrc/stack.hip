@@ -191,13 +191,13 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
             r.wk = pk;
             r.wplan.pk = true;
             r.wplan.krsc = krsc;
-        } else if (krsc_eligible(r)) {
-            // Pre-computing: pack the filters once, KRSC, for every replay.
+        } else if (r.pack_per_call || krsc_eligible(r)) {
+            // Pre-computing: pack the filters once, in the layout the kernel
+            // reads, for every replay.
             void *pk = nullptr;
-            const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
             e = hipMalloc(&pk, packed_bytes(r));
             if (e == hipSuccess) s->packed.push_back(pk);
-            if (e == hipSuccess) e = launch_pack_krsc(r.p, r.w, pk, elem, nullptr);
+            if (e == hipSuccess) e = launch_pack(r, pk, nullptr);
             if (e != hipSuccess) {
                 miconv_stack_destroy(s);
                 return set_hip_error(e);

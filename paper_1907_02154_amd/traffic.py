@@ -46,6 +46,8 @@ SOURCES = {
     "conv_direct_kernel": "conv_direct.hip",
     "pack_krsc_kernel": "pack.hip",
     "pack_wave_kernel": "pack.hip",
+    "stem7_bf16_kernel": "conv_stem_bf16.hip",
+    "pack_stem_kernel": "conv_stem_bf16.hip",
 }
 
 

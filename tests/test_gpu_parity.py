@@ -155,6 +155,32 @@ def test_bf16_small_int_bitwise(oracle_lib, case, algo):
     np.testing.assert_array_equal(y.cpu().numpy(), ref)
 
 
+STEM_CASES = [  # (N, C, H, W, K): 7x7 stride-2 pad-3 stems with 112 output columns
+    (2, 3, 224, 224, 64),     # ResNet's stem
+    (1, 1, 224, 224, 32),     # one channel, half a filter tile
+    (1, 4, 223, 223, 96),     # odd width (scalar row loads), two filter tiles, the second partial
+]
+
+
+@pytest.mark.parametrize("case", STEM_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_bf16_stem_small_int_bitwise(oracle_lib, case):
+    """The dedicated bf16 stem kernel (tap-pair reduction order, packed
+    filters per call) against the oracle on small integers, with and without
+    ReLU and bias."""
+    N, C, H, W, K = case
+    assert miconv.conv2d_describe(N, C, H, W, K, 7, 7, 2, 3, 1, "bf16")[0].endswith("stem7_bf16_kernel")
+    seed = 3500 + sum(case)
+    x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
+    w = wl.to_bf16_bits(ints((K, C, 7, 7), -4, 4, seed + 1))
+    b = ints((K,), -8, 8, seed + 2)
+    for relu, bias in ((True, b), (False, None)):
+        ref = oracle_lib.conv2d_bf16(x, w, bias, 2, 3, 1, relu)
+        y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), None if bias is None else dev(bias), 2, 3, 1,
+                          relu)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"{case} relu={relu}")
+
+
 def _layers(config):
     """Unique layer shapes of a config with the index of their first use."""
     seen, out = set(), []
