@@ -234,7 +234,7 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
             r.pack_per_call = true;
         }
     } else if (r.impl == IMPL_NHWC_BF16) {
-        r.nplan = plan_nhwc_bf16(r.p, cu_count());
+        r.nplan = plan_nhwc_bf16(r.p, cu_count(), x);
         r.pack_per_call = krsc_eligible(r);   // 1x1 filters are already in KRSC order
     } else if (r.impl == IMPL_STEM_BF16) {
         r.pack_per_call = true;               // filters in tap-pair order

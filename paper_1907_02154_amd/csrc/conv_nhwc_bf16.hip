@@ -319,8 +319,19 @@ __device__ inline void wait_vmcnt()
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 
-template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST>
+// NCHWB (1x1, stride 1, H*W % 8 == 0, 128-pixel tiles): the pixel operand is
+// read from the NCHW input itself, no channel-last copy.  A chunk's pixel tile
+// is staged as 64 channel rows of 128 pixels (16 units of 8 pixels, unit s of
+// row c stored at s ^ 4*(c & 3)), and each MFMA fragment (8 channels of one
+// pixel per lane) is assembled by two ds_read_b64_tr_b16: in every group of 16
+// lanes, lane 4e+t points at 4 pixels of channel row e and lane i receives
+// pixel i of the 4 rows.  The permuted units put the 4 rows of one read in 4
+// different 64-byte bank groups.
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, bool NCHWB>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
 {
     constexpr int NT = 64 * WPX * WCH;
@@ -332,6 +343,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
     constexpr int LOADS = LA + LB;
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UB % NT == 0, "tile shape");
     static_assert(NST >= 2 && NST <= 4, "pipeline depth");
+    static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1), "NCHW pixel operand: 1x1, 128-pixel tiles");
 
     __shared__ __attribute__((aligned(16))) uint4 smem[NST * (UA + UB)];
 
@@ -390,6 +402,19 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
         const int u = i * NT + tid;
+        if constexpr (NCHWB) {
+            // unit u: channel row c = u / 16 of the chunk, 8 pixels at unit s
+            const int c = u >> 4;
+            const int sl = (u & 15) ^ (4 * (c & 3));
+            const int m = m0 + 8 * sl;
+            const bool ok = m < a.M;
+            const int mm = ok ? m : 0;
+            const int n = mm / a.HW;
+            bih[i] = ok ? 0 : -(1 << 28);               // 1x1: only the pixel range test
+            biw[i] = 0;
+            boffs[i] = (int)(((long)n * a.C + (long)g * a.Cg + c) * a.HW + (mm - n * a.HW));
+            continue;
+        }
         const int row = u >> 3;
         const int kg = (u & 7) ^ unit_swz(row);
         const int m = m0 + row;
@@ -425,9 +450,15 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
-            const bool ok = (unsigned)(bih[i] + r) < (unsigned)a.H &&
-                            (unsigned)(biw[i] + s) < (unsigned)a.W;
-            const unsigned off = ok ? 2u * (unsigned)(boffs[i] + delta) : kOutside;
+            bool ok;
+            unsigned off;
+            if constexpr (NCHWB) {
+                ok = bih[i] == 0;
+                off = ok ? 2u * (unsigned)(boffs[i] + c0 * a.HW) : kOutside;
+            } else {
+                ok = (unsigned)(bih[i] + r) < (unsigned)a.H && (unsigned)(biw[i] + s) < (unsigned)a.W;
+                off = ok ? 2u * (unsigned)(boffs[i] + delta) : kOutside;
+            }
             __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_void_t *)(st + UA + i * NT + wid * 64),
                                                      16, off, 0, 0, 0);
         }
@@ -463,8 +494,22 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
             for (int bi = 0; bi < BI; ++bi)
                 wv[ks][bi] = *reinterpret_cast<const bf16x8 *>(st + aoff[bi] + slot);
 #pragma unroll
-            for (int bj = 0; bj < BJ; ++bj)
-                xv[ks][bj] = *reinterpret_cast<const bf16x8 *>(st + boff[bj] + slot);
+            for (int bj = 0; bj < BJ; ++bj) {
+                if constexpr (NCHWB) {
+                    // rows kb+e and kb+4+e of the chunk, pixels n0 + 4t .. n0 + 4t + 3
+                    const int kb = 16 * ks + 8 * (lane >> 5) + ((lane >> 2) & 3);
+                    const int px = wpx * TPX + bj * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+                    const char *base = reinterpret_cast<const char *>(st + UA);
+                    const int o1 = (kb * 16 + ((px >> 3) ^ (4 * (kb & 3)))) * 16 + (px & 7) * 2;
+                    const int o2 = ((kb + 4) * 16 + ((px >> 3) ^ (4 * (kb & 3)))) * 16 + (px & 7) * 2;
+                    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(base + o1));
+                    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(base + o2));
+                    const v8i16 both = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    xv[ks][bj] = __builtin_bit_cast(bf16x8, both);
+                } else {
+                    xv[ks][bj] = *reinterpret_cast<const bf16x8 *>(st + boff[bj] + slot);
+                }
+            }
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -590,10 +635,18 @@ template <int R_, int S_>
 void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     switch (tile) {
-    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
-    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
-    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a); break;
+    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
+    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
+    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
     }
+}
+
+void launch_dma_nchw(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+{
+    if (tile == 0)
+        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
+    else
+        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
 }
 
 void launch_dma(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
@@ -616,7 +669,7 @@ bool nhwc_bf16_eligible(const ConvProblem &p) { return p.Cg % 32 == 0; }
 // CU; below that, 128 x 64 while it still covers every CU, then 64 x 64.
 // Filters of at most 64 channels take the 64-wide channel tiles.  A launch
 // with fewer than half as many 64 x 64 tiles as CUs splits the reduction.
-static NhwcPlan plan_dma(const ConvProblem &p, int num_cus)
+static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
 {
     NhwcPlan plan{};
     plan.dma = 1;
@@ -642,16 +695,19 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus)
     plan.splits = splits;
     plan.kr_per_split = ceil_div(chunks, splits) * 64;
     plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
-    plan.xcl_bytes = (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
+    // 1x1 stride-1 layers with 8-pixel rows read x in NCHW directly
+    plan.nchwb = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && (p.H * p.W) % 8 == 0 &&
+                 plan.tile <= 1 && (uintptr_t)x % 16 == 0;
+    plan.xcl_bytes = plan.nchwb ? 0 : (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
     return plan;
 }
 
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus)
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x)
 {
     // the direct-to-LDS kernel addresses x and w through 32-bit buffer offsets
     const bool fits = (long)p.N * p.C * p.H * p.W * 2 < (1L << 31) &&
                       (long)p.K * p.Cg * p.R * p.S * 2 < (1L << 31);
-    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus);
+    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus, x);
     NhwcPlan plan{};
     plan.krc = p.Cg % 64 == 0 ? 64 : 32;
     plan.tile = 1;
@@ -686,9 +742,11 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
              p.C % 8 == 0 ? "true" : "false");
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
-        snprintf(buf, len, "%s + igemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d>%s", tname, R, S, d.bpx,
-                 d.bkc, d.wpx, d.wch, d.nst,
-                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s>%s",
+                 plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
+                 plan.nchwb ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+        *launches = (plan.nchwb ? 1 : 2) + (plan.splits > 1 ? 1 : 0);
+        return;
     } else {
         const TileN &t = kTilesN[plan.tile];
         snprintf(buf, len, "%s + igemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s", tname, R, S, t.bkc,
@@ -702,7 +760,25 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
                             const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
                             float *partials, hipStream_t st, const LaunchHook *hook)
 {
-    hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
+    hipError_t e = hipSuccess;
+    if (plan.dma && plan.nchwb) {
+        ConvArgs a = make_args(p);
+        a.x = x;
+        a.w = w_krsc;
+        a.bias = bias;
+        a.y = y;
+        a.ws = plan.splits > 1 ? partials : nullptr;
+        a.splits = plan.splits;
+        a.kr_per_split = plan.kr_per_split;
+        const TileD &d = kTilesD[plan.tile];
+        const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
+        if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+        launch_dma_nchw(a, plan.tile, dim3((unsigned)wgs), st);
+        if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
+        if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+        return launch_splitk_reduce(a, st);
+    }
+    e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
     const int HW = p.H * p.W;
     const int th = ceil_div(HW, 64), tc = ceil_div(p.C, 64);

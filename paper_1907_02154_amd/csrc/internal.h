@@ -114,6 +114,7 @@ void describe_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast,
 // bf16 through an internal channel-last copy of x (C/groups % 32 == 0).
 struct NhwcPlan {
     int dma;              // direct-to-LDS kernel (64-channel chunks), else the register-staged one
+    bool nchwb;           // (dma, 1x1 stride 1) pixel operand read from NCHW x: no channel-last copy
     int tile;             // index into the kernel family's tile table
     int krc;              // reduction chunk (64 or 32 channels at one filter position)
     int splits;
@@ -122,7 +123,7 @@ struct NhwcPlan {
     size_t xcl_bytes;     // the channel-last copy of x
 };
 bool nhwc_bf16_eligible(const ConvProblem &p);
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus);
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x);
 hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const uint16_t *x,
                             const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
                             float *partials, hipStream_t st, const LaunchHook *hook = nullptr);

@@ -155,6 +155,31 @@ def test_bf16_small_int_bitwise(oracle_lib, case, algo):
     np.testing.assert_array_equal(y.cpu().numpy(), ref)
 
 
+NCHW_1X1_CASES = [  # (N, C, H, W, K, groups): 1x1 stride-1 layers whose pixel operand comes from NCHW x
+    (3, 64, 56, 56, 520, 1),     # image boundaries inside pixel tiles, ragged M and K (128 x 64 tiles)
+    (4, 64, 56, 56, 512, 1),     # 128 x 128 tiles
+    (2, 192, 64, 64, 256, 1),    # three reduction chunks
+    (8, 128, 64, 64, 256, 2),    # two groups of 64 channels
+]
+
+
+@pytest.mark.parametrize("case", NCHW_1X1_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_bf16_1x1_nchw_operand_small_int_bitwise(oracle_lib, case):
+    """bf16 1x1 layers that skip the channel-last copy (pixel operand read from
+    NCHW x through LDS transpose reads) against the oracle on small integers."""
+    N, C, H, W, K, g = case
+    name = miconv.conv2d_describe(N, C, H, W, K, 1, 1, 1, 0, g, "bf16")[0]
+    assert "nchw_to_nhwc" not in name and name.endswith(", true>"), name
+    seed = 3700 + sum(case)
+    x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
+    w = wl.to_bf16_bits(ints((K, C // g, 1, 1), -4, 4, seed + 1))
+    b = ints((K,), -8, 8, seed + 2)
+    ref = oracle_lib.conv2d_bf16(x, w, b, 1, 0, g, True)
+    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), 1, 0, g, True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=str(case))
+
+
 STEM_CASES = [  # (N, C, H, W, K): 7x7 stride-2 pad-3 stems with 112 output columns
     (2, 3, 224, 224, 64),     # ResNet's stem
     (1, 1, 224, 224, 32),     # one channel, half a filter tile
