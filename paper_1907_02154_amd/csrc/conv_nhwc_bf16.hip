@@ -345,7 +345,9 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
     static_assert(NST >= 2 && NST <= 4, "pipeline depth");
     static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1), "NCHW pixel operand: 1x1, 128-pixel tiles");
 
-    __shared__ __attribute__((aligned(16))) uint4 smem[NST * (UA + UB)];
+    constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
+    constexpr int SMEM = NST * (UA + UB) > BKC * OP / 4 ? NST * (UA + UB) : BKC * OP / 4;
+    __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];
 
     const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
     const uint16_t *__restrict__ wp = static_cast<const uint16_t *>(a.w);    // [K][R][S][Cg]
@@ -538,23 +540,22 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         compute(t);
     }
 
-    // Epilogue: lane l holds channel column l%32 and, per group of 4
-    // registers, 4 consecutive pixels.
-    const bool vec = a.splits == 1 && (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
-    const long cstride = a.splits > 1 ? (long)a.M : (long)a.PQ;
-    float *out = a.splits > 1 ? a.ws + (long)split * a.K * a.M : a.y;
+    // Epilogue through LDS: the tile (BKC channels x BPX pixels, fp32, bias and
+    // activation applied) is laid out channel-major in the shared buffer, free
+    // once every wavefront has passed the barrier, then each channel row is
+    // written out with contiguous 16-byte stores (a lane's own accumulators
+    // would give 32 scattered 32-byte pieces per store instruction).
+    __syncthreads();
+    float *ot = reinterpret_cast<float *>(smem);
 #pragma unroll
     for (int bi = 0; bi < BI; ++bi) {
-        const int k = k0 + wch * TCH + bi * 32 + ll;
-        if (k >= a.Kg) continue;
-        const int kg = g * a.Kg + k;
-        const float bv = (a.splits == 1 && a.bias) ? a.bias[kg] : 0.f;
-        const long coff = (long)kg * cstride;
+        const int kl = wch * TCH + bi * 32 + ll;
+        const int k = k0 + kl;
+        const float bv = (a.splits == 1 && a.bias && k < a.Kg) ? a.bias[g * a.Kg + k] : 0.f;
 #pragma unroll
         for (int bj = 0; bj < BJ; ++bj) {
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
-                const int mb = m0 + wpx * TPX + bj * 32 + 8 * q4 + 4 * h;   // first of 4 pixels
                 float v4[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -565,21 +566,36 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
                     }
                     v4[e] = val;
                 }
-                if (vec && mb + 3 < a.M) {
-                    const int n = mb / a.PQ;
-                    const long off = (long)n * a.K * a.PQ + (mb - n * a.PQ) + coff;
-                    *reinterpret_cast<float4 *>(out + off) = make_float4(v4[0], v4[1], v4[2], v4[3]);
-                } else {
+                const int pl = wpx * TPX + bj * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<float4 *>(ot + kl * OP + pl) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+            }
+        }
+    }
+    __syncthreads();
+    const bool split_out = a.splits > 1;
+    float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
+    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
+    constexpr int C4 = BPX / 4;
+    for (int idx = tid; idx < BKC * C4; idx += NT) {
+        const int kl = idx / C4, c4 = idx - kl * C4;
+        const int k = k0 + kl;
+        const int m = m0 + 4 * c4;
+        if (k >= a.Kg || m >= a.M) continue;
+        const int kg = g * a.Kg + k;
+        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
+        const float ve[4] = {v.x, v.y, v.z, v.w};
+        if (vec && m + 3 < a.M) {
+            const int n = split_out ? 0 : m / a.PQ;
+            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
+            *reinterpret_cast<float4 *>(out + off) = v;
+        } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int m = mb + e;
-                        if (m >= a.M) continue;
-                        const int n = m / a.PQ;
-                        const long off = a.splits > 1 ? (long)m + coff
-                                                      : (long)n * a.K * a.PQ + (m - n * a.PQ) + coff;
-                        out[off] = v4[e];
-                    }
-                }
+            for (int e = 0; e < 4; ++e) {
+                const int mm = m + e;
+                if (mm >= a.M) break;
+                const int n = split_out ? 0 : mm / a.PQ;
+                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
+                out[off] = ve[e];
             }
         }
     }
