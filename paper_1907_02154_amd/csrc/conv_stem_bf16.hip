@@ -22,8 +22,8 @@
 //    of 16 bytes, so 16 consecutive filter rows also hit distinct banks.
 // A work-group computes 4 output rows (448 pixels = 14 blocks of 32) x 64
 // filters with 7 wavefronts, each 2 pixel blocks x 2 filter blocks of
-// v_mfma_f32_32x32x16_bf16 with pixels as the A operand, so every lane stores
-// 4 consecutive output pixels of one filter as one 16-byte write.
+// v_mfma_f32_32x32x16_bf16 with filters as the A operand and pixels as B, so
+// each store instruction writes runs of 32 consecutive output pixels.
 #include "internal.h"
 
 #include <cstdio>
@@ -138,30 +138,26 @@ __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
         for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int f = 0; f < 2; ++f)
-                acc[b][f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[b], wv[f], acc[b][f], 0, 0, 0);
+                acc[b][f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[f], xv[b], acc[b][f], 0, 0, 0);
     }
 
-    // 4. epilogue: register v of lane l = pixel 8*(v/4) + 4*h + v%4 of the block,
-    // filter l%32 of the filter block; 4 consecutive pixels per store
+    // 4. epilogue: filters are the MFMA rows and pixels its columns, so register
+    // v of lane l is filter 8*(v/4) + 4*h + v%4 of the filter block and pixel
+    // l%32 of the pixel block: each store instruction writes 32 consecutive
+    // pixels (128 bytes) of two filter planes.
     const long plane = (long)a.P * kQ;
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
-        const int k = k0 + f * 32 + ll;
-        if (k >= a.K) continue;
-        const float bv = a.bias ? a.bias[k] : 0.f;
-        float *yk = a.y + ((long)n * a.K + k) * plane + (long)p0 * kQ;
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int v = 0; v < 16; ++v) {
+            const int k = k0 + f * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (k >= a.K) continue;
+            const float bv = a.bias ? a.bias[k] : 0.f;
+            float *yk = a.y + ((long)n * a.K + k) * plane + (long)p0 * kQ;
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int m = 32 * (2 * wave + b) + 8 * q4 + 4 * h;
-                float v4[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float v = acc[b][f][4 * q4 + e] + bv;
-                    v4[e] = a.relu ? fmaxf(v, 0.f) : v;
-                }
-                *reinterpret_cast<float4 *>(yk + m) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+            for (int b = 0; b < 2; ++b) {
+                const float val = acc[b][f][v] + bv;
+                yk[32 * (2 * wave + b) + ll] = a.relu ? fmaxf(val, 0.f) : val;
             }
         }
     }
