@@ -215,19 +215,26 @@ struct DwRunShape {
     static constexpr int HW = H_ * W_;
     static constexpr int PQ = P * Q;
     static constexpr int G0 = (W_ + 1 + 3) / 4 * 4;                     // gap before plane 0
-    static constexpr int PP = (HW + W_ + 1 + 3) / 4 * 4;               // plane pitch (plane + gap)
+    // Stride-1 planes up to 14x14 take whole output columns as work items
+    // (item = plane * Q + column), so a wavefront's LDS reads of one input row
+    // sit at plane * PP + column: with PP = Q (mod 64 banks) they are 64
+    // consecutive banks, conflict-free.  Other shapes pad the pitch to 4.
+    static constexpr bool WHOLE = ST == 1 && P <= 14;
+    static constexpr int PP_MIN = HW + W_ + 1;
+    static constexpr int PP = WHOLE ? PP_MIN + (((Q - PP_MIN) % 64) + 64) % 64 : (PP_MIN + 3) / 4 * 4;
+    static constexpr int PUTV = HW % 4 == 0 ? (PP % 4 == 0 ? 4 : (PP % 2 == 0 ? 2 : 1)) : 1;
     static constexpr bool RIGHT_MASK = (Q - 1) * ST + 1 >= W_;         // a right tap can leave the image
     // float4 per lane staged per run (odd planes scatter element-wise and
     // take more registers, so they stage less)
     static constexpr int STAGE4 = HW % 4 == 0 ? 7 : 5;
     static constexpr int STAGE_FLOATS = STAGE4 * 4 * 256;
-    static constexpr int MAX_PB_LDS = (kRunLds - G0) / (PP + kTapStride);
+    static constexpr int MAX_PB_LDS = (kRunLds - G0 - 3) / (PP + kTapStride);   // + taps, 16-byte aligned
     static constexpr int MAX_PB = STAGE_FLOATS / HW < MAX_PB_LDS ? STAGE_FLOATS / HW : MAX_PB_LDS;
     static constexpr int NW = (MAX_PB * kTapStride + 255) / 256;       // tap words staged per lane
     // A lane's work item is a column of RG output rows of one plane: the
     // (RG-1)*ST+3 input rows it reads feed all RG outputs, so each input
     // element is read from LDS about once per item instead of 9 times.
-    static constexpr int RG = P % 7 == 0 ? 7 : P;
+    static constexpr int RG = WHOLE ? P : (P % 7 == 0 ? 7 : P);
     static constexpr int NG = P / RG;                                  // row groups per plane
     static constexpr int IPP = NG * Q;                                 // items per plane
     static_assert(P % RG == 0, "row groups tile the plane");
@@ -261,7 +268,7 @@ __global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
     using S = DwRunShape<H_, W_, ST>;
     __shared__ __attribute__((aligned(16))) float lds[kRunLds];
     const int tid = threadIdx.x;
-    float *taps = lds + S::G0 + a.PB * S::PP;      // 16-byte aligned: G0 and PP are multiples of 4
+    float *taps = lds + ((S::G0 + a.PB * S::PP + 3) & ~3);      // 16-byte aligned
 
     // The gaps are written here once and never again: runs only write plane slots.
     for (int i = tid; i < kRunLds / 4; i += 256)
@@ -309,10 +316,15 @@ __global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
             const int j4 = tid + i * 256;
             if (j4 < c4) {
                 const int j = 4 * j4;
-                if constexpr (S::HW % 4 == 0) {
+                if constexpr (S::PUTV == 4) {
                     const int pl = j / S::HW;
                     *reinterpret_cast<float4 *>(lds + S::G0 + pl * S::PP + (j - pl * S::HW)) =
                         stage[i];
+                } else if constexpr (S::PUTV == 2) {
+                    const int pl = j / S::HW;
+                    float2 *d = reinterpret_cast<float2 *>(lds + S::G0 + pl * S::PP + (j - pl * S::HW));
+                    d[0] = make_float2(stage[i].x, stage[i].y);
+                    d[1] = make_float2(stage[i].z, stage[i].w);
                 } else {
                     // a vector may cross into the next plane (at most once: HW >= 4)
                     const float e[4] = {stage[i].x, stage[i].y, stage[i].z, stage[i].w};
