@@ -211,11 +211,11 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         return MICONV_ERR_UNSUPPORTED;
     }
     if (r.impl == IMPL_IGEMM) {
-        // Small GEMM extents (too few 128x128 output tiles to fill the chip) go
+        // Small GEMM extents (fewer than 1.5 128x128 output tiles per CU) go
         // to the wave-direct kernel, unless the caller forced the tiled one.
         const int cus = cu_count();
         const long big_tiles = (long)ceil_div(r.p.M, 128) * ceil_div(r.p.Kg, 128) * r.p.groups;
-        if (algo != MICONV_ALGO_IGEMM && big_tiles < 2L * cus) {
+        if (algo != MICONV_ALGO_IGEMM && 2 * big_tiles < 3L * cus) {
             r.impl = IMPL_WAVE;
             r.wplan = plan_wave_f32(r.p, cus, (uintptr_t)w % 16 == 0);
         } else {
