@@ -44,6 +44,8 @@ ConvArgs make_args(const ConvProblem &p)
     a.splits = 1;
     a.kr_per_split = p.Kred;
     a.relu = p.relu;
+    a.dv_pq = make_fastdiv(p.P * p.Q);
+    a.dv_q = make_fastdiv(p.Q);
     return a;
 }
 
@@ -215,14 +217,17 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         // to the wave-direct kernel, unless the caller forced the tiled one.
         const int cus = cu_count();
         const long big_tiles = (long)ceil_div(r.p.M, 128) * ceil_div(r.p.Kg, 128) * r.p.groups;
-        if (algo != MICONV_ALGO_IGEMM && 2 * big_tiles < 3L * cus) {
+        if (algo != MICONV_ALGO_IGEMM && 2 * big_tiles < 3L * cus && wave_fits(r.p)) {
             r.impl = IMPL_WAVE;
-            r.wplan = plan_wave_f32(r.p, cus, (uintptr_t)w % 16 == 0);
+            r.wplan = plan_wave_f32(r.p, cus);
+            r.pack_per_call = true;   // filters in the wavefront load order
         } else {
             r.plan = plan_igemm_f32(r.p, cus);
         }
     } else if (r.impl == IMPL_WAVE) {
-        r.wplan = plan_wave_f32(r.p, cu_count(), (uintptr_t)w % 16 == 0);
+        if (!wave_fits(r.p)) return MICONV_ERR_UNSUPPORTED;
+        r.wplan = plan_wave_f32(r.p, cu_count());
+        r.pack_per_call = true;
     } else if (r.impl == IMPL_IGEMM_BF16) {
         r.plan = plan_igemm_bf16(r.p, cu_count());
         r.bfast = bf16_fast_1x1(r.p, x);
@@ -252,6 +257,7 @@ bool krsc_eligible(const Resolved &r)
 size_t packed_bytes(const Resolved &r)
 {
     if (r.impl == IMPL_STEM_BF16) return stem_packed_bytes(r.p);
+    if (r.impl == IMPL_WAVE) return wave_packed_floats(r.p) * sizeof(float);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     return (size_t)r.p.K * r.p.Cg * r.p.R * r.p.S * elem;
 }
@@ -266,11 +272,14 @@ void set_krsc(Resolved &r, const void *packed)
 static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
 // The filter copy a layer's kernel reads: tap-pair order for the bf16 stem,
-// KRSC otherwise.
+// the wavefront load order for the wave kernel, KRSC otherwise.
 hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
 {
     if (r.impl == IMPL_STEM_BF16)
         return launch_pack_stem(r.p, static_cast<const uint16_t *>(r.w), static_cast<uint16_t *>(dst), st);
+    if (r.impl == IMPL_WAVE)
+        return launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(dst), r.wplan.krsc,
+                                st);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     return launch_pack_krsc(r.p, r.w, dst, elem, st);
 }
@@ -343,9 +352,9 @@ size_t workspace_bytes(const Resolved &r)
 void describe(const Resolved &r, char *buf, int len, int *launches)
 {
     if (r.pack_per_call) {
-        const int n = r.impl == IMPL_STEM_BF16
-                          ? snprintf(buf, len, "pack_stem_kernel + ")
-                          : snprintf(buf, len, "pack_krsc_kernel<%s> + ",
+        const int n = r.impl == IMPL_STEM_BF16 ? snprintf(buf, len, "pack_stem_kernel + ")
+                      : r.impl == IMPL_WAVE    ? snprintf(buf, len, "pack_wave_kernel + ")
+                                               : snprintf(buf, len, "pack_krsc_kernel<%s> + ",
                                      r.kind == OP_DENSE_BF16 ? "unsigned short" : "float");
         if (n > 0 && n < len) {
             describe_kernel(r, buf + n, len - n, launches);

@@ -30,21 +30,46 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// ok ? off : out, as one v_cndmask.  Written as a plain select, the compiler
+// turns each guarded load into two branches with a load on each side.
+__device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigned out)
+{
+    unsigned r;
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(out), "v"(off), "s"(__builtin_amdgcn_ballot_w64(ok)));
+    return r;
+}
 
-// BJ = 32-pixel blocks per wavefront tile; VA = the filter row length allows
-// 16-byte loads (Kred % 4 == 0); KRSC = filters pre-packed [K][R][S][C/groups]
-// (reduction ordered r, s, c with C/groups % 8 == 0), so the 4 taps of a
-// half-block are 4 channels at one filter position: one padding check and
-// one address per half-block.
-template <int R_, int S_, int WAVES, int BJ, bool VA, bool KRSC, bool PK>
+
+// BJ = 32-pixel blocks per wavefront tile; KRSC = the reduction is ordered
+// (r, s, c) with C/groups % 8 == 0, so the 4 taps of a half-block are 4
+// channels at one filter position: one padding check and one address per
+// half-block.  Filters are always read pre-packed (pack_wave_kernel):
+// w_pk[g][k/32][kr/8][lane][4] holds W[k0 + l%32][8*blk + 4*h + e], zero past
+// K and Kred, so a wavefront's A load is 1 KB contiguous.
+//
+// Both operands are read through buffer resources.  A tap outside the image,
+// a pixel past M, a block past the split and a tap past the reduction get the
+// offset kOut, which the hardware range check turns into a zero: the loads
+// need no branches, which keeps the executed code short.  At batch 1 a
+// launch runs a few hundred instructions per wavefront from a cold
+// instruction cache, so code size is a first-order cost here.
+template <int R_, int S_, int WAVES, int BJ, bool KRSC>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
-    const float *__restrict__ x = static_cast<const float *>(a.x);
-    const float *__restrict__ w = static_cast<const float *>(a.w);
+    // Offsets at or past 2^31 bytes are out of range: the x and packed filter
+    // buffers are smaller than that (checked by the planner), and adding a
+    // channel stride to kOut stays below 2^32.
+    constexpr unsigned kOut = 0x80000000u;
     const int R = R_ ? R_ : a.R;
     const int S = S_ ? S_ : a.S;
     const int RS = R * S;
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void *>(a.x), (short)0, (int)((long)a.N * a.C * a.HW * 4), 0x00020000);
+    const int kblocks = ceil_div(a.Kred, 8);
+    const unsigned ktiles = ceil_div(a.Kg, 32);
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void *>(a.w), (short)0, (int)((long)a.groups * ktiles * kblocks * 1024), 0x00020000);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -54,89 +79,110 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     // round-robin (work-group b runs on XCD b % 8), so logical tiles are
     // renumbered to give each XCD one contiguous range, pixel tiles fastest:
     // the work-groups that read the same filter rows share an L2.
-    const int mtiles = ceil_div(a.M, 32 * BJ), ktiles = ceil_div(a.Kg, 32);
-    const int T = gridDim.x;
-    const int xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
-    const int L = xcd * (T / 8) + min(xcd, T % 8) + jx;
-    const int mx = L % mtiles;
-    const int ky = (L / mtiles) % ktiles;
-    const int z = L / (mtiles * ktiles);
-    const int g = z % a.groups;
-    const int split = z / a.groups;
+    const unsigned mtiles = ceil_div(a.M, 32 * BJ);
+    const unsigned T = gridDim.x;
+    const unsigned xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
+    const unsigned L = xcd * (T / 8) + min(xcd, T % 8) + jx;
+    const unsigned t1 = fdiv(L, a.dv_mt);
+    const unsigned mx = L - t1 * mtiles;
+    const unsigned t2 = fdiv(t1, a.dv_kt);
+    const unsigned ky = t1 - t2 * ktiles;
+    const int split = fdiv(t2, a.dv_g);
+    const int g = t2 - split * a.groups;
     const int m0 = mx * (32 * BJ);
     const int k0 = ky * 32;
     const int kr_begin = split * a.kr_per_split;
     const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
     const int nblk = kr_end > kr_begin ? ceil_div(kr_end - kr_begin, 8) : 0;
 
-    // A: this lane's filter row, or (PK) its 16-byte slot of the packed
-    // filters: w_pk[g][k/32][kr/8][lane][4] holds W[k0 + l%32][8*blk + 4*h + e],
-    // zero past K and Kred, so a wavefront's A load is 1 KB contiguous.
-    const int kA = k0 + ll;
-    const bool kvalid = kA < a.Kg;
-    const float *wrow = w + ((long)g * a.Kg + (kvalid ? kA : 0)) * a.Kred;
-    const float *wpk = w + (((long)(g * ktiles + ky) * ceil_div(a.Kred, 8) + kr_begin / 8) * 64 + lane) * 4;
+    // A: byte offset of this lane's 16-byte slot in block 0 of the split.
+    const unsigned aoff = ((((unsigned)g * ktiles + ky) * kblocks + kr_begin / 8) * 64 + lane) * 16;
 
     // B: this lane's output pixels, one per 32-pixel block.
     int ih0[BJ], iw0[BJ];
     bool mvalid[BJ];
-    const float *xb[BJ];
+    unsigned xoff[BJ];   // element offset of (n, channel g*Cg, 0, 0)
 #pragma unroll
     for (int j = 0; j < BJ; ++j) {
         const int m = m0 + j * 32 + ll;
         mvalid[j] = m < a.M;
         const int mm = mvalid[j] ? m : 0;
-        const int n = mm / a.PQ;
+        const int n = fdiv(mm, a.dv_pq);
         const int pq = mm - n * a.PQ;
-        const int p = pq / a.Q;
+        const int p = fdiv(pq, a.dv_q);
         const int q = pq - p * a.Q;
         ih0[j] = p * a.stride - a.pad;
         iw0[j] = q * a.stride - a.pad;
-        xb[j] = x + ((long)n * a.C + (long)g * a.Cg) * a.HW;
+        xoff[j] = ((unsigned)n * a.C + (unsigned)g * a.Cg) * a.HW;
     }
+    const unsigned hw4 = 4u * a.HW;   // bytes between channel planes
 
     struct Frag {
         float av[4];
         float bv[BJ][4];
     };
 
-    // Block blk of this split: taps kr_begin + 8*blk + 4h + e, e = 0..3.
+    // KRSC: the filter position of the wavefront's next block, tracked as
+    // (block index) = rsq * cb + rsr with cb = C/groups / 8 blocks per filter
+    // position; blocks advance by WAVES, so one division at the start.
+    const int cb = a.Cg / 8;
+    int rsq = 0, rsr = 0, drq = 0, drr = 0;
+    if constexpr (KRSC && !(R_ == 1 && S_ == 1)) {
+        const int b0 = kr_begin / 8 + wave;
+        rsq = fdiv(b0, a.dv_cb);
+        rsr = b0 - rsq * cb;
+        drq = WAVES / cb;
+        drr = WAVES - drq * cb;
+    }
+
+    // Block blk (< nblk) of this split: taps kr_begin + 8*blk + 4h + e,
+    // e = 0..3.  Called for the wavefront's blocks in increasing order.
     auto load = [&](Frag &f, int blk) {
         const int kr0 = kr_begin + 8 * blk + 4 * h;
-        const bool live = blk < nblk;
-        if (PK) {
-            const float4 v = live ? *reinterpret_cast<const float4 *>(wpk + (long)blk * 256)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
-            f.av[0] = v.x;
-            f.av[1] = v.y;
-            f.av[2] = v.z;
-            f.av[3] = v.w;
-        } else if (VA && live && kvalid && kr0 + 4 <= kr_end) {
-            const float4 v = *reinterpret_cast<const float4 *>(wrow + kr0);
-            f.av[0] = v.x;
-            f.av[1] = v.y;
-            f.av[2] = v.z;
-            f.av[3] = v.w;
-        } else {
+        {
+            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(wres, aoff + blk * 1024u, 0, 0);
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                f.av[e] = (live && kvalid && kr0 + e < kr_end) ? wrow[kr0 + e] : 0.f;
+            for (int e = 0; e < 4; ++e) f.av[e] = __uint_as_float(v[e]);
         }
         if constexpr (KRSC) {
-            const int krb = kr_begin + 8 * blk;        // block base: one filter position
-            const int rs = krb / a.Cg;
-            const int c0 = krb - rs * a.Cg + 4 * h;
-            const int r = rs / S;
-            const int s = rs - r * S;
+            // The block is one filter position (r, s) and 8 channels; the
+            // reduction length is a multiple of 8, so its 4 taps per half are
+            // live together and one channel stride apart.
+            int c0 = kr0, r = 0, s = 0;
+            if constexpr (!(R_ == 1 && S_ == 1)) {
+                c0 = 8 * rsr + 4 * h;
+                r = rsq / S;
+                s = rsq - r * S;
+                rsq += drq;
+                rsr += drr;
+                if (rsr >= cb) {
+                    rsr -= cb;
+                    ++rsq;
+                }
+            }
 #pragma unroll
             for (int j = 0; j < BJ; ++j) {
                 const int ih = ih0[j] + r, iw = iw0[j] + s;
-                const bool okp = live && mvalid[j] && (unsigned)ih < (unsigned)a.H &&
-                                 (unsigned)iw < (unsigned)a.W;
-                const float *src = xb[j] + (long)c0 * a.HW + ih * a.W + iw;
+                const bool ok = mvalid[j] && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+                const unsigned off = select_offset(ok, 4u * (xoff[j] + (unsigned)c0 * a.HW + ih * a.W + iw), kOut);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    f.bv[j][e] = (okp && kr0 + e < kr_end) ? src[(long)e * a.HW] : 0.f;
+                    f.bv[j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, e * hw4, 0));
+            }
+        } else if constexpr (R_ == 1 && S_ == 1) {
+            // 1x1 with C/groups % 8 != 0: tap kr is channel kr at the pixel's
+            // own input position; the last block of the reduction is partial.
+#pragma unroll
+            for (int j = 0; j < BJ; ++j) {
+                const int ih = ih0[j], iw = iw0[j];
+                const bool ok = mvalid[j] && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+                const unsigned base = 4u * (xoff[j] + (unsigned)kr0 * a.HW + ih * a.W + iw);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const unsigned off = select_offset(ok && kr0 + e < kr_end, base + e * hw4, kOut);
+                    f.bv[j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+                }
             }
         } else {
 #pragma unroll
@@ -149,13 +195,31 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 #pragma unroll
                 for (int j = 0; j < BJ; ++j) {
                     const int ih = ih0[j] + r, iw = iw0[j] + s;
-                    const bool ok = live && kr < kr_end && mvalid[j] && (unsigned)ih < (unsigned)a.H &&
+                    const bool ok = kr < kr_end && mvalid[j] && (unsigned)ih < (unsigned)a.H &&
                                     (unsigned)iw < (unsigned)a.W;
-                    f.bv[j][e] = ok ? xb[j][(long)c * a.HW + ih * a.W + iw] : 0.f;
+                    const unsigned off = select_offset(ok, 4u * (xoff[j] + (unsigned)c * a.HW + ih * a.W + iw), kOut);
+                    f.bv[j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
                 }
             }
         }
     };
+
+    // The epilogue's bias values, loaded now so that their round trip
+    // overlaps the main loop (a missing bias is an empty buffer: zeros).
+    constexpr int kE = BJ * 16 / WAVES;   // output elements per thread
+    float bias_v[kE];
+    {
+        const __amdgpu_buffer_rsrc_t bres = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(a.bias), (short)0, a.bias ? a.K * 4 : 0, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < kE; ++i) {
+            const int idx = tid + i * 64 * WAVES;
+            const int v = (idx >> 6) & 15, l = idx & 63;
+            const int k = k0 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+            bias_v[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                bres, select_offset(k < a.Kg, 4u * (g * a.Kg + k), kOut), 0, 0));
+        }
+    }
 
     floatx16 acc[BJ];
 #pragma unroll
@@ -163,24 +227,24 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
 
-    // This wavefront takes blocks wave, wave + WAVES, ...; kDepth in flight.
+    // This wavefront takes blocks wave, wave + WAVES, ... with kDepth blocks
+    // of loads in flight: pass it issues the loads of its blocks it .. it +
+    // kDepth - 1 and runs the MFMAs of the previous pass's blocks.  One copy
+    // of the loop body serves the whole pipeline (no separate prologue).
     const int my_blocks = nblk > wave ? ceil_div(nblk - wave, WAVES) : 0;
     Frag f[kDepth];
-#pragma unroll
-    for (int d = 0; d < kDepth; ++d) load(f[d], d < my_blocks ? wave + d * WAVES : nblk);
-    for (int it = 0; it < my_blocks; it += kDepth) {
+#pragma clang loop unroll(disable)
+    for (int it = 0; it < my_blocks + kDepth; it += kDepth) {
 #pragma unroll
         for (int d = 0; d < kDepth; ++d) {
-            if (it + d < my_blocks) {
+            if (it >= kDepth && it - kDepth + d < my_blocks) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
 #pragma unroll
                     for (int j = 0; j < BJ; ++j)
-                        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f[d].av[e], f[d].bv[j][e],
-                                                                      acc[j], 0, 0, 0);
+                        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f[d].av[e], f[d].bv[j][e], acc[j], 0, 0, 0);
             }
-            const int nxt = it + d + kDepth;
-            load(f[d], nxt < my_blocks ? wave + nxt * WAVES : nblk);
+            if (it + d < my_blocks) load(f[d], wave + (it + d) * WAVES);
         }
     }
 
@@ -194,7 +258,9 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 #pragma unroll
         for (int v = 0; v < 16; ++v) red[wave][j * 16 + v][lane] = acc[j][v];
     __syncthreads();
-    for (int idx = tid; idx < BJ * 16 * 64; idx += 64 * WAVES) {
+#pragma unroll
+    for (int i = 0; i < kE; ++i) {
+        const int idx = tid + i * 64 * WAVES;
         const int jv = idx >> 6, l = idx & 63;
         const int j = jv >> 4, v = jv & 15;
         float sum = red[0][jv][l];
@@ -207,35 +273,24 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
         if (a.splits > 1) {
             a.ws[((long)split * a.K + kg) * a.M + m] = sum;
         } else {
-            const int n = m / a.PQ;
+            const int n = fdiv(m, a.dv_pq);
             const int pq = m - n * a.PQ;
-            float val = sum + (a.bias ? a.bias[kg] : 0.f);
+            float val = sum + bias_v[i];
             if (a.relu) val = fmaxf(val, 0.f);
             a.y[((long)n * a.K + kg) * a.PQ + pq] = val;
         }
     }
 }
 
-template <int R_, int S_, int WAVES, int BJ, bool KRSC>
-void launch_va(const ConvArgs &a, bool va, bool pk, dim3 grid, hipStream_t st)
-{
-    if (pk)
-        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, true>), grid, dim3(64 * WAVES), 0, st, a);
-    else if (va)
-        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, true, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
-    else
-        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, false, KRSC, false>), grid, dim3(64 * WAVES), 0, st, a);
-}
-
 template <int R_, int S_, bool KRSC>
-void launch_rs(const ConvArgs &a, int waves, int bj, bool va, bool pk, dim3 grid, hipStream_t st)
+void launch_rs(const ConvArgs &a, int waves, int bj, dim3 grid, hipStream_t st)
 {
     if (waves == 8) {
-        if (bj == 2) launch_va<R_, S_, 8, 2, KRSC>(a, va, pk, grid, st);
-        else launch_va<R_, S_, 8, 1, KRSC>(a, va, pk, grid, st);
+        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 2, KRSC>), grid, dim3(512), 0, st, a);
+        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 1, KRSC>), grid, dim3(512), 0, st, a);
     } else {
-        if (bj == 2) launch_va<R_, S_, 4, 2, KRSC>(a, va, pk, grid, st);
-        else launch_va<R_, S_, 4, 1, KRSC>(a, va, pk, grid, st);
+        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, KRSC>), grid, dim3(256), 0, st, a);
+        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 1, KRSC>), grid, dim3(256), 0, st, a);
     }
 }
 
@@ -251,10 +306,15 @@ int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 // then per round of work-groups over the CUs, each wavefront's MFMA time
 // (blocks * BJ * 4 MFMAs * 64 cycles) plus ~1.2 us per dependent round of
 // loads (kDepth blocks in flight), plus ~2.5 us for a split-K reduce launch.
-WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, bool w_aligned16)
+bool wave_fits(const ConvProblem &p)
+{
+    return (long)p.N * p.C * p.H * p.W * 4 < (1L << 31) && (long)wave_packed_floats(p) * 4 < (1L << 31);
+}
+
+WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
 {
     WavePlan best{};
-    best.va = p.Kred % 4 == 0 && w_aligned16;
+    best.krsc = p.Cg % 8 == 0;
     const int blocks = ceil_div(p.Kred, 8);
     double best_us = 1e30;
     for (int bj = 1; bj <= 2; ++bj) {
@@ -290,11 +350,9 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
 {
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R == 0 || S == 0 || R != S) R = S = 0;
-    if (plan.krsc && R != 3) R = S = 0;
-    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %s, %s, %s>%s", R, S, plan.waves, plan.bj,
-             (plan.va || plan.pk) ? "true" : "false", plan.krsc ? "true" : "false",
-             plan.pk ? "true" : "false",
-             plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    if (plan.krsc && R != 3 && R != 1) R = S = 0;
+    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %s>%s", R, S, plan.waves, plan.bj,
+             plan.krsc ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     *launches = plan.splits > 1 ? 2 : 1;
 }
 
@@ -310,24 +368,29 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
     a.ws = plan.splits > 1 ? ws : nullptr;
     a.splits = plan.splits;
     a.kr_per_split = plan.kr_per_split;
-    const bool va = plan.va && (uintptr_t)w % 16 == 0;
+    a.dv_mt = make_fastdiv(ceil_div(p.M, 32 * plan.bj));
+    a.dv_kt = make_fastdiv(ceil_div(p.Kg, 32));
+    a.dv_g = make_fastdiv(p.groups);
+    a.dv_cb = make_fastdiv(p.Cg / 8 > 0 ? p.Cg / 8 : 1);
     const dim3 grid((unsigned)((long)ceil_div(p.M, 32 * plan.bj) * ceil_div(p.Kg, 32) * p.groups *
                                plan.splits));
     hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
-    if (plan.krsc) {   // filters packed KRSC (R * S > 1)
-        if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, true>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+    if (plan.krsc) {   // reduction ordered (r, s, c) in the packed filters
+        if (p.R == 1 && p.S == 1)
+            launch_rs<1, 1, true>(a, plan.waves, plan.bj, grid, st);
+        else if (p.R == 3 && p.S == 3)
+            launch_rs<3, 3, true>(a, plan.waves, plan.bj, grid, st);
         else
-            launch_rs<0, 0, true>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+            launch_rs<0, 0, true>(a, plan.waves, plan.bj, grid, st);
     } else if (p.R == 1 && p.S == 1) {
-        launch_rs<1, 1, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+        launch_rs<1, 1, false>(a, plan.waves, plan.bj, grid, st);
     } else if (p.R == 3 && p.S == 3) {
-        launch_rs<3, 3, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+        launch_rs<3, 3, false>(a, plan.waves, plan.bj, grid, st);
     } else if (p.R == 7 && p.S == 7) {
-        launch_rs<7, 7, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+        launch_rs<7, 7, false>(a, plan.waves, plan.bj, grid, st);
     } else {
-        launch_rs<0, 0, false>(a, plan.waves, plan.bj, va, plan.pk, grid, st);
+        launch_rs<0, 0, false>(a, plan.waves, plan.bj, grid, st);
     }
     e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return e;

@@ -35,6 +35,24 @@ struct ConvProblem {
     int relu;
 };
 
+// Division by a divisor d >= 1 fixed at launch, for numerators below 2^31:
+// n / d = (mulhi(n, mul) + n) >> shift with shift = ceil(log2 d) and
+// mul = floor(2^32 (2^shift - d) / d) + 1 (the round-up method of Granlund
+// and Montgomery, 1994; the sum stays below 2^32 for n < 2^31).  Three
+// instructions in place of a ~20-instruction integer division.
+struct FastDiv {
+    unsigned mul, shift;
+};
+
+inline FastDiv make_fastdiv(unsigned d)
+{
+    unsigned l = 0;
+    while ((1ull << l) < d) ++l;
+    return FastDiv{(unsigned)(((1ull << 32) * ((1ull << l) - d)) / d + 1), l};
+}
+
+__device__ __forceinline__ unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(n, f.mul) + n) >> f.shift; }
+
 // Kernel argument block for the dense paths (passed by value).
 struct ConvArgs {
     const void *x;        // fp32 or bf16 bits, [N][C][H][W]
@@ -48,6 +66,8 @@ struct ConvArgs {
     int kr_per_split;     // reduction length per split, a multiple of the chunk size
     int relu;
     int vec4;             // split-K reduce may use 16-byte accesses (one image, aligned)
+    FastDiv dv_pq, dv_q;  // division by P*Q and by Q
+    FastDiv dv_mt, dv_kt, dv_g, dv_cb;   // wave kernel: pixel tiles, filter tiles, groups, C/groups/8
 };
 
 ConvArgs make_args(const ConvProblem &p);
@@ -89,14 +109,14 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
 struct WavePlan {
     int bj;             // 32-pixel blocks per work-group tile (1 or 2)
     int waves;          // wavefronts per work-group splitting the reduction (4 or 8)
-    bool va;            // 16-byte filter loads
     int splits;         // reduction splits across work-groups
     int kr_per_split;
     size_t ws_bytes;
-    bool krsc;          // filters pre-packed [K][R][S][C/groups]
-    bool pk;            // filters pre-packed in the wavefront load order (launch_pack_wave)
+    bool krsc;          // reduction ordered (r, s, c) in the packed filters
 };
-WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, bool w_aligned16);
+// The wave kernel addresses x and its packed filters with 32-bit offsets.
+bool wave_fits(const ConvProblem &p);
+WavePlan plan_wave_f32(const ConvProblem &p, int num_cus);
 hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const float *x,
                            const float *w, const float *bias, float *y, float *ws,
                            hipStream_t st, const LaunchHook *hook = nullptr);

@@ -174,24 +174,7 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
             miconv_stack_destroy(s);
             return rc;
         }
-        if (r.impl == IMPL_WAVE) {
-            // Pre-computing: pack the filters once, in the wave kernel's
-            // operand order, for every replay.
-            void *pk = nullptr;
-            const bool krsc = r.p.R * r.p.S > 1 && r.p.Cg % 8 == 0;
-            e = hipMalloc(&pk, wave_packed_floats(r.p) * sizeof(float));
-            if (e == hipSuccess) s->packed.push_back(pk);
-            if (e == hipSuccess)
-                e = launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(pk), krsc,
-                                     nullptr);
-            if (e != hipSuccess) {
-                miconv_stack_destroy(s);
-                return set_hip_error(e);
-            }
-            r.wk = pk;
-            r.wplan.pk = true;
-            r.wplan.krsc = krsc;
-        } else if (r.pack_per_call || krsc_eligible(r)) {
+        if (r.pack_per_call || krsc_eligible(r)) {
             // Pre-computing: pack the filters once, in the layout the kernel
             // reads, for every replay.
             void *pk = nullptr;
