@@ -187,49 +187,65 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
 }
 
 // Sum the split partials in split order (deterministic), add bias, apply the
-// activation and store NCHW.  Lanes walk m, so reads and writes are contiguous.
-// With one image the partials' [K][M] order is y's own order, so (when the
-// sizes and pointers allow) lanes take four consecutive elements with
-// 16-byte accesses.
+// activation and store NCHW.  Lanes walk the partials' [K][M] order, so reads
+// are contiguous.  A thread requests its bias value and the partials of up to
+// eight splits before it adds any of them: the launch costs one memory round
+// trip, not one per split.  Partials are read through a buffer resource, so
+// the slots past the last split read as zeros (adding them changes nothing).
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
 {
-    const long total = (long)a.K * a.M;
-    long start = 0;
+    constexpr int kGroup = 8;
+    const unsigned total = (unsigned)a.K * a.M;
+    const unsigned stride = gridDim.x * blockDim.x;
+    const __amdgpu_buffer_rsrc_t wsr = __builtin_amdgcn_make_buffer_rsrc(
+        a.ws, (short)0, (int)(a.splits * total * 4u), 0x00020000);
     if (a.vec4) {
-        const long n4 = total / 4;
-        const float4 *ws4 = reinterpret_cast<const float4 *>(a.ws);
-        for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
-             i += (long)gridDim.x * blockDim.x) {
-            float4 s = ws4[i];
-            for (int sp = 1; sp < a.splits; ++sp) {
-                const float4 v = ws4[(long)sp * n4 + i];
-                s.x += v.x;
-                s.y += v.y;
-                s.z += v.z;
-                s.w += v.w;
-            }
-            float o[4] = {s.x, s.y, s.z, s.w};
+        // One image with M % 4 == 0: the partials' order is y's own order and
+        // four consecutive elements share one filter.
+        const unsigned n4 = total / 4;
+        for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+            const unsigned k = fdiv(4 * i, a.dv_m);
+            const float bv = a.bias ? a.bias[k] : 0.f;
+            float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int sp = 0; sp < a.splits; sp += kGroup) {
+                float4 v[kGroup];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int k = (int)((4 * i + e) / a.M);
-                o[e] += a.bias ? a.bias[k] : 0.f;
-                if (a.relu) o[e] = fmaxf(o[e], 0.f);
+                for (int u = 0; u < kGroup; ++u)
+                    v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                          wsr, ((sp + u) * n4 + i) * 16u, 0, 0));
+#pragma unroll
+                for (int u = 0; u < kGroup; ++u) {
+                    s.x += v[u].x;
+                    s.y += v[u].y;
+                    s.z += v[u].z;
+                    s.w += v[u].w;
+                }
             }
+            float o[4] = {s.x + bv, s.y + bv, s.z + bv, s.w + bv};
+            if (a.relu)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.f);
             reinterpret_cast<float4 *>(a.y)[i] = make_float4(o[0], o[1], o[2], o[3]);
         }
-        start = 4 * n4;
+        return;
     }
-    for (long i = start + (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (long)gridDim.x * blockDim.x) {
-        const int k = (int)(i / a.M);
-        const int m = (int)(i - (long)k * a.M);
-        float s = a.ws[i];
-        for (int sp = 1; sp < a.splits; ++sp) s += a.ws[(long)sp * total + i];
-        s += a.bias ? a.bias[k] : 0.f;
+    for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const unsigned k = fdiv(i, a.dv_m);
+        const unsigned m = i - k * a.M;
+        const float bv = a.bias ? a.bias[k] : 0.f;
+        float s = 0.f;
+        for (int sp = 0; sp < a.splits; sp += kGroup) {
+            float v[kGroup];
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u)
+                v[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wsr, ((sp + u) * total + i) * 4u, 0, 0));
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) s += v[u];
+        }
+        s += bv;
         if (a.relu) s = fmaxf(s, 0.f);
-        const int n = m / a.PQ;
-        const int pq = m - n * a.PQ;
-        a.y[((long)n * a.K + k) * a.PQ + pq] = s;
+        const unsigned n = fdiv(m, a.dv_pq);
+        a.y[((size_t)n * a.K + k) * a.PQ + (m - n * a.PQ)] = s;
     }
 }
 
@@ -336,7 +352,10 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
 hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
 {
     const long total = (long)a.K * a.M;
-    a.vec4 = a.N == 1 && total % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0;
+    // 32-bit offsets, also for the zero-reading slots of the last group of 8
+    if ((long)(a.splits + 7) * total * 4 >= (1L << 31)) return hipErrorInvalidValue;
+    a.vec4 = a.N == 1 && a.M % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0;
+    a.dv_m = make_fastdiv(a.M);
     long blocks = (a.vec4 ? total / 4 : total + 255) / 256 + 1;
     if (blocks > 8192) blocks = 8192;
     launch_kernel(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);

@@ -67,6 +67,7 @@ struct ConvArgs {
     int relu;
     int vec4;             // split-K reduce may use 16-byte accesses (one image, aligned)
     FastDiv dv_pq, dv_q;  // division by P*Q and by Q
+    FastDiv dv_m;         // division by M (split-K reduce)
     FastDiv dv_mt, dv_kt, dv_g, dv_cb;   // wave kernel: pixel tiles, filter tiles, groups, C/groups/8
 };
 
