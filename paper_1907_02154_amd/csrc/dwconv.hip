@@ -228,7 +228,13 @@ struct DwRunShape {
     // take more registers, so they stage less)
     static constexpr int STAGE4 = HW % 4 == 0 ? 7 : 5;
     static constexpr int STAGE_FLOATS = STAGE4 * 4 * 256;
-    static constexpr int MAX_PB_LDS = (kRunLds - G0 - 3) / (PP + kTapStride);   // + taps, 16-byte aligned
+    // Planes of at most 14 output columns also keep an output region in LDS:
+    // items write their columns there and the run's outputs, one contiguous
+    // stretch of y, leave with consecutive lanes on consecutive floats.
+    // (Stored straight from the items, a store instruction would write
+    // column pieces of many small planes: short, scattered segments.)
+    static constexpr bool OUT_LDS = Q <= 14;
+    static constexpr int MAX_PB_LDS = (kRunLds - G0 - 3) / (PP + kTapStride + (OUT_LDS ? PQ : 0));
     static constexpr int MAX_PB = STAGE_FLOATS / HW < MAX_PB_LDS ? STAGE_FLOATS / HW : MAX_PB_LDS;
     static constexpr int NW = (MAX_PB * kTapStride + 255) / 256;       // tap words staged per lane
     // A lane's work item is a column of RG output rows of one plane: the
@@ -269,6 +275,7 @@ __global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
     __shared__ __attribute__((aligned(16))) float lds[kRunLds];
     const int tid = threadIdx.x;
     float *taps = lds + ((S::G0 + a.PB * S::PP + 3) & ~3);      // 16-byte aligned
+    float *outs = taps + a.PB * kTapStride;                      // OUT_LDS: [plane][P][Q]
 
     // The gaps are written here once and never again: runs only write plane slots.
     for (int i = tid; i < kRunLds / 4; i += 256)
@@ -391,9 +398,20 @@ __global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
                     }
                 }
             }
-            float *yo = dst + pl * S::PQ + p0 * S::Q + q;
+            float *yo = (S::OUT_LDS ? outs : dst) + pl * S::PQ + p0 * S::Q + q;
 #pragma unroll
             for (int j = 0; j < S::RG; ++j) yo[j * S::Q] = a.relu ? fmaxf(acc[j], 0.f) : acc[j];
+        }
+        if constexpr (S::OUT_LDS) {
+            __syncthreads();
+            const int ocnt = np * S::PQ;
+            if (((uintptr_t)dst & 15) == 0) {          // outs is 16-byte aligned
+                for (int i = tid; i < ocnt / 4; i += 256)
+                    reinterpret_cast<float4 *>(dst)[i] = reinterpret_cast<const float4 *>(outs)[i];
+                for (int i = ocnt / 4 * 4 + tid; i < ocnt; i += 256) dst[i] = outs[i];
+            } else {
+                for (int i = tid; i < ocnt; i += 256) dst[i] = outs[i];
+            }
         }
         __syncthreads();                            // LDS free for the next run
         put();
