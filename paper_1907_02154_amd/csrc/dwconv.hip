@@ -228,12 +228,14 @@ struct DwRunShape {
     // take more registers, so they stage less)
     static constexpr int STAGE4 = HW % 4 == 0 ? 7 : 5;
     static constexpr int STAGE_FLOATS = STAGE4 * 4 * 256;
-    // Planes of at most 14 output columns also keep an output region in LDS:
-    // items write their columns there and the run's outputs, one contiguous
-    // stretch of y, leave with consecutive lanes on consecutive floats.
-    // (Stored straight from the items, a store instruction would write
-    // column pieces of many small planes: short, scattered segments.)
-    static constexpr bool OUT_LDS = Q <= 14;
+    // Planes of at most 14 output columns (28 at stride 1) also keep an output
+    // region in LDS: items write their columns there and the run's outputs,
+    // one contiguous stretch of y, leave with consecutive lanes on
+    // consecutive floats.  (Stored straight from the items, a store
+    // instruction would write column pieces of many small planes: short,
+    // scattered segments.  At 56x56 stride 2 the direct stores measured
+    // faster.)
+    static constexpr bool OUT_LDS = Q <= 14 || (ST == 1 && Q <= 28);
     static constexpr int MAX_PB_LDS = (kRunLds - G0 - 3) / (PP + kTapStride + (OUT_LDS ? PQ : 0));
     static constexpr int MAX_PB = STAGE_FLOATS / HW < MAX_PB_LDS ? STAGE_FLOATS / HW : MAX_PB_LDS;
     static constexpr int NW = (MAX_PB * kTapStride + 255) / 256;       // tap words staged per lane
