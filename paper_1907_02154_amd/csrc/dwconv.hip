@@ -258,6 +258,10 @@ int dw_run_planes_for(long planes, long grid)
     using S = DwRunShape<H_, W_, ST>;
     const int align = S::HW % 4 == 0 ? 1 : (S::HW % 2 == 0 ? 2 : 4);  // PB*HW % 4 == 0
     long pbmax = S::MAX_PB;
+    // A run whose items fill the 256 lanes k times plus a small remainder
+    // costs k + 1 passes: trim it to k whole passes.
+    const long items = pbmax * S::IPP;
+    if (items >= 256 && items % 256 < 128) pbmax = items / 256 * 256 / S::IPP;
     pbmax = pbmax / align * align;
     if (pbmax < align) return 0;
     long rounds = (planes + pbmax * grid - 1) / (pbmax * grid);
