@@ -51,7 +51,10 @@ inline FastDiv make_fastdiv(unsigned d)
     return FastDiv{(unsigned)(((1ull << 32) * ((1ull << l) - d)) / d + 1), l};
 }
 
-__device__ __forceinline__ unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(n, f.mul) + n) >> f.shift; }
+__host__ __device__ __forceinline__ unsigned fdiv(unsigned n, FastDiv f)
+{
+    return ((unsigned)(((unsigned long long)n * f.mul) >> 32) + n) >> f.shift;   // v_mul_hi_u32 on the GPU
+}
 
 // Kernel argument block for the dense paths (passed by value).
 struct ConvArgs {
