@@ -278,7 +278,10 @@ def main():
             if name.startswith("splitk_reduce"):
                 g["bytes"] += l.N * l.K * d["P"] * d["Q"] * 4
             elif name.startswith("nchw_to_nhwc"):
-                g["bytes"] += 2 * l.N * l.C * l.H * l.W * (2 if bf16 else 4)
+                # a 1x1 strided layer without padding copies only its sampled pixels
+                sub = l.R == 1 and l.S == 1 and l.pad == 0 and l.stride > 1
+                px = d["P"] * d["Q"] if sub else l.H * l.W
+                g["bytes"] += 2 * l.N * l.C * px * (2 if bf16 else 4)
             else:
                 g["bytes"] += 2 * l.K * (l.C // l.groups) * l.R * l.S * (2 if bf16 else 4)
         g["layers"].append(d["layer"].name)
@@ -300,11 +303,15 @@ def main():
                 share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
 
     if args.layers:
+        parts = [[] for _ in layers]
+        for j in range(n_launch):
+            parts[launch_info[j][0]].append(float(launch_ms[j]) * 1e3)
         for j, d in enumerate(layers):
             l = d["layer"]
             t = float(layer_ms[j])
+            split = " [" + " + ".join(f"{u:.2f}" for u in parts[j]) + "]" if len(parts[j]) > 1 else ""
             print(f"{j:3d} {l.name:10s} {d['kernel']:45s} {t * 1e3:9.2f} us "
-                  f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s",
+                  f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s{split}",
                   file=sys.stderr)
 
     # CPU baseline: the oracle on a bounded prefix of the same layers.

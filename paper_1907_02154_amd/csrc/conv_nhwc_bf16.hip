@@ -24,75 +24,77 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// x [N][C][HW] -> x_cl [N][HW][C] in 64 x 64 tiles (channels x pixels),
-// exchanged through LDS so that both sides of the copy are contiguous.  A
-// lane reads RV consecutive pixels of one channel per global load (RV = 8, 4
-// or 1: the widest that HW's alignment allows) and, with C % 8 == 0 (WV),
-// writes 8 channels of one pixel per 16-byte store.
-template <int RV, bool WV>
-__global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(const uint16_t *__restrict__ x,
-                                                                uint16_t *__restrict__ xt, int C,
-                                                                int HW, int tiles_hw, int tiles_c)
+// x [N][C][H][W] -> x_cl [N][P][Q][C], where P x Q are the pixels the conv
+// reads in channel-last form: all of them (P = H, Q = W, S = 1), or, for a
+// 1x1 stride-S layer without padding, only the ones it samples (row p*S,
+// column q*S), so the layer then runs as a stride-1 conv on a P x Q image
+// and reads 1/S^2 of x.  The pixel axis is flattened over images (a tile of
+// 64 pixels may span images), so small planes waste no lanes.  A
+// work-group moves 64 channels x 64 pixels through LDS: a lane reads RV
+// consecutive pixels of one channel per load (RV = 8 or 4 when S = 1 and
+// H*W and the base address allow it; 1 otherwise) and writes 8 channels of
+// one pixel per 16-byte store (C % 8 == 0 on every path that uses it).
+struct NhwcCopyArgs {
+    const uint16_t *x;
+    uint16_t *xt;
+    int C, H, W, Q, S, HW, PQ;
+    int npq;             // N * P * Q
+    int tiles_c;
+    FastDiv dv_hw, dv_pq, dv_q;
+};
+
+template <int RV>
+__global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];   // [channel][pixel]
     const int t = threadIdx.x;
-    const int b = blockIdx.x;
-    const int th = b % tiles_hw;
-    const int tc = (b / tiles_hw) % tiles_c;
-    const long n = b / ((long)tiles_hw * tiles_c);
-    const int c0 = tc * 64, p0 = th * 64;
-    const uint16_t *src = x + n * (long)C * HW;
-    uint16_t *dst = xt + n * (long)C * HW;
-    if constexpr (RV == 8) {
+    const int c0 = (blockIdx.x % a.tiles_c) * 64;
+    const int p0 = (blockIdx.x / a.tiles_c) * 64;
+    if constexpr (RV > 1) {
+        constexpr int GR = 64 / RV;                 // pixel groups per channel row
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {   // 64 channels x 8 pixel octets
+        for (int i = 0; i < 64 * GR / 256; ++i) {
             const int id = t + 256 * i;
-            const int c = id >> 3, o = id & 7;
-            const bool ok = c0 + c < C && p0 + 8 * o < HW;
-            const uint4 v = ok ? *reinterpret_cast<const uint4 *>(src + (long)(c0 + c) * HW + p0 + 8 * o)
-                               : make_uint4(0, 0, 0, 0);
-            *reinterpret_cast<uint4 *>(&tile[c][8 * o]) = v;
-        }
-    } else if constexpr (RV == 4) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {   // 64 channels x 16 pixel quads
-            const int id = t + 256 * i;
-            const int c = id >> 4, o = id & 15;
-            const bool ok = c0 + c < C && p0 + 4 * o < HW;
-            const uint2 v = ok ? *reinterpret_cast<const uint2 *>(src + (long)(c0 + c) * HW + p0 + 4 * o)
-                               : make_uint2(0, 0);
-            *reinterpret_cast<uint2 *>(&tile[c][4 * o]) = v;
-        }
-    } else {
-        const int px = t & 63;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int c = (t >> 6) + 4 * i;
-            const bool ok = c0 + c < C && p0 + px < HW;
-            tile[c][px] = ok ? src[(long)(c0 + c) * HW + p0 + px] : 0;
-        }
-    }
-    __syncthreads();
-    if constexpr (WV) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {   // 64 pixels x 8 channel octets
-            const int id = t + 256 * i;
-            const int px = id >> 3, o = id & 7;
-            if (c0 + 8 * o < C && p0 + px < HW) {
-                uint32_t d[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    d[e] = (uint32_t)tile[8 * o + 2 * e][px] | ((uint32_t)tile[8 * o + 2 * e + 1][px] << 16);
-                *reinterpret_cast<uint4 *>(dst + (long)(p0 + px) * C + c0 + 8 * o) =
-                    make_uint4(d[0], d[1], d[2], d[3]);
+            const int c = id / GR, o = id % GR;
+            const int px = p0 + RV * o;             // a group never spans images: H*W % RV == 0
+            const bool ok = c0 + c < a.C && px < a.npq;
+            const unsigned n = fdiv(ok ? px : 0, a.dv_hw);
+            const uint16_t *src = a.x + ((long)n * a.C + c0 + c) * a.HW + (px - (int)n * a.HW);
+            if constexpr (RV == 8) {
+                const uint4 v = ok ? *reinterpret_cast<const uint4 *>(src) : make_uint4(0, 0, 0, 0);
+                *reinterpret_cast<uint4 *>(&tile[c][8 * o]) = v;
+            } else {
+                const uint2 v = ok ? *reinterpret_cast<const uint2 *>(src) : make_uint2(0, 0);
+                *reinterpret_cast<uint2 *>(&tile[c][4 * o]) = v;
             }
         }
     } else {
-        const int cc = t & 63;
+        const int px = p0 + (t & 63);
+        const bool pok = px < a.npq;
+        const unsigned n = fdiv(pok ? px : 0, a.dv_pq);
+        const unsigned pq = (pok ? px : 0) - n * a.PQ;
+        const unsigned pp = fdiv(pq, a.dv_q);
+        const unsigned q = pq - pp * a.Q;
+        const long off = (long)(pp * a.S) * a.W + q * a.S;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const int p = (t >> 6) + 4 * i;
-            if (c0 + cc < C && p0 + p < HW) dst[(long)(p0 + p) * C + c0 + cc] = tile[cc][p];
+            const int c = (t >> 6) + 4 * i;
+            const bool ok = pok && c0 + c < a.C;
+            tile[c][t & 63] = ok ? a.x[((long)n * a.C + c0 + c) * a.HW + off] : 0;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {   // 64 pixels x 8 channel octets
+        const int id = t + 256 * i;
+        const int px = id >> 3, o = id & 7;
+        if (c0 + 8 * o < a.C && p0 + px < a.npq) {
+            uint32_t d[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                d[e] = (uint32_t)tile[8 * o + 2 * e][px] | ((uint32_t)tile[8 * o + 2 * e + 1][px] << 16);
+            *reinterpret_cast<uint4 *>(a.xt + (long)(p0 + px) * a.C + c0 + 8 * o) =
+                make_uint4(d[0], d[1], d[2], d[3]);
         }
     }
 }
@@ -628,13 +630,35 @@ void launch_krc(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 
 int rs_template(int v) { return (v == 1 || v == 3) ? v : 0; }
 
-// Pixels per global read of the NCHW -> NHWC copy (x may be null: describe).
-int transpose_read_width(int HW, const void *x)
+// 1x1 layers with stride > 1 and no padding copy only the pixels they
+// sample into the channel-last buffer.
+bool copy_subsamples(const ConvProblem &p)
+{
+    return p.R == 1 && p.S == 1 && p.pad == 0 && p.stride > 1;
+}
+
+// Pixels per global read of the channel-last copy (x may be null: describe).
+int copy_read_width(const ConvProblem &p, const void *x)
 {
     const uintptr_t xa = (uintptr_t)x;
+    const int HW = p.H * p.W;
+    if (copy_subsamples(p)) return 1;
     if (HW % 8 == 0 && xa % 16 == 0) return 8;
     if (HW % 4 == 0 && xa % 8 == 0) return 4;
     return 1;
+}
+
+// The problem the GEMM kernels see after the copy: a subsampling copy turns
+// a 1x1 stride-S layer into a stride-1 layer on its P x Q sampled pixels.
+ConvProblem copied_problem(const ConvProblem &p)
+{
+    ConvProblem q = p;
+    if (copy_subsamples(p)) {
+        q.H = p.P;
+        q.W = p.Q;
+        q.stride = 1;
+    }
+    return q;
 }
 // Direct-to-LDS tiles: pixels x channels, wavefronts along pixels x channels,
 // pipeline depth.  LDS per work-group = depth * (bpx + bkc) * 128 bytes.
@@ -714,7 +738,8 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     // 1x1 stride-1 layers with 8-pixel rows read x in NCHW directly
     plan.nchwb = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && (p.H * p.W) % 8 == 0 &&
                  plan.tile <= 1 && (uintptr_t)x % 16 == 0;
-    plan.xcl_bytes = plan.nchwb ? 0 : (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
+    const ConvProblem cp = copied_problem(p);
+    plan.xcl_bytes = plan.nchwb ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
     return plan;
 }
 
@@ -744,7 +769,8 @@ NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x)
         plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
         break;
     }
-    plan.xcl_bytes = (size_t)p.N * p.C * p.H * p.W * sizeof(uint16_t);
+    const ConvProblem cp = copied_problem(p);
+    plan.xcl_bytes = (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
     return plan;
 }
 
@@ -754,8 +780,7 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R != S) R = S = 0;
     char tname[64];
-    snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d, %s>", transpose_read_width(p.H * p.W, nullptr),
-             p.C % 8 == 0 ? "true" : "false");
+    snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", copy_read_width(p, nullptr));
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s>%s",
@@ -796,22 +821,34 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     }
     e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
-    const int HW = p.H * p.W;
-    const int th = ceil_div(HW, 64), tc = ceil_div(p.C, 64);
-    const int rv = transpose_read_width(HW, x);
-    const bool wv = p.C % 8 == 0;
-    const dim3 tg((unsigned)((long)th * tc * p.N)), tb(256);
-    if (wv && rv == 8)
-        launch_kernel((nchw_to_nhwc_bf16_kernel<8, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
-    else if (wv && rv == 4)
-        launch_kernel((nchw_to_nhwc_bf16_kernel<4, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
-    else if (wv)
-        launch_kernel((nchw_to_nhwc_bf16_kernel<1, true>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+    if (p.C % 8 != 0) return hipErrorInvalidValue;   // every channel-last path has C % 32 == 0
+    const ConvProblem cp = copied_problem(p);
+    NhwcCopyArgs ca{};
+    ca.x = x;
+    ca.xt = xcl;
+    ca.C = p.C;
+    ca.H = p.H;
+    ca.W = p.W;
+    ca.Q = cp.W;
+    ca.S = copy_subsamples(p) ? p.stride : 1;
+    ca.HW = p.H * p.W;
+    ca.PQ = cp.H * cp.W;
+    ca.npq = p.N * ca.PQ;
+    ca.tiles_c = ceil_div(p.C, 64);
+    ca.dv_hw = make_fastdiv(ca.HW);
+    ca.dv_pq = make_fastdiv(ca.PQ);
+    ca.dv_q = make_fastdiv(ca.Q);
+    const dim3 tg((unsigned)((long)ceil_div(ca.npq, 64) * ca.tiles_c)), tb(256);
+    const int rv = copy_read_width(p, x);
+    if (rv == 8)
+        launch_kernel(nchw_to_nhwc_bf16_kernel<8>, tg, tb, 0, st, ca);
+    else if (rv == 4)
+        launch_kernel(nchw_to_nhwc_bf16_kernel<4>, tg, tb, 0, st, ca);
     else
-        launch_kernel((nchw_to_nhwc_bf16_kernel<1, false>), tg, tb, 0, st, x, xcl, p.C, HW, th, tc);
+        launch_kernel(nchw_to_nhwc_bf16_kernel<1>, tg, tb, 0, st, ca);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
-    ConvArgs a = make_args(p);
+    ConvArgs a = make_args(cp);
     a.x = xcl;
     a.w = w_krsc;
     a.bias = bias;

@@ -138,6 +138,13 @@ BF16_CASES = DENSE_CASES[:9] + [
     (1, 64, 9, 9, 48, 3, 3, 1, 1, 2),        # channel-last path, grouped (C/groups = 32)
     (3, 96, 13, 11, 130, 1, 1, 1, 0, 1),     # channel-last 1x1, chunk of 32 channels
     (1, 256, 7, 7, 520, 3, 3, 1, 1, 1),      # long reduction: split across work-groups
+    (2, 64, 14, 14, 128, 1, 1, 2, 0, 1),     # 1x1 stride 2: only the sampled pixels are copied
+    (3, 64, 7, 9, 72, 1, 1, 2, 0, 1),        # sampled copy, odd plane, P x Q = 4 x 5
+    (1, 128, 28, 28, 64, 1, 1, 3, 0, 1),     # sampled copy, stride 3
+    (2, 96, 10, 10, 64, 1, 1, 2, 0, 1),      # sampled copy, 32-channel chunks
+    (2, 64, 9, 9, 64, 1, 1, 2, 1, 1),        # 1x1 stride 2 with padding: full copy
+    (5, 64, 7, 7, 64, 1, 1, 1, 0, 1),        # 49-pixel planes: copy tiles span images
+    (3, 64, 14, 14, 96, 3, 3, 1, 1, 1),      # 196-pixel planes: 4-pixel copy reads
 ]
 
 
