@@ -213,11 +213,11 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         return MICONV_ERR_UNSUPPORTED;
     }
     if (r.impl == IMPL_IGEMM) {
-        // Small GEMM extents (fewer than 1.5 128x128 output tiles per CU) go
-        // to the wave-direct kernel, unless the caller forced the tiled one.
+        // The wave kernel serves every size it can address (measured faster
+        // than the LDS-tiled kernel from batch-1 ResNet layers to VGG-16 at
+        // batch 32), unless the caller forced the tiled one.
         const int cus = cu_count();
-        const long big_tiles = (long)ceil_div(r.p.M, 128) * ceil_div(r.p.Kg, 128) * r.p.groups;
-        if (algo != MICONV_ALGO_IGEMM && 2 * big_tiles < 3L * cus && wave_fits(r.p)) {
+        if (algo != MICONV_ALGO_IGEMM && wave_fits(r.p)) {
             r.impl = IMPL_WAVE;
             r.wplan = plan_wave_f32(r.p, cus);
             r.pack_per_call = true;   // filters in the wavefront load order

@@ -298,6 +298,11 @@ int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 
 }  // namespace
 
+bool wave_fits(const ConvProblem &p)
+{
+    return (long)p.N * p.C * p.H * p.W * 4 < (1L << 31) && (long)wave_packed_floats(p) * 4 < (1L << 31);
+}
+
 // Work-group tile 32 channels x 32*BJ pixels; a work-group runs on one CU,
 // so the parallelism across CUs is the number of work-groups, and its
 // wavefronts (4 or 8, splitting the tile's reduction) fill that CU's SIMDs.
@@ -305,12 +310,8 @@ int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 // this part: a fixed ~4.5 us per launch (dispatch, first loads, epilogue),
 // then per round of work-groups over the CUs, each wavefront's MFMA time
 // (blocks * BJ * 4 MFMAs * 64 cycles) plus ~1.2 us per dependent round of
-// loads (kDepth blocks in flight), plus ~2.5 us for a split-K reduce launch.
-bool wave_fits(const ConvProblem &p)
-{
-    return (long)p.N * p.C * p.H * p.W * 4 < (1L << 31) && (long)wave_packed_floats(p) * 4 < (1L << 31);
-}
-
+// loads (kDepth blocks in flight), plus, for a split reduction, ~2.5 us for
+// the reduce launch and the partials' HBM round trip.
 WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
 {
     WavePlan best{};
@@ -321,7 +322,7 @@ WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
         if (bj == 2 && p.M < 64) continue;
         const long tiles = (long)ceil_div(p.M, 32 * bj) * ceil_div(p.Kg, 32) * p.groups;
         const int depth = bj == 2 ? 2 : 4;
-        for (int waves : {8, 4}) {
+        for (int waves : {4, 8}) {   // on a tie the smaller work-group: no idle wavefronts
             for (int sp = 1; sp <= 16; ++sp) {
                 const int per = ceil_div(blocks, sp);
                 if (sp > 1 && per < 2 * waves) break;           // at least 2 blocks per wavefront
@@ -329,8 +330,9 @@ WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
                 const long wgs = tiles * sp;
                 const long rounds = (wgs + num_cus - 1) / num_cus;
                 const int bw = ceil_div(per, waves);             // blocks per wavefront
+                // a split also writes and re-reads sp fp32 partial planes (~4 TB/s)
                 const double us = 4.5 + rounds * (bw * bj * 4 * 64 / 2400.0 + ceil_div(bw, depth) * 1.2) +
-                                  (sp > 1 ? 2.5 : 0.0);
+                                  (sp > 1 ? 2.5 + 2.0 * sp * p.K * (double)p.M * 4 / 4.0e6 : 0.0);
                 if (us < best_us - 1e-9) {
                     best_us = us;
                     best.bj = bj;
