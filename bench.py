@@ -287,12 +287,16 @@ def main():
         g["layers"].append(d["layer"].name)
     dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
     avg_launch_us = dom["ms"] / dom["launches"] * 1e3
-    if dom_name.startswith("dw") or dom["flops"] == 0:
+    # The bound is the lower ceiling for the kernel's arithmetic intensity:
+    # HBM when its FLOP per algorithmic byte is below the ridge point
+    # (MFMA peak / HBM peak), else the MFMA peak of its dtype.
+    peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if dom_name.startswith("dw") or dom["flops"] < ridge * dom["bytes"]:
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(achieved, 2), peak=PEAK_HBM_GBS, unit="GB/s",
                     frac=round(achieved / PEAK_HBM_GBS, 4))
     else:
-        peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
         achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                     frac=round(achieved / peak, 4))
@@ -301,6 +305,12 @@ def main():
                 kernel=dom_name, launches_per_step=dom["launches"],
                 avg_launch_us=round(avg_launch_us, 3),
                 share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
+
+    # Stack-wide fraction of roofline: sum over layers of the time the layer
+    # needs at the binding peak (MFMA or HBM, whichever is slower for it),
+    # over the summed measured layer times.
+    t_roof = sum(max(d["flops"] / (peak * 1e12), d["bytes"] / (PEAK_HBM_GBS * 1e9)) for d in layers)
+    stack_roof_frac = t_roof / (float(layer_ms.sum()) * 1e-3)
 
     if args.layers:
         parts = [[] for _ in layers]
@@ -359,7 +369,8 @@ def main():
                    "wall_s_timed": round(wall, 4),
                    "timing": "value: one HIP graph of K passes between two events; roofline: kernel "
                              "execution times stamped by the runtime on K eager passes",
-                   "kernel_ms_per_step": round(float(launch_ms.sum()), 5)},
+                   "kernel_ms_per_step": round(float(launch_ms.sum()), 5),
+                   "stack_roofline_frac": round(stack_roof_frac, 4)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }
