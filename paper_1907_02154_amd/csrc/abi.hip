@@ -278,8 +278,7 @@ hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
     if (r.impl == IMPL_STEM_BF16)
         return launch_pack_stem(r.p, static_cast<const uint16_t *>(r.w), static_cast<uint16_t *>(dst), st);
     if (r.impl == IMPL_WAVE)
-        return launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(dst), r.wplan.krsc,
-                                st);
+        return launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(dst), st);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     return launch_pack_krsc(r.p, r.w, dst, elem, st);
 }

@@ -40,10 +40,11 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 }
 
 
-// BJ = 32-pixel blocks per wavefront tile; KRSC = the reduction is ordered
-// (r, s, c) with C/groups % 8 == 0, so the 4 taps of a half-block are 4
-// channels at one filter position: one padding check and one address per
-// half-block.  Filters are always read pre-packed (pack_wave_kernel):
+// BJ = 32-pixel blocks per wavefront tile; ORD = reduction order of the
+// packed filters: 1 = (r, s, c) with C/groups % 8 == 0, so the 4 taps of a
+// half-block are 4 channels at one filter position (one padding check and
+// one address per half-block); 2 = (r, s, c4), C/groups <= 4 padded to 4
+// channels (the stems: a half-block is one filter position); 0 = (c, r, s).  Filters are always read pre-packed (pack_wave_kernel):
 // w_pk[g][k/32][kr/8][lane][4] holds W[k0 + l%32][8*blk + 4*h + e], zero past
 // K and Kred, so a wavefront's A load is 1 KB contiguous.
 //
@@ -53,7 +54,7 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 // need no branches, which keeps the executed code short.  At batch 1 a
 // launch runs a few hundred instructions per wavefront from a cold
 // instruction cache, so code size is a first-order cost here.
-template <int R_, int S_, int WAVES, int BJ, bool KRSC>
+template <int R_, int S_, int WAVES, int BJ, int ORD>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     // position; blocks advance by WAVES, so one division at the start.
     const int cb = a.Cg / 8;
     int rsq = 0, rsr = 0, drq = 0, drr = 0;
-    if constexpr (KRSC && !(R_ == 1 && S_ == 1)) {
+    if constexpr (ORD == 1 && !(R_ == 1 && S_ == 1)) {
         const int b0 = kr_begin / 8 + wave;
         rsq = fdiv(b0, a.dv_cb);
         rsr = b0 - rsq * cb;
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 #pragma unroll
             for (int e = 0; e < 4; ++e) f.av[e] = __uint_as_float(v[e]);
         }
-        if constexpr (KRSC) {
+        if constexpr (ORD == 1) {
             // The block is one filter position (r, s) and 8 channels; the
             // reduction length is a multiple of 8, so its 4 taps per half are
             // live together and one channel stride apart.
@@ -169,6 +170,24 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     f.bv[j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, e * hw4, 0));
+            }
+        } else if constexpr (ORD == 2) {
+            // Half-block = filter position 2 * (block) + h, channels e < C/groups
+            // (the packed filters are zero for the padding channels and past R*S).
+            const int pos = 2 * (kr_begin / 8 + blk) + h;
+            const int r = pos / S;
+            const int s = pos - r * S;
+            const bool pok = pos < RS;
+#pragma unroll
+            for (int j = 0; j < BJ; ++j) {
+                const int ih = ih0[j] + r, iw = iw0[j] + s;
+                const bool ok = pok && mvalid[j] && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+                const unsigned base = 4u * (xoff[j] + ih * a.W + iw);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const unsigned off = select_offset(ok && e < a.Cg, base + e * hw4, kOut);
+                    f.bv[j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+                }
             }
         } else if constexpr (R_ == 1 && S_ == 1) {
             // 1x1 with C/groups % 8 != 0: tap kr is channel kr at the pixel's
@@ -282,15 +301,15 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     }
 }
 
-template <int R_, int S_, bool KRSC>
+template <int R_, int S_, int ORD>
 void launch_rs(const ConvArgs &a, int waves, int bj, dim3 grid, hipStream_t st)
 {
     if (waves == 8) {
-        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 2, KRSC>), grid, dim3(512), 0, st, a);
-        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 1, KRSC>), grid, dim3(512), 0, st, a);
+        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 2, ORD>), grid, dim3(512), 0, st, a);
+        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 1, ORD>), grid, dim3(512), 0, st, a);
     } else {
-        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, KRSC>), grid, dim3(256), 0, st, a);
-        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 1, KRSC>), grid, dim3(256), 0, st, a);
+        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, ORD>), grid, dim3(256), 0, st, a);
+        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 1, ORD>), grid, dim3(256), 0, st, a);
     }
 }
 
@@ -315,8 +334,8 @@ bool wave_fits(const ConvProblem &p)
 WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
 {
     WavePlan best{};
-    best.krsc = p.Cg % 8 == 0;
-    const int blocks = ceil_div(p.Kred, 8);
+    best.order = wave_order(p);
+    const int blocks = ceil_div(wave_kred(p), 8);
     double best_us = 1e30;
     for (int bj = 1; bj <= 2; ++bj) {
         if (bj == 2 && p.M < 64) continue;
@@ -352,9 +371,10 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
 {
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R == 0 || S == 0 || R != S) R = S = 0;
-    if (plan.krsc && R != 3 && R != 1) R = S = 0;
-    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %s>%s", R, S, plan.waves, plan.bj,
-             plan.krsc ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    if (plan.order == 1 && R != 3 && R != 1) R = S = 0;
+    if (plan.order == 2 && R != 3 && R != 7) R = S = 0;
+    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %d>%s", R, S, plan.waves, plan.bj, plan.order,
+             plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     *launches = plan.splits > 1 ? 2 : 1;
 }
 
@@ -370,6 +390,7 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
     a.ws = plan.splits > 1 ? ws : nullptr;
     a.splits = plan.splits;
     a.kr_per_split = plan.kr_per_split;
+    a.Kred = wave_kred(p);   // the packed reduction (padded channel quads for order 2)
     a.dv_mt = make_fastdiv(ceil_div(p.M, 32 * plan.bj));
     a.dv_kt = make_fastdiv(ceil_div(p.Kg, 32));
     a.dv_g = make_fastdiv(p.groups);
@@ -378,21 +399,24 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
                                plan.splits));
     hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
-    if (plan.krsc) {   // reduction ordered (r, s, c) in the packed filters
+    if (plan.order == 1) {   // reduction ordered (r, s, c) in the packed filters
         if (p.R == 1 && p.S == 1)
-            launch_rs<1, 1, true>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<1, 1, 1>(a, plan.waves, plan.bj, grid, st);
         else if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, true>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<3, 3, 1>(a, plan.waves, plan.bj, grid, st);
         else
-            launch_rs<0, 0, true>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<0, 0, 1>(a, plan.waves, plan.bj, grid, st);
+    } else if (plan.order == 2) {   // (r, s, c4): C/groups <= 4
+        if (p.R == 3 && p.S == 3)
+            launch_rs<3, 3, 2>(a, plan.waves, plan.bj, grid, st);
+        else if (p.R == 7 && p.S == 7)
+            launch_rs<7, 7, 2>(a, plan.waves, plan.bj, grid, st);
+        else
+            launch_rs<0, 0, 2>(a, plan.waves, plan.bj, grid, st);
     } else if (p.R == 1 && p.S == 1) {
-        launch_rs<1, 1, false>(a, plan.waves, plan.bj, grid, st);
-    } else if (p.R == 3 && p.S == 3) {
-        launch_rs<3, 3, false>(a, plan.waves, plan.bj, grid, st);
-    } else if (p.R == 7 && p.S == 7) {
-        launch_rs<7, 7, false>(a, plan.waves, plan.bj, grid, st);
+        launch_rs<1, 1, 0>(a, plan.waves, plan.bj, grid, st);
     } else {
-        launch_rs<0, 0, false>(a, plan.waves, plan.bj, grid, st);
+        launch_rs<0, 0, 0>(a, plan.waves, plan.bj, grid, st);
     }
     e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return e;

@@ -116,7 +116,7 @@ struct WavePlan {
     int splits;         // reduction splits across work-groups
     int kr_per_split;
     size_t ws_bytes;
-    bool krsc;          // reduction ordered (r, s, c) in the packed filters
+    int order;          // reduction order of the packed filters (wave_order)
 };
 // The wave kernel addresses x and its packed filters with 32-bit offsets.
 bool wave_fits(const ConvProblem &p);
@@ -216,9 +216,13 @@ size_t packed_bytes(const Resolved &r);      // bytes of the KRSC copy of the fi
 void set_krsc(Resolved &r, const void *packed);  // read filters pre-packed at `packed`
 // Filters in the wave kernel's A-operand order, w_pk[g][ceil(Kg/32)][ceil(Kred/8)][64][4]
 // (reduction order r, s, c when `krsc`, else c, r, s), zero-padded.
+// Reduction order of the wave kernel's packed filters: 0 = (c, r, s),
+// 1 = (r, s, c) for C/groups % 8 == 0, 2 = (r, s, c4) with C/groups <= 4
+// padded to 4 channels (R*S > 1); wave_kred is the packed reduction length.
+int wave_order(const ConvProblem &p);
+int wave_kred(const ConvProblem &p);
 size_t wave_packed_floats(const ConvProblem &p);
-hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, bool krsc,
-                            hipStream_t st);
+hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, hipStream_t st);
 hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
                             hipStream_t st);
 int set_hip_error(hipError_t e);   // records e for miconv_last_hip_error, returns MICONV_ERR_HIP

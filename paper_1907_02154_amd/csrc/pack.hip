@@ -27,13 +27,15 @@ __global__ __launch_bounds__(256) void pack_krsc_kernel(const T *__restrict__ sr
 
 // Wave-kernel order: one slot per (group, 32-filter block kb, 8-tap block b,
 // lane l, element e) holding W[kb*32 + l%32][8*b + 4*(l/32) + e], where the
-// reduction index runs over (r, s, c) when `krsc`, else over (c, r, s);
-// zero past K/groups and past C/groups*R*S.
+// reduction index runs over (c, r, s) (order 0), (r, s, c) (order 1) or
+// (r, s, c4) with C/groups <= 4 padded to 4 channels (order 2); zero past
+// K/groups and past the reduction.
 __global__ __launch_bounds__(256) void pack_wave_kernel(const float *__restrict__ src,
                                                         float *__restrict__ dst, int Kg, int Cg,
-                                                        int RS, int KB, int NB, int krsc, long total)
+                                                        int RS, int KB, int NB, int order, long total)
 {
-    const int Kred = Cg * RS;
+    const int Kred = Cg * RS;                        // source row length
+    const int Kpad = order == 2 ? 4 * RS : Kred;     // packed reduction length
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (long)gridDim.x * blockDim.x) {
         const int e = (int)(i & 3);
@@ -46,9 +48,12 @@ __global__ __launch_bounds__(256) void pack_wave_kernel(const float *__restrict_
         const int k = kb * 32 + (l & 31);
         const int kr = 8 * b + 4 * (l >> 5) + e;
         float v = 0.f;
-        if (k < Kg && kr < Kred) {
+        if (k < Kg && kr < Kpad) {
             const long row = ((long)g * Kg + k) * Kred;
-            if (krsc) {
+            if (order == 2) {
+                const int rs = kr >> 2, c = kr & 3;
+                if (c < Cg) v = src[row + (long)c * RS + rs];
+            } else if (order == 1) {
                 const int rs = kr / Cg, c = kr - rs * Cg;
                 v = src[row + (long)c * RS + rs];
             } else {
@@ -61,19 +66,27 @@ __global__ __launch_bounds__(256) void pack_wave_kernel(const float *__restrict_
 
 }  // namespace
 
-size_t wave_packed_floats(const ConvProblem &p)
+int wave_order(const ConvProblem &p)
 {
-    return (size_t)p.groups * ceil_div(p.Kg, 32) * ceil_div(p.Kred, 8) * 256;
+    if (p.Cg % 8 == 0) return 1;
+    if (p.Cg <= 4 && p.R * p.S > 1) return 2;
+    return 0;
 }
 
-hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, bool krsc,
-                            hipStream_t st)
+int wave_kred(const ConvProblem &p) { return wave_order(p) == 2 ? 4 * p.R * p.S : p.Kred; }
+
+size_t wave_packed_floats(const ConvProblem &p)
+{
+    return (size_t)p.groups * ceil_div(p.Kg, 32) * ceil_div(wave_kred(p), 8) * 256;
+}
+
+hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, hipStream_t st)
 {
     const long total = (long)wave_packed_floats(p);
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     launch_kernel(pack_wave_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, packed, p.Kg,
-                       p.Cg, p.R * p.S, ceil_div(p.Kg, 32), ceil_div(p.Kred, 8), krsc ? 1 : 0, total);
+                  p.Cg, p.R * p.S, ceil_div(p.Kg, 32), ceil_div(wave_kred(p), 8), wave_order(p), total);
     return hipGetLastError();
 }
 

@@ -77,6 +77,10 @@ DENSE_CASES = [
     (1, 1024, 7, 7, 40, 3, 3, 1, 1, 1),      # Kred 9216: wave split + work-group split
     (2, 250, 9, 9, 33, 1, 1, 1, 0, 1),       # Kred not a multiple of 4
     (1, 64, 60, 60, 64, 3, 3, 1, 1, 1),      # M >= 2048: two pixel blocks per tile
+    (1, 3, 45, 47, 40, 7, 7, 2, 3, 1),       # C <= 4 stem: reduction over (r, s, 4 channels), odd R*S
+    (2, 2, 19, 17, 33, 3, 3, 2, 1, 1),       # two channels padded to four
+    (1, 4, 13, 13, 20, 5, 5, 1, 2, 1),       # four channels, generic 5x5
+    (1, 8, 12, 10, 64, 3, 2, 1, 1, 2),       # C/groups = 4 in each of two groups, R != S
 ]
 
 
