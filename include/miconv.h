@@ -64,7 +64,10 @@ enum miconv_algo {
     MICONV_ALGO_DIRECT = 1, /* one output per lane, plain FMA loop: any shape and groups */
     MICONV_ALGO_IGEMM = 2,  /* implicit GEMM on MFMA with LDS-staged tiles (+ split-K when small) */
     MICONV_ALGO_WAVE = 3    /* implicit GEMM on MFMA fed straight from global memory by each
-                               wavefront, reduction split across wavefronts (small layers) */
+                               wavefront, reduction split across wavefronts; what AUTO picks for
+                               fp32 dense layers whose x and packed filters fit 2 GiB.  Packs the
+                               filters on every call (a stack packs them once); larger tensors:
+                               MICONV_ERR_UNSUPPORTED. */
 };
 
 /* Output extent: floor((H + 2*pad - R)/stride) + 1 and likewise for W.
