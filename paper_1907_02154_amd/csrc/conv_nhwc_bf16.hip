@@ -46,12 +46,17 @@ struct NhwcCopyArgs {
 template <int RV>
 __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];   // [channel][pixel]
+    constexpr int PX = 64;
+    // [channel][pixel]; channel row c is stored at row c ^ ((c >> 3) & 7), so
+    // the transposed reads (8 lanes on channel rows 8*o + e, o = 0..7) fall in
+    // 8 distinct bank groups
+    __shared__ __attribute__((aligned(16))) uint16_t tile[64][PX + 8];
+    auto row = [](int c) { return c ^ ((c >> 3) & 7); };
     const int t = threadIdx.x;
     const int c0 = (blockIdx.x % a.tiles_c) * 64;
-    const int p0 = (blockIdx.x / a.tiles_c) * 64;
+    const int p0 = (blockIdx.x / a.tiles_c) * PX;
     if constexpr (RV > 1) {
-        constexpr int GR = 64 / RV;                 // pixel groups per channel row
+        constexpr int GR = PX / RV;                 // pixel groups per channel row
 #pragma unroll
         for (int i = 0; i < 64 * GR / 256; ++i) {
             const int id = t + 256 * i;
@@ -62,37 +67,40 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
             const uint16_t *src = a.x + ((long)n * a.C + c0 + c) * a.HW + (px - (int)n * a.HW);
             if constexpr (RV == 8) {
                 const uint4 v = ok ? *reinterpret_cast<const uint4 *>(src) : make_uint4(0, 0, 0, 0);
-                *reinterpret_cast<uint4 *>(&tile[c][8 * o]) = v;
+                *reinterpret_cast<uint4 *>(&tile[row(c)][8 * o]) = v;
             } else {
                 const uint2 v = ok ? *reinterpret_cast<const uint2 *>(src) : make_uint2(0, 0);
-                *reinterpret_cast<uint2 *>(&tile[c][4 * o]) = v;
+                *reinterpret_cast<uint2 *>(&tile[row(c)][4 * o]) = v;
             }
         }
     } else {
-        const int px = p0 + (t & 63);
-        const bool pok = px < a.npq;
-        const unsigned n = fdiv(pok ? px : 0, a.dv_pq);
-        const unsigned pq = (pok ? px : 0) - n * a.PQ;
-        const unsigned pp = fdiv(pq, a.dv_q);
-        const unsigned q = pq - pp * a.Q;
-        const long off = (long)(pp * a.S) * a.W + q * a.S;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int c = (t >> 6) + 4 * i;
-            const bool ok = pok && c0 + c < a.C;
-            tile[c][t & 63] = ok ? a.x[((long)n * a.C + c0 + c) * a.HW + off] : 0;
+        for (int sub = 0; sub < PX / 64; ++sub) {
+            const int px = p0 + 64 * sub + (t & 63);
+            const bool pok = px < a.npq;
+            const unsigned n = fdiv(pok ? px : 0, a.dv_pq);
+            const unsigned pq = (pok ? px : 0) - n * a.PQ;
+            const unsigned pp = fdiv(pq, a.dv_q);
+            const unsigned q = pq - pp * a.Q;
+            const long off = (long)(pp * a.S) * a.W + q * a.S;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int c = (t >> 6) + 4 * i;
+                const bool ok = pok && c0 + c < a.C;
+                tile[row(c)][64 * sub + (t & 63)] = ok ? a.x[((long)n * a.C + c0 + c) * a.HW + off] : 0;
+            }
         }
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {   // 64 pixels x 8 channel octets
+    for (int i = 0; i < PX / 32; ++i) {   // PX pixels x 8 channel octets
         const int id = t + 256 * i;
         const int px = id >> 3, o = id & 7;
         if (c0 + 8 * o < a.C && p0 + px < a.npq) {
             uint32_t d[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                d[e] = (uint32_t)tile[8 * o + 2 * e][px] | ((uint32_t)tile[8 * o + 2 * e + 1][px] << 16);
+                d[e] = (uint32_t)tile[row(8 * o + 2 * e)][px] | ((uint32_t)tile[row(8 * o + 2 * e + 1)][px] << 16);
             *reinterpret_cast<uint4 *>(a.xt + (long)(p0 + px) * a.C + c0 + 8 * o) =
                 make_uint4(d[0], d[1], d[2], d[3]);
         }
@@ -660,6 +668,7 @@ ConvProblem copied_problem(const ConvProblem &p)
     }
     return q;
 }
+
 // Direct-to-LDS tiles: pixels x channels, wavefronts along pixels x channels,
 // pipeline depth.  LDS per work-group = depth * (bpx + bkc) * 128 bytes.
 struct TileD {
@@ -838,8 +847,8 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     ca.dv_hw = make_fastdiv(ca.HW);
     ca.dv_pq = make_fastdiv(ca.PQ);
     ca.dv_q = make_fastdiv(ca.Q);
-    const dim3 tg((unsigned)((long)ceil_div(ca.npq, 64) * ca.tiles_c)), tb(256);
     const int rv = copy_read_width(p, x);
+    const dim3 tg((unsigned)((long)ceil_div(ca.npq, 64) * ca.tiles_c)), tb(256);
     if (rv == 8)
         launch_kernel(nchw_to_nhwc_bf16_kernel<8>, tg, tb, 0, st, ca);
     else if (rv == 4)

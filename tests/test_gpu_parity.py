@@ -149,6 +149,9 @@ BF16_CASES = DENSE_CASES[:9] + [
     (2, 64, 9, 9, 64, 1, 1, 2, 1, 1),        # 1x1 stride 2 with padding: full copy
     (5, 64, 7, 7, 64, 1, 1, 1, 0, 1),        # 49-pixel planes: copy tiles span images
     (3, 64, 14, 14, 96, 3, 3, 1, 1, 1),      # 196-pixel planes: 4-pixel copy reads
+    (10, 256, 62, 62, 16, 1, 1, 1, 0, 1),    # large copy: 256-pixel tiles, 4-pixel reads
+    (32, 256, 63, 63, 16, 1, 1, 2, 0, 1),    # large sampled copy: 256-pixel tiles
+    (24, 256, 45, 45, 16, 1, 1, 1, 0, 1),    # large copy of odd planes: 256-pixel tiles, scalar reads
 ]
 
 
