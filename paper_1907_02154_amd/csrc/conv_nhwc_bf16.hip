@@ -726,16 +726,26 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     auto wgs = [&](int t) {
         return (long)ceil_div(p.M, kTilesD[t].bpx) * ceil_div(p.Kg, kTilesD[t].bkc) * p.groups;
     };
-    if (p.Kg > 64 && wgs(0) * 2 >= 3L * num_cus)
+    const int chunks = p.Kred / 64;
+    // Long reductions over few pixels (3x3 filters on 512 channels at 7x7):
+    // 128 x 128 tiles with the reduction split to about 1.5 work-groups per
+    // CU beat 64 x 64 tiles over the whole reduction (measured at batch 64:
+    // 25 + ~8 us reduce vs 44 us).
+    const bool long_red = p.R * p.S > 1 && chunks >= 64 && p.Kg > 64 && wgs(0) * 2 < num_cus;
+    if (long_red || (p.Kg > 64 && wgs(0) * 2 >= 3L * num_cus))
         plan.tile = 0;
     else if (wgs(1) >= num_cus)
         plan.tile = 1;
     else
         plan.tile = 2;
-    const int chunks = p.Kred / 64;
     int splits = 1;
     const long tiles = wgs(plan.tile);
-    if (tiles * 2 < num_cus && chunks >= 8) {
+    if (long_red) {
+        splits = (int)((3L * num_cus / 2 + tiles - 1) / tiles);
+        if (splits > chunks / 8) splits = chunks / 8;
+        const int per = ceil_div(chunks, splits);
+        splits = ceil_div(chunks, per);
+    } else if (tiles * 2 < num_cus && chunks >= 8) {
         splits = (int)((num_cus + tiles - 1) / tiles);
         if (splits > chunks / 4) splits = chunks / 4;
         const int per = ceil_div(chunks, splits);
