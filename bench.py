@@ -156,7 +156,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
-              "(this build has no multi-GPU path)", file=sys.stderr)
+              "(there is no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
     if args.dw_sweep:
         dw_sweep(args)

@@ -1,6 +1,6 @@
 """HBM traffic per kernel launch from rocprofv3 counter runs.
 
-Usage (on the GPU machine, after four counter runs, see below):
+Usage (on a machine with the GPU, after four counter runs, see below):
 
     python -m paper_1907_02154_amd.traffic --fetch DIR --write DIR \
         --copy-fetch DIR --copy-write DIR [--copy-bytes N] > traffic.txt
