@@ -597,7 +597,9 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         if (vec && m + 3 < a.M) {
             const int n = split_out ? 0 : m / a.PQ;
             const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
-            *reinterpret_cast<float4 *>(out + off) = v;
+            typedef float f32x4 __attribute__((ext_vector_type(4)));
+            const f32x4 nv = {v.x, v.y, v.z, v.w};
+            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
