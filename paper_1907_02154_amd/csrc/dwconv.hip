@@ -26,6 +26,9 @@
 namespace miconv {
 namespace {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+
 template <int V> struct VecT;
 template <> struct VecT<1> { typedef float type; };
 template <> struct VecT<2> { typedef float2 type; };
@@ -413,7 +416,8 @@ __global__ __launch_bounds__(256, 4) void dw_run_kernel(DwRunArgs a)
             const int ocnt = np * S::PQ;
             if (((uintptr_t)dst & 15) == 0) {          // outs is 16-byte aligned
                 for (int i = tid; i < ocnt / 4; i += 256)
-                    reinterpret_cast<float4 *>(dst)[i] = reinterpret_cast<const float4 *>(outs)[i];
+                    __builtin_nontemporal_store(reinterpret_cast<const f32x4 *>(outs)[i],
+                                                reinterpret_cast<f32x4 *>(dst) + i);
                 for (int i = ocnt / 4 * 4 + tid; i < ocnt; i += 256) dst[i] = outs[i];
             } else {
                 for (int i = tid; i < ocnt; i += 256) dst[i] = outs[i];
@@ -530,7 +534,7 @@ __global__ __launch_bounds__(256, 4) void dw_band_kernel(DwRunArgs a)
             }
             float *yo = dst + p0 * S::Q + q;
 #pragma unroll
-            for (int j = 0; j < S::RG; ++j) yo[j * S::Q] = a.relu ? fmaxf(acc[j], 0.f) : acc[j];
+            for (int j = 0; j < S::RG; ++j) __builtin_nontemporal_store(a.relu ? fmaxf(acc[j], 0.f) : acc[j], &yo[j * S::Q]);
         }
         __syncthreads();
         put();
