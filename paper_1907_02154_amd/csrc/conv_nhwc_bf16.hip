@@ -729,11 +729,11 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
         return (long)ceil_div(p.M, kTilesD[t].bpx) * ceil_div(p.Kg, kTilesD[t].bkc) * p.groups;
     };
     const int chunks = p.Kred / 64;
-    // Long reductions over few pixels (3x3 filters on 512 channels at 7x7):
-    // 128 x 128 tiles with the reduction split to about 1.5 work-groups per
-    // CU beat 64 x 64 tiles over the whole reduction (measured at batch 64:
-    // 25 + ~8 us reduce vs 44 us).
-    const bool long_red = p.R * p.S > 1 && chunks >= 64 && p.Kg > 64 && wgs(0) * 2 < num_cus;
+    // Long reductions over few pixels (512-channel 3x3 and 2048-channel 1x1
+    // layers at 7x7): 128 x 128 tiles with the reduction split to about 1.5
+    // work-groups per CU beat 64 x 64 tiles over the whole reduction
+    // (measured at batch 64: 3x3 25 + 8 us reduce vs 44 us; 1x1 15 + 9 vs 28).
+    const bool long_red = chunks >= 32 && p.Kg > 64 && wgs(0) * 2 < num_cus;
     if (long_red || (p.Kg > 64 && wgs(0) * 2 >= 3L * num_cus))
         plan.tile = 0;
     else if (wgs(1) >= num_cus)
