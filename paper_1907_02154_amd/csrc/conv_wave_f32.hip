@@ -1,6 +1,8 @@
-// Dense conv2d in fp32 for small GEMM extents (batch-1 layers): an implicit
-// GEMM in which every wavefront feeds the matrix cores straight from global
-// memory, with no LDS staging and no barriers in the main loop.
+// Dense conv2d in fp32 as an implicit GEMM in which every wavefront feeds
+// the matrix cores straight from global memory: no LDS staging and no
+// barriers in the main loop.  It serves every fp32 dense layer whose tensors
+// it can address with 32-bit offsets, from batch-1 ResNet layers to VGG-16
+// at batch 32.
 //
 // Why: at batch 1 the layers of ResNet-50 / MobileNet have N*P*Q = 49..12544
 // output pixels, so an LDS-staged tile kernel runs few chunks per
@@ -9,16 +11,18 @@
 // reduction with several blocks of loads in flight, and the parallelism the
 // output tiles lack is recovered by splitting the reduction across the
 // wavefronts of a work-group (combined through LDS in a fixed order) and, for
-// the smallest layers, across work-groups (splitk_reduce_kernel).
+// the smallest layers, across work-groups (splitk_reduce_kernel).  At large
+// batch the same structure needs no LDS reuse: an fp32 MFMA consumes one
+// 4-byte operand per lane per 64 cycles, which the L1 path sustains.
 //
 // MFMA v_mfma_f32_32x32x2_f32, lane l of 64, half h = l / 32:
 //   A operand = W[k0 + l%32][kr],  B operand = X[kr][m0 + l%32]
 // The reduction is walked in blocks of 8 taps; in block b, step e (0..3),
 // half h supplies tap kr = 8b + 4h + e.  The MFMA sums over both halves, so
 // the 4 steps cover the block's 8 taps once, and a lane's A values for the 4
-// steps are 4 consecutive floats of a KCRS filter row: one 16-byte load.  Its
-// B values are 4 gathered taps of the im2col matrix for one output pixel;
-// the 32 lanes of a half read 32 consecutive pixels of the same tap.
+// steps are 4 consecutive floats of a packed filter row: one 16-byte load.
+// Its B values are 4 gathered taps of the im2col matrix for one output
+// pixel; the 32 lanes of a half read 32 consecutive pixels of the same tap.
 // Output: D reg v is channel 8*(v/4) + 4*h + v%4 and pixel l%32, so every
 // store writes 32 consecutive pixels (128 bytes) of one NCHW channel plane.
 #include "internal.h"
@@ -44,9 +48,10 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 // packed filters: 1 = (r, s, c) with C/groups % 8 == 0, so the 4 taps of a
 // half-block are 4 channels at one filter position (one padding check and
 // one address per half-block); 2 = (r, s, c4), C/groups <= 4 padded to 4
-// channels (the stems: a half-block is one filter position); 0 = (c, r, s).  Filters are always read pre-packed (pack_wave_kernel):
-// w_pk[g][k/32][kr/8][lane][4] holds W[k0 + l%32][8*blk + 4*h + e], zero past
-// K and Kred, so a wavefront's A load is 1 KB contiguous.
+// channels (the stems: a half-block is one filter position); 0 = (c, r, s).
+// Filters are always read pre-packed (pack_wave_kernel): w_pk[g][k/32][kr/8]
+// [lane][4] holds W[k0 + l%32][8*blk + 4*h + e], zero past K and the
+// reduction, so a wavefront's A load is 1 KB contiguous.
 //
 // Both operands are read through buffer resources.  A tap outside the image,
 // a pixel past M, a block past the split and a tap past the reduction get the
