@@ -40,6 +40,7 @@ struct NhwcCopyArgs {
     int C, H, W, Q, S, HW, PQ;
     int npq;             // N * P * Q
     int tiles_c;
+    int cb;              // channels per work-group (whole-plane kernel)
     FastDiv dv_hw, dv_pq, dv_q;
 };
 
@@ -104,6 +105,42 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
             *reinterpret_cast<uint4 *>(a.xt + (long)(p0 + px) * a.C + c0 + 8 * o) =
                 make_uint4(d[0], d[1], d[2], d[3]);
         }
+    }
+}
+
+// Small planes (32*H*W <= kPlaneElems): a work-group moves one image's block
+// of cb channels (64, or fewer so that the block fits in LDS and the grid
+// still fills the chip; a multiple of 8).  In NCHW that block, [cb][H][W], is one contiguous run of cb*H*W
+// values, so it is read with 16-byte loads whatever H*W is (no pixel group of
+// a load can straddle two images), staged in LDS as is, and each lane then
+// gathers 8 channels of one sampled pixel from LDS and writes them as one
+// 16-byte store.  Requires C % 8 == 0 and a 16-byte aligned x.
+constexpr int kPlaneElems = 16384;    // 32 KB of LDS
+
+__global__ __launch_bounds__(256) void nchw_to_nhwc_plane_bf16_kernel(NhwcCopyArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t plane[kPlaneElems];
+    const int t = threadIdx.x;
+    const int n = blockIdx.x / a.tiles_c;
+    const int c0 = (blockIdx.x % a.tiles_c) * a.cb;
+    const int cn = min(a.cb, a.C - c0);                // a multiple of 8
+    const uint4 *src = reinterpret_cast<const uint4 *>(a.x + ((long)n * a.C + c0) * a.HW);
+    const int units = cn * a.HW / 8;
+    uint4 *dst = reinterpret_cast<uint4 *>(plane);
+    for (int u = t; u < units; u += 256) dst[u] = src[u];
+    __syncthreads();
+    const int oct = cn / 8;
+    uint16_t *out = a.xt + (long)n * a.PQ * a.C + c0;
+    for (int id = t; id < a.PQ * oct; id += 256) {
+        const int pq = id / oct, o = id - pq * oct;
+        const int pp = (int)fdiv((unsigned)pq, a.dv_q);
+        const int hw = pp * a.S * a.W + (pq - pp * a.Q) * a.S;
+        const uint16_t *col = plane + 8 * o * a.HW + hw;
+        uint32_t d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            d[e] = (uint32_t)col[2 * e * a.HW] | ((uint32_t)col[(2 * e + 1) * a.HW] << 16);
+        *reinterpret_cast<uint4 *>(out + (long)pq * a.C + 8 * o) = make_uint4(d[0], d[1], d[2], d[3]);
     }
 }
 
@@ -322,10 +359,36 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
 // and each load instruction still fills 1 KB of LDS contiguously.
 __device__ inline int unit_swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
+// 32-channel chunks (rows of 4 units, 64 bytes): unit u of row r sits at
+// slot u ^ ((r >> 2) & 3), so 16 consecutive rows read at one logical unit
+// cover all 16 bank groups of 256 bytes.
+template <int UPR>
+__device__ inline int row_swz(int row)
+{
+    if constexpr (UPR == 8) return unit_swz(row);
+    else return (row >> 2) & 3;
+}
+
 template <int N>
 __device__ inline void wait_vmcnt()
 {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `ahead` (uniform, 0 <= ahead <= MAXA) groups of LOADS
+// loads of this lane are outstanding.
+template <int LOADS, int MAXA>
+__device__ inline void wait_ahead(int ahead)
+{
+    if constexpr (MAXA > 0) {
+        if (ahead >= MAXA) {
+            wait_vmcnt<MAXA * LOADS>();
+            return;
+        }
+        wait_ahead<LOADS, MAXA - 1>(ahead);
+    } else {
+        wait_vmcnt<0>();
+    }
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -341,19 +404,20 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // lanes, lane 4e+t points at 4 pixels of channel row e and lane i receives
 // pixel i of the 4 rows.  The permuted units put the 4 rows of one read in 4
 // different 64-byte bank groups.
-template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, bool NCHWB>
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, bool NCHWB, int KRC = 64>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
 {
     constexpr int NT = 64 * WPX * WCH;
-    constexpr int KRC = 64;
+    constexpr int UPR = KRC / 8;                        // 16-byte units per operand row
     constexpr int TPX = BPX / WPX, TCH = BKC / WCH;     // one wavefront's tile
     constexpr int BJ = TPX / 32, BI = TCH / 32;         // pixel blocks, channel blocks
-    constexpr int UA = BKC * 8, UB = BPX * 8;           // 16-byte units per stage
+    constexpr int UA = BKC * UPR, UB = BPX * UPR;       // 16-byte units per stage
     constexpr int LA = UA / NT, LB = UB / NT;           // load instructions per lane per chunk
     constexpr int LOADS = LA + LB;
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UB % NT == 0, "tile shape");
-    static_assert(NST >= 2 && NST <= 4, "pipeline depth");
-    static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1), "NCHW pixel operand: 1x1, 128-pixel tiles");
+    static_assert(NST >= 2 && NST <= 8 && (NST - 2) * LOADS <= 63, "pipeline depth");
+    static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1 && KRC == 64), "NCHW pixel operand: 1x1, 128-pixel tiles");
+    static_assert(KRC == 64 || KRC == 32, "reduction chunk");
 
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
     constexpr int SMEM = NST * (UA + UB) > BKC * OP / 4 ? NST * (UA + UB) : BKC * OP / 4;
@@ -404,8 +468,8 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
         const int u = i * NT + tid;
-        const int row = u >> 3;
-        const int kg = (u & 7) ^ unit_swz(row);
+        const int row = u / UPR;
+        const int kg = (u % UPR) ^ row_swz<UPR>(row);
         const int k = k0 + row;
         aok[i] = k < a.Kg;
         aoffs[i] = (unsigned)((((long)g * a.Kg + (aok[i] ? k : 0)) * a.Kred + kg * 8) * 2);
@@ -427,8 +491,8 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
             boffs[i] = (int)(((long)n * a.C + (long)g * a.Cg + c) * a.HW + (mm - n * a.HW));
             continue;
         }
-        const int row = u >> 3;
-        const int kg = (u & 7) ^ unit_swz(row);
+        const int row = u / UPR;
+        const int kg = (u % UPR) ^ row_swz<UPR>(row);
         const int m = m0 + row;
         const bool ok = m < a.M;
         const int mm = ok ? m : 0;
@@ -478,12 +542,12 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 
     // Operand reads: row offsets (in units) and the permuted slot of unit
     // 2*ks + h, per 16-wide reduction step ks.
-    const int fl = unit_swz(ll);
+    const int fl = row_swz<UPR>(ll);
     int aoff[BI], boff[BJ];
 #pragma unroll
-    for (int bi = 0; bi < BI; ++bi) aoff[bi] = (wch * TCH + bi * 32 + ll) * 8;
+    for (int bi = 0; bi < BI; ++bi) aoff[bi] = (wch * TCH + bi * 32 + ll) * UPR;
 #pragma unroll
-    for (int bj = 0; bj < BJ; ++bj) boff[bj] = UA + (wpx * TPX + bj * 32 + ll) * 8;
+    for (int bj = 0; bj < BJ; ++bj) boff[bj] = UA + (wpx * TPX + bj * 32 + ll) * UPR;
 
     floatx16 acc[BJ][BI];
 #pragma unroll
@@ -541,9 +605,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         // this lane's loads of chunk t are done once at most `ahead` later
         // chunks' loads are outstanding
         const int ahead = min(NST - 2, nchunks - 1 - t);
-        if (NST >= 4 && ahead == 2) wait_vmcnt<2 * LOADS>();
-        else if (NST >= 3 && ahead == 1) wait_vmcnt<LOADS>();
-        else wait_vmcnt<0>();
+        wait_ahead<LOADS, NST - 2>(ahead);
         // every lane's chunk t is in LDS, and every wavefront is done with chunk t-1
         asm volatile("s_barrier" ::: "memory");
         if (t + NST - 1 < nchunks) issue(t + NST - 1);
@@ -647,11 +709,19 @@ bool copy_subsamples(const ConvProblem &p)
     return p.R == 1 && p.S == 1 && p.pad == 0 && p.stride > 1;
 }
 
-// Pixels per global read of the channel-last copy (x may be null: describe).
+// Pixels per global read of the channel-last copy (x may be null: describe);
+// 0 selects the whole-plane kernel, used for planes of up to 512 pixels that
+// the tiled kernel could only read pixel by pixel (measured at batch 64:
+// 49-pixel planes 10 -> 4.5 us, 14x14 planes sampled at stride 2 12 -> 7.8
+// us; 28x28 planes sampled at stride 2, in 16-channel blocks, 15.3 -> 16.6
+// us, so larger planes stay with the tiled kernel; for 196-pixel planes, which
+// it reads 4 pixels at a time, the two are even).
 int copy_read_width(const ConvProblem &p, const void *x)
 {
     const uintptr_t xa = (uintptr_t)x;
     const int HW = p.H * p.W;
+    const bool scalar = copy_subsamples(p) || HW % 4 != 0;
+    if (scalar && 32 * HW <= kPlaneElems && p.C % 8 == 0 && xa % 16 == 0) return 0;
     if (copy_subsamples(p)) return 1;
     if (HW % 8 == 0 && xa % 16 == 0) return 8;
     if (HW % 4 == 0 && xa % 8 == 0) return 4;
@@ -671,6 +741,17 @@ ConvProblem copied_problem(const ConvProblem &p)
     return q;
 }
 
+// Channel block of the whole-plane copy: 64, halved (down to 8) while the
+// block exceeds the LDS buffer or the grid of N * C / cb work-groups would
+// hold fewer than two per CU.
+int plane_copy_block(const ConvProblem &p, int num_cus)
+{
+    const long hw = (long)p.H * p.W;
+    int cb = 64;
+    while (cb > 8 && (cb * hw > kPlaneElems || (long)p.N * ceil_div(p.C, cb) < 2L * num_cus)) cb /= 2;
+    return cb;
+}
+
 // Direct-to-LDS tiles: pixels x channels, wavefronts along pixels x channels,
 // pipeline depth.  LDS per work-group = depth * (bpx + bkc) * 128 bytes.
 struct TileD {
@@ -679,7 +760,8 @@ struct TileD {
 const TileD kTilesD[] = {
     {128, 128, 2, 2, 2},   // 64 KB: two work-groups per CU, wavefront tile 64 x 64
     {128, 64, 2, 2, 2},    // 48 KB: three per CU, wavefront tile 64 x 32
-    {64, 64, 2, 2, 2},     // 32 KB: four per CU, wavefront tile 32 x 32
+    {64, 64, 2, 2, 3},     // 48 KB: three per CU, wavefront tile 32 x 32, three stages
+    {128, 64, 2, 2, 3},    // tile 1 with a third stage: 72 KB, two per CU
 };
 
 template <int R_, int S_>
@@ -688,7 +770,8 @@ void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
     switch (tile) {
     case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
     case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
-    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
+    case 2: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 3, false>), grid, dim3(256), 0, st, a); break;
+    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 3, false>), grid, dim3(256), 0, st, a); break;
     }
 }
 
@@ -759,8 +842,17 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     // 1x1 stride-1 layers with 8-pixel rows read x in NCHW directly
     plan.nchwb = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && (p.H * p.W) % 8 == 0 &&
                  plan.tile <= 1 && (uintptr_t)x % 16 == 0;
+    // A 128 x 64 grid that fits in two work-groups per CU loses no occupancy
+    // to a third LDS stage, which then hides more of the global -> LDS
+    // latency (measured at batch 64: 14x14 3x3 layers 33.2 -> 29.2 us,
+    // 1024-channel 1x1 at 14x14 19.0 -> 16.0 us; grids of several rounds, as
+    // at 56x56, lose 10%).  64 x 64 grids are never larger than that (the
+    // planner takes them only when 128 x 64 leaves CUs idle), so tile 2 always
+    // has three stages (1024-channel 1x1, stride 2, 14x14 -> 7x7: 17.7 -> 14.1 us).
+    if (!plan.nchwb && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
     const ConvProblem cp = copied_problem(p);
     plan.xcl_bytes = plan.nchwb ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
+    plan.copy_cb = plane_copy_block(p, num_cus);
     return plan;
 }
 
@@ -792,6 +884,7 @@ NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x)
     }
     const ConvProblem cp = copied_problem(p);
     plan.xcl_bytes = (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
+    plan.copy_cb = plane_copy_block(p, num_cus);
     return plan;
 }
 
@@ -801,7 +894,11 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R != S) R = S = 0;
     char tname[64];
-    snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", copy_read_width(p, nullptr));
+    const int rv = copy_read_width(p, nullptr);
+    if (rv == 0)
+        snprintf(tname, sizeof tname, "nchw_to_nhwc_plane_bf16_kernel");
+    else
+        snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s>%s",
@@ -861,7 +958,14 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     ca.dv_q = make_fastdiv(ca.Q);
     const int rv = copy_read_width(p, x);
     const dim3 tg((unsigned)((long)ceil_div(ca.npq, 64) * ca.tiles_c)), tb(256);
-    if (rv == 8)
+    if (rv == 0) {
+        // the block must fit the kernel's LDS buffer (32 * H*W always does here)
+        ca.cb = plan.copy_cb >= 8 ? plan.copy_cb : 64;
+        while (ca.cb > 8 && ca.cb * ca.HW > kPlaneElems) ca.cb /= 2;
+        ca.tiles_c = ceil_div(p.C, ca.cb);
+        launch_kernel(nchw_to_nhwc_plane_bf16_kernel, dim3((unsigned)((long)p.N * ca.tiles_c)), tb, 0, st, ca);
+    }
+    else if (rv == 8)
         launch_kernel(nchw_to_nhwc_bf16_kernel<8>, tg, tb, 0, st, ca);
     else if (rv == 4)
         launch_kernel(nchw_to_nhwc_bf16_kernel<4>, tg, tb, 0, st, ca);

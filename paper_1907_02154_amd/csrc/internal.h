@@ -145,6 +145,7 @@ struct NhwcPlan {
     int kr_per_split;
     size_t partial_bytes; // split-K partials
     size_t xcl_bytes;     // the channel-last copy of x
+    int copy_cb;          // channels per work-group of the whole-plane copy
 };
 bool nhwc_bf16_eligible(const ConvProblem &p);
 NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x);

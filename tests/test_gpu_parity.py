@@ -142,16 +142,21 @@ BF16_CASES = DENSE_CASES[:9] + [
     (1, 64, 9, 9, 48, 3, 3, 1, 1, 2),        # channel-last path, grouped (C/groups = 32)
     (3, 96, 13, 11, 130, 1, 1, 1, 0, 1),     # channel-last 1x1, chunk of 32 channels
     (1, 256, 7, 7, 520, 3, 3, 1, 1, 1),      # long reduction: split across work-groups
-    (2, 64, 14, 14, 128, 1, 1, 2, 0, 1),     # 1x1 stride 2: only the sampled pixels are copied
-    (3, 64, 7, 9, 72, 1, 1, 2, 0, 1),        # sampled copy, odd plane, P x Q = 4 x 5
-    (1, 128, 28, 28, 64, 1, 1, 3, 0, 1),     # sampled copy, stride 3
-    (2, 96, 10, 10, 64, 1, 1, 2, 0, 1),      # sampled copy, 32-channel chunks
-    (2, 64, 9, 9, 64, 1, 1, 2, 1, 1),        # 1x1 stride 2 with padding: full copy
-    (5, 64, 7, 7, 64, 1, 1, 1, 0, 1),        # 49-pixel planes: copy tiles span images
+    (2, 64, 14, 14, 128, 1, 1, 2, 0, 1),     # 1x1 stride 2: only the sampled pixels are copied (whole-plane copy)
+    (3, 64, 7, 9, 72, 1, 1, 2, 0, 1),        # sampled whole-plane copy, odd plane, P x Q = 4 x 5
+    (1, 128, 28, 28, 64, 1, 1, 3, 0, 1),     # sampled copy, stride 3, scalar reads
+    (2, 96, 10, 10, 64, 1, 1, 2, 0, 1),      # sampled whole-plane copy, a 32-channel block
+    (2, 64, 9, 9, 64, 1, 1, 2, 1, 1),        # 1x1 stride 2 with padding: full (whole-plane) copy
+    (5, 64, 7, 7, 64, 1, 1, 1, 0, 1),        # 49-pixel planes (whole-plane copy)
     (3, 64, 14, 14, 96, 3, 3, 1, 1, 1),      # 196-pixel planes: 4-pixel copy reads
+    (2, 64, 15, 17, 64, 3, 3, 1, 1, 1),      # 255-pixel planes: the largest whole-plane copy
+    (2, 64, 17, 16, 64, 3, 3, 1, 1, 1),      # 272-pixel planes: 8-pixel copy reads
+    (3, 160, 7, 7, 64, 1, 1, 1, 0, 1),       # whole-plane copy with a last block of 32 channels
+    (2, 64, 15, 17, 64, 1, 1, 2, 0, 1),      # sampled whole-plane copy, 255-pixel planes, P x Q = 8 x 9
     (10, 256, 62, 62, 16, 1, 1, 1, 0, 1),    # large copy: 256-pixel tiles, 4-pixel reads
     (32, 256, 63, 63, 16, 1, 1, 2, 0, 1),    # large sampled copy: 256-pixel tiles
     (24, 256, 45, 45, 16, 1, 1, 1, 0, 1),    # large copy of odd planes: 256-pixel tiles, scalar reads
+    (2, 64, 21, 23, 64, 3, 3, 1, 1, 1),      # 483-pixel planes: whole-plane copy in 32-channel blocks
 ]
 
 
@@ -167,6 +172,39 @@ def test_bf16_small_int_bitwise(oracle_lib, case, algo):
     y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True, algo=algo)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), ref)
+
+
+OFFSET_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups) run on x and y at odd element offsets
+    (2, 64, 7, 7, 64, 1, 1, 1, 0, 1),
+    (2, 64, 14, 14, 96, 3, 3, 1, 1, 1),
+    (2, 64, 14, 14, 64, 1, 1, 2, 0, 1),
+    (1, 64, 16, 16, 128, 1, 1, 1, 0, 1),
+]
+
+
+@pytest.mark.parametrize("case", OFFSET_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_bf16_offset_pointers_small_int_bitwise(oracle_lib, case):
+    """x one bf16 element and y one float past a 16-byte boundary: the
+    channel-last copy falls back to reads that need no alignment, the 1x1
+    layer that would read x in NCHW takes the copy, and the epilogue stores
+    element by element; results stay exact on small integers."""
+    N, C, H, W, K, R, S, st, pad, g = case
+    seed = 3900 + sum(case)
+    x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
+    w = wl.to_bf16_bits(ints((K, C // g, R, S), -4, 4, seed + 1))
+    b = ints((K,), -8, 8, seed + 2)
+    ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
+    xb = torch.empty(x.size + 8, dtype=torch.int16, device="cuda")
+    xb[1:1 + x.size] = torch.from_numpy(x.reshape(-1).view(np.int16)).cuda()
+    tx = xb[1:1 + x.size].view(torch.bfloat16).view(N, C, H, W)
+    assert tx.data_ptr() % 16 == 2
+    P, Q = miconv.out_dims(H, W, R, S, st, pad)
+    yb = torch.full((N * K * P * Q + 4,), float("nan"), device="cuda")
+    ty = yb[1:1 + N * K * P * Q].view(N, K, P, Q)
+    miconv.conv2d_fwd_bf16(tx, dev_bf16_bits(w), dev(b), ty, st, pad, g, True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ty.cpu().numpy(), ref, err_msg=str(case))
+    assert torch.isnan(yb[0]) and torch.isnan(yb[-3:]).all()   # nothing written outside y
 
 
 NCHW_1X1_CASES = [  # (N, C, H, W, K, groups): 1x1 stride-1 layers whose pixel operand comes from NCHW x
