@@ -335,6 +335,40 @@ def test_dense_deterministic():
     assert torch.equal(y1, y2)
 
 
+SPLIT_CASES = [  # batch-1 layers whose reduction the wave planner splits (ResNet-50 s3/s4/s5)
+    (1, 128, 28, 28, 128, 3, 3, 1, 1, 1),
+    (1, 1024, 14, 14, 256, 1, 1, 1, 0, 1),
+    (1, 512, 7, 7, 512, 3, 3, 1, 1, 1),
+]
+
+
+def test_split_reduction_shared_workspace(oracle_lib):
+    """Split layers write their partials into the per-stream workspace, which
+    channel-last bf16 calls in between also use (for x's copy and their own
+    partials): calls of different shapes, repeated and interleaved, must all
+    stay exact on small integers."""
+    data = []
+    for i, (N, C, H, W, K, R, S, st, pad, g) in enumerate(SPLIT_CASES):
+        x = ints((N, C, H, W), -3, 3, 4100 + i)
+        w = ints((K, C // g, R, S), -3, 3, 4200 + i)
+        b = ints((K,), -8, 8, 4300 + i)
+        name, launches = miconv.conv2d_describe(N, C, H, W, K, R, S, st, pad, g, "f32")
+        assert "igemm_wave_f32_kernel" in name and "splitk_reduce" in name, name
+        data.append((x, w, b, st, pad, g, oracle_lib.conv2d(x, w, b, st, pad, g, True)))
+    bx = wl.to_bf16_bits(ints((2, 64, 30, 30), -4, 4, 4400))
+    bw = wl.to_bf16_bits(ints((64, 64, 3, 3), -4, 4, 4401))
+    bb = ints((64,), -8, 8, 4402)
+    bref = oracle_lib.conv2d_bf16(bx, bw, bb, 1, 1, 1, True)
+    for order in ([0, 1, 2, 0], [2, 1, 0, 2, 2]):
+        for j in order:
+            x, w, b, st, pad, g, ref = data[j]
+            y = miconv.conv2d(dev(x), dev(w), dev(b), st, pad, g, True)
+            yb = miconv.conv2d(dev_bf16_bits(bx), dev_bf16_bits(bw), dev(bb), 1, 1, 1, True)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"case {j}")
+            np.testing.assert_array_equal(yb.cpu().numpy(), bref)
+
+
 def test_maxpool_add_cast(oracle_lib):
     rng = np.random.default_rng(0)
     for (N, C, H, W, R, st, pad) in [(1, 64, 112, 112, 3, 2, 1), (2, 64, 224, 224, 2, 2, 0), (1, 3, 7, 9, 3, 2, 1)]:
