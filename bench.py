@@ -23,6 +23,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -56,6 +57,44 @@ def measured_traffic(kernel: str):
                     return None
                 return int(parts[2]) + int(parts[3])
     return None
+
+
+def gpu_info(torch) -> dict:
+    """Device properties, plus clocks and socket power from amd-smi when it answers."""
+    p = torch.cuda.get_device_properties(0)
+    info = dict(name=p.name, arch=getattr(p, "gcnArchName", "").split(":")[0],
+                cus=p.multi_processor_count, hbm_gib=round(p.total_memory / 2 ** 30))
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--power", "--json"],
+                           capture_output=True, text=True, timeout=30)
+        d = json.loads(r.stdout)
+        d = (d["gpu_data"] if isinstance(d, dict) else d)[0]
+        info["gfx_clk_max_mhz"] = d["clock"]["gfx_0"]["max_clk"]["value"]
+        info["mem_clk_max_mhz"] = d["clock"]["mem_0"]["max_clk"]["value"]
+        info["socket_power_w_after_run"] = d["power"]["socket_power"]["value"]
+    except Exception:
+        pass
+    try:
+        r = subprocess.run(["rocm-smi", "--showmaxpower", "--json"], capture_output=True, text=True,
+                           timeout=30)
+        for card in json.loads(r.stdout).values():
+            for k, v in card.items():
+                if "Power" in k:
+                    info["power_cap_w"] = float(v)
+    except Exception:
+        pass
+    return info
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def parse():
@@ -144,7 +183,7 @@ def dw_sweep(args):
            "ms_per_step": round(tot_ms, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "f32", "data": "synthetic (device-seeded uniform)",
            "config": {"workload": f"MobileNet-v1 depthwise layers, batch {args.dw_sweep}",
-                      "algorithmic_bytes": tot_bytes},
+                      "algorithmic_bytes": tot_bytes, "device": gpu_info(torch)},
            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
            "copy_ceiling_GBs": round(copy_gbs, 1),
@@ -313,15 +352,21 @@ def main():
     stack_roof_frac = t_roof / (float(layer_ms.sum()) * 1e-3)
 
     if args.layers:
+        # per layer: mean over the K passes (the launch parts), and the median,
+        # 10th and 90th percentile of the layer's per-pass time
         parts = [[] for _ in layers]
+        per_pass = np.zeros((per_launch_ms.shape[0], len(layers)))
         for j in range(n_launch):
             parts[launch_info[j][0]].append(float(launch_ms[j]) * 1e3)
+            per_pass[:, launch_info[j][0]] += per_launch_ms[:, j]
         for j, d in enumerate(layers):
             l = d["layer"]
             t = float(layer_ms[j])
+            p10, med, p90 = (float(v) * 1e3 for v in np.percentile(per_pass[:, j], [10, 50, 90]))
             split = " [" + " + ".join(f"{u:.2f}" for u in parts[j]) + "]" if len(parts[j]) > 1 else ""
             print(f"{j:3d} {l.name:10s} {d['kernel']:45s} {t * 1e3:9.2f} us "
-                  f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s{split}",
+                  f"{d['flops'] / t / 1e9:8.2f} TFLOP/s {d['bytes'] / t / 1e6:8.1f} GB/s "
+                  f"(median {med:.2f}, p10 {p10:.2f}, p90 {p90:.2f} us){split}",
                   file=sys.stderr)
 
     # CPU baseline: the oracle on a bounded prefix of the same layers.
@@ -346,7 +391,7 @@ def main():
             if t_cpu > args.cpu_seconds:
                 break
         cpu = dict(value=round(done_flops / t_cpu / 1e12, 6), unit="TFLOP/s",
-                   cores=oracle.num_threads(), kind="oracle",
+                   cores=oracle.num_threads(), cpu=cpu_model(), kind="oracle",
                    sample=f"{len(sample)} of {len(layers)} layers ({sample[0]}..{sample[-1]}), "
                           f"{done_flops / 1e9:.3f} GFLOP in {t_cpu:.2f} s, fp64 accumulation")
 
@@ -365,7 +410,7 @@ def main():
         "dtype": "bf16-in/f32-acc" if bf16 else "f32",
         "data": "synthetic (seeded uniform/He-normal per layer, resident in HBM)",
         "config": {"workload": wk.name, "convs": len(layers), "batch": wk.layers[0].N,
-                   "gflop_per_step": round(step_flops / 1e9, 4), "device": torch.cuda.get_device_name(0),
+                   "gflop_per_step": round(step_flops / 1e9, 4), "device": gpu_info(torch),
                    "wall_s_timed": round(wall, 4),
                    "timing": "value: one HIP graph of K passes between two events; roofline: kernel "
                              "execution times stamped by the runtime on K eager passes",

@@ -901,7 +901,8 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
         snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
-        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s>%s",
+        // the instantiation's full name, reduction chunk included (every launch uses 64)
+        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s, 64>%s",
                  plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
                  plan.nchwb ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
         *launches = (plan.nchwb ? 1 : 2) + (plan.splits > 1 ? 1 : 0);

@@ -16,6 +16,12 @@ namespaces and argument list dropped), giving the mean calibrated bytes read
 and written per dispatch, the scales, the dispatch count, and the SHA-1 of the
 HIP source that defines the kernel, so a reader can tell when the numbers no
 longer describe the code.
+
+    python -m paper_1907_02154_amd.traffic --counters DIR [DIR ...] [--match TEXT]
+
+prints, for every kernel whose name contains TEXT, the mean per dispatch of
+every counter found in the given counter-run directories (any counters), with
+the dispatch count and the source SHA-1.
 """
 from __future__ import annotations
 
@@ -39,6 +45,7 @@ SOURCES = {
     "igemm_bf16_nhwc_kernel": "conv_nhwc_bf16.hip",
     "igemm_bf16_dma_kernel": "conv_nhwc_bf16.hip",
     "nchw_to_nhwc_bf16_kernel": "conv_nhwc_bf16.hip",
+    "nchw_to_nhwc_plane_bf16_kernel": "conv_nhwc_bf16.hip",
     "dw_run_kernel": "dwconv.hip",
     "dw_band_kernel": "dwconv.hip",
     "dw3x3_kernel": "dwconv.hip",
@@ -102,14 +109,43 @@ def calibration(d: str, counter: str, nbytes: int) -> float:
     return nbytes / (max(v) * 1024.0)
 
 
+def counter_means(dirs, match: str):
+    """{kernel: {counter: mean per dispatch}} and {kernel: dispatches} over counter runs."""
+    vals = defaultdict(lambda: defaultdict(list))
+    for d in dirs:
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            sys.exit(f"no counter_collection.csv under {d}")
+        for p in files:
+            with open(p) as f:
+                for r in csv.DictReader(f):
+                    name = short_name(r["Kernel_Name"])
+                    if match in name:
+                        vals[name][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    means = {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in vals.items()}
+    counts = {k: max(len(v) for v in cs.values()) for k, cs in vals.items()}
+    return means, counts
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
-    ap.add_argument("--copy-fetch", required=True)
-    ap.add_argument("--copy-write", required=True)
+    ap.add_argument("--counters", nargs="+")
+    ap.add_argument("--match", default="")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-fetch")
+    ap.add_argument("--copy-write")
     ap.add_argument("--copy-bytes", type=int, default=256 << 20)
     a = ap.parse_args()
+    if a.counters:
+        means, counts = counter_means(a.counters, a.match)
+        for name in sorted(means):
+            print(f"{name}\tsource_sha1 {source_sha(name)}\tdispatches {counts[name]}")
+            for c in sorted(means[name]):
+                print(f"\t{c}\t{means[name][c]:.1f}")
+        return
+    if not (a.fetch and a.write and a.copy_fetch and a.copy_write):
+        ap.error("--fetch, --write, --copy-fetch and --copy-write are required without --counters")
     sf = calibration(a.copy_fetch, "FETCH_SIZE", a.copy_bytes)
     sw = calibration(a.copy_write, "WRITE_SIZE", a.copy_bytes)
     fetch = read_counter(a.fetch, "FETCH_SIZE")

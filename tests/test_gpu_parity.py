@@ -221,7 +221,7 @@ def test_bf16_1x1_nchw_operand_small_int_bitwise(oracle_lib, case):
     NCHW x through LDS transpose reads) against the oracle on small integers."""
     N, C, H, W, K, g = case
     name = miconv.conv2d_describe(N, C, H, W, K, 1, 1, 1, 0, g, "bf16")[0]
-    assert "nchw_to_nhwc" not in name and name.endswith(", true>"), name
+    assert "nchw_to_nhwc" not in name and name.endswith(", true, 64>"), name
     seed = 3700 + sum(case)
     x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
     w = wl.to_bf16_bits(ints((K, C // g, 1, 1), -4, 4, seed + 1))
