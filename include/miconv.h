@@ -111,6 +111,36 @@ int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, in
                  int groups, const float *x, const float *w, const float *bias, float *y,
                  int relu, void *stream);
 
+/* Filters packed once for repeated calls of one layer (the pre-computing step
+ * of the paper's graph-level optimisation, Sec. 3.2.3), outside a stack.
+ * The packed layout is the one the kernel chosen for this shape reads: the
+ * wavefront load order of the fp32 wave kernel, (r, s, c) order for the bf16
+ * channel-last kernels, tap pairs for the bf16 7x7 stem.  dtype 0 = fp32
+ * (conv2d_fwd), 1 = bf16 (conv2d_fwd_bf16).  Shapes as in conv2d_fwd.
+ *
+ * conv2d_packed_weight_bytes returns the size in bytes of the packed buffer,
+ * 0 when the kernel reads w as given (then conv2d_fwd_packed takes w itself),
+ * or a negative miconv_status (invalid shape, groups or dtype). */
+long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
+                                int pad, int groups, int dtype);
+
+/* Pack w (device, [K][C/groups][R][S], fp32 or bf16 bits) into `packed`
+ * (device, caller-owned, conv2d_packed_weight_bytes bytes, 16-byte aligned;
+ * the library keeps no reference) on `stream`.  Nothing is launched when the
+ * packed size is 0. */
+int conv2d_pack_weights(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                        int groups, int dtype, const void *w, void *packed, void *stream);
+
+/* conv2d_fwd (dtype 0) or conv2d_fwd_bf16 (dtype 1) with the filters from
+ * conv2d_pack_weights for the same shape and dtype (or w itself when the
+ * packed size is 0).  No packing launch.  The kernel is chosen again from the
+ * actual pointers; if their alignment selects a kernel with another filter
+ * layout than the one packed for (x and y at 256-byte boundaries never do),
+ * the call fails with MICONV_ERR_ALIGN and launches nothing. */
+int conv2d_fwd_packed(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                      int groups, int dtype, const void *x, const void *packed, const float *bias,
+                      float *y, int relu, void *stream);
+
 /* Glue operators of the evaluated networks (not part of the conv operator). */
 
 /* Max-pool fp32 NCHW with an R x S window, stride and symmetric pad

@@ -271,6 +271,28 @@ void set_krsc(Resolved &r, const void *packed)
 
 static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
+// The filter layout a resolved layer's kernel reads: 0 = w as given, else
+// 1 = bf16 stem tap pairs, 2 = wave kernel load order, 3 = KRSC.
+int filter_layout(const Resolved &r)
+{
+    if (!r.pack_per_call && !krsc_eligible(r)) return 0;
+    if (r.impl == IMPL_STEM_BF16) return 1;
+    if (r.impl == IMPL_WAVE) return 2;
+    return 3;
+}
+
+// The layer as conv2d_fwd[_bf16] resolves it for tensors at 256-byte
+// boundaries (w may be null: 256-aligned stand-in).
+int resolve_for_packing(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                        int groups, int dtype, const void *w, Resolved *out)
+{
+    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
+    alignas(256) static const float stand_in[64] = {};
+    return resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S,
+                   stride, pad, groups, stand_in, w ? w : stand_in, nullptr, const_cast<float *>(stand_in),
+                   0, out);
+}
+
 // The filter copy a layer's kernel reads: tap-pair order for the bf16 stem,
 // the wavefront load order for the wave kernel, KRSC otherwise.
 hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
@@ -440,6 +462,44 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
 {
     return conv2d_fwd_bf16_algo(N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y, relu,
                                 MICONV_ALGO_AUTO, stream);
+}
+
+long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
+                                int pad, int groups, int dtype)
+{
+    Resolved r;
+    const int rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, nullptr, &r);
+    if (rc != MICONV_OK) return rc;
+    return filter_layout(r) ? (long)packed_bytes(r) : 0;
+}
+
+int conv2d_pack_weights(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                        int groups, int dtype, const void *w, void *packed, void *stream)
+{
+    if (!w || !packed) return MICONV_ERR_NULL;
+    Resolved r;
+    const int rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, w, &r);
+    if (rc != MICONV_OK) return rc;
+    if (!filter_layout(r)) return MICONV_OK;
+    if ((uintptr_t)packed % 16 != 0) return MICONV_ERR_ALIGN;
+    return finish(launch_pack(r, packed, static_cast<hipStream_t>(stream)));
+}
+
+int conv2d_fwd_packed(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                      int groups, int dtype, const void *x, const void *packed, const float *bias,
+                      float *y, int relu, void *stream)
+{
+    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
+    Resolved r, ref;
+    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S,
+                     stride, pad, groups, x, packed, bias, y, relu, &r);
+    if (rc != MICONV_OK) return rc;
+    rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, nullptr, &ref);
+    if (rc != MICONV_OK) return rc;
+    const int layout = filter_layout(r);
+    if (layout != filter_layout(ref)) return MICONV_ERR_ALIGN;
+    if (layout) set_krsc(r, packed);
+    return run(r, static_cast<hipStream_t>(stream));
 }
 
 int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,

@@ -53,6 +53,12 @@ def lib() -> ctypes.CDLL:
         L.maxpool2d_fwd.argtypes = [i] * 8 + [p, p, p]
         L.add_act_fwd.argtypes = [l, p, p, p, i, p]
         L.cast_f32_to_bf16.argtypes = [l, p, p, p]
+        L.conv2d_packed_weight_bytes.argtypes = [i] * 11
+        L.conv2d_packed_weight_bytes.restype = l
+        L.conv2d_pack_weights.argtypes = [i] * 11 + [p, p, p]
+        L.conv2d_pack_weights.restype = i
+        L.conv2d_fwd_packed.argtypes = [i] * 11 + [p, p, p, p, i, p]
+        L.conv2d_fwd_packed.restype = i
         L.conv2d_describe.argtypes = [i] * 12 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
         L.conv2d_describe.restype = i
         L.miconv_stack_create.argtypes = [p, i, ctypes.POINTER(p)]
@@ -167,6 +173,46 @@ def conv2d_fwd_algo(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, algo=A
     _dev(x, torch.float32, "x", 4)
     return _conv_common(f, x, w, bias, y, stride, pad, groups, relu, stream, torch.float32,
                         extra=(int(algo),))
+
+
+class PackedFilters:
+    """Filters packed once for repeated calls of one layer shape
+    (conv2d_pack_weights); ``forward`` runs conv2d_fwd_packed.  Holds the
+    packed device buffer (or, when the kernel reads w as given, w itself)."""
+
+    def __init__(self, w, x_shape, stride=1, pad=0, groups=1, stream=None):
+        dtype = 1 if w.dtype == torch.bfloat16 else 0
+        _dev(w, torch.bfloat16 if dtype else torch.float32, "w", 4)
+        N, C, H, W = x_shape
+        K, Cg, R, S = w.shape
+        if groups <= 0 or Cg * groups != C:
+            raise ValueError("w.shape[1] * groups must equal C")
+        self.shape = (N, C, H, W, K, R, S, stride, pad, groups, dtype)
+        nbytes = lib().conv2d_packed_weight_bytes(*self.shape)
+        if nbytes < 0:
+            raise MiconvError(int(nbytes), "conv2d_packed_weight_bytes")
+        self.nbytes = nbytes
+        if nbytes == 0:
+            self.buf = w
+        else:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=w.device)
+            _check(lib().conv2d_pack_weights(*self.shape, _ptr(w), _ptr(self.buf), _stream(stream)),
+                   "conv2d_pack_weights")
+
+    def forward(self, x, bias, y, relu=False, stream=None):
+        N, C, H, W, K, R, S, stride, pad, groups, dtype = self.shape
+        _dev(x, torch.bfloat16 if dtype else torch.float32, "x", 4)
+        _dev(y, torch.float32, "y", 4)
+        if bias is not None:
+            _dev(bias, torch.float32, "bias", 1)
+        if tuple(x.shape) != (N, C, H, W):
+            raise ValueError(f"x must have shape {(N, C, H, W)}")
+        P, Q = out_dims(H, W, R, S, stride, pad)
+        if tuple(y.shape) != (N, K, P, Q):
+            raise ValueError(f"y must have shape {(N, K, P, Q)}")
+        _check(lib().conv2d_fwd_packed(*self.shape, _ptr(x), _ptr(self.buf), _ptr(bias), _ptr(y),
+                                       1 if relu else 0, _stream(stream)), "conv2d_fwd_packed")
+        return y
 
 
 def conv2d_fwd_bf16(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, stream=None):

@@ -82,3 +82,31 @@ def test_strerror_and_version(L):
     assert miconv.strerror(-99) == "unknown status"
     assert L.miconv_version() >= 100
     assert L.miconv_last_hip_error() == 0
+
+
+def test_packed_weight_sizes(L):
+    """Packed filter sizes follow the layout of the kernel each shape takes:
+    wave order (fp32: [groups][K/32][Kred/8][64 lanes][4]), KRSC (bf16 3x3),
+    tap pairs (bf16 7x7 stem: [K][28][8]); 0 when the kernel reads w as given."""
+    f = L.conv2d_packed_weight_bytes
+    assert f(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 0) == 2 * 72 * 256 * 4          # fp32 wave, Kred 576
+    assert f(1, 64, 56, 56, 256, 1, 1, 1, 0, 1, 0) == 8 * 8 * 256 * 4          # fp32 wave, Kred 64
+    assert f(64, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1) == 64 * 64 * 9 * 2          # bf16 KRSC
+    assert f(64, 3, 224, 224, 64, 7, 7, 2, 3, 1, 1) == 64 * 28 * 8 * 2         # bf16 stem
+    assert f(64, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1) == 0                       # bf16 1x1: w as given
+    assert f(1, 32, 56, 56, 32, 3, 3, 1, 1, 32, 0) == 0                        # depthwise
+    assert f(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 2) == miconv.ERR_UNSUPPORTED    # no such dtype
+    assert f(0, 64, 56, 56, 64, 3, 3, 1, 1, 1, 0) == miconv.ERR_SHAPE
+    assert f(1, 64, 56, 56, 64, 3, 3, 1, 1, 3, 0) == miconv.ERR_GROUPS
+
+
+def test_packed_entry_points_validate_first(L):
+    shape = (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 0)
+    assert L.conv2d_pack_weights(*shape, None, FAKE, None) == miconv.ERR_NULL
+    assert L.conv2d_pack_weights(*shape, FAKE, None, None) == miconv.ERR_NULL
+    assert L.conv2d_pack_weights(*shape[:-1], 5, FAKE, FAKE, None) == miconv.ERR_UNSUPPORTED
+    assert L.conv2d_fwd_packed(*shape, None, FAKE, None, FAKE, 0, None) == miconv.ERR_NULL
+    assert L.conv2d_fwd_packed(*shape, FAKE, None, None, FAKE, 0, None) == miconv.ERR_NULL
+    assert L.conv2d_fwd_packed(*shape[:-1], 7, FAKE, FAKE, None, FAKE, 0, None) == miconv.ERR_UNSUPPORTED
+    assert L.conv2d_fwd_packed(1, 64, 56, 56, 64, 3, 3, 0, 1, 1, 0, FAKE, FAKE, None, FAKE, 0,
+                               None) == miconv.ERR_SHAPE

@@ -335,6 +335,62 @@ def test_dense_deterministic():
     assert torch.equal(y1, y2)
 
 
+PACKED_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups, dtype): filters packed once
+    (1, 64, 20, 20, 48, 3, 3, 1, 1, 1, 0),     # fp32 wave kernel, (r, s, c) order
+    (2, 32, 15, 15, 40, 1, 1, 2, 0, 1, 0),     # fp32 1x1 stride 2
+    (1, 32, 10, 10, 48, 3, 3, 1, 1, 2, 0),     # fp32 grouped
+    (1, 3, 40, 40, 32, 7, 7, 2, 3, 1, 0),      # fp32 stem, (r, s, c4) order
+    (1, 512, 7, 7, 512, 3, 3, 1, 1, 1, 0),     # fp32 split reduction
+    (2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1),     # bf16 channel-last, KRSC
+    (1, 3, 224, 224, 64, 7, 7, 2, 3, 1, 1),    # bf16 stem, tap pairs
+    (2, 64, 16, 16, 128, 1, 1, 1, 0, 1, 1),    # bf16 1x1: w read as given (0 packed bytes)
+    (1, 32, 12, 12, 32, 3, 3, 1, 1, 32, 0),    # depthwise: w read as given
+]
+
+
+@pytest.mark.parametrize("case", PACKED_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_packed_filters_match_plain_calls(oracle_lib, case):
+    """conv2d_pack_weights + conv2d_fwd_packed run the kernel the plain entry
+    point runs, minus the packing launch: bitwise the same output, exact
+    against the oracle on small integers, for two calls on one packing."""
+    N, C, H, W, K, R, S, st, pad, g, dtype = case
+    seed = 4600 + sum(case)
+    x = ints((N, C, H, W), -4, 4, seed)
+    w = ints((K, C // g, R, S), -4, 4, seed + 1)
+    b = ints((K,), -8, 8, seed + 2)
+    if dtype:
+        x, w = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+        tx, tw = dev_bf16_bits(x), dev_bf16_bits(w)
+        ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
+    else:
+        tx, tw = dev(x), dev(w)
+        ref = oracle_lib.conv2d(x, w, b, st, pad, g, True)
+    plain = miconv.conv2d(tx, tw, dev(b), st, pad, g, True)
+    pk = miconv.PackedFilters(tw, (N, C, H, W), st, pad, g)
+    assert (pk.nbytes == 0) == ((R == 1 and dtype == 1) or g == C), pk.nbytes
+    for _ in range(2):
+        y = torch.full_like(plain, float("nan"))
+        pk.forward(tx, dev(b), y, relu=True)
+        torch.cuda.synchronize()
+        assert torch.equal(y, plain)
+    np.testing.assert_array_equal(y.cpu().numpy(), ref)
+
+
+def test_packed_filters_reject_a_kernel_change():
+    """The bf16 stem kernel needs y at a 16-byte boundary; with y one float
+    off, the layer would take a kernel that reads w unpacked, so the call on
+    stem-packed filters fails instead of reading them wrongly."""
+    N, C, H, W, K = 1, 3, 224, 224, 64
+    tx = dev_bf16_bits(wl.to_bf16_bits(ints((N, C, H, W), -4, 4, 4700)))
+    tw = dev_bf16_bits(wl.to_bf16_bits(ints((K, C, 7, 7), -4, 4, 4701)))
+    pk = miconv.PackedFilters(tw, (N, C, H, W), 2, 3, 1)
+    assert pk.nbytes > 0
+    yb = torch.zeros(N * K * 112 * 112 + 1, device="cuda")
+    with pytest.raises(miconv.MiconvError) as e:
+        pk.forward(tx, None, yb[1:].view(N, K, 112, 112))
+    assert e.value.status == miconv.ERR_ALIGN
+
+
 SPLIT_CASES = [  # batch-1 layers whose reduction the wave planner splits (ResNet-50 s3/s4/s5)
     (1, 128, 28, 28, 128, 3, 3, 1, 1, 1),
     (1, 1024, 14, 14, 256, 1, 1, 1, 0, 1),
