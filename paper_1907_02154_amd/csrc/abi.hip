@@ -272,12 +272,14 @@ void set_krsc(Resolved &r, const void *packed)
 static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
 // The filter layout a resolved layer's kernel reads: 0 = w as given, else
-// 1 = bf16 stem tap pairs, 2 = wave kernel load order, 3 = KRSC.
+// 1 = bf16 stem tap pairs, 2 = wave kernel load order, 3 = KRSC, 4 = KRSC per
+// 64-channel block.
 int filter_layout(const Resolved &r)
 {
     if (!r.pack_per_call && !krsc_eligible(r)) return 0;
     if (r.impl == IMPL_STEM_BF16) return 1;
     if (r.impl == IMPL_WAVE) return 2;
+    if (r.impl == IMPL_NHWC_BF16 && r.nplan.halo) return 4;   // KRSC per 64-channel block
     return 3;
 }
 
@@ -302,7 +304,8 @@ hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
     if (r.impl == IMPL_WAVE)
         return launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(dst), st);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
-    return launch_pack_krsc(r.p, r.w, dst, elem, st);
+    const int cblk = r.impl == IMPL_NHWC_BF16 && r.nplan.halo ? 64 : 0;   // (block, r, s, c) order
+    return launch_pack_krsc(r.p, r.w, dst, elem, st, cblk);
 }
 
 hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHook *hook)

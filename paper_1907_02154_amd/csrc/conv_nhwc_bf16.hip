@@ -675,6 +675,247 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
     }
 }
 
+// 3x3, stride 1, padding 1 (the middle layers of bottleneck blocks): the
+// pixel operand of all nine taps of one 64-channel block comes from one
+// staged patch.  In the channel-last copy, flattened over (n, p, q), output
+// pixel m reads input pixel m + (r-1)*W + (s-1) at tap (r, s), so the pixels
+// that output pixels m0 .. m0+BPX-1 read at any tap lie in the contiguous run
+// m0-W-1 .. m0+BPX+W: the work-group stages that run once per channel block
+// (rows of 64 channels, units permuted as in igemm_bf16_dma_kernel) and reads
+// tap (r, s) at row offset r*W + s.  Taps that fall into the padding (input
+// row or column outside the image, which in the flattened run is a
+// neighbouring row or image) are zeroed after the read.  The pixel operand
+// moves once per channel block instead of once per tap: 3.5x less staging
+// traffic for a 128-pixel tile at 28x28.  Filters are packed in 64-channel
+// blocks ((block, r, s, c) order), so chunk t = (block t/9, tap t%9) is again
+// 64 contiguous values per filter, double-buffered in LDS; the patches are
+// double-buffered by block parity, the next block's patch loaded with the
+// last tap of the current one.  PR = patch rows allocated (BPX + 2W + 2 used).
+template <int BPX, int BKC, int WPX, int WCH, int PR>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArgs a)
+{
+    constexpr int NT = 64 * WPX * WCH;
+    constexpr int TPX = BPX / WPX, TCH = BKC / WCH;     // one wavefront's tile
+    constexpr int BJ = TPX / 32, BI = TCH / 32;         // pixel blocks, channel blocks
+    constexpr int UA = BKC * 8;                         // 16-byte units per filter stage
+    constexpr int UP = PR * 8;                          // 16-byte units per patch buffer
+    constexpr int LA = UA / NT;
+    static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UP % NT == 0, "tile shape");
+    constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
+    constexpr int SMEM = 2 * (UA + UP) > BKC * OP / 4 ? 2 * (UA + UP) : BKC * OP / 4;
+    __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];   // [A 0][A 1][patch 0][patch 1]
+
+    const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
+    const uint16_t *__restrict__ wp = static_cast<const uint16_t *>(a.w);    // [K][Cg/64][3][3][64]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wpx = wid % WPX, wch = wid / WPX;
+    const int h = lane >> 5, ll = lane & 31;
+    // XCD-aware tile order, as in igemm_bf16_dma_kernel
+    const int T = gridDim.x;
+    const int xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
+    const int L = xcd * (T / 8) + min(xcd, T % 8) + jx;
+    const int ktiles = (a.Kg + BKC - 1) / BKC;
+    const int mtiles = (a.M + BPX - 1) / BPX;
+    const int ky = L % ktiles;
+    const int mx = (L / ktiles) % mtiles;
+    const int z = L / (ktiles * mtiles);
+    const int g = z % a.groups;
+    const int split = z / a.groups;
+    const int m0 = mx * BPX;
+    const int k0 = ky * BKC;
+    const int t_begin = split * a.kr_per_split / 64;
+    const int t_end = min(a.Kred, (split + 1) * a.kr_per_split) / 64;
+
+    constexpr unsigned kOutside = 0xffffffffu;
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(wp), (short)0, (int)((long)a.K * a.Kred * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(xcl), (short)0, (int)((long)a.N * a.H * a.W * a.C * 2), 0x00020000);
+
+    // Filter loader: load i of lane tid fills unit u = i*NT + tid (row u/8).
+    unsigned aoffs[LA];
+    bool aok[LA];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int u = i * NT + tid;
+        const int row = u >> 3;
+        const int kg = (u & 7) ^ unit_swz(row);
+        const int k = k0 + row;
+        aok[i] = k < a.Kg;
+        aoffs[i] = (unsigned)((((long)g * a.Kg + (aok[i] ? k : 0)) * a.Kred + kg * 8) * 2);
+    }
+    auto issue_a = [&](int t) {
+        const int kr0 = __builtin_amdgcn_readfirstlane(t * 64);
+        uint4 *st = smem + (t & 1) * UA;
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            const unsigned off = aok[i] ? aoffs[i] + 2u * kr0 : kOutside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_void_t *)(st + i * NT + wid * 64), 16,
+                                                     off, 0, 0, 0);
+        }
+    };
+    // Patch loader: rows 0 .. BPX+2W+1 are pixels m0-W-1+row, 64 channels of
+    // block cb; pixels outside 0 .. M-1 load as zeros.
+    const int prow = BPX + 2 * a.W + 2;
+    if (prow > PR) return;                              // the launcher never sends such a layer
+    const int pinstr = (prow * 8 + NT - 1) / NT;        // uniform
+    auto issue_patch = [&](int cb) {
+        uint4 *pb = smem + 2 * UA + (cb & 1) * UP;
+        const int cbase = g * a.Cg + cb * 64;
+        for (int i = 0; i < pinstr; ++i) {
+            const int u = i * NT + tid;
+            const int row = u >> 3;
+            const int kg = (u & 7) ^ unit_swz(row);
+            const int gm = m0 - a.W - 1 + row;
+            const bool ok = row < prow && gm >= 0 && gm < a.M;
+            const unsigned off = ok ? (unsigned)(((long)gm * a.C + cbase + kg * 8) * 2) : kOutside;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_void_t *)(pb + i * NT + wid * 64), 16,
+                                                     off, 0, 0, 0);
+        }
+    };
+
+    // This lane's output pixels (one per 32-pixel block): row and column.
+    int pp[BJ], qq[BJ];
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj) {
+        const int m = m0 + wpx * TPX + bj * 32 + ll;
+        const int mm = m < a.M ? m : 0;
+        const int pq = mm - (int)fdiv(mm, a.dv_pq) * a.PQ;
+        const int p = fdiv(pq, a.dv_q);
+        pp[bj] = m < a.M ? p : -4;                     // never inside the image
+        qq[bj] = pq - p * a.Q;
+    }
+    const int fl = unit_swz(ll);
+    int aoff[BI];
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) aoff[bi] = (wch * TCH + bi * 32 + ll) * 8;
+
+    floatx16 acc[BJ][BI];
+#pragma unroll
+    for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+        for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[bj][bi][v] = 0.f;
+
+    auto compute = [&](int t) {
+        const int cb = t / 9, tap = t - cb * 9;
+        const int r = tap / 3, s = tap - r * 3;
+        const uint4 *sa = smem + (t & 1) * UA;
+        const uint4 *pb = smem + 2 * UA + (cb & 1) * UP;
+        bf16x8 wv[4][BI], xv[4][BJ];
+        int prow_l[BJ];
+        bool ok[BJ];
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj) {
+            prow_l[bj] = wpx * TPX + bj * 32 + ll + r * a.W + s;
+            ok[bj] = (unsigned)(pp[bj] + r - 1) < (unsigned)a.H && (unsigned)(qq[bj] + s - 1) < (unsigned)a.W;
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int slot = (2 * ks + h) ^ fl;
+#pragma unroll
+            for (int bi = 0; bi < BI; ++bi)
+                wv[ks][bi] = *reinterpret_cast<const bf16x8 *>(sa + aoff[bi] + slot);
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj) {
+                const int row = prow_l[bj];
+                xv[ks][bj] = *reinterpret_cast<const bf16x8 *>(pb + row * 8 + ((2 * ks + h) ^ unit_swz(row)));
+            }
+        }
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj)
+            if (!ok[bj])
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) xv[ks][bj] = bf16x8{};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+                for (int bi = 0; bi < BI; ++bi)
+                    acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
+                                                                         acc[bj][bi], 0, 0, 0);
+    };
+
+    if (t_begin < t_end) {
+        issue_a(t_begin);
+        issue_patch(t_begin / 9);
+    }
+    for (int t = t_begin; t < t_end; ++t) {
+        // every lane's loads of chunk t (and of its patch) are done ...
+        wait_vmcnt<0>();
+        // ... and every wavefront is done with chunk t-1
+        asm volatile("s_barrier" ::: "memory");
+        if (t + 1 < t_end) {
+            issue_a(t + 1);
+            if ((t + 1) % 9 == 0) issue_patch((t + 1) / 9);
+        }
+        compute(t);
+    }
+
+    // Epilogue through LDS, as in igemm_bf16_dma_kernel.
+    __syncthreads();
+    float *ot = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) {
+        const int kl = wch * TCH + bi * 32 + ll;
+        const int k = k0 + kl;
+        const float bv = (a.splits == 1 && a.bias && k < a.Kg) ? a.bias[g * a.Kg + k] : 0.f;
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj) {
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                float v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float val = acc[bj][bi][4 * q4 + e];
+                    if (a.splits == 1) {
+                        val += bv;
+                        if (a.relu) val = fmaxf(val, 0.f);
+                    }
+                    v4[e] = val;
+                }
+                const int pl = wpx * TPX + bj * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<float4 *>(ot + kl * OP + pl) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+            }
+        }
+    }
+    __syncthreads();
+    const bool split_out = a.splits > 1;
+    float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
+    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
+    constexpr int C4 = BPX / 4;
+    for (int idx = tid; idx < BKC * C4; idx += NT) {
+        const int kl = idx / C4, c4 = idx - kl * C4;
+        const int k = k0 + kl;
+        const int m = m0 + 4 * c4;
+        if (k >= a.Kg || m >= a.M) continue;
+        const int kg = g * a.Kg + k;
+        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
+        const float ve[4] = {v.x, v.y, v.z, v.w};
+        if (vec && m + 3 < a.M) {
+            const int n = split_out ? 0 : m / a.PQ;
+            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
+            typedef float f32x4 __attribute__((ext_vector_type(4)));
+            const f32x4 nv = {v.x, v.y, v.z, v.w};
+            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int mm = m + e;
+                if (mm >= a.M) break;
+                const int n = split_out ? 0 : mm / a.PQ;
+                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
+                out[off] = ve[e];
+            }
+        }
+    }
+}
+
 struct TileN {
     int bkc, bpx;
 };
@@ -783,6 +1024,17 @@ void launch_dma_nchw(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
         launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
 }
 
+// The halo kernel instance: 128 x 128 tiles, patches of up to 192 rows
+// (BPX + 2W + 2 rows: W <= 31); 80 KB of LDS, two work-groups per CU.
+hipError_t launch_halo(const ConvArgs &a, int bkc, int pr, dim3 grid, hipStream_t st)
+{
+    if (bkc != 128 || pr != 192 || 128 + 2 * a.W + 2 > pr || a.R != 3 || a.S != 3 || a.stride != 1 ||
+        a.pad != 1 || a.Cg % 64 != 0)
+        return hipErrorInvalidValue;
+    launch_kernel((igemm_bf16_halo_kernel<128, 128, 2, 2, 192>), grid, dim3(256), 0, st, a);
+    return hipSuccess;
+}
+
 void launch_dma(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     if (a.R == 1 && a.S == 1)
@@ -850,6 +1102,13 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     // planner takes them only when 128 x 64 leaves CUs idle), so tile 2 always
     // has three stages (1024-channel 1x1, stride 2, 14x14 -> 7x7: 17.7 -> 14.1 us).
     if (!plan.nchwb && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
+    // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
+    // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
+    // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With
+    // 128 x 64 tiles its 64-80 KB of LDS cost a work-group per CU: 56x56 32.3
+    // -> 35.5 us, 14x14 even.
+    if (p.R == 3 && p.S == 3 && p.stride == 1 && p.pad == 1 && plan.tile == 0 && 128 + 2 * p.W + 2 <= 192)
+        plan.halo = 192;
     const ConvProblem cp = copied_problem(p);
     plan.xcl_bytes = plan.nchwb ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
     plan.copy_cb = plane_copy_block(p, num_cus);
@@ -899,6 +1158,13 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
         snprintf(tname, sizeof tname, "nchw_to_nhwc_plane_bf16_kernel");
     else
         snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
+    if (plan.dma && plan.halo) {
+        const TileD &d = kTilesD[plan.tile];
+        snprintf(buf, len, "%s + igemm_bf16_halo_kernel<%d, %d, 2, 2, %d>%s", tname, d.bpx, d.bkc, plan.halo,
+                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+        *launches = 2 + (plan.splits > 1 ? 1 : 0);
+        return;
+    }
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         // the instantiation's full name, reduction chunk included (every launch uses 64)
@@ -986,7 +1252,10 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
-        launch_dma(a, plan.tile, dim3((unsigned)wgs), st);
+        if (plan.halo) {
+            if ((e = launch_halo(a, d.bkc, plan.halo, dim3((unsigned)wgs), st)) != hipSuccess) return e;
+        } else
+            launch_dma(a, plan.tile, dim3((unsigned)wgs), st);
         if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
         if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
         return launch_splitk_reduce(a, st);

@@ -146,6 +146,8 @@ struct NhwcPlan {
     size_t partial_bytes; // split-K partials
     size_t xcl_bytes;     // the channel-last copy of x
     int copy_cb;          // channels per work-group of the whole-plane copy
+    int halo;             // 3x3 stride-1 layers: patch rows of the halo kernel (0: not used);
+                          // its filters are packed in 64-channel blocks
 };
 bool nhwc_bf16_eligible(const ConvProblem &p);
 NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x);
@@ -224,8 +226,9 @@ int wave_order(const ConvProblem &p);
 int wave_kred(const ConvProblem &p);
 size_t wave_packed_floats(const ConvProblem &p);
 hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed, hipStream_t st);
+// cblk: channel block of the (block, r, s, c) order; 0 = C/groups (plain KRSC).
 hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
-                            hipStream_t st);
+                            hipStream_t st, int cblk = 0);
 int set_hip_error(hipError_t e);   // records e for miconv_last_hip_error, returns MICONV_ERR_HIP
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }

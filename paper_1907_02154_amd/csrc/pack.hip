@@ -1,5 +1,7 @@
 // Weight pre-packing ("pre-computing" at graph level, Sec. 3.2.3): KCRS
-// filters -> KRSC, i.e. w_p[k][(r*S + s)*Cg + c] = w[k][c][r][s].
+// filters -> KRSC, i.e. w_p[k][(r*S + s)*Cg + c] = w[k][c][r][s], or, with a
+// channel block B < Cg, KRSC per block of B channels:
+// w_p[k][((c/B)*R*S + r*S + s)*B + c%B] = w[k][c][r][s].
 //
 // With the reduction ordered (r, s, c), c innermost, any 8 consecutive
 // reduction indices (Cg % 8 == 0) are 8 channels at one filter tap: a conv
@@ -13,14 +15,16 @@ namespace {
 
 template <typename T>
 __global__ __launch_bounds__(256) void pack_krsc_kernel(const T *__restrict__ src, T *__restrict__ dst,
-                                                        int K, int Cg, int RS, long total)
+                                                        int K, int Cg, int RS, int cblk, long total)
 {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (long)gridDim.x * blockDim.x) {
         const long k = i / ((long)Cg * RS);
-        const int rem = (int)(i - k * Cg * RS);   // (rs, c) with c fastest
-        const int rs = rem / Cg;
-        const int c = rem - rs * Cg;
+        const int rem = (int)(i - k * Cg * RS);   // (channel block, rs, c) with c fastest
+        const int cb = rem / (RS * cblk);
+        const int rem2 = rem - cb * RS * cblk;
+        const int rs = rem2 / cblk;
+        const int c = cb * cblk + (rem2 - rs * cblk);
         dst[i] = src[(k * Cg + c) * RS + rs];
     }
 }
@@ -91,19 +95,21 @@ hipError_t launch_pack_wave(const ConvProblem &p, const float *w, float *packed,
 }
 
 hipError_t launch_pack_krsc(const ConvProblem &p, const void *w, void *packed, size_t elem,
-                            hipStream_t st)
+                            hipStream_t st, int cblk)
 {
     const long total = (long)p.K * p.Cg * p.R * p.S;
+    if (cblk <= 0) cblk = p.Cg;
+    if (p.Cg % cblk != 0) return hipErrorInvalidValue;
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     if (elem == sizeof(float))
         launch_kernel(pack_krsc_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st,
                            static_cast<const float *>(w), static_cast<float *>(packed), p.K, p.Cg,
-                           p.R * p.S, total);
+                           p.R * p.S, cblk, total);
     else
         launch_kernel(pack_krsc_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
                            static_cast<const uint16_t *>(w), static_cast<uint16_t *>(packed), p.K,
-                           p.Cg, p.R * p.S, total);
+                           p.Cg, p.R * p.S, cblk, total);
     return hipGetLastError();
 }
 

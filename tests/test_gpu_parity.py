@@ -207,6 +207,34 @@ def test_bf16_offset_pointers_small_int_bitwise(oracle_lib, case):
     assert torch.isnan(yb[0]) and torch.isnan(yb[-3:]).all()   # nothing written outside y
 
 
+HALO_CASES = [  # (N, C, H, W, K, groups): bf16 3x3 stride-1 layers that take the halo-patch kernel
+    (64, 128, 28, 28, 128, 1),   # ResNet-50 s3 at batch 64: two channel blocks
+    (63, 128, 27, 29, 128, 1),   # odd plane: tiles and patches cross rows and images, ragged last tile
+    (64, 192, 28, 28, 128, 1),   # three channel blocks
+    (42, 256, 28, 28, 256, 2),   # two groups of 128 channels
+    (1, 512, 7, 7, 512, 1),      # reduction split across work-groups
+    (1, 256, 9, 31, 130, 1),     # widest plane (a 192-row patch), ragged filter tile, split
+]
+
+
+@pytest.mark.parametrize("case", HALO_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_bf16_halo_small_int_bitwise(oracle_lib, case):
+    """bf16 3x3 layers whose pixel operand is staged once per 64-channel block
+    for all nine taps (padding taps zeroed after the read) against the
+    oracle on small integers, bias and ReLU included."""
+    N, C, H, W, K, g = case
+    name = miconv.conv2d_describe(N, C, H, W, K, 3, 3, 1, 1, g, "bf16")[0]
+    assert "igemm_bf16_halo_kernel" in name, name
+    seed = 3800 + sum(case)
+    x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
+    w = wl.to_bf16_bits(ints((K, C // g, 3, 3), -4, 4, seed + 1))
+    b = ints((K,), -8, 8, seed + 2)
+    ref = oracle_lib.conv2d_bf16(x, w, b, 1, 1, g, True)
+    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), 1, 1, g, True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=str(case))
+
+
 NCHW_1X1_CASES = [  # (N, C, H, W, K, groups): 1x1 stride-1 layers whose pixel operand comes from NCHW x
     (3, 64, 56, 56, 520, 1),     # image boundaries inside pixel tiles, ragged M and K (128 x 64 tiles)
     (4, 64, 56, 56, 512, 1),     # 128 x 128 tiles
