@@ -59,7 +59,7 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 // need no branches, which keeps the executed code short.  At batch 1 a
 // launch runs a few hundred instructions per wavefront from a cold
 // instruction cache, so code size is a first-order cost here.
-template <int R_, int S_, int WAVES, int BJ, int ORD>
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
@@ -88,7 +88,13 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     const unsigned mtiles = ceil_div(a.M, 32 * BJ);
     const unsigned T = gridDim.x;
     const unsigned xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
-    const unsigned L = xcd * (T / 8) + min(xcd, T % 8) + jx;
+    const unsigned LW = xcd * (T / 8) + min(xcd, T % 8) + jx;
+    // IND: every wavefront owns a tile of its own (WAVES consecutive tiles per
+    // work-group) and runs its whole reduction: for short reductions over
+    // many tiles, where splitting 8-tap blocks across wavefronts would leave
+    // most of them idle and add an LDS combine per tile.
+    const unsigned L = IND ? LW * WAVES + (threadIdx.x >> 6) : LW;
+    if (IND && L >= (unsigned)(ceil_div(a.M, 32 * BJ) * ceil_div(a.Kg, 32) * a.groups)) return;
     const unsigned t1 = fdiv(L, a.dv_mt);
     const unsigned mx = L - t1 * mtiles;
     const unsigned t2 = fdiv(t1, a.dv_kt);
@@ -134,11 +140,12 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     const int cb = a.Cg / 8;
     int rsq = 0, rsr = 0, drq = 0, drr = 0;
     if constexpr (ORD == 1 && !(R_ == 1 && S_ == 1)) {
-        const int b0 = kr_begin / 8 + wave;
+        constexpr int kStep = IND ? 1 : WAVES;   // blocks between a wavefront's blocks
+        const int b0 = kr_begin / 8 + (IND ? 0 : wave);
         rsq = fdiv(b0, a.dv_cb);
         rsr = b0 - rsq * cb;
-        drq = WAVES / cb;
-        drr = WAVES - drq * cb;
+        drq = kStep / cb;
+        drr = kStep - drq * cb;
     }
 
     // Block blk (< nblk) of this split: taps kr_begin + 8*blk + 4h + e,
@@ -230,14 +237,15 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 
     // The epilogue's bias values, loaded now so that their round trip
     // overlaps the main loop (a missing bias is an empty buffer: zeros).
-    constexpr int kE = BJ * 16 / WAVES;   // output elements per thread
+    constexpr int kE = IND ? 16 : BJ * 16 / WAVES;   // bias values per thread
     float bias_v[kE];
     {
         const __amdgpu_buffer_rsrc_t bres = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<float *>(a.bias), (short)0, a.bias ? a.K * 4 : 0, 0x00020000);
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
-            const int idx = tid + i * 64 * WAVES;
+            // IND: the filters of the lane's own accumulator registers v = i
+            const int idx = IND ? i * 64 + lane : tid + i * 64 * WAVES;
             const int v = (idx >> 6) & 15, l = idx & 63;
             const int k = k0 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
             bias_v[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
@@ -255,7 +263,7 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     // of loads in flight: pass it issues the loads of its blocks it .. it +
     // kDepth - 1 and runs the MFMAs of the previous pass's blocks.  One copy
     // of the loop body serves the whole pipeline (no separate prologue).
-    const int my_blocks = nblk > wave ? ceil_div(nblk - wave, WAVES) : 0;
+    const int my_blocks = IND ? nblk : nblk > wave ? ceil_div(nblk - wave, WAVES) : 0;
     Frag f[kDepth];
 #pragma clang loop unroll(disable)
     for (int it = 0; it < my_blocks + kDepth; it += kDepth) {
@@ -268,47 +276,74 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
                     for (int j = 0; j < BJ; ++j)
                         acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f[d].av[e], f[d].bv[j][e], acc[j], 0, 0, 0);
             }
-            if (it + d < my_blocks) load(f[d], wave + (it + d) * WAVES);
+            if (it + d < my_blocks) load(f[d], IND ? it + d : wave + (it + d) * WAVES);
         }
     }
 
-    // Combine the wavefronts' partial tiles through LDS: every element is
-    // summed over the wavefronts in wave order (deterministic), and all lanes
-    // of the work-group share the epilogue.  Element (jv, l) of a tile is
-    // accumulator register v = jv % 16 of pixel block j = jv / 16 in lane l.
-    __shared__ float red[WAVES][BJ * 16][64];
+    if constexpr (IND) {
+        // Straight from the accumulators: register v of pixel block j holds
+        // pixel m0 + 32j + l%32 and filter k0 + 8(v/4) + 4(l/32) + v%4, so each
+        // store writes two runs of 32 consecutive pixels.
 #pragma unroll
-    for (int j = 0; j < BJ; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) red[wave][j * 16 + v][lane] = acc[j][v];
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kE; ++i) {
-        const int idx = tid + i * 64 * WAVES;
-        const int jv = idx >> 6, l = idx & 63;
-        const int j = jv >> 4, v = jv & 15;
-        float sum = red[0][jv][l];
-#pragma unroll
-        for (int ww = 1; ww < WAVES; ++ww) sum += red[ww][jv][l];
-        const int m = m0 + j * 32 + (l & 31);
-        const int k = k0 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
-        if (m >= a.M || k >= a.Kg) continue;
-        const int kg = g * a.Kg + k;
-        if (a.splits > 1) {
-            a.ws[((long)split * a.K + kg) * a.M + m] = sum;
-        } else {
+        for (int j = 0; j < BJ; ++j) {
+            const int m = m0 + j * 32 + ll;
+            if (m >= a.M) continue;
             const int n = fdiv(m, a.dv_pq);
-            const int pq = m - n * a.PQ;
-            float val = sum + bias_v[i];
-            if (a.relu) val = fmaxf(val, 0.f);
-            a.y[((long)n * a.K + kg) * a.PQ + pq] = val;
+            float *yp = a.y + ((long)n * a.K + g * a.Kg) * a.PQ + (m - n * a.PQ);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int k = k0 + 8 * (v >> 2) + 4 * h + (v & 3);
+                if (k >= a.Kg) continue;
+                float val = acc[j][v] + bias_v[v];
+                if (a.relu) val = fmaxf(val, 0.f);
+                yp[(long)k * a.PQ] = val;
+            }
+        }
+    } else {
+        // Combine the wavefronts' partial tiles through LDS: every element is
+        // summed over the wavefronts in wave order (deterministic), and all lanes
+        // of the work-group share the epilogue.  Element (jv, l) of a tile is
+        // accumulator register v = jv % 16 of pixel block j = jv / 16 in lane l.
+        __shared__ float red[WAVES][BJ * 16][64];
+#pragma unroll
+        for (int j = 0; j < BJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) red[wave][j * 16 + v][lane] = acc[j][v];
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kE; ++i) {
+            const int idx = tid + i * 64 * WAVES;
+            const int jv = idx >> 6, l = idx & 63;
+            const int j = jv >> 4, v = jv & 15;
+            float sum = red[0][jv][l];
+#pragma unroll
+            for (int ww = 1; ww < WAVES; ++ww) sum += red[ww][jv][l];
+            const int m = m0 + j * 32 + (l & 31);
+            const int k = k0 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+            if (m >= a.M || k >= a.Kg) continue;
+            const int kg = g * a.Kg + k;
+            if (a.splits > 1) {
+                a.ws[((long)split * a.K + kg) * a.M + m] = sum;
+            } else {
+                const int n = fdiv(m, a.dv_pq);
+                const int pq = m - n * a.PQ;
+                float val = sum + bias_v[i];
+                if (a.relu) val = fmaxf(val, 0.f);
+                a.y[((long)n * a.K + kg) * a.PQ + pq] = val;
+            }
         }
     }
 }
 
 template <int R_, int S_, int ORD>
-void launch_rs(const ConvArgs &a, int waves, int bj, dim3 grid, hipStream_t st)
+void launch_rs(const ConvArgs &a, int waves, int bj, bool ind, dim3 grid, hipStream_t st)
 {
+    if constexpr (ORD == 2 && R_ != 7) {
+        if (ind) {   // the planner takes IND with 4 wavefronts and 2 pixel blocks only
+            launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, ORD, true>), grid, dim3(256), 0, st, a);
+            return;
+        }
+    }
     if (waves == 8) {
         if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 2, ORD>), grid, dim3(512), 0, st, a);
         else launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 1, ORD>), grid, dim3(512), 0, st, a);
@@ -367,6 +402,18 @@ WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
             }
         }
     }
+    // Short reductions (C <= 4 channels, 3x3: at most 8 blocks of 8 taps)
+    // over many tiles: one tile per wavefront (VGG-16's first layer at batch 8,
+    // 12544 tiles of 64 pixels x 32 filters: the split across wavefronts left
+    // 3 of 8 idle and paid an LDS combine per 5 blocks).
+    const long tiles2 = (long)ceil_div(p.M, 64) * ceil_div(p.Kg, 32) * p.groups;
+    if (best.order == 2 && p.R != 7 && blocks <= 8 && p.M >= 64 && tiles2 >= 16L * num_cus) {
+        best.ind = true;
+        best.waves = 4;
+        best.bj = 2;
+        best.splits = 1;
+        best.kr_per_split = blocks * 8;
+    }
     best.ws_bytes = best.splits > 1 ? (size_t)best.splits * p.K * p.M * sizeof(float) : 0;
     return best;
 }
@@ -378,8 +425,8 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
     if (R == 0 || S == 0 || R != S) R = S = 0;
     if (plan.order == 1 && R != 3 && R != 1) R = S = 0;
     if (plan.order == 2 && R != 3 && R != 7) R = S = 0;
-    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %d>%s", R, S, plan.waves, plan.bj, plan.order,
-             plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %d, %s>%s", R, S, plan.waves, plan.bj,
+             plan.order, plan.ind ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     *launches = plan.splits > 1 ? 2 : 1;
 }
 
@@ -400,28 +447,30 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
     a.dv_kt = make_fastdiv(ceil_div(p.Kg, 32));
     a.dv_g = make_fastdiv(p.groups);
     a.dv_cb = make_fastdiv(p.Cg / 8 > 0 ? p.Cg / 8 : 1);
-    const dim3 grid((unsigned)((long)ceil_div(p.M, 32 * plan.bj) * ceil_div(p.Kg, 32) * p.groups *
-                               plan.splits));
+    const long tiles = (long)ceil_div(p.M, 32 * plan.bj) * ceil_div(p.Kg, 32) * p.groups * plan.splits;
+    if (plan.ind && (plan.order != 2 || p.R == 7 || plan.waves != 4 || plan.bj != 2 || plan.splits != 1))
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(plan.ind ? (tiles + plan.waves - 1) / plan.waves : tiles));
     hipError_t e = hook ? hook->before_launch(hook->ctx, st) : hipSuccess;
     if (e != hipSuccess) return e;
     if (plan.order == 1) {   // reduction ordered (r, s, c) in the packed filters
         if (p.R == 1 && p.S == 1)
-            launch_rs<1, 1, 1>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<1, 1, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
         else if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, 1>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<3, 3, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
         else
-            launch_rs<0, 0, 1>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<0, 0, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
     } else if (plan.order == 2) {   // (r, s, c4): C/groups <= 4
         if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, 2>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<3, 3, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
         else if (p.R == 7 && p.S == 7)
-            launch_rs<7, 7, 2>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<7, 7, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
         else
-            launch_rs<0, 0, 2>(a, plan.waves, plan.bj, grid, st);
+            launch_rs<0, 0, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
     } else if (p.R == 1 && p.S == 1) {
-        launch_rs<1, 1, 0>(a, plan.waves, plan.bj, grid, st);
+        launch_rs<1, 1, 0>(a, plan.waves, plan.bj, plan.ind, grid, st);
     } else {
-        launch_rs<0, 0, 0>(a, plan.waves, plan.bj, grid, st);
+        launch_rs<0, 0, 0>(a, plan.waves, plan.bj, plan.ind, grid, st);
     }
     e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return e;

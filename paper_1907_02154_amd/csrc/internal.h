@@ -117,6 +117,8 @@ struct WavePlan {
     int kr_per_split;
     size_t ws_bytes;
     int order;          // reduction order of the packed filters (wave_order)
+    bool ind;           // each wavefront owns a tile and its whole reduction (short
+                        // reductions over many tiles); waves then groups tiles
 };
 // The wave kernel addresses x and its packed filters with 32-bit offsets.
 bool wave_fits(const ConvProblem &p);

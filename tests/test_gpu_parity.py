@@ -363,6 +363,32 @@ def test_dense_deterministic():
     assert torch.equal(y1, y2)
 
 
+IND_CASES = [  # (N, C, H, W, K, stride): C <= 4 3x3 layers with one tile per wavefront
+    (3, 3, 224, 224, 64, 1),     # VGG-16's first layer at batch 3
+    (3, 3, 223, 221, 40, 1),     # ragged pixel and filter tiles
+    (12, 3, 224, 224, 64, 2),    # stride 2 (MobileNet's stem at batch 12)
+    (3, 2, 224, 224, 64, 1),     # two channels, padded to four
+]
+
+
+@pytest.mark.parametrize("case", IND_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_wave_independent_tiles_small_int_bitwise(oracle_lib, case):
+    """Short reductions over many tiles run one tile per wavefront, the
+    epilogue stored straight from the accumulators: exact against the oracle
+    on small integers."""
+    N, C, H, W, K, st = case
+    name = miconv.conv2d_describe(N, C, H, W, K, 3, 3, st, 1, 1, "f32")[0]
+    assert name.endswith("igemm_wave_f32_kernel<3, 3, 4, 2, 2, true>"), name
+    seed = 4800 + sum(case)
+    x = ints((N, C, H, W), -4, 4, seed)
+    w = ints((K, C, 3, 3), -4, 4, seed + 1)
+    b = ints((K,), -8, 8, seed + 2)
+    for relu, bias in ((True, b), (False, None)):
+        ref = oracle_lib.conv2d(x, w, bias, st, 1, 1, relu)
+        np.testing.assert_array_equal(gpu_conv(x, w, bias, st, 1, 1, relu, miconv.ALGO_AUTO), ref,
+                                      err_msg=f"{case} relu={relu}")
+
+
 PACKED_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups, dtype): filters packed once
     (1, 64, 20, 20, 48, 3, 3, 1, 1, 1, 0),     # fp32 wave kernel, (r, s, c) order
     (2, 32, 15, 15, 40, 1, 1, 2, 0, 1, 0),     # fp32 1x1 stride 2

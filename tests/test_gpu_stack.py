@@ -145,7 +145,7 @@ def test_stack_packed_filters_small_ints(oracle_lib, config, idxs):
     names = [s.describe(j) for j in range(len(ops))]
     # 3x3 layers read filters packed once at create (reduction order r, s, c):
     # no per-call packing kernel
-    assert any(n.startswith("igemm_wave_f32_kernel<3, 3") and n.split(" + ")[0].endswith(", 1>") or "nhwc" in n
+    assert any(n.startswith("igemm_wave_f32_kernel<3, 3") and n.split(" + ")[0].endswith(", 1, false>") or "nhwc" in n
                for n in names), names
     assert not any("pack_" in n for n in names), names
     s.launch()
