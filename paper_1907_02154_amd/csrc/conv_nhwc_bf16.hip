@@ -404,7 +404,14 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // lanes, lane 4e+t points at 4 pixels of channel row e and lane i receives
 // pixel i of the 4 rows.  The permuted units put the 4 rows of one read in 4
 // different 64-byte bank groups.
-template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, bool NCHWB, int KRC = 64>
+//
+// NCHWB == 2 (even H*W that is not a multiple of 8, e.g. 14x14): 8 pixels of
+// a channel may straddle two images, so the rows are loaded 4 bytes per lane
+// (2 pixels, never straddling): one load instruction fills one 256-byte
+// channel row, each lane fetching the pixel pair its LDS dword holds under
+// the unit permutation.  Same bandwidth per byte through the load path,
+// 4x the instructions.
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
 {
     constexpr int NT = 64 * WPX * WCH;
@@ -413,10 +420,11 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
     constexpr int BJ = TPX / 32, BI = TCH / 32;         // pixel blocks, channel blocks
     constexpr int UA = BKC * UPR, UB = BPX * UPR;       // 16-byte units per stage
     constexpr int LA = UA / NT, LB = UB / NT;           // load instructions per lane per chunk
-    constexpr int LOADS = LA + LB;
+    constexpr int LOADS = LA + (NCHWB == 2 ? KRC / (WPX * WCH) : LB);
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UB % NT == 0, "tile shape");
     static_assert(NST >= 2 && NST <= 8 && (NST - 2) * LOADS <= 63, "pipeline depth");
     static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1 && KRC == 64), "NCHW pixel operand: 1x1, 128-pixel tiles");
+    static_assert(NCHWB != 2 || (KRC / WPX / WCH) * WPX * WCH == KRC, "one channel row per load");
     static_assert(KRC == 64 || KRC == 32, "reduction chunk");
 
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
@@ -475,10 +483,25 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         aoffs[i] = (unsigned)((((long)g * a.Kg + (aok[i] ? k : 0)) * a.Kred + kg * 8) * 2);
     }
     int bih[LB], biw[LB], boffs[LB];
+    // NCHWB == 2: byte offset of the lane's pixel pair at channel 0 of the
+    // group, for each value of (row & 3) (the permutation of the row's units)
+    unsigned doff[4];
+    if constexpr (NCHWB == 2) {
+#pragma unroll
+        for (int c3 = 0; c3 < 4; ++c3) {
+            const int sl = (lane >> 2) ^ (4 * c3);              // logical 8-pixel unit of LDS unit lane/4
+            const int m = m0 + 8 * sl + 2 * (lane & 3);
+            const int n = m / a.HW;
+            doff[c3] = m < a.M ? (unsigned)((((long)n * a.C + (long)g * a.Cg) * a.HW + (m - n * a.HW)) * 2)
+                               : 0x80000000u;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
         const int u = i * NT + tid;
-        if constexpr (NCHWB) {
+        if constexpr (NCHWB == 2) {
+            break;
+        } else if constexpr (NCHWB) {
             // unit u: channel row c = u / 16 of the chunk, 8 pixels at unit s
             const int c = u >> 4;
             const int sl = (u & 15) ^ (4 * (c & 3));
@@ -523,6 +546,17 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
             const unsigned off = aok[i] ? aoffs[i] + 2u * kr0 : kOutside;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_void_t *)(st + i * NT + wid * 64), 16,
                                                      off, 0, 0, 0);
+        }
+        if constexpr (NCHWB == 2) {
+            // channel rows wid, wid + NW, ...: one 256-byte row per load
+            constexpr int NW = WPX * WCH;
+#pragma unroll
+            for (int i = 0; i < KRC / NW; ++i) {
+                const int c = wid + i * NW;
+                const unsigned off = doff[c & 3] + 2u * (unsigned)((c0 + c) * a.HW);   // >= 2^31: zeros
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_void_t *)(st + UA + c * 16), 4, off, 0, 0, 0);
+            }
+            return;
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
@@ -1009,19 +1043,27 @@ template <int R_, int S_>
 void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     switch (tile) {
-    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
-    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2, false>), grid, dim3(256), 0, st, a); break;
-    case 2: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 3, false>), grid, dim3(256), 0, st, a); break;
-    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 3, false>), grid, dim3(256), 0, st, a); break;
+    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2, 0>), grid, dim3(256), 0, st, a); break;
+    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2, 0>), grid, dim3(256), 0, st, a); break;
+    case 2: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 3, 0>), grid, dim3(256), 0, st, a); break;
+    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 3, 0>), grid, dim3(256), 0, st, a); break;
     }
 }
 
-void launch_dma_nchw(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
+void launch_dma_nchw(const ConvArgs &a, int tile, int mode, dim3 grid, hipStream_t st)
 {
-    if (tile == 0)
-        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
-    else
-        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
+    if (mode == 2) {
+        if (tile == 0)
+            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, 2>), grid, dim3(256), 0, st, a);
+        else if (tile == 3)
+            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 3, 2>), grid, dim3(256), 0, st, a);
+        else
+            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    } else if (tile == 0) {
+        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, 1>), grid, dim3(256), 0, st, a);
+    } else {
+        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1>), grid, dim3(256), 0, st, a);
+    }
 }
 
 // The halo kernel instance: 128 x 128 tiles, patches of up to 192 rows
@@ -1091,9 +1133,14 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     plan.splits = splits;
     plan.kr_per_split = ceil_div(chunks, splits) * 64;
     plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
-    // 1x1 stride-1 layers with 8-pixel rows read x in NCHW directly
-    plan.nchwb = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && (p.H * p.W) % 8 == 0 &&
-                 plan.tile <= 1 && (uintptr_t)x % 16 == 0;
+    // 1x1 stride-1 layers read x in NCHW directly: 16-byte loads when every
+    // 8-pixel group lies in one image; for other even planes 4-byte loads, 4x
+    // the load instructions, which pays off only for short reductions
+    // (measured at batch 64, 14x14: 256 -> 1024 channels 26.4 + 6.7 us copy ->
+    // 32.2 us; 1024 -> 256 channels 15.7 + 11.3 us copy -> 28.7 us)
+    const bool nchw_ok = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && plan.tile <= 1;
+    plan.nchwb = nchw_ok && (p.H * p.W) % 8 == 0 && (uintptr_t)x % 16 == 0 ? 1
+                 : nchw_ok && (p.H * p.W) % 2 == 0 && (uintptr_t)x % 4 == 0 && chunks <= 8 ? 2 : 0;
     // A 128 x 64 grid that fits in two work-groups per CU loses no occupancy
     // to a third LDS stage, which then hides more of the global -> LDS
     // latency (measured at batch 64: 14x14 3x3 layers 33.2 -> 29.2 us,
@@ -1101,7 +1148,7 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     // at 56x56, lose 10%).  64 x 64 grids are never larger than that (the
     // planner takes them only when 128 x 64 leaves CUs idle), so tile 2 always
     // has three stages (1024-channel 1x1, stride 2, 14x14 -> 7x7: 17.7 -> 14.1 us).
-    if (!plan.nchwb && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
+    if (plan.nchwb != 1 && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
     // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
     // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
     // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With
@@ -1168,9 +1215,9 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         // the instantiation's full name, reduction chunk included (every launch uses 64)
-        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %s, 64>%s",
+        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %d, 64>%s",
                  plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
-                 plan.nchwb ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+                 plan.nchwb, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
         *launches = (plan.nchwb ? 1 : 2) + (plan.splits > 1 ? 1 : 0);
         return;
     } else {
@@ -1199,7 +1246,7 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
         const TileD &d = kTilesD[plan.tile];
         const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
         if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
-        launch_dma_nchw(a, plan.tile, dim3((unsigned)wgs), st);
+        launch_dma_nchw(a, plan.tile, plan.nchwb, dim3((unsigned)wgs), st);
         if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
         if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
         return launch_splitk_reduce(a, st);

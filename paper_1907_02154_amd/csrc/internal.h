@@ -140,7 +140,8 @@ void describe_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast,
 // bf16 through an internal channel-last copy of x (C/groups % 32 == 0).
 struct NhwcPlan {
     int dma;              // direct-to-LDS kernel (64-channel chunks), else the register-staged one
-    bool nchwb;           // (dma, 1x1 stride 1) pixel operand read from NCHW x: no channel-last copy
+    int nchwb;            // (dma, 1x1 stride 1) pixel operand read from NCHW x, no channel-last
+                          // copy: 1 = 16-byte loads (H*W % 8 == 0), 2 = 4-byte loads (H*W even)
     int tile;             // index into the kernel family's tile table
     int krc;              // reduction chunk (64 or 32 channels at one filter position)
     int splits;

@@ -235,21 +235,28 @@ def test_bf16_halo_small_int_bitwise(oracle_lib, case):
     np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=str(case))
 
 
-NCHW_1X1_CASES = [  # (N, C, H, W, K, groups): 1x1 stride-1 layers whose pixel operand comes from NCHW x
-    (3, 64, 56, 56, 520, 1),     # image boundaries inside pixel tiles, ragged M and K (128 x 64 tiles)
-    (4, 64, 56, 56, 512, 1),     # 128 x 128 tiles
-    (2, 192, 64, 64, 256, 1),    # three reduction chunks
-    (8, 128, 64, 64, 256, 2),    # two groups of 64 channels
+NCHW_1X1_CASES = [  # (N, C, H, W, K, groups, loads): 1x1 stride-1 layers whose pixel operand comes from NCHW x
+    (3, 64, 56, 56, 520, 1, 1),     # image boundaries inside pixel tiles, ragged M and K (128 x 64 tiles)
+    (4, 64, 56, 56, 512, 1, 1),     # 128 x 128 tiles
+    (2, 192, 64, 64, 256, 1, 1),    # three reduction chunks
+    (8, 128, 64, 64, 256, 2, 1),    # two groups of 64 channels
+    (64, 64, 14, 14, 256, 1, 2),    # 196-pixel planes: 8-pixel groups straddle images, 4-byte loads
+    (64, 256, 14, 14, 1024, 1, 2),  # ResNet-50 s4 expansion layer, 128 x 128 tiles
+    (200, 64, 10, 13, 256, 1, 2),   # 130-pixel planes, ragged last tile
+    (64, 128, 14, 14, 256, 2, 2),   # two groups, 4-byte loads (three LDS stages)
+    (340, 64, 14, 14, 64, 1, 2),    # 128 x 64 tiles, two LDS stages
 ]
 
 
 @pytest.mark.parametrize("case", NCHW_1X1_CASES, ids=lambda c: "x".join(map(str, c)))
 def test_bf16_1x1_nchw_operand_small_int_bitwise(oracle_lib, case):
     """bf16 1x1 layers that skip the channel-last copy (pixel operand read from
-    NCHW x through LDS transpose reads) against the oracle on small integers."""
-    N, C, H, W, K, g = case
+    NCHW x through LDS transpose reads; 16-byte loads of 8 pixels, or 4-byte
+    loads of 2 pixels when 8-pixel groups can straddle images) against the
+    oracle on small integers."""
+    N, C, H, W, K, g, mode = case
     name = miconv.conv2d_describe(N, C, H, W, K, 1, 1, 1, 0, g, "bf16")[0]
-    assert "nchw_to_nhwc" not in name and name.endswith(", true, 64>"), name
+    assert "nchw_to_nhwc" not in name and name.endswith(f", {mode}, 64>"), name
     seed = 3700 + sum(case)
     x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
     w = wl.to_bf16_bits(ints((K, C // g, 1, 1), -4, 4, seed + 1))
