@@ -44,6 +44,7 @@ SOURCES = {
     "igemm_bf16_kernel": "conv_igemm_bf16.hip",
     "igemm_bf16_nhwc_kernel": "conv_nhwc_bf16.hip",
     "igemm_bf16_dma_kernel": "conv_nhwc_bf16.hip",
+    "igemm_bf16_halo_kernel": "conv_nhwc_bf16.hip",
     "nchw_to_nhwc_bf16_kernel": "conv_nhwc_bf16.hip",
     "nchw_to_nhwc_plane_bf16_kernel": "conv_nhwc_bf16.hip",
     "dw_run_kernel": "dwconv.hip",

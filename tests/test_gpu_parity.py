@@ -360,6 +360,53 @@ def test_config5_resnet_bf16_sampled(oracle_lib):
         _check_layer(oracle_lib, 5, i, l, images=[0, l.N - 1], kmax=24, tol=TOL_BF16)
 
 
+ERROR_BOUND_CASES = [  # (config, layer index): layers on seeded random data
+    (1, 0),     # 64 -> 64 3x3 at 56x56, batch 1
+    (2, 0),     # ResNet-50 stem, 7x7 over 3 channels
+    (2, 51),    # ResNet-50 s5 3x3: reduction of 4608 split across work-groups
+    (3, 26),    # MobileNet's last pointwise layer, split
+    (4, 0),     # VGG-16's first layer at batch 8, one tile per wavefront
+    (5, 16),    # ResNet-50 s3 3x3 at batch 64, bf16 (halo-patch kernel)
+    (5, 30),    # ResNet-50 s4 expansion at batch 64, bf16 (4-byte NCHW loads)
+]
+
+
+@pytest.mark.parametrize("config,idx", ERROR_BOUND_CASES, ids=lambda v: str(v))
+def test_elementwise_error_bound(oracle_lib, config, idx):
+    """Every output element within the a priori bound of recursive summation:
+    |y - y_ref| <= (gamma_n + u) * (sum |w x| + |b|), n = C/groups*R*S + 1,
+    gamma_n = n u / (1 - n u), with u = 2^-23 (twice fp32's unit roundoff:
+    room for accumulators that round toward zero), sum |w x| + |b| computed by
+    the oracle on |x|, |w|, |b|, and u |ref| covering the oracle's own final
+    rounding.  Rounding the inputs or products to bf16 inside an fp32 layer
+    would break it by orders of magnitude.  ReLU is 1-Lipschitz, so it keeps
+    the bound."""
+    l = wl.workload(config).layers[idx]
+    x, w, b = wl.layer_tensors(config, idx, l)
+    bf16 = wl.workload(config).dtype == "bf16"
+    if bf16:
+        x, w = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+        y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), l.stride, l.pad, l.groups, l.relu)
+        ref = oracle_lib.conv2d_bf16(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        # |x|, |w| in bf16: the sign bit cleared
+        mag = oracle_lib.conv2d_bf16(x & 0x7FFF, w & 0x7FFF, np.abs(b), l.stride, l.pad, l.groups, False)
+    else:
+        y = miconv.conv2d(dev(x), dev(w), dev(b), l.stride, l.pad, l.groups, l.relu)
+        ref = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        mag = oracle_lib.conv2d(np.abs(x), np.abs(w), np.abs(b), l.stride, l.pad, l.groups, False)
+    torch.cuda.synchronize()
+    mag = mag.astype(np.float64) * (1 + 2.0 ** -23)   # the oracle rounds it to fp32 once
+    n = (l.C // l.groups) * l.R * l.S + 1
+    u = 2.0 ** -23
+    gamma = n * u / (1 - n * u)
+    err = np.abs(y.cpu().numpy().astype(np.float64) - ref.astype(np.float64))
+    bound = (gamma + u) * mag
+    worst = np.max(err - bound)
+    assert worst <= 0, f"config {config} layer {idx} {l.name}: max excess {worst:.3e}"
+    # typical error sits far below the worst case (about sqrt(n) u)
+    assert np.median(err / np.maximum(mag, 1e-30)) < 8 * np.sqrt(n) * 2.0 ** -24
+
+
 def test_dense_deterministic():
     l = wl.workload(2).layers[-2]      # s5 3x3: small M, split-K
     x, w, b = wl.layer_tensors(2, 51, l)
