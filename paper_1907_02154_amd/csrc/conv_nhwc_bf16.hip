@@ -725,7 +725,9 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 // 64 contiguous values per filter, double-buffered in LDS; the patches are
 // double-buffered by block parity, the next block's patch loaded with the
 // last tap of the current one.  PR = patch rows allocated (BPX + 2W + 2 used).
-template <int BPX, int BKC, int WPX, int WCH, int PR>
+// NPB = 1 (one channel block, C/groups == 64): a single patch buffer, loaded
+// once, which keeps a 128 x 64 tile at 48 KB of LDS (three work-groups per CU).
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArgs a)
 {
     constexpr int NT = 64 * WPX * WCH;
@@ -736,8 +738,10 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
     constexpr int LA = UA / NT;
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UP % NT == 0, "tile shape");
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
-    constexpr int SMEM = 2 * (UA + UP) > BKC * OP / 4 ? 2 * (UA + UP) : BKC * OP / 4;
+    static_assert(NPB == 1 || NPB == 2, "patch buffers");
+    constexpr int SMEM = 2 * UA + NPB * UP > BKC * OP / 4 ? 2 * UA + NPB * UP : BKC * OP / 4;
     __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];   // [A 0][A 1][patch 0][patch 1]
+    if (NPB == 1 && a.Cg != 64) return;                 // the launcher never sends such a layer
 
     const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
     const uint16_t *__restrict__ wp = static_cast<const uint16_t *>(a.w);    // [K][Cg/64][3][3][64]
@@ -797,7 +801,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
     if (prow > PR) return;                              // the launcher never sends such a layer
     const int pinstr = (prow * 8 + NT - 1) / NT;        // uniform
     auto issue_patch = [&](int cb) {
-        uint4 *pb = smem + 2 * UA + (cb & 1) * UP;
+        uint4 *pb = smem + 2 * UA + (NPB == 2 ? (cb & 1) * UP : 0);
         const int cbase = g * a.Cg + cb * 64;
         for (int i = 0; i < pinstr; ++i) {
             const int u = i * NT + tid;
@@ -839,7 +843,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
         const int cb = t / 9, tap = t - cb * 9;
         const int r = tap / 3, s = tap - r * 3;
         const uint4 *sa = smem + (t & 1) * UA;
-        const uint4 *pb = smem + 2 * UA + (cb & 1) * UP;
+        const uint4 *pb = smem + 2 * UA + (NPB == 2 ? (cb & 1) * UP : 0);
         bf16x8 wv[4][BI], xv[4][BJ];
         int prow_l[BJ];
         bool ok[BJ];
@@ -1066,14 +1070,20 @@ void launch_dma_nchw(const ConvArgs &a, int tile, int mode, dim3 grid, hipStream
     }
 }
 
-// The halo kernel instance: 128 x 128 tiles, patches of up to 192 rows
-// (BPX + 2W + 2 rows: W <= 31); 80 KB of LDS, two work-groups per CU.
+// Halo kernel instances: 128 x 128 tiles with patches of up to 192 rows
+// (BPX + 2W + 2 rows: W <= 31; 80 KB of LDS, two work-groups per CU), and
+// 128 x 64 tiles over one 64-channel block with one patch of up to 256 rows
+// (W <= 63; 48 KB, three per CU).
 hipError_t launch_halo(const ConvArgs &a, int bkc, int pr, dim3 grid, hipStream_t st)
 {
-    if (bkc != 128 || pr != 192 || 128 + 2 * a.W + 2 > pr || a.R != 3 || a.S != 3 || a.stride != 1 ||
-        a.pad != 1 || a.Cg % 64 != 0)
+    if (128 + 2 * a.W + 2 > pr || a.R != 3 || a.S != 3 || a.stride != 1 || a.pad != 1 || a.Cg % 64 != 0)
         return hipErrorInvalidValue;
-    launch_kernel((igemm_bf16_halo_kernel<128, 128, 2, 2, 192>), grid, dim3(256), 0, st, a);
+    if (bkc == 128 && pr == 192)
+        launch_kernel((igemm_bf16_halo_kernel<128, 128, 2, 2, 192>), grid, dim3(256), 0, st, a);
+    else if (bkc == 64 && pr == 256 && a.Cg == 64 && a.splits == 1)
+        launch_kernel((igemm_bf16_halo_kernel<128, 64, 2, 2, 256, 1>), grid, dim3(256), 0, st, a);
+    else
+        return hipErrorInvalidValue;
     return hipSuccess;
 }
 
@@ -1156,6 +1166,9 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     // -> 35.5 us, 14x14 even.
     if (p.R == 3 && p.S == 3 && p.stride == 1 && p.pad == 1 && plan.tile == 0 && 128 + 2 * p.W + 2 <= 192)
         plan.halo = 192;
+    else if (p.R == 3 && p.S == 3 && p.stride == 1 && p.pad == 1 && plan.tile == 1 && p.Cg == 64 &&
+             splits == 1 && 128 + 2 * p.W + 2 <= 256)
+        plan.halo = 256;
     const ConvProblem cp = copied_problem(p);
     plan.xcl_bytes = plan.nchwb ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
     plan.copy_cb = plane_copy_block(p, num_cus);
@@ -1207,8 +1220,8 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
         snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
     if (plan.dma && plan.halo) {
         const TileD &d = kTilesD[plan.tile];
-        snprintf(buf, len, "%s + igemm_bf16_halo_kernel<%d, %d, 2, 2, %d>%s", tname, d.bpx, d.bkc, plan.halo,
-                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+        snprintf(buf, len, "%s + igemm_bf16_halo_kernel<%d, %d, 2, 2, %d, %d>%s", tname, d.bpx, d.bkc, plan.halo,
+                 d.bkc == 64 ? 1 : 2, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
         *launches = 2 + (plan.splits > 1 ? 1 : 0);
         return;
     }

@@ -214,6 +214,8 @@ HALO_CASES = [  # (N, C, H, W, K, groups): bf16 3x3 stride-1 layers that take th
     (42, 256, 28, 28, 256, 2),   # two groups of 128 channels
     (1, 512, 7, 7, 512, 1),      # reduction split across work-groups
     (1, 256, 9, 31, 130, 1),     # widest plane (a 192-row patch), ragged filter tile, split
+    (21, 64, 56, 56, 64, 1),     # one 64-channel block: 128 x 64 tiles, one 242-row patch
+    (12, 128, 55, 53, 128, 2),   # two groups of 64 channels, odd 55 x 53 planes
 ]
 
 
