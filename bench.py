@@ -114,7 +114,127 @@ def parse():
     ap.add_argument("--dw-sweep", type=int, default=0, metavar="N",
                     help="instead: HBM bandwidth of the depthwise kernel on the 13 MobileNet "
                          "depthwise shapes at batch N (e.g. 256)")
+    ap.add_argument("--residual-join", action="store_true",
+                    help="instead: the ResNet-50 join layers (last 1x1 of each bottleneck block) "
+                         "with the shortcut add + ReLU fused into the conv epilogue, against the "
+                         "same convs followed by a separate add kernel (--config 2 or 5)")
     return ap.parse_args()
+
+
+def _graph_ms(torch, fn, steps, stream):
+    """Mean ms of one call of fn(s) (which enqueues on stream s) over a HIP graph
+    of `steps` calls, captured on a side stream and replayed on `stream` once
+    untimed and once timed."""
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        for _ in range(steps):
+            fn(side)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def residual_join(args):
+    """Operator fusion of the residual join (ResNet bottleneck: y = relu(conv +
+    bias + shortcut)).  The 16 join layers of ResNet-50 (c3 of every block) run
+    as one stack with the shortcut read in the conv epilogue, and as the same
+    stack without it followed by one add + ReLU kernel per layer (in place, as
+    a framework without fusion runs it).  Both variants are timed as HIP graphs
+    of K passes with every tensor resident; inputs are seeded as in the
+    configuration (shortcuts normal(0, 1))."""
+    import torch
+    from paper_1907_02154_amd import miconv
+    from paper_1907_02154_amd import workloads as wl
+
+    if args.config not in (2, 5):
+        print("--residual-join runs on --config 2 or 5 (ResNet-50)", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    wk = wl.workload(args.config, args.batch)
+    bf16 = wk.dtype == "bf16"
+    op = miconv.OP_CONV_BF16 if bf16 else miconv.OP_CONV_F32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(wl.SEED_BASE + 4242)
+    fused, plain, adds, elems, conv_flops = [], [], [], 0, 0
+    for i, l in enumerate(wk.layers):
+        if not l.name.endswith("c3"):
+            continue
+        x, w, b = wl.layer_tensors(args.config, i, l)
+        if bf16:
+            tx = torch.from_numpy(wl.to_bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
+            tw = torch.from_numpy(wl.to_bf16_bits(w).view(np.int16)).cuda().view(torch.bfloat16)
+        else:
+            tx, tw = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+        tb = torch.from_numpy(b).cuda()
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        res = torch.randn((l.N, l.K, P, Q), device="cuda", generator=gen)
+        yf = torch.empty_like(res)
+        yp = torch.empty_like(res)
+        fused.append((op, tx, tw, tb, yf, l.stride, l.pad, l.groups, True, res))
+        plain.append((op, tx, tw, tb, yp, l.stride, l.pad, l.groups, False))
+        adds.append((yp, res))
+        elems += res.numel()
+        conv_flops += wl.flops(l, P, Q)
+    sf, sp = miconv.Stack(fused), miconv.Stack(plain)
+    stream = torch.cuda.current_stream()
+    for _ in range(max(1, args.warmup)):
+        sf.launch(stream)
+        sp.launch(stream)
+        for y, r in adds:
+            miconv.add_act_fwd(y, r, y, True, stream)
+    torch.cuda.synchronize()
+    # the two variants agree (one fp32 rounding of the conv sum apart at most)
+    sf.launch(stream)
+    sp.launch(stream)
+    for y, r in adds:
+        miconv.add_act_fwd(y, r, y, True, stream)
+    torch.cuda.synchronize()
+    diff = max(float((f[4] - a[0]).abs().max()) / max(float(a[0].abs().max()), 1e-30)
+               for f, a in zip(fused, adds))
+    K = args.steps
+    sf.capture(K, timed=False, stream=stream)
+    sp.capture(K, timed=False, stream=stream)
+    ms = {}
+    for name, st in (("fused", sf), ("conv_only", sp)):
+        st.replay(stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st.replay(stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms[name] = e0.elapsed_time(e1) / K
+
+    def add_pass(strm):
+        for y, r in adds:
+            miconv.add_act_fwd(y, r, y, True, strm)
+    ms["add_kernels"] = _graph_ms(torch, add_pass, K, stream)
+    sf.close()
+    sp.close()
+    unfused = ms["conv_only"] + ms["add_kernels"]
+    out = {"metric": "ResNet-50 join layers: conv + residual add + ReLU, ms per pass",
+           "value": round(ms["fused"], 4), "unit": "ms", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": round(ms["fused"], 4), "higher_is_better": False,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if bf16 else "f32",
+           "data": "synthetic",
+           "config": {"workload": f"{wk.name}: its 16 bottleneck join layers (c3)",
+                      "join_elements": elems, "conv_flops": conv_flops,
+                      "device": gpu_info(torch)},
+           "unfused_ms": round(unfused, 4), "conv_only_ms": round(ms["conv_only"], 4),
+           "add_kernels_ms": round(ms["add_kernels"], 4),
+           "fused_join_overhead_ms": round(ms["fused"] - ms["conv_only"], 4),
+           "speedup": round(unfused / ms["fused"], 3),
+           "algorithmic_join_bytes": {"fused": 4 * elems, "separate": 12 * elems},
+           "max_rel_diff_fused_vs_separate": diff}
+    print(json.dumps(out), flush=True)
 
 
 def dw_sweep(args):
@@ -199,6 +319,9 @@ def main():
         sys.exit(2)
     if args.dw_sweep:
         dw_sweep(args)
+        return
+    if args.residual_join:
+        residual_join(args)
         return
     if args.copy_calibration:
         import torch

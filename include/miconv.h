@@ -111,6 +111,23 @@ int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, in
                  int groups, const float *x, const float *w, const float *bias, float *y,
                  int relu, void *stream);
 
+/* Dense conv2d with a residual join fused into the epilogue (the operator
+ * fusion of the paper's graph-level optimisation, Sec. 3.2.3, applied to the
+ * shortcut add of ResNet's bottleneck blocks):
+ *   y = act(conv(x, w) + bias + res),  act = ReLU when relu != 0, else identity,
+ * with the sum taken in fp32 in that order.  dtype 0: x, w fp32 (conv2d_fwd);
+ * dtype 1: x, w bf16 bit patterns (conv2d_fwd_bf16).  algo as for
+ * conv2d_fwd_algo / conv2d_fwd_bf16_algo.  res is device fp32
+ * [N][K][P][Q], caller-owned, or NULL (then the call equals the plain entry
+ * point).  res may be y itself (in-place join: each element is read before it
+ * is written, by the same thread); it must not otherwise overlap y.  res must
+ * be 4-byte aligned and lie at the same offset modulo 16 bytes as y (the
+ * kernels read it with y's own vector accesses), else MICONV_ERR_ALIGN.
+ * Depthwise shapes (groups == C == K with fp32): MICONV_ERR_UNSUPPORTED. */
+int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                   int groups, int dtype, int algo, const void *x, const void *w,
+                   const float *bias, const float *res, float *y, int relu, void *stream);
+
 /* Filters packed once for repeated calls of one layer (the pre-computing step
  * of the paper's graph-level optimisation, Sec. 3.2.3), outside a stack.
  * The packed layout is the one the kernel chosen for this shape reads: the
@@ -176,6 +193,8 @@ typedef struct miconv_conv_desc {
     const void *w;
     const float *bias;         /* may be NULL */
     float *y;
+    const float *res;          /* residual joined before the activation, as in
+                                  conv2d_fwd_res (dense ops only); may be NULL */
 } miconv_conv_desc;
 
 typedef struct miconv_stack miconv_stack;

@@ -57,12 +57,14 @@ def _load():
                 sig = [i] * 10 + [p, p, p, p, i]
                 lib.ref_conv2d_f32.argtypes = sig
                 lib.ref_conv2d_bf16.argtypes = sig
+                lib.ref_conv2d_res.argtypes = [i] * 11 + [p, p, p, p, p, i]
                 lib.ref_dwconv2d_f32.argtypes = [i] * 8 + [p, p, p, p, i]
                 lib.ref_maxpool2d_f32.argtypes = [i] * 8 + [p, p]
                 lib.ref_add_act_f32.argtypes = [v, p, p, p, i]
                 lib.ref_f32_to_bf16.argtypes = [v, p, p]
                 lib.ref_num_threads.argtypes = []
                 for f in ("ref_num_threads", "ref_out_dims", "ref_conv2d_f32", "ref_conv2d_bf16",
+                          "ref_conv2d_res",
                           "ref_dwconv2d_f32", "ref_maxpool2d_f32", "ref_add_act_f32",
                           "ref_f32_to_bf16"):
                     getattr(lib, f).restype = i
@@ -95,7 +97,7 @@ def out_dims(H, W, R, S, stride, pad):
     return P.value, Q.value
 
 
-def _conv(fn, x, w, bias, stride, pad, groups, relu, xdtype):
+def _conv(fn, x, w, bias, stride, pad, groups, relu, xdtype, res=None):
     x = _c(x, xdtype)
     w = _c(w, xdtype)
     N, C, H, W = x.shape
@@ -109,6 +111,16 @@ def _conv(fn, x, w, bias, stride, pad, groups, relu, xdtype):
     if P <= 0 or Q <= 0:
         raise ValueError("empty output")
     y = np.empty((N, K, P, Q), np.float32)
+    if res is not None:
+        r = _c(res, np.float32)
+        if r.shape != y.shape:
+            raise ValueError("res must have the output's shape")
+        rc = _load().ref_conv2d_res(N, C, H, W, K, R, S, stride, pad, groups,
+                                    1 if xdtype == np.uint16 else 0, _ptr(x), _ptr(w), _ptr(b),
+                                    _ptr(r), _ptr(y), 1 if relu else 0)
+        if rc != 0:
+            raise RuntimeError(f"oracle conv failed ({rc})")
+        return y
     rc = fn(N, C, H, W, K, R, S, stride, pad, groups, _ptr(x), _ptr(w), _ptr(b), _ptr(y),
             1 if relu else 0)
     if rc != 0:
@@ -116,15 +128,18 @@ def _conv(fn, x, w, bias, stride, pad, groups, relu, xdtype):
     return y
 
 
-def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False):
-    """Conv2D on fp32 arrays: x [N][C][H][W], w [K][C/groups][R][S] -> y [N][K][P][Q]."""
-    return _conv(_load().ref_conv2d_f32, x, w, bias, stride, pad, groups, relu, np.float32)
+def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False, res=None):
+    """Conv2D on fp32 arrays: x [N][C][H][W], w [K][C/groups][R][S] -> y [N][K][P][Q].
+
+    With ``res`` (fp32, y's shape): the fused residual join of a bottleneck
+    block (operator fusion, Sec. 3.2.3), act(conv + bias + res) summed in fp64."""
+    return _conv(_load().ref_conv2d_f32, x, w, bias, stride, pad, groups, relu, np.float32, res)
 
 
-def conv2d_bf16(x_bits, w_bits, bias=None, stride=1, pad=0, groups=1, relu=False):
-    """Conv2D with x and w given as bf16 bit patterns (uint16); bias and y are fp32."""
+def conv2d_bf16(x_bits, w_bits, bias=None, stride=1, pad=0, groups=1, relu=False, res=None):
+    """Conv2D with x and w given as bf16 bit patterns (uint16); bias, res and y are fp32."""
     return _conv(_load().ref_conv2d_bf16, x_bits, w_bits, bias, stride, pad, groups, relu,
-                 np.uint16)
+                 np.uint16, res)
 
 
 def dwconv2d(x, w, bias=None, stride=1, pad=0, relu=False):

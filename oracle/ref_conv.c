@@ -100,7 +100,7 @@ static double ref_load_bf16(const void *base, size_t i)
 static int ref_conv2d_any(int N, int C, int H, int W, int K, int R, int S,
                           int stride, int pad, int groups,
                           const void *x, const void *w, ref_load_fn load,
-                          const float *bias, float *y, int relu)
+                          const float *bias, const float *res, float *y, int relu)
 {
     if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || R <= 0 || S <= 0 ||
         stride <= 0 || pad < 0 || groups <= 0 || !x || !w || !y)
@@ -148,8 +148,10 @@ static int ref_conv2d_any(int N, int C, int H, int W, int K, int R, int S,
                     }
                 }
                 float *yp = y + (size_t)((n * K + k) * PQ);
+                const float *rp = res ? res + (size_t)((n * K + k) * PQ) : NULL;
                 for (long i = 0; i < PQ; ++i) {
                     double v = acc[i];
+                    if (rp) v += (double)rp[i];   /* residual join, before the activation */
                     if (relu && v < 0.0) v = 0.0;
                     yp[i] = (float)v;
                 }
@@ -167,7 +169,20 @@ int ref_conv2d_f32(int N, int C, int H, int W, int K, int R, int S, int stride, 
                    int relu)
 {
     return ref_conv2d_any(N, C, H, W, K, R, S, stride, pad, groups, x, w, ref_load_f32,
-                          bias, y, relu);
+                          bias, NULL, y, relu);
+}
+
+/* Conv2D followed by the residual join of a bottleneck block, fused as the
+ * graph-level operator fusion does (Sec. 3.2.3):
+ * y = act(conv(x, w) + bias + res), res [N][K][P][Q] fp32, the whole sum in
+ * fp64 and rounded once.  x16 != 0: x and w are bf16 bit patterns. */
+int ref_conv2d_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                   int groups, int x16, const void *x, const void *w, const float *bias,
+                   const float *res, float *y, int relu)
+{
+    if (!res) return REF_EINVAL;
+    return ref_conv2d_any(N, C, H, W, K, R, S, stride, pad, groups, x, w,
+                          x16 ? ref_load_bf16 : ref_load_f32, bias, res, y, relu);
 }
 
 /* Same operator with x and w stored as bf16 bit patterns (widened exactly);
@@ -177,15 +192,15 @@ int ref_conv2d_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
                     float *y, int relu)
 {
     return ref_conv2d_any(N, C, H, W, K, R, S, stride, pad, groups, x, w, ref_load_bf16,
-                          bias, y, relu);
+                          bias, NULL, y, relu);
 }
 
 /* Depthwise conv: one R x S filter per channel, w [C][1][R][S]. */
 int ref_dwconv2d_f32(int N, int C, int H, int W, int R, int S, int stride, int pad,
                      const float *x, const float *w, const float *bias, float *y, int relu)
 {
-    return ref_conv2d_any(N, C, H, W, C, R, S, stride, pad, C, x, w, ref_load_f32, bias, y,
-                          relu);
+    return ref_conv2d_any(N, C, H, W, C, R, S, stride, pad, C, x, w, ref_load_f32, bias, NULL,
+                          y, relu);
 }
 
 /*

@@ -44,6 +44,7 @@ ConvArgs make_args(const ConvProblem &p)
     a.splits = 1;
     a.kr_per_split = p.Kred;
     a.relu = p.relu;
+    a.res = p.res;
     a.dv_pq = make_fastdiv(p.P * p.Q);
     a.dv_q = make_fastdiv(p.Q);
     return a;
@@ -245,6 +246,17 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         r.pack_per_call = true;               // filters in tap-pair order
     }
     *out = r;
+    return MICONV_OK;
+}
+
+int set_residual(Resolved &r, const float *res)
+{
+    if (!res) return MICONV_OK;
+    // Kernels read it with the same (possibly 16-byte) accesses as they write y.
+    if ((uintptr_t)res % sizeof(float) || ((uintptr_t)res - (uintptr_t)r.y) % 16)
+        return MICONV_ERR_ALIGN;
+    if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
+    r.p.res = res;
     return MICONV_OK;
 }
 
@@ -465,6 +477,18 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
 {
     return conv2d_fwd_bf16_algo(N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y, relu,
                                 MICONV_ALGO_AUTO, stream);
+}
+
+int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                   int groups, int dtype, int algo, const void *x, const void *w,
+                   const float *bias, const float *res, float *y, int relu, void *stream)
+{
+    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
+    Resolved r;
+    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride,
+                     pad, groups, x, w, bias, y, relu, &r);
+    if (rc == MICONV_OK) rc = set_residual(r, res);
+    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
 }
 
 long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,

@@ -46,6 +46,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(ConvArgs a)
             }
         }
         float v = acc + (a.bias ? a.bias[k] : 0.f);
+        if (a.res) v += a.res[i];
         if (a.relu) v = fmaxf(v, 0.f);
         a.y[i] = v;
     }

@@ -295,6 +295,7 @@ __global__ __launch_bounds__(256) void igemm_bf16_kernel(ConvArgs a)
                 float val = acc[bi][bj][v];
                 if (a.splits == 1) {
                     val += bv;
+                    if (a.res) val += a.res[ybase[bj] + coff];
                     if (a.relu) val = fmaxf(val, 0.f);
                 }
                 out[ybase[bj] + coff] = val;

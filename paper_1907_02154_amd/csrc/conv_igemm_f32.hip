@@ -178,6 +178,7 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
                     a.ws[((long)split * a.K + kg) * a.M + m] = acc[bi][bj][v];
                 } else {
                     float val = acc[bi][bj][v] + (a.bias ? a.bias[kg] : 0.f);
+                    if (a.res) val += a.res[ybase + (long)kg * a.PQ];
                     if (a.relu) val = fmaxf(val, 0.f);
                     a.y[ybase + (long)kg * a.PQ] = val;
                 }
@@ -186,8 +187,8 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
     }
 }
 
-// Sum the split partials in split order (deterministic), add bias, apply the
-// activation and store NCHW.  Lanes walk the partials' [K][M] order, so reads
+// Sum the split partials in split order (deterministic), add bias and the
+// residual, apply the activation and store NCHW.  Lanes walk the partials' [K][M] order, so reads
 // are contiguous.  A thread requests its bias value and the partials of up to
 // eight splits before it adds any of them: the launch costs one memory round
 // trip, not one per split.  Partials are read through a buffer resource, so
@@ -222,6 +223,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
                 }
             }
             float o[4] = {s.x + bv, s.y + bv, s.z + bv, s.w + bv};
+            if (a.res) {
+                const float4 r = reinterpret_cast<const float4 *>(a.res)[i];
+                o[0] += r.x;
+                o[1] += r.y;
+                o[2] += r.z;
+                o[3] += r.w;
+            }
             if (a.relu)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.f);
@@ -243,9 +251,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
             for (int u = 0; u < kGroup; ++u) s += v[u];
         }
         s += bv;
-        if (a.relu) s = fmaxf(s, 0.f);
         const unsigned n = fdiv(m, a.dv_pq);
-        a.y[((size_t)n * a.K + k) * a.PQ + (m - n * a.PQ)] = s;
+        const size_t yo = ((size_t)n * a.K + k) * a.PQ + (m - n * a.PQ);
+        if (a.res) s += a.res[yo];
+        if (a.relu) s = fmaxf(s, 0.f);
+        a.y[yo] = s;
     }
 }
 
@@ -354,7 +364,8 @@ hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
     const long total = (long)a.K * a.M;
     // 32-bit offsets, also for the zero-reading slots of the last group of 8
     if ((long)(a.splits + 7) * total * 4 >= (1L << 31)) return hipErrorInvalidValue;
-    a.vec4 = a.N == 1 && a.M % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0;
+    a.vec4 = a.N == 1 && a.M % 4 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.ws % 16 == 0 &&
+             (uintptr_t)a.res % 16 == 0;
     a.dv_m = make_fastdiv(a.M);
     long blocks = (a.vec4 ? total / 4 : total + 255) / 256 + 1;
     if (blocks > 8192) blocks = 8192;

@@ -324,13 +324,22 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
                     float val = acc[bj][bi][4 * q4 + e];
                     if (a.splits == 1) {
                         val += bv;
-                        if (a.relu) val = fmaxf(val, 0.f);
+                        if (a.relu && !a.res) val = fmaxf(val, 0.f);
                     }
                     v4[e] = val;
                 }
                 if (vec && mb + 3 < a.M) {
                     const int n = mb / a.PQ;
                     const long off = (long)n * a.K * a.PQ + (mb - n * a.PQ) + coff;
+                    if (a.res) {
+                        const float4 r = *reinterpret_cast<const float4 *>(a.res + off);
+                        const float re[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            v4[e] += re[e];
+                            if (a.relu) v4[e] = fmaxf(v4[e], 0.f);
+                        }
+                    }
                     *reinterpret_cast<float4 *>(out + off) = make_float4(v4[0], v4[1], v4[2], v4[3]);
                 } else {
 #pragma unroll
@@ -340,7 +349,12 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
                         const int n = m / a.PQ;
                         const long off = a.splits > 1 ? (long)m + coff
                                                       : (long)n * a.K * a.PQ + (m - n * a.PQ) + coff;
-                        out[off] = v4[e];
+                        float val = v4[e];
+                        if (a.splits == 1 && a.res) {
+                            val += a.res[off];
+                            if (a.relu) val = fmaxf(val, 0.f);
+                        }
+                        out[off] = val;
                     }
                 }
             }
@@ -357,6 +371,131 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
 // f(row) = (row & 7) ^ ((row >> 3) & 1): the MFMA operand reads (16
 // consecutive rows, one unit each) then hit 16 distinct 16-byte bank groups,
 // and each load instruction still fills 1 KB of LDS contiguously.
+// The LDS epilogue of the channel-last kernels writes the tile [BKC filters]
+// [BPX pixels] (row pitch OP floats, bias added, activation applied unless a
+// residual follows) in rows of 4 pixels: element (filter kl, pixels 4*c4 ..
+// 4*c4+3) is row idx = kl * BPX/4 + c4, and thread tid takes rows tid,
+// tid + NT, ...  Rows go to y -- or, with a reduction split, to this split's
+// partials [K][M] -- as 16-byte stores where y's alignment and the plane
+// allow.
+template <int BPX, int BKC, int NT, int OP>
+__device__ inline void store_tile(const ConvArgs &a, const float *ot, int tid, int k0, int m0, int g,
+                                  int split)
+{
+    const bool split_out = a.splits > 1;
+    float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
+    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
+    constexpr int C4 = BPX / 4;
+    for (int idx = tid; idx < BKC * C4; idx += NT) {
+        const int kl = idx / C4, c4 = idx - kl * C4;
+        const int k = k0 + kl;
+        const int m = m0 + 4 * c4;
+        if (k >= a.Kg || m >= a.M) continue;
+        const int kg = g * a.Kg + k;
+        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
+        const float ve[4] = {v.x, v.y, v.z, v.w};
+        if (vec && m + 3 < a.M) {
+            const int n = split_out ? 0 : m / a.PQ;
+            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
+            typedef float f32x4 __attribute__((ext_vector_type(4)));
+            const f32x4 nv = {v.x, v.y, v.z, v.w};
+            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int mm = m + e;
+                if (mm >= a.M) break;
+                const int n = split_out ? 0 : mm / a.PQ;
+                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
+                out[off] = ve[e];
+            }
+        }
+    }
+}
+
+// The same rows with the residual joined (no split).  load_res_tile requests
+// every residual value this thread needs in one burst, before the epilogue's
+// barriers, so the loads overlap each other and the accumulator pass; they all
+// precede the thread's first store, so res may be y itself.  store_tile_res
+// then joins, activates and stores.
+template <int BPX, int BKC, int NT>
+__device__ inline void load_res_tile(const ConvArgs &a, int tid, int k0, int m0, int g,
+                                     float (&rv)[BKC * (BPX / 4) / NT][4])
+{
+    constexpr int C4 = BPX / 4;
+    constexpr int IT = BKC * C4 / NT;
+    static_assert(BKC * C4 % NT == 0, "epilogue rows per thread");
+    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int idx = tid + it * NT;
+        const int kl = idx / C4, c4 = idx - kl * C4;
+        const int k = k0 + kl;
+        const int m = m0 + 4 * c4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rv[it][e] = 0.f;
+        if (k >= a.Kg || m >= a.M) continue;
+        const int kg = g * a.Kg + k;
+        if (vec && m + 3 < a.M) {
+            const int n = m / a.PQ;
+            const float4 r = *reinterpret_cast<const float4 *>(
+                a.res + ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ));
+            rv[it][0] = r.x;
+            rv[it][1] = r.y;
+            rv[it][2] = r.z;
+            rv[it][3] = r.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int mm = m + e;
+                if (mm >= a.M) break;
+                const int n = mm / a.PQ;
+                rv[it][e] = a.res[((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ)];
+            }
+        }
+    }
+}
+
+template <int BPX, int BKC, int NT, int OP>
+__device__ inline void store_tile_res(const ConvArgs &a, const float *ot, int tid, int k0, int m0, int g,
+                                      const float (&rv)[BKC * (BPX / 4) / NT][4])
+{
+    constexpr int C4 = BPX / 4;
+    constexpr int IT = BKC * C4 / NT;
+    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int idx = tid + it * NT;
+        const int kl = idx / C4, c4 = idx - kl * C4;
+        const int k = k0 + kl;
+        const int m = m0 + 4 * c4;
+        if (k >= a.Kg || m >= a.M) continue;
+        const int kg = g * a.Kg + k;
+        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
+        float ve[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            ve[e] += rv[it][e];
+            if (a.relu) ve[e] = fmaxf(ve[e], 0.f);
+        }
+        if (vec && m + 3 < a.M) {
+            const int n = m / a.PQ;
+            typedef float f32x4 __attribute__((ext_vector_type(4)));
+            const f32x4 nv = {ve[0], ve[1], ve[2], ve[3]};
+            __builtin_nontemporal_store(
+                nv, reinterpret_cast<f32x4 *>(a.y + ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ)));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int mm = m + e;
+                if (mm >= a.M) break;
+                const int n = mm / a.PQ;
+                a.y[((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ)] = ve[e];
+            }
+        }
+    }
+}
+
 __device__ inline int unit_swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // 32-channel chunks (rows of 4 units, 64 bytes): unit u of row r sits at
@@ -411,8 +550,8 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // channel row, each lane fetching the pixel pair its LDS dword holds under
 // the unit permutation.  Same bandwidth per byte through the load path,
 // 4x the instructions.
-template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
-__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC, bool RES>
+__device__ __forceinline__ void dma_body(const ConvArgs &a)
 {
     constexpr int NT = 64 * WPX * WCH;
     constexpr int UPR = KRC / 8;                        // 16-byte units per operand row
@@ -651,6 +790,8 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
     // once every wavefront has passed the barrier, then each channel row is
     // written out with contiguous 16-byte stores (a lane's own accumulators
     // would give 32 scattered 32-byte pieces per store instruction).
+    float rv[RES ? BKC * (BPX / 4) / NT : 1][4];
+    if constexpr (RES) load_res_tile<BPX, BKC, NT>(a, tid, k0, m0, g, rv);
     __syncthreads();
     float *ot = reinterpret_cast<float *>(smem);
 #pragma unroll
@@ -668,7 +809,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
                     float val = acc[bj][bi][4 * q4 + e];
                     if (a.splits == 1) {
                         val += bv;
-                        if (a.relu) val = fmaxf(val, 0.f);
+                        if (a.relu && !RES) val = fmaxf(val, 0.f);
                     }
                     v4[e] = val;
                 }
@@ -678,35 +819,25 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
         }
     }
     __syncthreads();
-    const bool split_out = a.splits > 1;
-    float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
-    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
-    constexpr int C4 = BPX / 4;
-    for (int idx = tid; idx < BKC * C4; idx += NT) {
-        const int kl = idx / C4, c4 = idx - kl * C4;
-        const int k = k0 + kl;
-        const int m = m0 + 4 * c4;
-        if (k >= a.Kg || m >= a.M) continue;
-        const int kg = g * a.Kg + k;
-        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
-        const float ve[4] = {v.x, v.y, v.z, v.w};
-        if (vec && m + 3 < a.M) {
-            const int n = split_out ? 0 : m / a.PQ;
-            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
-            typedef float f32x4 __attribute__((ext_vector_type(4)));
-            const f32x4 nv = {v.x, v.y, v.z, v.w};
-            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int mm = m + e;
-                if (mm >= a.M) break;
-                const int n = split_out ? 0 : mm / a.PQ;
-                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
-                out[off] = ve[e];
-            }
-        }
-    }
+    if constexpr (RES)
+        store_tile_res<BPX, BKC, NT, OP>(a, ot, tid, k0, m0, g, rv);
+    else
+        store_tile<BPX, BKC, NT, OP>(a, ot, tid, k0, m0, g, split);
+}
+
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
+{
+    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, false>(a);
+}
+
+// The same kernel with the residual join in its epilogue (layers without a
+// reduction split): the residual loads are issued before the epilogue's
+// barriers, which costs registers the plain kernel does not spend.
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
+__global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_dma_res_kernel(ConvArgs a)
+{
+    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, true>(a);
 }
 
 // 3x3, stride 1, padding 1 (the middle layers of bottleneck blocks): the
@@ -727,8 +858,8 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 // last tap of the current one.  PR = patch rows allocated (BPX + 2W + 2 used).
 // NPB = 1 (one channel block, C/groups == 64): a single patch buffer, loaded
 // once, which keeps a 128 x 64 tile at 48 KB of LDS (three work-groups per CU).
-template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
-__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArgs a)
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB, bool RES>
+__device__ __forceinline__ void halo_body(const ConvArgs &a)
 {
     constexpr int NT = 64 * WPX * WCH;
     constexpr int TPX = BPX / WPX, TCH = BKC / WCH;     // one wavefront's tile
@@ -896,6 +1027,8 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
     }
 
     // Epilogue through LDS, as in igemm_bf16_dma_kernel.
+    float rv[RES ? BKC * (BPX / 4) / NT : 1][4];
+    if constexpr (RES) load_res_tile<BPX, BKC, NT>(a, tid, k0, m0, g, rv);
     __syncthreads();
     float *ot = reinterpret_cast<float *>(smem);
 #pragma unroll
@@ -913,7 +1046,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
                     float val = acc[bj][bi][4 * q4 + e];
                     if (a.splits == 1) {
                         val += bv;
-                        if (a.relu) val = fmaxf(val, 0.f);
+                        if (a.relu && !RES) val = fmaxf(val, 0.f);
                     }
                     v4[e] = val;
                 }
@@ -923,35 +1056,45 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArg
         }
     }
     __syncthreads();
-    const bool split_out = a.splits > 1;
-    float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
-    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
-    constexpr int C4 = BPX / 4;
-    for (int idx = tid; idx < BKC * C4; idx += NT) {
-        const int kl = idx / C4, c4 = idx - kl * C4;
-        const int k = k0 + kl;
-        const int m = m0 + 4 * c4;
-        if (k >= a.Kg || m >= a.M) continue;
-        const int kg = g * a.Kg + k;
-        const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
-        const float ve[4] = {v.x, v.y, v.z, v.w};
-        if (vec && m + 3 < a.M) {
-            const int n = split_out ? 0 : m / a.PQ;
-            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
-            typedef float f32x4 __attribute__((ext_vector_type(4)));
-            const f32x4 nv = {v.x, v.y, v.z, v.w};
-            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int mm = m + e;
-                if (mm >= a.M) break;
-                const int n = split_out ? 0 : mm / a.PQ;
-                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
-                out[off] = ve[e];
-            }
-        }
-    }
+    if constexpr (RES)
+        store_tile_res<BPX, BKC, NT, OP>(a, ot, tid, k0, m0, g, rv);
+    else
+        store_tile<BPX, BKC, NT, OP>(a, ot, tid, k0, m0, g, split);
+}
+
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArgs a)
+{
+    halo_body<BPX, BKC, WPX, WCH, PR, NPB, false>(a);
+}
+
+// With the residual join in the epilogue (no reduction split).
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
+__global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_halo_res_kernel(ConvArgs a)
+{
+    halo_body<BPX, BKC, WPX, WCH, PR, NPB, true>(a);
+}
+
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
+void launch_dma(const ConvArgs &a, dim3 grid, hipStream_t st)
+{
+    if (a.res && a.splits == 1)
+        launch_kernel((igemm_bf16_dma_res_kernel<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC>), grid,
+                      dim3(64 * WPX * WCH), 0, st, a);
+    else
+        launch_kernel((igemm_bf16_dma_kernel<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC>), grid,
+                      dim3(64 * WPX * WCH), 0, st, a);
+}
+
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
+void launch_halo_k(const ConvArgs &a, dim3 grid, hipStream_t st)
+{
+    if (a.res && a.splits == 1)
+        launch_kernel((igemm_bf16_halo_res_kernel<BPX, BKC, WPX, WCH, PR, NPB>), grid,
+                      dim3(64 * WPX * WCH), 0, st, a);
+    else
+        launch_kernel((igemm_bf16_halo_kernel<BPX, BKC, WPX, WCH, PR, NPB>), grid, dim3(64 * WPX * WCH),
+                      0, st, a);
 }
 
 struct TileN {
@@ -1047,10 +1190,10 @@ template <int R_, int S_>
 void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 {
     switch (tile) {
-    case 0: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 128, 2, 2, 2, 0>), grid, dim3(256), 0, st, a); break;
-    case 1: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 2, 0>), grid, dim3(256), 0, st, a); break;
-    case 2: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 64, 64, 2, 2, 3, 0>), grid, dim3(256), 0, st, a); break;
-    default: launch_kernel((igemm_bf16_dma_kernel<R_, S_, 128, 64, 2, 2, 3, 0>), grid, dim3(256), 0, st, a); break;
+    case 0: launch_dma<R_, S_, 128, 128, 2, 2, 2, 0>(a, grid, st); break;
+    case 1: launch_dma<R_, S_, 128, 64, 2, 2, 2, 0>(a, grid, st); break;
+    case 2: launch_dma<R_, S_, 64, 64, 2, 2, 3, 0>(a, grid, st); break;
+    default: launch_dma<R_, S_, 128, 64, 2, 2, 3, 0>(a, grid, st); break;
     }
 }
 
@@ -1058,15 +1201,15 @@ void launch_dma_nchw(const ConvArgs &a, int tile, int mode, dim3 grid, hipStream
 {
     if (mode == 2) {
         if (tile == 0)
-            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, 2>), grid, dim3(256), 0, st, a);
+            launch_dma<1, 1, 128, 128, 2, 2, 2, 2>(a, grid, st);
         else if (tile == 3)
-            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 3, 2>), grid, dim3(256), 0, st, a);
+            launch_dma<1, 1, 128, 64, 2, 2, 3, 2>(a, grid, st);
         else
-            launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 2>), grid, dim3(256), 0, st, a);
+            launch_dma<1, 1, 128, 64, 2, 2, 2, 2>(a, grid, st);
     } else if (tile == 0) {
-        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 128, 2, 2, 2, 1>), grid, dim3(256), 0, st, a);
+        launch_dma<1, 1, 128, 128, 2, 2, 2, 1>(a, grid, st);
     } else {
-        launch_kernel((igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1>), grid, dim3(256), 0, st, a);
+        launch_dma<1, 1, 128, 64, 2, 2, 2, 1>(a, grid, st);
     }
 }
 
@@ -1079,9 +1222,9 @@ hipError_t launch_halo(const ConvArgs &a, int bkc, int pr, dim3 grid, hipStream_
     if (128 + 2 * a.W + 2 > pr || a.R != 3 || a.S != 3 || a.stride != 1 || a.pad != 1 || a.Cg % 64 != 0)
         return hipErrorInvalidValue;
     if (bkc == 128 && pr == 192)
-        launch_kernel((igemm_bf16_halo_kernel<128, 128, 2, 2, 192>), grid, dim3(256), 0, st, a);
+        launch_halo_k<128, 128, 2, 2, 192>(a, grid, st);
     else if (bkc == 64 && pr == 256 && a.Cg == 64 && a.splits == 1)
-        launch_kernel((igemm_bf16_halo_kernel<128, 64, 2, 2, 256, 1>), grid, dim3(256), 0, st, a);
+        launch_halo_k<128, 64, 2, 2, 256, 1>(a, grid, st);
     else
         return hipErrorInvalidValue;
     return hipSuccess;
@@ -1220,7 +1363,8 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
         snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
     if (plan.dma && plan.halo) {
         const TileD &d = kTilesD[plan.tile];
-        snprintf(buf, len, "%s + igemm_bf16_halo_kernel<%d, %d, 2, 2, %d, %d>%s", tname, d.bpx, d.bkc, plan.halo,
+        snprintf(buf, len, "%s + igemm_bf16_halo%s_kernel<%d, %d, 2, 2, %d, %d>%s", tname,
+                 p.res && plan.splits == 1 ? "_res" : "", d.bpx, d.bkc, plan.halo,
                  d.bkc == 64 ? 1 : 2, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
         *launches = 2 + (plan.splits > 1 ? 1 : 0);
         return;
@@ -1228,8 +1372,9 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         // the instantiation's full name, reduction chunk included (every launch uses 64)
-        snprintf(buf, len, "%s%sigemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %d, 64>%s",
-                 plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
+        snprintf(buf, len, "%s%sigemm_bf16_dma%s_kernel<%d, %d, %d, %d, %d, %d, %d, %d, 64>%s",
+                 plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", p.res && plan.splits == 1 ? "_res" : "",
+                 R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
                  plan.nchwb, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
         *launches = (plan.nchwb ? 1 : 2) + (plan.splits > 1 ? 1 : 0);
         return;

@@ -289,14 +289,15 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             const int m = m0 + j * 32 + ll;
             if (m >= a.M) continue;
             const int n = fdiv(m, a.dv_pq);
-            float *yp = a.y + ((long)n * a.K + g * a.Kg) * a.PQ + (m - n * a.PQ);
+            const long yo = ((long)n * a.K + g * a.Kg) * a.PQ + (m - n * a.PQ);
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int k = k0 + 8 * (v >> 2) + 4 * h + (v & 3);
                 if (k >= a.Kg) continue;
                 float val = acc[j][v] + bias_v[v];
+                if (a.res) val += a.res[yo + (long)k * a.PQ];
                 if (a.relu) val = fmaxf(val, 0.f);
-                yp[(long)k * a.PQ] = val;
+                a.y[yo + (long)k * a.PQ] = val;
             }
         }
     } else {
@@ -327,9 +328,11 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             } else {
                 const int n = fdiv(m, a.dv_pq);
                 const int pq = m - n * a.PQ;
+                const long yo = ((long)n * a.K + kg) * a.PQ + pq;
                 float val = sum + bias_v[i];
+                if (a.res) val += a.res[yo];
                 if (a.relu) val = fmaxf(val, 0.f);
-                a.y[((long)n * a.K + kg) * a.PQ + pq] = val;
+                a.y[yo] = val;
             }
         }
     }

@@ -33,6 +33,7 @@ struct ConvProblem {
     int Kred;        // Cg * R * S: the GEMM reduction length
     int M;           // N * P * Q: the GEMM pixel extent
     int relu;
+    const float *res;  // [N][K][P][Q] added to the conv + bias before the activation, or nullptr
 };
 
 // Division by a divisor d >= 1 fixed at launch, for numerators below 2^31:
@@ -62,6 +63,8 @@ struct ConvArgs {
     const void *w;        // fp32 or bf16 bits, [K][Cg][R][S]
     const float *bias;    // [K] or nullptr
     float *y;             // [N][K][P][Q]
+    const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may
+                          // be y itself (every element is read and written by one thread)
     float *ws;            // split-K partials [splits][K][M] (nullptr when splits == 1)
     int N, C, H, W, K, R, S, stride, pad, groups;
     int P, Q, Cg, Kg, Kred, M, PQ, HW;
@@ -213,6 +216,9 @@ struct Resolved {
 int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S, int stride,
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
             int relu, Resolved *out);
+// Adds a residual [N][K][P][Q] (read at y's indices, before the activation) to
+// a resolved dense layer; nullptr leaves it unchanged.
+int set_residual(Resolved &r, const float *res);
 hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
 void describe(const Resolved &r, char *buf, int len, int *launches);
 size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + split partials

@@ -53,6 +53,7 @@ def lib() -> ctypes.CDLL:
         L.maxpool2d_fwd.argtypes = [i] * 8 + [p, p, p]
         L.add_act_fwd.argtypes = [l, p, p, p, i, p]
         L.cast_f32_to_bf16.argtypes = [l, p, p, p]
+        L.conv2d_fwd_res.argtypes = [i] * 12 + [p, p, p, p, p, i, p]
         L.conv2d_packed_weight_bytes.argtypes = [i] * 11
         L.conv2d_packed_weight_bytes.restype = l
         L.conv2d_pack_weights.argtypes = [i] * 11 + [p, p, p]
@@ -175,6 +176,26 @@ def conv2d_fwd_algo(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, algo=A
                         extra=(int(algo),))
 
 
+def conv2d_fwd_res(x, w, bias, res, y, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO,
+                   stream=None):
+    """y = act(conv(x, w) + bias + res) with the join in the conv's epilogue.
+
+    x and w fp32 or bf16 (the dtype selects conv2d_fwd or conv2d_fwd_bf16),
+    res fp32 shaped like y, or None; res may be y itself."""
+    xdt = torch.bfloat16 if x.dtype == torch.bfloat16 else torch.float32
+    if res is not None:
+        _dev(res, torch.float32, "res", 4)
+        if tuple(res.shape) != tuple(y.shape):
+            raise ValueError("res must have y's shape")
+    f = lib().conv2d_fwd_res
+
+    def call(N, C, H, W, K, R, S, stride_, pad_, groups_, px, pw, pb, py, relu_, stream_):
+        return f(N, C, H, W, K, R, S, stride_, pad_, groups_, 1 if xdt == torch.bfloat16 else 0,
+                 int(algo), px, pw, pb, _ptr(res), py, relu_, stream_)
+    call.__name__ = "conv2d_fwd_res"
+    return _conv_common(call, x, w, bias, y, stride, pad, groups, relu, stream, xdt)
+
+
 class PackedFilters:
     """Filters packed once for repeated calls of one layer shape
     (conv2d_pack_weights); ``forward`` runs conv2d_fwd_packed.  Holds the
@@ -284,21 +305,28 @@ class ConvDesc(ctypes.Structure):
                                          ("N", "C", "H", "W", "K", "R", "S", "stride", "pad",
                                           "groups", "relu")] + \
                [("x", ctypes.c_void_p), ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
-                ("y", ctypes.c_void_p)]
+                ("y", ctypes.c_void_p), ("res", ctypes.c_void_p)]
 
 
 class Stack:
     """A list of conv layers planned once by the library's stack executor.
 
     ``layers`` holds tuples ``(op, x, w, bias, y, stride, pad, groups, relu)``
-    of device tensors (bias may be None).  The tensors are kept referenced
-    for the executor's lifetime.
+    of device tensors (bias may be None), optionally with a tenth element
+    ``res``: a residual shaped like y joined before the activation (or None).
+    The tensors are kept referenced for the executor's lifetime.
     """
 
     def __init__(self, layers):
         self._keep = []
         descs = (ConvDesc * len(layers))()
-        for d, (op, x, w, bias, y, stride, pad, groups, relu) in zip(descs, layers):
+        for d, layer in zip(descs, layers):
+            op, x, w, bias, y, stride, pad, groups, relu = layer[:9]
+            res = layer[9] if len(layer) > 9 else None
+            if res is not None:
+                _dev(res, torch.float32, "res", 4)
+                if tuple(res.shape) != tuple(y.shape):
+                    raise ValueError("res must have y's shape")
             xdt = torch.bfloat16 if op == OP_CONV_BF16 else torch.float32
             _dev(x, xdt, "x", 4)
             _dev(w, xdt, "w", 4)
@@ -310,7 +338,8 @@ class Stack:
             d.op, d.N, d.C, d.H, d.W, d.K, d.R, d.S = op, N, C, H, W, K, R, S
             d.stride, d.pad, d.groups, d.relu = stride, pad, groups, 1 if relu else 0
             d.x, d.w, d.bias, d.y = x.data_ptr(), w.data_ptr(), _ptr(bias), y.data_ptr()
-            self._keep.append((x, w, bias, y))
+            d.res = _ptr(res)
+            self._keep.append((x, w, bias, y, res))
         self.n = len(layers)
         self.steps = 0
         h = ctypes.c_void_p()

@@ -110,3 +110,19 @@ def test_packed_entry_points_validate_first(L):
     assert L.conv2d_fwd_packed(*shape[:-1], 7, FAKE, FAKE, None, FAKE, 0, None) == miconv.ERR_UNSUPPORTED
     assert L.conv2d_fwd_packed(1, 64, 56, 56, 64, 3, 3, 0, 1, 1, 0, FAKE, FAKE, None, FAKE, 0,
                                None) == miconv.ERR_SHAPE
+
+
+def test_residual_entry_point_validates_first(L):
+    """conv2d_fwd_res checks dtype, pointers, the residual's alignment and the
+    operator kind before anything is launched (no GPU needed)."""
+    shape = (1, 64, 56, 56, 64, 3, 3, 1, 1, 1)
+    A = miconv.ALGO_AUTO
+    assert L.conv2d_fwd_res(*shape, 2, A, FAKE, FAKE, None, FAKE, FAKE, 0, None) == miconv.ERR_UNSUPPORTED
+    assert L.conv2d_fwd_res(*shape, 0, A, None, FAKE, None, FAKE, FAKE, 0, None) == miconv.ERR_NULL
+    assert L.conv2d_fwd_res(*shape, 1, A, FAKE, FAKE, None, FAKE, None, 0, None) == miconv.ERR_NULL
+    assert L.conv2d_fwd_res(*shape, 0, 9, FAKE, FAKE, None, FAKE, FAKE, 0, None) == miconv.ERR_UNSUPPORTED
+    for off in (2, 4, 8, 12):   # not at y's offset modulo 16 bytes
+        assert L.conv2d_fwd_res(*shape, 0, A, FAKE, FAKE, None, FAKE + off, FAKE, 0,
+                                None) == miconv.ERR_ALIGN, off
+    dw = (1, 32, 28, 28, 32, 3, 3, 1, 1, 32)
+    assert L.conv2d_fwd_res(*dw, 0, A, FAKE, FAKE, None, FAKE, FAKE, 0, None) == miconv.ERR_UNSUPPORTED

@@ -277,3 +277,64 @@ def test_rejects_bad_arguments(oracle_lib):
         oracle_lib.conv2d(x, np.zeros((2, 2, 3, 3), np.float32), groups=2)   # C % groups
     with pytest.raises(ValueError):
         oracle_lib.conv2d(x, np.zeros((2, 3, 5, 5), np.float32))             # empty output
+
+
+def test_hand_residual(oracle_lib, gold):
+    """The fused residual join, act(conv + bias + res), on a hand-worked 1x1
+    example; the activation comes after the join (relu before it gives a
+    different, wrong, answer on this example)."""
+    d = gold["residual"]
+    x = _f32(d["x"])[None, None]
+    w = _f32([[[[d["w"]]]]])
+    b = _f32([d["bias"]])
+    res = _f32(d["res"])[None, None]
+    y = oracle_lib.conv2d(x, w, b, relu=True, res=res)
+    np.testing.assert_array_equal(y[0, 0], _f32(d["y_relu"]))
+    np.testing.assert_array_equal(oracle_lib.conv2d(x, w, b, relu=False, res=res)[0, 0],
+                                  _f32(d["y_linear"]))
+    wrong = oracle_lib.conv2d(x, w, b, relu=True) + res
+    np.testing.assert_array_equal(wrong[0, 0], _f32(d["y_relu_before_join"]))
+    assert not np.array_equal(wrong, y)
+    # bf16 entry: the same values are exact in bf16
+    xb, wb = oracle_lib.f32_to_bf16(x), oracle_lib.f32_to_bf16(w)
+    np.testing.assert_array_equal(oracle_lib.conv2d_bf16(xb, wb, b, relu=True, res=res), y)
+
+
+def test_residual_brute_force_against_torch_float64(oracle_lib):
+    """act(conv + bias + res) against torch float64 conv2d plus the residual,
+    on random tiny shapes (strides, padding, groups)."""
+    rng = np.random.default_rng(77)
+    cases = list(_tiny_grid())
+    for i in rng.choice(len(cases), size=300, replace=False):
+        N, C, K, H, W, R, S, st, pad, groups = cases[i]
+        x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+        w = rng.standard_normal((K, C // groups, R, S)).astype(np.float32)
+        b = rng.standard_normal(K).astype(np.float32)
+        ref = F.conv2d(torch.from_numpy(x).double(), torch.from_numpy(w).double(),
+                       torch.from_numpy(b).double(), stride=st, padding=pad, groups=groups)
+        res = rng.standard_normal(tuple(ref.shape)).astype(np.float32)
+        relu = bool(rng.integers(0, 2))
+        ref = ref + torch.from_numpy(res).double()
+        if relu:
+            ref = torch.relu(ref)
+        y = oracle_lib.conv2d(x, w, b, st, pad, groups, relu, res=res)
+        np.testing.assert_allclose(y, ref.numpy().astype(np.float32), rtol=2.0 ** -22, atol=1e-12,
+                                   err_msg=str(cases[i]))
+
+
+def test_residual_small_integers_exact(oracle_lib):
+    """On small integers every sum is exact: the fused join equals the plain
+    conv plus the residual, and res = 0 gives the plain conv."""
+    rng = np.random.default_rng(5)
+    x = rng.integers(-4, 5, (2, 6, 7, 5)).astype(np.float32)
+    w = rng.integers(-4, 5, (4, 3, 3, 3)).astype(np.float32)
+    b = rng.integers(-8, 9, 4).astype(np.float32)
+    plain = oracle_lib.conv2d(x, w, b, 2, 1, 2)
+    res = rng.integers(-50, 51, plain.shape).astype(np.float32)
+    np.testing.assert_array_equal(oracle_lib.conv2d(x, w, b, 2, 1, 2, res=res), plain + res)
+    np.testing.assert_array_equal(oracle_lib.conv2d(x, w, b, 2, 1, 2, True, res=res),
+                                  np.maximum(plain + res, 0))
+    np.testing.assert_array_equal(oracle_lib.conv2d(x, w, b, 2, 1, 2, True, res=np.zeros_like(plain)),
+                                  oracle_lib.conv2d(x, w, b, 2, 1, 2, True))
+    with pytest.raises(ValueError):
+        oracle_lib.conv2d(x, w, b, 2, 1, 2, res=res[:, :2])
