@@ -124,8 +124,30 @@ def _vgg16(N: int) -> List[ConvLayer]:
     return L
 
 
+def _squeezenet10(N: int) -> List[ConvLayer]:
+    """SqueezeNet 1.0 (Iandola et al., 2016; the third classification model of
+    Sec. 4.1): 7x7/2 stem to 96 channels (no padding, 224 -> 109), 3x3/2
+    max-pools (ceil mode: 109 -> 54 -> 27 -> 13) before fire2, fire5 and
+    fire9, eight fire modules, each a 1x1 squeeze conv followed by a 1x1 and a
+    3x3 (pad 1) expand conv whose outputs are concatenated along channels
+    (expand1x1 first), and a 1x1 classifier conv to 1000 channels; bias +
+    ReLU after every conv."""
+    L = [ConvLayer("conv1", N, 3, 224, 224, 96, 7, 7, 2, 0, relu=True)]
+    # (fire index, input channels, squeeze, expand per branch, extent)
+    fires = [(2, 96, 16, 64, 54), (3, 128, 16, 64, 54), (4, 128, 32, 128, 54),
+             (5, 256, 32, 128, 27), (6, 256, 48, 192, 27), (7, 384, 48, 192, 27),
+             (8, 384, 64, 256, 27), (9, 512, 64, 256, 13)]
+    for f, cin, sq, ex, e in fires:
+        L.append(ConvLayer(f"fire{f}_squeeze", N, cin, e, e, sq, 1, 1, 1, 0, relu=True))
+        L.append(ConvLayer(f"fire{f}_expand1x1", N, sq, e, e, ex, 1, 1, 1, 0, relu=True))
+        L.append(ConvLayer(f"fire{f}_expand3x3", N, sq, e, e, ex, 3, 3, 1, 1, relu=True))
+    L.append(ConvLayer("conv10", N, 512, 13, 13, 1000, 1, 1, 1, 0, relu=True))
+    return L
+
+
 def workload(config: int, batch: Optional[int] = None) -> Workload:
-    """The five evaluation configurations (1-based)."""
+    """The five evaluation configurations (1-based), and 6: SqueezeNet 1.0 at
+    batch 1 (the paper's third model)."""
     if config == 1:
         L = [ConvLayer("conv3x3_64", 1, 64, 56, 56, 64, 3, 3, 1, 1, relu=True)]
         w = Workload(1, "conv3x3 64->64 @56x56 b1 fp32", L)
@@ -137,6 +159,8 @@ def workload(config: int, batch: Optional[int] = None) -> Workload:
         w = Workload(4, "VGG-16 conv stack b8 fp32", _vgg16(8))
     elif config == 5:
         w = Workload(5, "ResNet-50 v1 conv stack b64 bf16-in fp32-acc", _resnet50_v1(64), dtype="bf16")
+    elif config == 6:
+        w = Workload(6, "SqueezeNet 1.0 conv stack b1 fp32", _squeezenet10(1))
     else:
         raise ValueError(f"no config {config}")
     if batch is not None:

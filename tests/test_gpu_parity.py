@@ -340,7 +340,7 @@ def _check_layer(oracle_lib, config, i, l, images=None, kmax=None, tol=TOL_F32):
     return y
 
 
-@pytest.mark.parametrize("config", [1, 2, 3])
+@pytest.mark.parametrize("config", [1, 2, 3, 6])
 def test_configs_full_oracle(oracle_lib, config):
     """Configs 1-3 (batch 1, fp32): every layer against the whole oracle output."""
     for i, l in _layers(config):

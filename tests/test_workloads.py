@@ -1,7 +1,7 @@
 """Layer tables of the evaluated networks: counts, chaining and FLOP totals.
 
-ResNet50_v1 and MobileNet1.0 are the classification models of the paper's
-evaluation (Sec. 4.1, Tables 1-3 and 5); VGG-16 is an extra dense stack.
+ResNet50_v1, MobileNet1.0 and SqueezeNet1.0 are the classification models of
+the paper's evaluation (Sec. 4.1); VGG-16 is an extra dense stack.
 The FLOP totals are the standard per-network conv counts at 224x224
 (2 FLOP per multiply-add).
 """
@@ -77,3 +77,27 @@ def test_seeded_inputs_are_deterministic():
     assert (x1 == x2).all() and (w1 == w2).all() and (b1 == b2).all()
     assert x1.min() >= 0 and x1.max() < 1
     assert abs(w1.std() - (2 / 576) ** 0.5) < 0.01 * (2 / 576) ** 0.5 * 10
+
+
+def test_squeezenet_table(oracle_lib):
+    """SqueezeNet 1.0: 26 convs; 0.82 G multiply-adds at 224x224 (the figure
+    published for the model); fire modules chain through 3x3/2 ceil-mode
+    pools (109 -> 54 -> 27 -> 13); each fire's expand branches read its
+    squeeze output and concatenate to the next fire's input channels."""
+    L = wl.workload(6).layers
+    assert len(L) == 26
+    macs = sum(wl.flops(l, *_out(oracle_lib, l)) for l in L) / 2
+    assert abs(macs / 0.82e9 - 1) < 0.01, macs
+    assert _out(oracle_lib, L[0]) == (109, 109)
+    pool = lambda h: -(-(h - 3) // 2) + 1          # 3x3/2, ceil mode
+    c, h = L[0].K, _out(oracle_lib, L[0])[0]
+    for f in range(8):
+        sq, e1, e3 = L[1 + 3 * f: 4 + 3 * f]
+        if sq.H != h:
+            assert sq.H == pool(h), sq.name
+            h = sq.H
+        assert (sq.C, sq.R) == (c, 1), sq.name
+        assert (e1.C, e3.C, e1.R, e3.R, e3.pad) == (sq.K, sq.K, 1, 3, 1), e1.name
+        assert e1.K == e3.K and _out(oracle_lib, e1) == _out(oracle_lib, e3) == (h, h)
+        c = e1.K + e3.K
+    assert (L[-1].C, L[-1].K, L[-1].H) == (c, 1000, h) == (512, 1000, 13)
