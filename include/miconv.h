@@ -128,6 +128,19 @@ int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, 
                    int groups, int dtype, int algo, const void *x, const void *w,
                    const float *bias, const float *res, float *y, int relu, void *stream);
 
+/* conv2d_fwd_res with the output written at an image stride: image n of y
+ * (and of res) starts y_image_stride elements after image n-1, each image
+ * being a dense [K][P][Q] block; 0 means K*P*Q (a dense y).  With a larger
+ * stride, y can be a channel range of a wider NCHW tensor, which is how the
+ * fire modules of SqueezeNet (Sec. 4.1) concatenate their two expand convs:
+ * each expand conv writes its channel range in place, at any batch.  The
+ * stride must be >= K*P*Q (images must not overlap; MICONV_ERR_SHAPE),
+ * (N-1)*stride + K*P*Q must stay below 2^31 (MICONV_ERR_TOO_LARGE), and
+ * depthwise shapes take no stride (MICONV_ERR_UNSUPPORTED). */
+int conv2d_fwd_ex(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
+                  const float *res, float *y, long y_image_stride, int relu, void *stream);
+
 /* Filters packed once for repeated calls of one layer (the pre-computing step
  * of the paper's graph-level optimisation, Sec. 3.2.3), outside a stack.
  * The packed layout is the one the kernel chosen for this shape reads: the
@@ -195,6 +208,7 @@ typedef struct miconv_conv_desc {
     float *y;
     const float *res;          /* residual joined before the activation, as in
                                   conv2d_fwd_res (dense ops only); may be NULL */
+    long y_image_stride;       /* as in conv2d_fwd_ex; 0 = dense y */
 } miconv_conv_desc;
 
 typedef struct miconv_stack miconv_stack;

@@ -45,6 +45,7 @@ ConvArgs make_args(const ConvProblem &p)
     a.kr_per_split = p.Kred;
     a.relu = p.relu;
     a.res = p.res;
+    a.ysn = p.ysn;
     a.dv_pq = make_fastdiv(p.P * p.Q);
     a.dv_q = make_fastdiv(p.Q);
     return a;
@@ -100,6 +101,8 @@ int validate(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     p->Kred = (int)(Cg * R * S);
     p->M = (int)((long)N * P * Q);
     p->relu = 0;
+    p->res = nullptr;
+    p->ysn = (long)K * P * Q;
     return MICONV_OK;
 }
 
@@ -257,6 +260,17 @@ int set_residual(Resolved &r, const float *res)
         return MICONV_ERR_ALIGN;
     if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
     r.p.res = res;
+    return MICONV_OK;
+}
+
+int set_output_stride(Resolved &r, long ysn)
+{
+    const long dense = (long)r.p.K * r.p.P * r.p.Q;
+    if (ysn == 0 || ysn == dense) return MICONV_OK;
+    if (ysn < dense) return MICONV_ERR_SHAPE;                  // images would overlap
+    if ((long)(r.p.N - 1) * ysn + dense > INT_MAX) return MICONV_ERR_TOO_LARGE;
+    if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
+    r.p.ysn = ysn;
     return MICONV_OK;
 }
 
@@ -479,16 +493,25 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
                                 MICONV_ALGO_AUTO, stream);
 }
 
-int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                   int groups, int dtype, int algo, const void *x, const void *w,
-                   const float *bias, const float *res, float *y, int relu, void *stream)
+int conv2d_fwd_ex(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
+                  const float *res, float *y, long y_image_stride, int relu, void *stream)
 {
     if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
     Resolved r;
     int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride,
                      pad, groups, x, w, bias, y, relu, &r);
+    if (rc == MICONV_OK) rc = set_output_stride(r, y_image_stride);
     if (rc == MICONV_OK) rc = set_residual(r, res);
     return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+}
+
+int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                   int groups, int dtype, int algo, const void *x, const void *w,
+                   const float *bias, const float *res, float *y, int relu, void *stream)
+{
+    return conv2d_fwd_ex(N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, x, w, bias, res, y, 0,
+                         relu, stream);
 }
 
 long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,

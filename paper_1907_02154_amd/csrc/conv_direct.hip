@@ -46,9 +46,10 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(ConvArgs a)
             }
         }
         float v = acc + (a.bias ? a.bias[k] : 0.f);
-        if (a.res) v += a.res[i];
+        const long yi = (long)n * a.ysn + ((long)k * a.P + p) * a.Q + q;
+        if (a.res) v += a.res[yi];
         if (a.relu) v = fmaxf(v, 0.f);
-        a.y[i] = v;
+        a.y[yi] = v;
     }
 }
 

@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void igemm_bf16_kernel(ConvArgs a)
         mok[bj] = m < a.M;
         const int mm = mok[bj] ? m : 0;
         const int n = mm / a.PQ;
-        ybase[bj] = a.splits > 1 ? (long)mm : (long)n * a.K * a.PQ + (mm - n * a.PQ);
+        ybase[bj] = a.splits > 1 ? (long)mm : (long)n * a.ysn + (mm - n * a.PQ);
     }
     const long cstride = a.splits > 1 ? (long)a.M : (long)a.PQ;
     float *out = a.splits > 1 ? a.ws + (long)split * a.K * a.M : a.y;

@@ -166,7 +166,7 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
         if (m >= a.M) continue;
         const int n = m / a.PQ;
         const int pq = m - n * a.PQ;
-        const long ybase = (long)n * a.K * a.PQ + pq;
+        const long ybase = (long)n * a.ysn + pq;
 #pragma unroll
         for (int bi = 0; bi < BI; ++bi) {
 #pragma unroll
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
         }
         s += bv;
         const unsigned n = fdiv(m, a.dv_pq);
-        const size_t yo = ((size_t)n * a.K + k) * a.PQ + (m - n * a.PQ);
+        const size_t yo = (size_t)n * a.ysn + (size_t)k * a.PQ + (m - n * a.PQ);
         if (a.res) s += a.res[yo];
         if (a.relu) s = fmaxf(s, 0.f);
         a.y[yo] = s;

@@ -303,7 +303,7 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
 
     // Epilogue: lane l holds channel column l%32 and, per group of 4
     // registers, 4 consecutive pixels.
-    const bool vec = a.splits == 1 && (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+    const bool vec = a.splits == 1 && (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0 && (a.ysn & 3) == 0;
     const long cstride = a.splits > 1 ? (long)a.M : (long)a.PQ;
     float *out = a.splits > 1 ? a.ws + (long)split * a.K * a.M : a.y;
 #pragma unroll
@@ -330,7 +330,7 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
                 }
                 if (vec && mb + 3 < a.M) {
                     const int n = mb / a.PQ;
-                    const long off = (long)n * a.K * a.PQ + (mb - n * a.PQ) + coff;
+                    const long off = (long)n * a.ysn + (mb - n * a.PQ) + coff;
                     if (a.res) {
                         const float4 r = *reinterpret_cast<const float4 *>(a.res + off);
                         const float re[4] = {r.x, r.y, r.z, r.w};
@@ -348,7 +348,7 @@ __global__ __launch_bounds__(256) void igemm_bf16_nhwc_kernel(ConvArgs a)
                         if (m >= a.M) continue;
                         const int n = m / a.PQ;
                         const long off = a.splits > 1 ? (long)m + coff
-                                                      : (long)n * a.K * a.PQ + (m - n * a.PQ) + coff;
+                                                      : (long)n * a.ysn + (m - n * a.PQ) + coff;
                         float val = v4[e];
                         if (a.splits == 1 && a.res) {
                             val += a.res[off];
@@ -384,7 +384,7 @@ __device__ inline void store_tile(const ConvArgs &a, const float *ot, int tid, i
 {
     const bool split_out = a.splits > 1;
     float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
-    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0);
+    const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0 && (a.ysn & 3) == 0);
     constexpr int C4 = BPX / 4;
     for (int idx = tid; idx < BKC * C4; idx += NT) {
         const int kl = idx / C4, c4 = idx - kl * C4;
@@ -395,8 +395,8 @@ __device__ inline void store_tile(const ConvArgs &a, const float *ot, int tid, i
         const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
         const float ve[4] = {v.x, v.y, v.z, v.w};
         if (vec && m + 3 < a.M) {
-            const int n = split_out ? 0 : m / a.PQ;
-            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ);
+            const int n = split_out ? 0 : (int)fdiv(m, a.dv_pq);
+            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.ysn + (long)kg * a.PQ) + (m - n * a.PQ);
             typedef float f32x4 __attribute__((ext_vector_type(4)));
             const f32x4 nv = {v.x, v.y, v.z, v.w};
             __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
@@ -405,8 +405,8 @@ __device__ inline void store_tile(const ConvArgs &a, const float *ot, int tid, i
             for (int e = 0; e < 4; ++e) {
                 const int mm = m + e;
                 if (mm >= a.M) break;
-                const int n = split_out ? 0 : mm / a.PQ;
-                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ);
+                const int n = split_out ? 0 : (int)fdiv(mm, a.dv_pq);
+                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.ysn + (long)kg * a.PQ) + (mm - n * a.PQ);
                 out[off] = ve[e];
             }
         }
@@ -425,7 +425,8 @@ __device__ inline void load_res_tile(const ConvArgs &a, int tid, int k0, int m0,
     constexpr int C4 = BPX / 4;
     constexpr int IT = BKC * C4 / NT;
     static_assert(BKC * C4 % NT == 0, "epilogue rows per thread");
-    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+    const int ysn = (int)a.ysn;   // every y offset is below 2^31 (checked on the host)
+    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0 && (ysn & 3) == 0;
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
         const int idx = tid + it * NT;
@@ -437,9 +438,9 @@ __device__ inline void load_res_tile(const ConvArgs &a, int tid, int k0, int m0,
         if (k >= a.Kg || m >= a.M) continue;
         const int kg = g * a.Kg + k;
         if (vec && m + 3 < a.M) {
-            const int n = m / a.PQ;
+            const int n = (int)fdiv(m, a.dv_pq);
             const float4 r = *reinterpret_cast<const float4 *>(
-                a.res + ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ));
+                a.res + (n * ysn + kg * a.PQ) + (m - n * a.PQ));
             rv[it][0] = r.x;
             rv[it][1] = r.y;
             rv[it][2] = r.z;
@@ -449,8 +450,8 @@ __device__ inline void load_res_tile(const ConvArgs &a, int tid, int k0, int m0,
             for (int e = 0; e < 4; ++e) {
                 const int mm = m + e;
                 if (mm >= a.M) break;
-                const int n = mm / a.PQ;
-                rv[it][e] = a.res[((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ)];
+                const int n = (int)fdiv(mm, a.dv_pq);
+                rv[it][e] = a.res[(n * ysn + kg * a.PQ) + (mm - n * a.PQ)];
             }
         }
     }
@@ -462,7 +463,8 @@ __device__ inline void store_tile_res(const ConvArgs &a, const float *ot, int ti
 {
     constexpr int C4 = BPX / 4;
     constexpr int IT = BKC * C4 / NT;
-    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0;
+    const int ysn = (int)a.ysn;
+    const bool vec = (a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0 && (ysn & 3) == 0;
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
         const int idx = tid + it * NT;
@@ -479,18 +481,18 @@ __device__ inline void store_tile_res(const ConvArgs &a, const float *ot, int ti
             if (a.relu) ve[e] = fmaxf(ve[e], 0.f);
         }
         if (vec && m + 3 < a.M) {
-            const int n = m / a.PQ;
+            const int n = (int)fdiv(m, a.dv_pq);
             typedef float f32x4 __attribute__((ext_vector_type(4)));
             const f32x4 nv = {ve[0], ve[1], ve[2], ve[3]};
             __builtin_nontemporal_store(
-                nv, reinterpret_cast<f32x4 *>(a.y + ((long)n * a.K + kg) * a.PQ + (m - n * a.PQ)));
+                nv, reinterpret_cast<f32x4 *>(a.y + (n * ysn + kg * a.PQ) + (m - n * a.PQ)));
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int mm = m + e;
                 if (mm >= a.M) break;
-                const int n = mm / a.PQ;
-                a.y[((long)n * a.K + kg) * a.PQ + (mm - n * a.PQ)] = ve[e];
+                const int n = (int)fdiv(mm, a.dv_pq);
+                a.y[(n * ysn + kg * a.PQ) + (mm - n * a.PQ)] = ve[e];
             }
         }
     }

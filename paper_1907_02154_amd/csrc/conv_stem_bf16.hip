@@ -49,6 +49,7 @@ struct StemArgs {
     const uint16_t *wp;       // [K][28][8] bf16, packed
     const float *bias;
     const float *res;         // [N][K][P][kQ] added before the activation, or nullptr
+    long ysn;                 // elements between images of y and res
     float *y;                 // [N][K][P][kQ]
     int N, C, H, W, K, P;
     int relu;
@@ -154,7 +155,7 @@ __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
             const int k = k0 + f * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
             if (k >= a.K) continue;
             const float bv = a.bias ? a.bias[k] : 0.f;
-            const long yo = ((long)n * a.K + k) * plane + (long)p0 * kQ;
+            const long yo = (long)n * a.ysn + (long)k * plane + (long)p0 * kQ;
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const long o = yo + 32 * (2 * wave + b) + ll;
@@ -215,6 +216,7 @@ hipError_t launch_stem_bf16(const ConvProblem &p, const uint16_t *x, const uint1
     a.wp = wpacked;
     a.bias = bias;
     a.res = p.res;
+    a.ysn = p.ysn;
     a.y = y;
     a.N = p.N;
     a.C = p.C;

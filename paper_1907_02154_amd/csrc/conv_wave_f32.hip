@@ -289,7 +289,7 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             const int m = m0 + j * 32 + ll;
             if (m >= a.M) continue;
             const int n = fdiv(m, a.dv_pq);
-            const long yo = ((long)n * a.K + g * a.Kg) * a.PQ + (m - n * a.PQ);
+            const long yo = (long)n * a.ysn + (long)(g * a.Kg) * a.PQ + (m - n * a.PQ);
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int k = k0 + 8 * (v >> 2) + 4 * h + (v & 3);
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             } else {
                 const int n = fdiv(m, a.dv_pq);
                 const int pq = m - n * a.PQ;
-                const long yo = ((long)n * a.K + kg) * a.PQ + pq;
+                const long yo = (long)n * a.ysn + (long)kg * a.PQ + pq;
                 float val = sum + bias_v[i];
                 if (a.res) val += a.res[yo];
                 if (a.relu) val = fmaxf(val, 0.f);

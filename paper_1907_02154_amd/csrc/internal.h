@@ -34,6 +34,7 @@ struct ConvProblem {
     int M;           // N * P * Q: the GEMM pixel extent
     int relu;
     const float *res;  // [N][K][P][Q] added to the conv + bias before the activation, or nullptr
+    long ysn;          // elements from one image of y (and res) to the next: K*P*Q when dense
 };
 
 // Division by a divisor d >= 1 fixed at launch, for numerators below 2^31:
@@ -65,6 +66,7 @@ struct ConvArgs {
     float *y;             // [N][K][P][Q]
     const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may
                           // be y itself (every element is read and written by one thread)
+    long ysn;             // elements from one image of y (and res) to the next (>= K*P*Q)
     float *ws;            // split-K partials [splits][K][M] (nullptr when splits == 1)
     int N, C, H, W, K, R, S, stride, pad, groups;
     int P, Q, Cg, Kg, Kred, M, PQ, HW;
@@ -219,6 +221,9 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
 // Adds a residual [N][K][P][Q] (read at y's indices, before the activation) to
 // a resolved dense layer; nullptr leaves it unchanged.
 int set_residual(Resolved &r, const float *res);
+// Sets the distance in elements between images of y (and res); 0 keeps the
+// dense K*P*Q.  A larger stride lets y be a channel range of a wider tensor.
+int set_output_stride(Resolved &r, long ysn);
 hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
 void describe(const Resolved &r, char *buf, int len, int *launches);
 size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + split partials

@@ -54,6 +54,7 @@ def lib() -> ctypes.CDLL:
         L.add_act_fwd.argtypes = [l, p, p, p, i, p]
         L.cast_f32_to_bf16.argtypes = [l, p, p, p]
         L.conv2d_fwd_res.argtypes = [i] * 12 + [p, p, p, p, p, i, p]
+        L.conv2d_fwd_ex.argtypes = [i] * 12 + [p, p, p, p, p, l, i, p]
         L.conv2d_packed_weight_bytes.argtypes = [i] * 11
         L.conv2d_packed_weight_bytes.restype = l
         L.conv2d_pack_weights.argtypes = [i] * 11 + [p, p, p]
@@ -133,6 +134,19 @@ def _dev(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None):
         raise ValueError(f"{name} must have {ndim} dims")
 
 
+def _image_strided(t: torch.Tensor, name: str) -> int:
+    """Checks that a 4-d fp32 device tensor is dense within each image (a
+    channel range of a wider NCHW tensor qualifies) and returns its image
+    stride in elements."""
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != torch.float32 \
+            or t.dim() != 4:
+        raise TypeError(f"{name} must be a 4-d float32 device tensor")
+    N, K, P, Q = t.shape
+    if t.stride()[1:] != (P * Q, Q, 1) and K * P * Q > 1:
+        raise ValueError(f"{name} must be dense within each image")
+    return t.stride(0) if N > 1 else K * P * Q
+
+
 def out_dims(H: int, W: int, R: int, S: int, stride: int, pad: int):
     P, Q = ctypes.c_int(), ctypes.c_int()
     rc = lib().miconv_out_dims(H, W, R, S, stride, pad, ctypes.byref(P), ctypes.byref(Q))
@@ -194,6 +208,34 @@ def conv2d_fwd_res(x, w, bias, res, y, stride=1, pad=0, groups=1, relu=False, al
                  int(algo), px, pw, pb, _ptr(res), py, relu_, stream_)
     call.__name__ = "conv2d_fwd_res"
     return _conv_common(call, x, w, bias, y, stride, pad, groups, relu, stream, xdt)
+
+
+def conv2d_fwd_ex(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None, algo=ALGO_AUTO,
+                  stream=None):
+    """y = act(conv(x, w) + bias [+ res]) where y (and res, with the same
+    strides) may be a channel range of a wider NCHW tensor, e.g. big[:, 64:128]:
+    its image stride is passed to the library."""
+    xdt = torch.bfloat16 if x.dtype == torch.bfloat16 else torch.float32
+    _dev(x, xdt, "x", 4)
+    _dev(w, xdt, "w", 4)
+    if bias is not None:
+        _dev(bias, torch.float32, "bias", 1)
+    ys = _image_strided(y, "y")
+    if res is not None:
+        if _image_strided(res, "res") != ys or tuple(res.shape) != tuple(y.shape):
+            raise ValueError("res must have y's shape and strides")
+    N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if groups <= 0 or Cg * groups != C:
+        raise ValueError("w.shape[1] * groups must equal C")
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, K, P, Q):
+        raise ValueError(f"y must have shape {(N, K, P, Q)}, got {tuple(y.shape)}")
+    rc = lib().conv2d_fwd_ex(N, C, H, W, K, R, S, stride, pad, groups, 1 if xdt == torch.bfloat16 else 0,
+                             int(algo), _ptr(x), _ptr(w), _ptr(bias), _ptr(res), _ptr(y), ys,
+                             1 if relu else 0, _stream(stream))
+    _check(rc, "conv2d_fwd_ex")
+    return y
 
 
 class PackedFilters:
@@ -305,7 +347,7 @@ class ConvDesc(ctypes.Structure):
                                          ("N", "C", "H", "W", "K", "R", "S", "stride", "pad",
                                           "groups", "relu")] + \
                [("x", ctypes.c_void_p), ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
-                ("y", ctypes.c_void_p), ("res", ctypes.c_void_p)]
+                ("y", ctypes.c_void_p), ("res", ctypes.c_void_p), ("y_image_stride", ctypes.c_long)]
 
 
 class Stack:
@@ -314,7 +356,8 @@ class Stack:
     ``layers`` holds tuples ``(op, x, w, bias, y, stride, pad, groups, relu)``
     of device tensors (bias may be None), optionally with a tenth element
     ``res``: a residual shaped like y joined before the activation (or None).
-    The tensors are kept referenced for the executor's lifetime.
+    y (and res, with the same strides) may be a channel range of a wider NCHW
+    tensor.  The tensors are kept referenced for the executor's lifetime.
     """
 
     def __init__(self, layers):
@@ -323,14 +366,13 @@ class Stack:
         for d, layer in zip(descs, layers):
             op, x, w, bias, y, stride, pad, groups, relu = layer[:9]
             res = layer[9] if len(layer) > 9 else None
+            ys = _image_strided(y, "y")
             if res is not None:
-                _dev(res, torch.float32, "res", 4)
-                if tuple(res.shape) != tuple(y.shape):
-                    raise ValueError("res must have y's shape")
+                if _image_strided(res, "res") != ys or tuple(res.shape) != tuple(y.shape):
+                    raise ValueError("res must have y's shape and strides")
             xdt = torch.bfloat16 if op == OP_CONV_BF16 else torch.float32
             _dev(x, xdt, "x", 4)
             _dev(w, xdt, "w", 4)
-            _dev(y, torch.float32, "y", 4)
             if bias is not None:
                 _dev(bias, torch.float32, "bias", 1)
             N, C, H, W = x.shape
@@ -339,6 +381,7 @@ class Stack:
             d.stride, d.pad, d.groups, d.relu = stride, pad, groups, 1 if relu else 0
             d.x, d.w, d.bias, d.y = x.data_ptr(), w.data_ptr(), _ptr(bias), y.data_ptr()
             d.res = _ptr(res)
+            d.y_image_stride = ys
             self._keep.append((x, w, bias, y, res))
         self.n = len(layers)
         self.steps = 0

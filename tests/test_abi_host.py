@@ -126,3 +126,16 @@ def test_residual_entry_point_validates_first(L):
                                 None) == miconv.ERR_ALIGN, off
     dw = (1, 32, 28, 28, 32, 3, 3, 1, 1, 32)
     assert L.conv2d_fwd_res(*dw, 0, A, FAKE, FAKE, None, FAKE, FAKE, 0, None) == miconv.ERR_UNSUPPORTED
+
+
+def test_output_stride_validation(L):
+    """conv2d_fwd_ex: the image stride of y must keep images apart, fit 32-bit
+    offsets, and is refused for depthwise shapes; checked before any launch."""
+    shape = (2, 64, 56, 56, 64, 3, 3, 1, 1, 1)
+    A = miconv.ALGO_AUTO
+    dense = 64 * 56 * 56
+    assert L.conv2d_fwd_ex(*shape, 0, A, FAKE, FAKE, None, None, FAKE, dense - 1, 0, None) == miconv.ERR_SHAPE
+    assert L.conv2d_fwd_ex(*shape, 0, A, FAKE, FAKE, None, None, FAKE, 1 << 31, 0, None) == miconv.ERR_TOO_LARGE
+    dw = (2, 32, 28, 28, 32, 3, 3, 1, 1, 32)
+    assert L.conv2d_fwd_ex(*dw, 0, A, FAKE, FAKE, None, None, FAKE, 64 * 28 * 28, 0, None) == miconv.ERR_UNSUPPORTED
+    assert L.conv2d_fwd_ex(*shape, 3, A, FAKE, FAKE, None, None, FAKE, 0, 0, None) == miconv.ERR_UNSUPPORTED

@@ -203,3 +203,25 @@ def test_stack_layers_with_residual(oracle_lib):
         for i, (o, ref) in enumerate(zip(ops, want)):
             np.testing.assert_array_equal(o[4].cpu().numpy(), ref, err_msg=f"replay {rep} layer {i}")
     s.close()
+
+
+@pytest.mark.parametrize("case", RES_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
+def test_output_image_stride(oracle_lib, case):
+    """y (and res) as a channel range of a wider NCHW tensor at batch >= 2
+    (conv2d_fwd_ex): every kernel writes image n at n * stride, joins the
+    residual read with the same strides, and leaves the other channels alone."""
+    N, C, H, W, K, R, S, st, pad, g, dt, algo, kernel = case
+    case2 = (max(N, 2),) + case[1:]
+    x, w, b, res, tx, tw = _inputs(case2, 7300 + sum(case[:10]))
+    n2, _, P, Q = res.shape
+    for off, extra in ((4, 8), (3, 5)):       # y 16-byte aligned or not
+        big = torch.full((n2, K + extra, P, Q), float("nan"), device="cuda")
+        rbig = torch.zeros((n2, K + extra, P, Q), device="cuda")
+        y, r = big[:, off:off + K], rbig[:, off:off + K]
+        r.copy_(dev(res))
+        miconv.conv2d_fwd_ex(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
+        torch.cuda.synchronize()
+        name = miconv.conv2d_describe(n2, C, H, W, K, R, S, st, pad, g, dt, algo)[0]
+        np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case2, x, w, b, res, True),
+                                      err_msg=f"{name} offset {off}")
+        assert torch.isnan(big[:, :off]).all() and torch.isnan(big[:, off + K:]).all()

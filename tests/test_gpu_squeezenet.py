@@ -72,3 +72,38 @@ def test_fire_module_concat_small_ints(oracle_lib, fire):
         torch.cuda.synchronize()
         np.testing.assert_array_equal(cat.cpu().numpy(), ref, err_msg=f"fire{f} replay {rep}")
     st.close()
+
+
+def test_fire_module_concat_batch4_strided(oracle_lib):
+    """At batch > 1 a channel range of the joint output is no longer one
+    contiguous run: the expand convs write it through the output image
+    stride (conv2d_fwd_ex, and stack layers whose y is such a view)."""
+    f, cin, sq, ex, e = 6, 256, 48, 192, 27
+    N, s0 = 4, 9500
+    x = wl.small_ints((N, cin, e, e), 0, 3, s0)
+    ws = wl.small_ints((sq, cin, 1, 1), -2, 2, s0 + 1)
+    w1 = wl.small_ints((ex, sq, 1, 1), -2, 2, s0 + 2)
+    w3 = wl.small_ints((ex, sq, 3, 3), -2, 2, s0 + 3)
+    bs, b1, b3 = (wl.small_ints((k,), -8, 8, s0 + 4 + i) for i, k in enumerate((sq, ex, ex)))
+    s_ref = oracle_lib.conv2d(x, ws, bs, 1, 0, 1, True)
+    ref = np.concatenate([oracle_lib.conv2d(s_ref, w1, b1, 1, 0, 1, True),
+                          oracle_lib.conv2d(s_ref, w3, b3, 1, 1, 1, True)], axis=1)
+    tx, tws, tw1, tw3, tbs, tb1, tb3 = map(dev, (x, ws, w1, w3, bs, b1, b3))
+    ts = torch.empty((N, sq, e, e), device="cuda")
+    cat = torch.full((N, 2 * ex, e, e), float("nan"), device="cuda")
+    lo, hi = cat[:, :ex], cat[:, ex:]
+    assert not lo.is_contiguous()
+    miconv.conv2d_fwd(tx, tws, tbs, ts, 1, 0, 1, True)
+    miconv.conv2d_fwd_ex(ts, tw1, tb1, lo, 1, 0, 1, True)
+    miconv.conv2d_fwd_ex(ts, tw3, tb3, hi, 1, 1, 1, True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(cat.cpu().numpy(), ref)
+    op = miconv.OP_CONV_F32
+    st = miconv.Stack([(op, tx, tws, tbs, ts, 1, 0, 1, True),
+                       (op, ts, tw1, tb1, lo, 1, 0, 1, True),
+                       (op, ts, tw3, tb3, hi, 1, 1, 1, True)])
+    cat.fill_(float("nan"))
+    st.launch()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(cat.cpu().numpy(), ref)
+    st.close()
