@@ -59,8 +59,8 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 // need no branches, which keeps the executed code short.  At batch 1 a
 // launch runs a few hundred instructions per wavefront from a cold
 // instruction cache, so code size is a first-order cost here.
-template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
-__global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND, bool GEN>
+__device__ __forceinline__ void wave_body(const ConvArgs &a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
     // Offsets at or past 2^31 bytes are out of range: the x and packed filter
@@ -289,13 +289,14 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             const int m = m0 + j * 32 + ll;
             if (m >= a.M) continue;
             const int n = fdiv(m, a.dv_pq);
-            const long yo = (long)n * a.ysn + (long)(g * a.Kg) * a.PQ + (m - n * a.PQ);
+            const long yo = GEN ? (long)n * a.ysn + (long)(g * a.Kg) * a.PQ + (m - n * a.PQ)
+                                 : ((long)n * a.K + g * a.Kg) * a.PQ + (m - n * a.PQ);
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int k = k0 + 8 * (v >> 2) + 4 * h + (v & 3);
                 if (k >= a.Kg) continue;
                 float val = acc[j][v] + bias_v[v];
-                if (a.res) val += a.res[yo + (long)k * a.PQ];
+                if (GEN && a.res) val += a.res[yo + (long)k * a.PQ];
                 if (a.relu) val = fmaxf(val, 0.f);
                 a.y[yo + (long)k * a.PQ] = val;
             }
@@ -328,9 +329,9 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
             } else {
                 const int n = fdiv(m, a.dv_pq);
                 const int pq = m - n * a.PQ;
-                const long yo = (long)n * a.ysn + (long)kg * a.PQ + pq;
+                const long yo = GEN ? (long)n * a.ysn + (long)kg * a.PQ + pq : ((long)n * a.K + kg) * a.PQ + pq;
                 float val = sum + bias_v[i];
-                if (a.res) val += a.res[yo];
+                if (GEN && a.res) val += a.res[yo];
                 if (a.relu) val = fmaxf(val, 0.f);
                 a.y[yo] = val;
             }
@@ -338,21 +339,48 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
     }
 }
 
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
+__global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
+{
+    wave_body<R_, S_, WAVES, BJ, ORD, IND, false>(a);
+}
+
+// The same kernel with the general epilogue: a residual join and/or an output
+// image stride other than K*P*Q.  The plain kernel keeps the dense epilogue,
+// whose few instructions matter in batch-1 layers of a few microseconds.
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
+__global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_gen_kernel(ConvArgs a)
+{
+    wave_body<R_, S_, WAVES, BJ, ORD, IND, true>(a);
+}
+
+bool general_epilogue(const ConvArgs &a) { return a.res || a.ysn != (long)a.K * a.PQ; }
+
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
+void launch_wave(const ConvArgs &a, dim3 grid, hipStream_t st)
+{
+    if (general_epilogue(a))
+        launch_kernel((igemm_wave_f32_gen_kernel<R_, S_, WAVES, BJ, ORD, IND>), grid, dim3(64 * WAVES), 0,
+                      st, a);
+    else
+        launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, ORD, IND>), grid, dim3(64 * WAVES), 0, st, a);
+}
+
 template <int R_, int S_, int ORD>
 void launch_rs(const ConvArgs &a, int waves, int bj, bool ind, dim3 grid, hipStream_t st)
 {
     if constexpr (ORD == 2 && R_ != 7) {
         if (ind) {   // the planner takes IND with 4 wavefronts and 2 pixel blocks only
-            launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, ORD, true>), grid, dim3(256), 0, st, a);
+            launch_wave<R_, S_, 4, 2, ORD, true>(a, grid, st);
             return;
         }
     }
     if (waves == 8) {
-        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 2, ORD>), grid, dim3(512), 0, st, a);
-        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 8, 1, ORD>), grid, dim3(512), 0, st, a);
+        if (bj == 2) launch_wave<R_, S_, 8, 2, ORD>(a, grid, st);
+        else launch_wave<R_, S_, 8, 1, ORD>(a, grid, st);
     } else {
-        if (bj == 2) launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 2, ORD>), grid, dim3(256), 0, st, a);
-        else launch_kernel((igemm_wave_f32_kernel<R_, S_, 4, 1, ORD>), grid, dim3(256), 0, st, a);
+        if (bj == 2) launch_wave<R_, S_, 4, 2, ORD>(a, grid, st);
+        else launch_wave<R_, S_, 4, 1, ORD>(a, grid, st);
     }
 }
 
@@ -428,7 +456,9 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
     if (R == 0 || S == 0 || R != S) R = S = 0;
     if (plan.order == 1 && R != 3 && R != 1) R = S = 0;
     if (plan.order == 2 && R != 3 && R != 7) R = S = 0;
-    snprintf(buf, len, "igemm_wave_f32_kernel<%d, %d, %d, %d, %d, %s>%s", R, S, plan.waves, plan.bj,
+    const bool gen = p.res || p.ysn != (long)p.K * p.P * p.Q;
+    snprintf(buf, len, "igemm_wave_f32%s_kernel<%d, %d, %d, %d, %d, %s>%s", gen ? "_gen" : "", R, S,
+             plan.waves, plan.bj,
              plan.order, plan.ind ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     *launches = plan.splits > 1 ? 2 : 1;
 }

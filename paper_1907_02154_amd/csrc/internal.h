@@ -64,9 +64,6 @@ struct ConvArgs {
     const void *w;        // fp32 or bf16 bits, [K][Cg][R][S]
     const float *bias;    // [K] or nullptr
     float *y;             // [N][K][P][Q]
-    const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may
-                          // be y itself (every element is read and written by one thread)
-    long ysn;             // elements from one image of y (and res) to the next (>= K*P*Q)
     float *ws;            // split-K partials [splits][K][M] (nullptr when splits == 1)
     int N, C, H, W, K, R, S, stride, pad, groups;
     int P, Q, Cg, Kg, Kred, M, PQ, HW;
@@ -77,6 +74,11 @@ struct ConvArgs {
     FastDiv dv_pq, dv_q;  // division by P*Q and by Q
     FastDiv dv_m;         // division by M (split-K reduce)
     FastDiv dv_mt, dv_kt, dv_g, dv_cb;   // wave kernel: pixel tiles, filter tiles, groups, C/groups/8
+    // Last, so that the fields every kernel reads first keep their offsets at
+    // the front of the argument block (batch-1 kernels run a few microseconds).
+    const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may
+                          // be y itself (every element is read and written by one thread)
+    long ysn;             // elements from one image of y (and res) to the next (>= K*P*Q)
 };
 
 ConvArgs make_args(const ConvProblem &p);
