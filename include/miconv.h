@@ -29,13 +29,14 @@
  *    validation error nothing is enqueued.
  *  - Tensor extents are limited to 2^31-1 elements each (MICONV_ERR_TOO_LARGE).
  *  - Dilation is not supported (the evaluated networks use none).
- *  - Entry points are thread-safe.  The split-K path of the dense conv keeps
- *    fp32 partial sums in a library-owned device workspace, one per
- *    (device, stream) pair, allocated by the first call on that stream that
- *    needs it and grown (hipMalloc) only when a larger layer arrives; it is
- *    released at process exit.  Calls on one stream are ordered by the
- *    stream, so they never race on it.  Capture such calls in a graph only
- *    after one eager call of the same or a larger layer on that stream.
+ *  - Entry points are stateless and thread-safe, and no call below allocates,
+ *    frees or synchronises (the stack executor allocates once, at create).
+ *    Scratch memory (split-K partial sums, an internal channel-last copy of
+ *    x, filters packed into the layout a kernel reads) comes only from a
+ *    caller-owned workspace passed to conv2d_fwd_ws; the entry points without
+ *    one run plans that need none (no split reduction, filters read as
+ *    given), so every call can be captured into a HIP graph, the first one
+ *    included.
  */
 #ifndef MICONV_H
 #define MICONV_H
@@ -59,7 +60,19 @@ enum miconv_status {
     MICONV_ERR_UNSUPPORTED = -4, /* valid but not provided (e.g. depthwise filter wider than 7) */
     MICONV_ERR_TOO_LARGE = -5,   /* a tensor exceeds 2^31-1 elements */
     MICONV_ERR_ALIGN = -6,       /* a pointer is not aligned to its element size */
-    MICONV_ERR_HIP = -7          /* a HIP call failed; see miconv_last_hip_error() */
+    MICONV_ERR_HIP = -7,         /* a HIP call failed; see miconv_last_hip_error() */
+    MICONV_ERR_WORKSPACE = -8    /* workspace missing, smaller than conv2d_workspace_bytes
+                                    reports, or not 256-byte aligned */
+};
+
+/* What a dense call may use besides its tensors, which decides its kernel
+ * plan (conv2d_describe names the kernels of each). */
+enum miconv_plan_mode {
+    MICONV_PLAN_PLAIN = 0,   /* conv2d_fwd, conv2d_fwd_bf16, *_algo, _res, _ex: no workspace */
+    MICONV_PLAN_WS = 1,      /* conv2d_fwd_ws: caller workspace (split reductions, channel-last
+                                copy of x, filters packed per call) */
+    MICONV_PLAN_PACKED = 2,  /* conv2d_fwd_packed: filters packed ahead, no workspace */
+    MICONV_PLAN_STACK = 3    /* a layer of miconv_stack: both */
 };
 
 /* Dense-conv algorithm selector for conv2d_fwd_algo (tests and A/B runs). */
@@ -69,9 +82,9 @@ enum miconv_algo {
     MICONV_ALGO_IGEMM = 2,  /* implicit GEMM on MFMA with LDS-staged tiles (+ split-K when small) */
     MICONV_ALGO_WAVE = 3    /* implicit GEMM on MFMA fed straight from global memory by each
                                wavefront, reduction split across wavefronts; what AUTO picks for
-                               fp32 dense layers whose x and packed filters fit 2 GiB.  Packs the
-                               filters on every call (a stack packs them once); larger tensors:
-                               MICONV_ERR_UNSUPPORTED. */
+                               fp32 dense layers whose x and filters fit 2 GiB.  Reads the filters
+                               as given (a stack or conv2d_fwd_packed reads them packed in the
+                               wavefront load order); larger tensors: MICONV_ERR_UNSUPPORTED. */
 };
 
 /* Output extent: floor((H + 2*pad - R)/stride) + 1 and likewise for W.
@@ -141,6 +154,28 @@ int conv2d_fwd_ex(int N, int C, int H, int W, int K, int R, int S, int stride, i
                   int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
                   const float *res, float *y, long y_image_stride, int relu, void *stream);
 
+/* Workspace for conv2d_fwd_ws.  conv2d_workspace_bytes returns the bytes of
+ * scratch the fastest plan for this shape needs (0: none), for any pointer
+ * alignment, or a negative miconv_status (invalid shape, groups, dtype or
+ * algo).  dtype 0 = fp32, 1 = bf16; algo as for conv2d_fwd_algo /
+ * conv2d_fwd_bf16_algo. */
+long conv2d_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                            int groups, int dtype, int algo);
+
+/* conv2d_fwd_ex with a caller-owned device workspace `ws` of `ws_bytes`
+ * bytes, 256-byte aligned, at least conv2d_workspace_bytes (NULL when that is
+ * 0).  With it the dense conv may split its reduction across work-groups
+ * (fp32 partial sums, reduced in a fixed order: results are run-to-run
+ * deterministic), stage x channel-last (bf16) and pack the filters into the
+ * order its kernel reads, all inside `ws`: the fastest single-call plans.
+ * The library keeps no reference to ws after the call's kernels are
+ * enqueued; they use it until they complete on `stream`, so concurrent calls
+ * need distinct workspaces.  Too small or unaligned: MICONV_ERR_WORKSPACE,
+ * nothing enqueued.  Everything else as conv2d_fwd_ex. */
+int conv2d_fwd_ws(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                  int dtype, int algo, const void *x, const void *w, const float *bias, const float *res,
+                  float *y, long y_image_stride, int relu, void *ws, size_t ws_bytes, void *stream);
+
 /* Filters packed once for repeated calls of one layer (the pre-computing step
  * of the paper's graph-level optimisation, Sec. 3.2.3), outside a stack.
  * The packed layout is the one the kernel chosen for this shape reads: the
@@ -163,10 +198,12 @@ int conv2d_pack_weights(int N, int C, int H, int W, int K, int R, int S, int str
 
 /* conv2d_fwd (dtype 0) or conv2d_fwd_bf16 (dtype 1) with the filters from
  * conv2d_pack_weights for the same shape and dtype (or w itself when the
- * packed size is 0).  No packing launch.  The kernel is chosen again from the
- * actual pointers; if their alignment selects a kernel with another filter
- * layout than the one packed for (x and y at 256-byte boundaries never do),
- * the call fails with MICONV_ERR_ALIGN and launches nothing. */
+ * packed size is 0).  No packing launch and no workspace (MICONV_PLAN_PACKED:
+ * no split reduction, no channel-last copy).  The kernel is chosen again from
+ * the actual pointers; if their alignment selects a kernel with another
+ * filter layout than the one packed for (x and y at 256-byte boundaries never
+ * do), or packed is not 16-byte aligned, the call fails with
+ * MICONV_ERR_ALIGN and launches nothing. */
 int conv2d_fwd_packed(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                       int groups, int dtype, const void *x, const void *packed, const float *bias,
                       float *y, int relu, void *stream);
@@ -187,8 +224,9 @@ int cast_f32_to_bf16(long count, const float *x, uint16_t *y, void *stream);
 /* ---- Stack executor: a network's conv layers planned once and replayed ----
  *
  * Batch-1 inference (the latency setting of Sec. 4.2) runs layers of a few
- * microseconds, so the executor validates and plans every layer once, owns
- * one split-K workspace for the whole stack, and can capture repeated passes
+ * microseconds, so the executor validates and plans every layer once, packs
+ * its filters once (the pre-computing of Sec. 3.2.3), owns one workspace for
+ * the whole stack (allocated at create), and can capture repeated passes
  * into a single HIP graph.  Tensor pointers are borrowed: they must stay
  * valid and keep their contents' meaning for the executor's lifetime (a
  * replay reads x/w/bias and writes y of every layer). */
@@ -214,7 +252,7 @@ typedef struct miconv_conv_desc {
 typedef struct miconv_stack miconv_stack;
 
 /* Validate and plan n layers (each as its entry point would); allocate the
- * executor and its split-K workspace on the current device.  On error
+ * executor, its packed filters and its workspace on the current device.  On error
  * nothing is allocated and *out is NULL. */
 int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **out);
 
@@ -258,14 +296,15 @@ int miconv_stack_times(const miconv_stack *s, float *ms, long capacity);
 /* Free the graph, events, workspace and the executor (NULL is a no-op). */
 int miconv_stack_destroy(miconv_stack *s);
 
-/* Names the kernels conv2d_fwd_algo (dtype 0) or conv2d_fwd_bf16 (dtype 1)
- * would launch for this shape on the current device, as a profiler prints
- * them (template arguments included, namespaces omitted), joined by " + ";
- * writes at most buflen bytes (NUL-terminated) into buf and the number of
- * kernel launches into *launches.  Validates like the conv entry points
- * (pointer alignment is taken as 256 bytes); enqueues nothing. */
+/* Names the kernels a dense call of this shape would launch on the current
+ * device (dtype 0 = fp32, 1 = bf16; algo as for conv2d_fwd_algo; mode = enum
+ * miconv_plan_mode: which entry point), as a profiler prints them (template
+ * arguments included, namespaces omitted), joined by " + "; writes at most
+ * buflen bytes (NUL-terminated) into buf and the number of kernel launches
+ * into *launches.  Validates like the conv entry points (pointer alignment
+ * is taken as 256 bytes); enqueues nothing. */
 int conv2d_describe(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                    int groups, int dtype, int algo, char *buf, int buflen, int *launches);
+                    int groups, int dtype, int algo, int mode, char *buf, int buflen, int *launches);
 
 /* Human-readable text for a miconv_status. */
 const char *miconv_strerror(int status);

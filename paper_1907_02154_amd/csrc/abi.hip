@@ -1,5 +1,8 @@
 // The C ABI of libmiconv (include/miconv.h): argument validation, output
-// extents, the shape -> kernel choice, and the per-stream split-K workspace.
+// extents and the shape -> kernel choice.  The library owns no device memory
+// on this path: a call that needs scratch (split partials, a channel-last
+// copy of x, packed filters) takes it from the caller's workspace, and the
+// entry points without a workspace pick plans that need none.
 //
 // The paper's observation that convolutions of different shapes need
 // different schedules (Sec. 2.2) is served here by a fixed, hand-written
@@ -14,7 +17,6 @@
 #include <climits>
 #include <map>
 #include <mutex>
-#include <utility>
 
 namespace miconv {
 
@@ -112,44 +114,6 @@ int check_bias(const float *bias)
 }
 
 
-// Split-K workspace (fp32 partials), one per (device, stream).
-struct Workspace {
-    void *ptr = nullptr;
-    size_t bytes = 0;
-};
-
-int get_workspace(hipStream_t st, size_t need, float **out)
-{
-    static std::mutex mu;
-    static std::map<std::pair<int, hipStream_t>, Workspace> table;
-    *out = nullptr;
-    if (need == 0) return MICONV_OK;
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return hip_fail(e);
-    std::lock_guard<std::mutex> lk(mu);
-    Workspace &ws = table[{dev, st}];
-    if (ws.bytes < need) {
-        const size_t bytes = std::max(need, (size_t)(1u << 20));
-        if (ws.ptr) {
-            // Kernels already queued on this stream may still use the old buffer.
-            e = hipStreamSynchronize(st);
-            if (e != hipSuccess) return hip_fail(e);
-            e = hipFree(ws.ptr);
-            if (e != hipSuccess) return hip_fail(e);
-            ws = Workspace{};
-        }
-        e = hipMalloc(&ws.ptr, bytes);
-        if (e != hipSuccess) {
-            ws.ptr = nullptr;
-            return hip_fail(e);
-        }
-        ws.bytes = bytes;
-    }
-    *out = static_cast<float *>(ws.ptr);
-    return MICONV_OK;
-}
-
 int finish(hipError_t e) { return e == hipSuccess ? MICONV_OK : hip_fail(e); }
 
 }  // namespace
@@ -172,8 +136,11 @@ int cu_count()
 
 int set_hip_error(hipError_t e) { return hip_fail(e); }
 
-// Validate one conv call and fix the kernel that serves it.
-int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S, int stride,
+// Validate one conv call and fix the kernel that serves it.  `mode` says what
+// the call may use besides its tensors (enum PlanMode): without a workspace
+// there is no split reduction, no channel-last copy and no per-call filter
+// packing, and filters are read as given unless they were packed ahead.
+int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int R, int S, int stride,
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
             int relu, Resolved *out)
 {
@@ -183,8 +150,13 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
     if (rc != MICONV_OK) return rc;
     if ((rc = check_bias(bias)) != MICONV_OK) return rc;
     if (algo < MICONV_ALGO_AUTO || algo > MICONV_ALGO_WAVE) return MICONV_ERR_UNSUPPORTED;
+    if (mode < MODE_FREE || mode > (MODE_SCRATCH | MODE_PREPACK)) return MICONV_ERR_UNSUPPORTED;
+    const bool scratch = mode & MODE_SCRATCH;
+    const bool can_pack = mode & (MODE_SCRATCH | MODE_PREPACK);   // per call, or ahead
+    const int max_splits = scratch ? 64 : 1;
     r.p.relu = relu ? 1 : 0;
     r.kind = kind;
+    r.mode = mode;
     r.x = x;
     r.w = w;
     r.bias = bias;
@@ -195,14 +167,40 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
         if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
         r.impl = IMPL_DW;
     } else if (kind == OP_DENSE_BF16) {
-        if (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8))
+        if (algo == MICONV_ALGO_DIRECT || (groups > 1 && r.p.Cg < 8)) {
             r.impl = IMPL_DIRECT;
-        else if (algo == MICONV_ALGO_AUTO && stem_bf16_eligible(r.p, y))
+        } else if (algo == MICONV_ALGO_AUTO && can_pack && stem_bf16_eligible(r.p, y)) {
             r.impl = IMPL_STEM_BF16;
-        else if (algo != MICONV_ALGO_IGEMM && nhwc_bf16_eligible(r.p))
-            r.impl = IMPL_NHWC_BF16;
-        else
+            r.wlayout = WL_STEM;
+        } else {
             r.impl = IMPL_IGEMM_BF16;
+            if (algo != MICONV_ALGO_IGEMM && nhwc_bf16_eligible(r.p)) {
+                const NhwcPlan np = plan_nhwc_bf16(r.p, cu_count(), x, max_splits);
+                const bool one = R * S == 1;
+                // a copy of x or split partials need a workspace; filters of
+                // more than one tap are read KRSC-packed; 1x1 filters are read
+                // as given, with 16-byte loads
+                const bool ok = ((np.xcl_bytes == 0 && np.splits == 1) || scratch) &&
+                                (one ? (uintptr_t)w % 16 == 0 : can_pack);
+                if (ok) {
+                    r.impl = IMPL_NHWC_BF16;
+                    r.nplan = np;
+                    r.wlayout = one ? WL_GIVEN : np.halo ? WL_KRSC_BLOCK : WL_KRSC;
+                }
+            }
+            if (r.impl == IMPL_IGEMM_BF16) {
+                r.plan = plan_igemm_bf16(r.p, cu_count(), max_splits);
+                r.bfast = bf16_fast_1x1(r.p, x);
+                // At the batch sizes the bf16 path serves, packing the filters
+                // costs far less than per-tap index decoding in the gather.
+                if (can_pack && R * S > 1 && r.p.Cg % 8 == 0) {
+                    r.plan.krsc = true;
+                    r.wlayout = WL_KRSC;
+                }
+                // 16-byte filter loads: packed copies are 256-byte aligned
+                r.bva = r.p.Kred % 8 == 0 && (r.wlayout != WL_GIVEN || (uintptr_t)w % 16 == 0);
+            }
+        }
     } else if (kind == OP_DENSE_F32) {
         if (algo == MICONV_ALGO_AUTO) {
             if (depthwise && R <= 7 && S <= 7)
@@ -213,41 +211,27 @@ int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S,
             r.impl = algo == MICONV_ALGO_DIRECT ? IMPL_DIRECT
                      : algo == MICONV_ALGO_WAVE ? IMPL_WAVE : IMPL_IGEMM;
         }
+        const int cus = cu_count();
+        if (r.impl == IMPL_IGEMM) {
+            // The wave kernel serves every size it can address (measured faster
+            // than the LDS-tiled kernel from batch-1 ResNet layers to VGG-16 at
+            // batch 32), unless the caller forced the tiled one.
+            if (algo != MICONV_ALGO_IGEMM && wave_fits(r.p))
+                r.impl = IMPL_WAVE;
+            else
+                r.plan = plan_igemm_f32(r.p, cus, max_splits);
+        }
+        if (r.impl == IMPL_WAVE) {
+            if (!wave_fits(r.p)) return MICONV_ERR_UNSUPPORTED;
+            r.wplan = plan_wave_f32(r.p, cus, max_splits);
+            // filters packed ahead in the wavefront load order, else read as given
+            r.wplan.kc = !(mode & MODE_PREPACK);
+            r.wlayout = r.wplan.kc ? WL_GIVEN : WL_WAVE;
+        }
     } else {
         return MICONV_ERR_UNSUPPORTED;
     }
-    if (r.impl == IMPL_IGEMM) {
-        // The wave kernel serves every size it can address (measured faster
-        // than the LDS-tiled kernel from batch-1 ResNet layers to VGG-16 at
-        // batch 32), unless the caller forced the tiled one.
-        const int cus = cu_count();
-        if (algo != MICONV_ALGO_IGEMM && wave_fits(r.p)) {
-            r.impl = IMPL_WAVE;
-            r.wplan = plan_wave_f32(r.p, cus);
-            r.pack_per_call = true;   // filters in the wavefront load order
-        } else {
-            r.plan = plan_igemm_f32(r.p, cus);
-        }
-    } else if (r.impl == IMPL_WAVE) {
-        if (!wave_fits(r.p)) return MICONV_ERR_UNSUPPORTED;
-        r.wplan = plan_wave_f32(r.p, cu_count());
-        r.pack_per_call = true;
-    } else if (r.impl == IMPL_IGEMM_BF16) {
-        r.plan = plan_igemm_bf16(r.p, cu_count());
-        r.bfast = bf16_fast_1x1(r.p, x);
-        r.bva = r.p.Kred % 8 == 0 && (uintptr_t)w % 16 == 0;
-        // At the batch sizes the bf16 path serves, packing the filters on every
-        // call costs far less than per-tap index decoding in the gather.
-        if (krsc_eligible(r)) {
-            r.plan.krsc = true;
-            r.pack_per_call = true;
-        }
-    } else if (r.impl == IMPL_NHWC_BF16) {
-        r.nplan = plan_nhwc_bf16(r.p, cu_count(), x);
-        r.pack_per_call = krsc_eligible(r);   // 1x1 filters are already in KRSC order
-    } else if (r.impl == IMPL_STEM_BF16) {
-        r.pack_per_call = true;               // filters in tap-pair order
-    }
+    r.pack_per_call = r.wlayout != WL_GIVEN && !(mode & MODE_PREPACK);
     *out = r;
     return MICONV_OK;
 }
@@ -274,63 +258,44 @@ int set_output_stride(Resolved &r, long ysn)
     return MICONV_OK;
 }
 
-bool krsc_eligible(const Resolved &r)
-{
-    return (r.impl == IMPL_IGEMM_BF16 || r.impl == IMPL_NHWC_BF16) && r.p.R * r.p.S > 1 &&
-           r.p.Cg % 8 == 0;
-}
-
 size_t packed_bytes(const Resolved &r)
 {
-    if (r.impl == IMPL_STEM_BF16) return stem_packed_bytes(r.p);
-    if (r.impl == IMPL_WAVE) return wave_packed_floats(r.p) * sizeof(float);
+    if (r.wlayout == WL_STEM) return stem_packed_bytes(r.p);
+    if (r.wlayout == WL_WAVE) return wave_packed_floats(r.p) * sizeof(float);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     return (size_t)r.p.K * r.p.Cg * r.p.R * r.p.S * elem;
 }
 
-void set_krsc(Resolved &r, const void *packed)
+void set_packed(Resolved &r, const void *packed)
 {
     r.wk = packed;
     r.pack_per_call = false;
-    if (r.impl == IMPL_IGEMM_BF16) r.plan.krsc = true;
 }
 
 static size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
-// The filter layout a resolved layer's kernel reads: 0 = w as given, else
-// 1 = bf16 stem tap pairs, 2 = wave kernel load order, 3 = KRSC, 4 = KRSC per
-// 64-channel block.
-int filter_layout(const Resolved &r)
-{
-    if (!r.pack_per_call && !krsc_eligible(r)) return 0;
-    if (r.impl == IMPL_STEM_BF16) return 1;
-    if (r.impl == IMPL_WAVE) return 2;
-    if (r.impl == IMPL_NHWC_BF16 && r.nplan.halo) return 4;   // KRSC per 64-channel block
-    return 3;
-}
-
-// The layer as conv2d_fwd[_bf16] resolves it for tensors at 256-byte
+// The layer as the entry point of `mode` resolves it for tensors at 256-byte
 // boundaries (w may be null: 256-aligned stand-in).
-int resolve_for_packing(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                        int groups, int dtype, const void *w, Resolved *out)
+int resolve_aligned(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                    int dtype, int algo, int mode, const void *w, Resolved *out)
 {
     if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
     alignas(256) static const float stand_in[64] = {};
-    return resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S,
-                   stride, pad, groups, stand_in, w ? w : stand_in, nullptr, const_cast<float *>(stand_in),
-                   0, out);
+    return resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, mode, N, C, H, W, K, R, S, stride,
+                   pad, groups, stand_in, w ? w : stand_in, nullptr, const_cast<float *>(stand_in), 0, out);
 }
 
 // The filter copy a layer's kernel reads: tap-pair order for the bf16 stem,
-// the wavefront load order for the wave kernel, KRSC otherwise.
+// the wavefront load order for the wave kernel, KRSC (per 64-channel block
+// for the halo kernel) otherwise.
 hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st)
 {
-    if (r.impl == IMPL_STEM_BF16)
+    if (r.wlayout == WL_STEM)
         return launch_pack_stem(r.p, static_cast<const uint16_t *>(r.w), static_cast<uint16_t *>(dst), st);
-    if (r.impl == IMPL_WAVE)
+    if (r.wlayout == WL_WAVE)
         return launch_pack_wave(r.p, static_cast<const float *>(r.w), static_cast<float *>(dst), st);
     const size_t elem = r.kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
-    const int cblk = r.impl == IMPL_NHWC_BF16 && r.nplan.halo ? 64 : 0;   // (block, r, s, c) order
+    const int cblk = r.wlayout == WL_KRSC_BLOCK ? 64 : 0;   // (block, r, s, c) order
     return launch_pack_krsc(r.p, r.w, dst, elem, st, cblk);
 }
 
@@ -402,8 +367,8 @@ size_t workspace_bytes(const Resolved &r)
 void describe(const Resolved &r, char *buf, int len, int *launches)
 {
     if (r.pack_per_call) {
-        const int n = r.impl == IMPL_STEM_BF16 ? snprintf(buf, len, "pack_stem_kernel + ")
-                      : r.impl == IMPL_WAVE    ? snprintf(buf, len, "pack_wave_kernel + ")
+        const int n = r.wlayout == WL_STEM ? snprintf(buf, len, "pack_stem_kernel + ")
+                      : r.wlayout == WL_WAVE ? snprintf(buf, len, "pack_wave_kernel + ")
                                                : snprintf(buf, len, "pack_krsc_kernel<%s> + ",
                                      r.kind == OP_DENSE_BF16 ? "unsigned short" : "float");
         if (n > 0 && n < len) {
@@ -430,16 +395,19 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
 
 namespace {
 
-int run(const Resolved &r, hipStream_t st)
+// Enqueue a resolved call on the caller's workspace (ws may be null when the
+// plan needs none).  Never allocates, frees or synchronises.
+int run(const Resolved &r, void *ws, size_t ws_bytes, hipStream_t st)
 {
-    float *ws = nullptr;
     const size_t need = workspace_bytes(r);
     if (need) {
-        int rc = get_workspace(st, need, &ws);
-        if (rc != MICONV_OK) return rc;
+        if (!ws || ws_bytes < need || (uintptr_t)ws % 256) return MICONV_ERR_WORKSPACE;
     }
-    return finish(enqueue(r, ws, st));
+    return finish(enqueue(r, need ? static_cast<float *>(ws) : nullptr, st));
 }
+
+// An entry point without a workspace: the plan takes none by construction.
+int run_free(const Resolved &r, hipStream_t st) { return run(r, nullptr, 0, st); }
 
 }  // namespace
 }  // namespace miconv
@@ -463,9 +431,9 @@ int conv2d_fwd_algo(int N, int C, int H, int W, int K, int R, int S, int stride,
                     int relu, int algo, void *stream)
 {
     Resolved r;
-    int rc = resolve(OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y,
-                     relu, &r);
-    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+    int rc = resolve(OP_DENSE_F32, algo, MODE_FREE, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias,
+                     y, relu, &r);
+    return rc != MICONV_OK ? rc : run_free(r, static_cast<hipStream_t>(stream));
 }
 
 int conv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
@@ -480,9 +448,9 @@ int conv2d_fwd_bf16_algo(int N, int C, int H, int W, int K, int R, int S, int st
                          float *y, int relu, int algo, void *stream)
 {
     Resolved r;
-    int rc = resolve(OP_DENSE_BF16, algo, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias, y,
-                     relu, &r);
-    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+    int rc = resolve(OP_DENSE_BF16, algo, MODE_FREE, N, C, H, W, K, R, S, stride, pad, groups, x, w, bias,
+                     y, relu, &r);
+    return rc != MICONV_OK ? rc : run_free(r, static_cast<hipStream_t>(stream));
 }
 
 int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -493,17 +461,36 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
                                 MICONV_ALGO_AUTO, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// conv2d_fwd_ex / conv2d_fwd_ws: one dense call with an optional residual and
+// output image stride, planned for `mode`.
+int resolve_ex(int mode, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+               int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
+               const float *res, float *y, long y_image_stride, int relu, Resolved *r)
+{
+    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
+    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, mode, N, C, H, W, K, R, S, stride,
+                     pad, groups, x, w, bias, y, relu, r);
+    if (rc == MICONV_OK) rc = set_output_stride(*r, y_image_stride);
+    if (rc == MICONV_OK) rc = set_residual(*r, res);
+    return rc;
+}
+
+}  // namespace
+
+extern "C" {
+
 int conv2d_fwd_ex(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                   int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
                   const float *res, float *y, long y_image_stride, int relu, void *stream)
 {
-    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
     Resolved r;
-    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride,
-                     pad, groups, x, w, bias, y, relu, &r);
-    if (rc == MICONV_OK) rc = set_output_stride(r, y_image_stride);
-    if (rc == MICONV_OK) rc = set_residual(r, res);
-    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+    const int rc = resolve_ex(MODE_FREE, N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, x, w, bias,
+                              res, y, y_image_stride, relu, &r);
+    return rc != MICONV_OK ? rc : run_free(r, static_cast<hipStream_t>(stream));
 }
 
 int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -514,13 +501,48 @@ int conv2d_fwd_res(int N, int C, int H, int W, int K, int R, int S, int stride, 
                          relu, stream);
 }
 
+long conv2d_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                            int groups, int dtype, int algo)
+{
+    // The plan depends on pointer alignment (16-byte loads, a stem kernel that
+    // needs a 16-byte aligned y): take the largest workspace over aligned and
+    // misaligned x, w and y, so the figure holds for any pointers.
+    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
+    alignas(256) static const float stand_in[256] = {};
+    const char *base = reinterpret_cast<const char *>(stand_in);
+    const int elem = dtype == 1 ? 2 : 4;
+    size_t most = 0;
+    for (int v = 0; v < 8; ++v) {
+        const void *x = base + ((v & 1) ? elem : 0);
+        const void *w = base + ((v & 2) ? elem : 0);
+        float *y = const_cast<float *>(reinterpret_cast<const float *>(base + ((v & 4) ? 4 : 0)));
+        Resolved r;
+        const int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, MODE_SCRATCH, N, C, H, W, K,
+                               R, S, stride, pad, groups, x, w, nullptr, y, 0, &r);
+        if (rc != MICONV_OK) return rc;
+        most = std::max(most, workspace_bytes(r));
+    }
+    return (long)most;
+}
+
+int conv2d_fwd_ws(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                  int dtype, int algo, const void *x, const void *w, const float *bias, const float *res,
+                  float *y, long y_image_stride, int relu, void *ws, size_t ws_bytes, void *stream)
+{
+    Resolved r;
+    const int rc = resolve_ex(MODE_SCRATCH, N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, x, w,
+                              bias, res, y, y_image_stride, relu, &r);
+    return rc != MICONV_OK ? rc : run(r, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
 long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
                                 int pad, int groups, int dtype)
 {
     Resolved r;
-    const int rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, nullptr, &r);
+    const int rc = resolve_aligned(N, C, H, W, K, R, S, stride, pad, groups, dtype, MICONV_ALGO_AUTO,
+                                   MODE_PREPACK, nullptr, &r);
     if (rc != MICONV_OK) return rc;
-    return filter_layout(r) ? (long)packed_bytes(r) : 0;
+    return r.wlayout != WL_GIVEN ? (long)packed_bytes(r) : 0;
 }
 
 int conv2d_pack_weights(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -528,9 +550,10 @@ int conv2d_pack_weights(int N, int C, int H, int W, int K, int R, int S, int str
 {
     if (!w || !packed) return MICONV_ERR_NULL;
     Resolved r;
-    const int rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, w, &r);
+    const int rc = resolve_aligned(N, C, H, W, K, R, S, stride, pad, groups, dtype, MICONV_ALGO_AUTO,
+                                   MODE_PREPACK, w, &r);
     if (rc != MICONV_OK) return rc;
-    if (!filter_layout(r)) return MICONV_OK;
+    if (r.wlayout == WL_GIVEN) return MICONV_OK;
     if ((uintptr_t)packed % 16 != 0) return MICONV_ERR_ALIGN;
     return finish(launch_pack(r, packed, static_cast<hipStream_t>(stream)));
 }
@@ -541,15 +564,18 @@ int conv2d_fwd_packed(int N, int C, int H, int W, int K, int R, int S, int strid
 {
     if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
     Resolved r, ref;
-    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S,
-                     stride, pad, groups, x, packed, bias, y, relu, &r);
+    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, MICONV_ALGO_AUTO, MODE_PREPACK, N, C, H, W,
+                     K, R, S, stride, pad, groups, x, packed, bias, y, relu, &r);
     if (rc != MICONV_OK) return rc;
-    rc = resolve_for_packing(N, C, H, W, K, R, S, stride, pad, groups, dtype, nullptr, &ref);
+    rc = resolve_aligned(N, C, H, W, K, R, S, stride, pad, groups, dtype, MICONV_ALGO_AUTO, MODE_PREPACK,
+                         nullptr, &ref);
     if (rc != MICONV_OK) return rc;
-    const int layout = filter_layout(r);
-    if (layout != filter_layout(ref)) return MICONV_ERR_ALIGN;
-    if (layout) set_krsc(r, packed);
-    return run(r, static_cast<hipStream_t>(stream));
+    if (r.wlayout != ref.wlayout) return MICONV_ERR_ALIGN;
+    if (r.wlayout != WL_GIVEN) {
+        if ((uintptr_t)packed % 16 != 0) return MICONV_ERR_ALIGN;
+        set_packed(r, packed);
+    }
+    return run_free(r, static_cast<hipStream_t>(stream));
 }
 
 int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
@@ -557,9 +583,9 @@ int dwconv2d_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, in
                  void *stream)
 {
     Resolved r;
-    int rc = resolve(OP_DW_F32, MICONV_ALGO_AUTO, N, C, H, W, K, R, S, stride, pad, groups, x, w,
+    int rc = resolve(OP_DW_F32, MICONV_ALGO_AUTO, MODE_FREE, N, C, H, W, K, R, S, stride, pad, groups, x, w,
                      bias, y, relu, &r);
-    return rc != MICONV_OK ? rc : run(r, static_cast<hipStream_t>(stream));
+    return rc != MICONV_OK ? rc : run_free(r, static_cast<hipStream_t>(stream));
 }
 
 int maxpool2d_fwd(int N, int C, int H, int W, int R, int S, int stride, int pad, const float *x,
@@ -594,16 +620,14 @@ int cast_f32_to_bf16(long count, const float *x, uint16_t *y, void *stream)
 }
 
 int conv2d_describe(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                    int groups, int dtype, int algo, char *buf, int buflen, int *launches)
+                    int groups, int dtype, int algo, int mode, char *buf, int buflen, int *launches)
 {
     if (!buf || buflen <= 0 || !launches) return MICONV_ERR_NULL;
     buf[0] = 0;
-    if (dtype != 0 && dtype != 1) return MICONV_ERR_UNSUPPORTED;
-    alignas(256) static const float dummy[64] = {};
     Resolved r;
-    int rc = resolve(dtype == 1 ? OP_DENSE_BF16 : OP_DENSE_F32, algo, N, C, H, W, K, R, S, stride,
-                     pad, groups, dummy, dummy, nullptr, const_cast<float *>(dummy), 0, &r);
+    int rc = resolve_aligned(N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, mode, nullptr, &r);
     if (rc != MICONV_OK) return rc;
+    if (mode & MODE_PREPACK) set_packed(r, r.w);   // filters packed ahead: no packing launch
     describe(r, buf, buflen, launches);
     return MICONV_OK;
 }
@@ -619,12 +643,13 @@ const char *miconv_strerror(int status)
     case MICONV_ERR_TOO_LARGE: return "tensor exceeds 2^31-1 elements";
     case MICONV_ERR_ALIGN: return "pointer not aligned to its element size";
     case MICONV_ERR_HIP: return "HIP runtime error";
+    case MICONV_ERR_WORKSPACE: return "workspace missing, too small or not 256-byte aligned for this plan";
     default: return "unknown status";
     }
 }
 
 int miconv_last_hip_error(void) { return g_last_hip_error; }
 
-int miconv_version(void) { return 100; }
+int miconv_version(void) { return 20000; }
 
 }  // extern "C"

@@ -338,7 +338,7 @@ int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 
 // The biggest tile that gives about two work-groups per CU, else the small
 // tile with a reduction split (at least 2 chunks of 64 taps per split).
-IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus)
+IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus, int max_splits)
 {
     IgemmPlan plan{1, 1, p.Kred, 0};
     const long target = 2L * num_cus;
@@ -348,7 +348,7 @@ IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus)
         plan.tile = t;
         const int chunks = ceil_div(p.Kred, kKrcB);
         int splits = tiles < target ? (int)((target + tiles - 1) / tiles) : 1;
-        const int max_splits = chunks / 2;
+        if (splits > chunks / 2) splits = chunks / 2;
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
         const int per = ceil_div(chunks, splits);

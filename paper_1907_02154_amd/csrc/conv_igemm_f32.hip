@@ -297,7 +297,7 @@ hipError_t launch_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
 // work-groups per CU (each split keeps at least one whole chunk).  Measured
 // on VGG-16 at batch 8: 64x64 runs the 64-filter conv1_2 at 68 TFLOP/s
 // against 41 for 128x128.
-IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus)
+IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus, int max_splits)
 {
     IgemmPlan plan{kNumTiles - 1, 1, p.Kred, 0};
     const long target = 3L * num_cus / 2;
@@ -309,6 +309,7 @@ IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus)
         const int chunks = ceil_div(p.Kred, krc);
         int splits = tiles < target ? (int)((2L * num_cus + tiles - 1) / tiles) : 1;
         if (splits > chunks) splits = chunks;
+        if (splits > max_splits) splits = max_splits;
         const int chunks_per = ceil_div(chunks, splits);
         splits = ceil_div(chunks, chunks_per);   // no empty splits
         plan.splits = splits;

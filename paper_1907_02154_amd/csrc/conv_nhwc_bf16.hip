@@ -1252,7 +1252,7 @@ bool nhwc_bf16_eligible(const ConvProblem &p) { return p.Cg % 32 == 0; }
 // CU; below that, 128 x 64 while it still covers every CU, then 64 x 64.
 // Filters of at most 64 channels take the 64-wide channel tiles.  A launch
 // with fewer than half as many 64 x 64 tiles as CUs splits the reduction.
-static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
+static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int max_splits)
 {
     NhwcPlan plan{};
     plan.dma = 1;
@@ -1285,6 +1285,7 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
         const int per = ceil_div(chunks, splits);
         splits = ceil_div(chunks, per);
     }
+    if (splits > max_splits) splits = max_splits;
     plan.splits = splits;
     plan.kr_per_split = ceil_div(chunks, splits) * 64;
     plan.partial_bytes = splits > 1 ? (size_t)splits * p.K * p.M * sizeof(float) : 0;
@@ -1320,12 +1321,12 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x)
     return plan;
 }
 
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x)
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits)
 {
     // the direct-to-LDS kernel addresses x and w through 32-bit buffer offsets
     const bool fits = (long)p.N * p.C * p.H * p.W * 2 < (1L << 31) &&
                       (long)p.K * p.Cg * p.R * p.S * 2 < (1L << 31);
-    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus, x);
+    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus, x, max_splits);
     NhwcPlan plan{};
     plan.krc = p.Cg % 64 == 0 ? 64 : 32;
     plan.tile = 1;
@@ -1336,7 +1337,7 @@ NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x)
         plan.tile = t;
         const int chunks = p.Kred / plan.krc;
         int splits = tiles < target ? (int)((target + tiles - 1) / tiles) : 1;
-        const int max_splits = chunks / 2;
+        if (splits > chunks / 2) splits = chunks / 2;
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
         const int per = ceil_div(chunks, splits);

@@ -27,6 +27,7 @@
 // store writes 32 consecutive pixels (128 bytes) of one NCHW channel plane.
 #include "internal.h"
 
+#include <algorithm>
 #include <cstdio>
 
 namespace miconv {
@@ -59,7 +60,7 @@ __device__ __forceinline__ unsigned select_offset(bool ok, unsigned off, unsigne
 // need no branches, which keeps the executed code short.  At batch 1 a
 // launch runs a few hundred instructions per wavefront from a cold
 // instruction cache, so code size is a first-order cost here.
-template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND, bool GEN>
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND, bool GEN, int KC>
 __device__ __forceinline__ void wave_body(const ConvArgs &a)
 {
     constexpr int kDepth = BJ == 2 ? 2 : 4;   // blocks of loads in flight per wavefront
@@ -74,8 +75,12 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
         const_cast<void *>(a.x), (short)0, (int)((long)a.N * a.C * a.HW * 4), 0x00020000);
     const int kblocks = ceil_div(a.Kred, 8);
     const unsigned ktiles = ceil_div(a.Kg, 32);
+    // KC: filters read as given, w[K][C/groups][R][S]; the row of filter k
+    // holds its C/groups*R*S taps in (c, r, s) order.
+    const int KR = a.Cg * RS;
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<void *>(a.w), (short)0, (int)((long)a.groups * ktiles * kblocks * 1024), 0x00020000);
+        const_cast<void *>(a.w), (short)0,
+        KC ? (int)((long)a.K * KR * 4) : (int)((long)a.groups * ktiles * kblocks * 1024), 0x00020000);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -107,8 +112,10 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
     const int kr_end = min(a.Kred, kr_begin + a.kr_per_split);
     const int nblk = kr_end > kr_begin ? ceil_div(kr_end - kr_begin, 8) : 0;
 
-    // A: byte offset of this lane's 16-byte slot in block 0 of the split.
-    const unsigned aoff = ((((unsigned)g * ktiles + ky) * kblocks + kr_begin / 8) * 64 + lane) * 16;
+    // A: byte offset of this lane's 16-byte slot in block 0 of the split
+    // (packed filters), or of its filter row (KC; kOut past K).
+    const unsigned aoff = KC ? (k0 + ll < a.Kg ? 4u * (unsigned)((g * a.Kg + k0 + ll) * KR) : kOut)
+                             : ((((unsigned)g * ktiles + ky) * kblocks + kr_begin / 8) * 64 + lane) * 16;
 
     // B: this lane's output pixels, one per 32-pixel block.
     int ih0[BJ], iw0[BJ];
@@ -152,11 +159,23 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
     // e = 0..3.  Called for the wavefront's blocks in increasing order.
     auto load = [&](Frag &f, int blk) {
         const int kr0 = kr_begin + 8 * blk + 4 * h;
-        {
-            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        if constexpr (KC == 0) {
             const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(wres, aoff + blk * 1024u, 0, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) f.av[e] = __uint_as_float(v[e]);
+        } else if constexpr (ORD == 0 || (ORD == 1 && R_ == 1 && S_ == 1)) {
+            // the 4 taps are consecutive in the filter row
+            if constexpr (KC == 1) {   // one 16-byte load (C/groups % 8 == 0, w 16-byte aligned)
+                const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(wres, aoff + 4u * kr0, 0, 0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) f.av[e] = __uint_as_float(v[e]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    f.av[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                        wres, select_offset(kr0 + e < kr_end, aoff + 4u * (kr0 + e), kOut), 0, 0));
+            }
         }
         if constexpr (ORD == 1) {
             // The block is one filter position (r, s) and 8 channels; the
@@ -167,6 +186,13 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
                 c0 = 8 * rsr + 4 * h;
                 r = rsq / S;
                 s = rsq - r * S;
+                if constexpr (KC != 0) {
+                    // taps (r, s) of channels c0 .. c0+3: R*S floats apart in the filter row
+                    const unsigned base = aoff + 4u * (unsigned)(c0 * RS + rsq);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        f.av[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wres, base, 4 * e * RS, 0));
+                }
                 rsq += drq;
                 rsr += drr;
                 if (rsr >= cb) {
@@ -190,6 +216,13 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
             const int r = pos / S;
             const int s = pos - r * S;
             const bool pok = pos < RS;
+            if constexpr (KC != 0) {
+                // tap (r, s) of channels e < C/groups, R*S floats apart; zero past them
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    f.av[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                        wres, select_offset(pok && e < a.Cg, aoff + 4u * (unsigned)(e * RS + pos), kOut), 0, 0));
+            }
 #pragma unroll
             for (int j = 0; j < BJ; ++j) {
                 const int ih = ih0[j] + r, iw = iw0[j] + s;
@@ -342,7 +375,7 @@ __device__ __forceinline__ void wave_body(const ConvArgs &a)
 template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 {
-    wave_body<R_, S_, WAVES, BJ, ORD, IND, false>(a);
+    wave_body<R_, S_, WAVES, BJ, ORD, IND, false, 0>(a);
 }
 
 // The same kernel with the general epilogue: a residual join and/or an output
@@ -351,36 +384,54 @@ __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kernel(ConvArgs a)
 template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
 __global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_gen_kernel(ConvArgs a)
 {
-    wave_body<R_, S_, WAVES, BJ, ORD, IND, true>(a);
+    wave_body<R_, S_, WAVES, BJ, ORD, IND, true, 0>(a);
+}
+
+// Filters read as given (KCRS), for calls that have no packed copy: the
+// single-layer entry points, which pack nothing.  KC = 1: the 4 taps of a
+// half-block are one 16-byte load (1x1, C/groups % 8 == 0, w 16-byte
+// aligned); KC = 2: four 4-byte loads.  General epilogue.
+template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND, int KC>
+__global__ __launch_bounds__(64 * WAVES) void igemm_wave_f32_kcrs_kernel(ConvArgs a)
+{
+    wave_body<R_, S_, WAVES, BJ, ORD, IND, true, KC>(a);
 }
 
 bool general_epilogue(const ConvArgs &a) { return a.res || a.ysn != (long)a.K * a.PQ; }
 
 template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
-void launch_wave(const ConvArgs &a, dim3 grid, hipStream_t st)
+void launch_wave(const ConvArgs &a, int kc, dim3 grid, hipStream_t st)
 {
-    if (general_epilogue(a))
+    if (kc == 1) {
+        if constexpr (ORD == 1 && R_ == 1 && S_ == 1 && !IND)
+            launch_kernel((igemm_wave_f32_kcrs_kernel<R_, S_, WAVES, BJ, ORD, IND, 1>), grid, dim3(64 * WAVES), 0,
+                          st, a);
+    } else if (kc == 2) {
+        launch_kernel((igemm_wave_f32_kcrs_kernel<R_, S_, WAVES, BJ, ORD, IND, 2>), grid, dim3(64 * WAVES), 0,
+                      st, a);
+    } else if (general_epilogue(a)) {
         launch_kernel((igemm_wave_f32_gen_kernel<R_, S_, WAVES, BJ, ORD, IND>), grid, dim3(64 * WAVES), 0,
                       st, a);
-    else
+    } else {
         launch_kernel((igemm_wave_f32_kernel<R_, S_, WAVES, BJ, ORD, IND>), grid, dim3(64 * WAVES), 0, st, a);
+    }
 }
 
 template <int R_, int S_, int ORD>
-void launch_rs(const ConvArgs &a, int waves, int bj, bool ind, dim3 grid, hipStream_t st)
+void launch_rs(const ConvArgs &a, int waves, int bj, bool ind, int kc, dim3 grid, hipStream_t st)
 {
     if constexpr (ORD == 2 && R_ != 7) {
         if (ind) {   // the planner takes IND with 4 wavefronts and 2 pixel blocks only
-            launch_wave<R_, S_, 4, 2, ORD, true>(a, grid, st);
+            launch_wave<R_, S_, 4, 2, ORD, true>(a, kc, grid, st);
             return;
         }
     }
     if (waves == 8) {
-        if (bj == 2) launch_wave<R_, S_, 8, 2, ORD>(a, grid, st);
-        else launch_wave<R_, S_, 8, 1, ORD>(a, grid, st);
+        if (bj == 2) launch_wave<R_, S_, 8, 2, ORD>(a, kc, grid, st);
+        else launch_wave<R_, S_, 8, 1, ORD>(a, kc, grid, st);
     } else {
-        if (bj == 2) launch_wave<R_, S_, 4, 2, ORD>(a, grid, st);
-        else launch_wave<R_, S_, 4, 1, ORD>(a, grid, st);
+        if (bj == 2) launch_wave<R_, S_, 4, 2, ORD>(a, kc, grid, st);
+        else launch_wave<R_, S_, 4, 1, ORD>(a, kc, grid, st);
     }
 }
 
@@ -402,7 +453,7 @@ bool wave_fits(const ConvProblem &p)
 // (blocks * BJ * 4 MFMAs * 64 cycles) plus ~1.2 us per dependent round of
 // loads (kDepth blocks in flight), plus, for a split reduction, ~2.5 us for
 // the reduce launch and the partials' HBM round trip.
-WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
+WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, int max_splits)
 {
     WavePlan best{};
     best.order = wave_order(p);
@@ -413,7 +464,7 @@ WavePlan plan_wave_f32(const ConvProblem &p, int num_cus)
         const long tiles = (long)ceil_div(p.M, 32 * bj) * ceil_div(p.Kg, 32) * p.groups;
         const int depth = bj == 2 ? 2 : 4;
         for (int waves : {4, 8}) {   // on a tie the smaller work-group: no idle wavefronts
-            for (int sp = 1; sp <= 16; ++sp) {
+            for (int sp = 1; sp <= std::min(16, max_splits); ++sp) {
                 const int per = ceil_div(blocks, sp);
                 if (sp > 1 && per < 2 * waves) break;           // at least 2 blocks per wavefront
                 if (ceil_div(blocks, per) != sp) continue;
@@ -457,9 +508,17 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
     if (plan.order == 1 && R != 3 && R != 1) R = S = 0;
     if (plan.order == 2 && R != 3 && R != 7) R = S = 0;
     const bool gen = p.res || p.ysn != (long)p.K * p.P * p.Q;
-    snprintf(buf, len, "igemm_wave_f32%s_kernel<%d, %d, %d, %d, %d, %s>%s", gen ? "_gen" : "", R, S,
-             plan.waves, plan.bj,
-             plan.order, plan.ind ? "true" : "false", plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    if (plan.kc) {
+        // the 16-byte filter loads need w 16-byte aligned: named as for an aligned w
+        const int kc = plan.order == 1 && p.R == 1 && p.S == 1 && !plan.ind ? 1 : 2;
+        snprintf(buf, len, "igemm_wave_f32_kcrs_kernel<%d, %d, %d, %d, %d, %s, %d>%s", R, S, plan.waves,
+                 plan.bj, plan.order, plan.ind ? "true" : "false", kc,
+                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    } else {
+        snprintf(buf, len, "igemm_wave_f32%s_kernel<%d, %d, %d, %d, %d, %s>%s", gen ? "_gen" : "", R, S,
+                 plan.waves, plan.bj, plan.order, plan.ind ? "true" : "false",
+                 plan.splits > 1 ? " + splitk_reduce_kernel" : "");
+    }
     *launches = plan.splits > 1 ? 2 : 1;
 }
 
@@ -467,6 +526,10 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
                            const float *w, const float *bias, float *y, float *ws,
                            hipStream_t st, const LaunchHook *hook)
 {
+    // filters as given: one 16-byte load per half-block where the 4 taps are
+    // consecutive and aligned (1x1, C/groups % 8 == 0), else four 4-byte loads
+    const int kc = !plan.kc ? 0
+                   : plan.order == 1 && p.R == 1 && p.S == 1 && !plan.ind && (uintptr_t)w % 16 == 0 ? 1 : 2;
     ConvArgs a = make_args(p);
     a.x = x;
     a.w = w;
@@ -488,22 +551,22 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
     if (e != hipSuccess) return e;
     if (plan.order == 1) {   // reduction ordered (r, s, c) in the packed filters
         if (p.R == 1 && p.S == 1)
-            launch_rs<1, 1, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<1, 1, 1>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
         else if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<3, 3, 1>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
         else
-            launch_rs<0, 0, 1>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<0, 0, 1>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     } else if (plan.order == 2) {   // (r, s, c4): C/groups <= 4
         if (p.R == 3 && p.S == 3)
-            launch_rs<3, 3, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<3, 3, 2>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
         else if (p.R == 7 && p.S == 7)
-            launch_rs<7, 7, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<7, 7, 2>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
         else
-            launch_rs<0, 0, 2>(a, plan.waves, plan.bj, plan.ind, grid, st);
+            launch_rs<0, 0, 2>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     } else if (p.R == 1 && p.S == 1) {
-        launch_rs<1, 1, 0>(a, plan.waves, plan.bj, plan.ind, grid, st);
+        launch_rs<1, 1, 0>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     } else {
-        launch_rs<0, 0, 0>(a, plan.waves, plan.bj, plan.ind, grid, st);
+        launch_rs<0, 0, 0>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     }
     e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return e;

@@ -111,7 +111,7 @@ struct IgemmPlan {
     size_t ws_bytes;    // bytes of fp32 partials (0 without a split)
     bool krsc;          // filters pre-packed [K][R][S][C/groups] (reduction order r, s, c)
 };
-IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus);
+IgemmPlan plan_igemm_f32(const ConvProblem &p, int num_cus, int max_splits);
 hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const float *x,
                             const float *w, const float *bias, float *y, float *ws,
                             hipStream_t st, const LaunchHook *hook = nullptr);
@@ -126,17 +126,18 @@ struct WavePlan {
     int order;          // reduction order of the packed filters (wave_order)
     bool ind;           // each wavefront owns a tile and its whole reduction (short
                         // reductions over many tiles); waves then groups tiles
+    bool kc;            // filters read as given (KCRS), not from a packed copy
 };
 // The wave kernel addresses x and its packed filters with 32-bit offsets.
 bool wave_fits(const ConvProblem &p);
-WavePlan plan_wave_f32(const ConvProblem &p, int num_cus);
+WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, int max_splits);
 hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const float *x,
                            const float *w, const float *bias, float *y, float *ws,
                            hipStream_t st, const LaunchHook *hook = nullptr);
 void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, int len,
                        int *launches);
 // bf16 inputs, fp32 accumulation (v_mfma_f32_32x32x16_bf16).
-IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus);
+IgemmPlan plan_igemm_bf16(const ConvProblem &p, int num_cus, int max_splits);
 bool bf16_fast_1x1(const ConvProblem &p, const void *x);
 hipError_t launch_igemm_bf16(const ConvProblem &p, const IgemmPlan &plan, bool fast, bool va,
                              const uint16_t *x, const uint16_t *w, const float *bias, float *y,
@@ -160,7 +161,7 @@ struct NhwcPlan {
                           // its filters are packed in 64-channel blocks
 };
 bool nhwc_bf16_eligible(const ConvProblem &p);
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x);
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits);
 hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const uint16_t *x,
                             const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
                             float *partials, hipStream_t st, const LaunchHook *hook = nullptr);
@@ -203,36 +204,57 @@ enum Impl {
     IMPL_NHWC_BF16 = 5,
     IMPL_STEM_BF16 = 6
 };
+// What a call may use besides its tensors.
+enum PlanMode {
+    MODE_FREE = 0,      // nothing: no workspace, filters read as given (plain entry points)
+    MODE_SCRATCH = 1,   // a caller workspace: split partials, a channel-last copy of x,
+                        // filters packed per call
+    MODE_PREPACK = 2    // filters packed ahead into a buffer of their own (stack executor,
+                        // packed-filter entry point); with MODE_SCRATCH: a stack layer
+};
+// The filter layout a resolved layer's kernel reads.
+enum WeightLayout {
+    WL_GIVEN = 0,       // w as the caller holds it, [K][C/groups][R][S]
+    WL_STEM = 1,        // bf16 7x7 stem: tap pairs
+    WL_WAVE = 2,        // fp32 wave kernel: wavefront load order
+    WL_KRSC = 3,        // [K][R][S][C/groups]
+    WL_KRSC_BLOCK = 4   // KRSC per block of 64 channels
+};
 struct Resolved {
     ConvProblem p;
     int kind;
     int impl;
+    int mode;           // enum PlanMode the plan was made for
+    int wlayout;        // enum WeightLayout the kernel reads
     IgemmPlan plan;     // IMPL_IGEMM only
     WavePlan wplan;     // IMPL_WAVE only
     bool bfast, bva;    // IMPL_IGEMM_BF16: vectorised 1x1 loader, 16-byte filter loads
     NhwcPlan nplan;     // IMPL_NHWC_BF16 only
-    bool pack_per_call; // enqueue packs the filters (KRSC) into the workspace first
+    bool pack_per_call; // enqueue packs the filters into the workspace first
     const void *wk;     // filters the conv kernel reads when they were packed ahead (else w)
     const void *x, *w;
     const float *bias;
     float *y;
 };
-int resolve(int kind, int algo, int N, int C, int H, int W, int K, int R, int S, int stride,
+int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int R, int S, int stride,
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
             int relu, Resolved *out);
+// resolve() for tensors at 256-byte boundaries (w may be null: a stand-in).
+int resolve_aligned(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                    int dtype, int algo, int mode, const void *w, Resolved *out);
 // Adds a residual [N][K][P][Q] (read at y's indices, before the activation) to
 // a resolved dense layer; nullptr leaves it unchanged.
 int set_residual(Resolved &r, const float *res);
 // Sets the distance in elements between images of y (and res); 0 keeps the
 // dense K*P*Q.  A larger stride lets y be a channel range of a wider tensor.
 int set_output_stride(Resolved &r, long ysn);
+// ws: the workspace of workspace_bytes(r) bytes, 256-byte aligned (nullptr when 0).
 hipError_t enqueue(const Resolved &r, float *ws, hipStream_t st, const LaunchHook *hook = nullptr);
 void describe(const Resolved &r, char *buf, int len, int *launches);
-size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + split partials
-bool krsc_eligible(const Resolved &r);       // the kernel can read KRSC-packed filters
+size_t workspace_bytes(const Resolved &r);   // packed filters (per-call packing) + copy + split partials
 hipError_t launch_pack(const Resolved &r, void *dst, hipStream_t st);   // the copy its kernel reads
-size_t packed_bytes(const Resolved &r);      // bytes of the KRSC copy of the filters
-void set_krsc(Resolved &r, const void *packed);  // read filters pre-packed at `packed`
+size_t packed_bytes(const Resolved &r);      // bytes of that copy
+void set_packed(Resolved &r, const void *packed);  // read filters packed ahead at `packed`
 // Filters in the wave kernel's A-operand order, w_pk[g][ceil(Kg/32)][ceil(Kred/8)][64][4]
 // (reduction order r, s, c when `krsc`, else c, r, s), zero-padded.
 // Reduction order of the wave kernel's packed filters: 0 = (c, r, s),

@@ -168,15 +168,15 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
     for (int i = 0; i < n; ++i) {
         const miconv_conv_desc &d = layers[i];
         Resolved r;
-        int rc = resolve(d.op, MICONV_ALGO_AUTO, d.N, d.C, d.H, d.W, d.K, d.R, d.S, d.stride,
-                         d.pad, d.groups, d.x, d.w, d.bias, d.y, d.relu, &r);
+        int rc = resolve(d.op, MICONV_ALGO_AUTO, MODE_SCRATCH | MODE_PREPACK, d.N, d.C, d.H, d.W, d.K, d.R,
+                         d.S, d.stride, d.pad, d.groups, d.x, d.w, d.bias, d.y, d.relu, &r);
         if (rc == MICONV_OK) rc = set_output_stride(r, d.y_image_stride);
         if (rc == MICONV_OK) rc = set_residual(r, d.res);
         if (rc != MICONV_OK) {
             miconv_stack_destroy(s);
             return rc;
         }
-        if (r.pack_per_call || krsc_eligible(r)) {
+        if (r.wlayout != WL_GIVEN) {
             // Pre-computing: pack the filters once, in the layout the kernel
             // reads, for every replay.
             void *pk = nullptr;
@@ -187,7 +187,7 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
                 miconv_stack_destroy(s);
                 return set_hip_error(e);
             }
-            set_krsc(r, pk);
+            set_packed(r, pk);
         }
         need_p = std::max(need_p, round_up(workspace_bytes(r), 256));
         s->layers.push_back(r);

@@ -20,8 +20,12 @@ LIB_PATH = os.path.join(_PKG, "libmiconv.so")
 HEADER = os.path.join(os.path.dirname(_PKG), "include", "miconv.h")
 
 OK = 0
-ERR_NULL, ERR_SHAPE, ERR_GROUPS, ERR_UNSUPPORTED, ERR_TOO_LARGE, ERR_ALIGN, ERR_HIP = range(-1, -8, -1)
+(ERR_NULL, ERR_SHAPE, ERR_GROUPS, ERR_UNSUPPORTED, ERR_TOO_LARGE, ERR_ALIGN, ERR_HIP,
+ ERR_WORKSPACE) = range(-1, -9, -1)
 ALGO_AUTO, ALGO_DIRECT, ALGO_IGEMM, ALGO_WAVE = 0, 1, 2, 3
+# enum miconv_plan_mode: which entry point a plan is made for
+PLAN_PLAIN, PLAN_WS, PLAN_PACKED, PLAN_STACK = 0, 1, 2, 3
+_PLAN = {"plain": PLAN_PLAIN, "ws": PLAN_WS, "packed": PLAN_PACKED, "stack": PLAN_STACK}
 
 _lib = None
 
@@ -61,7 +65,11 @@ def lib() -> ctypes.CDLL:
         L.conv2d_pack_weights.restype = i
         L.conv2d_fwd_packed.argtypes = [i] * 11 + [p, p, p, p, i, p]
         L.conv2d_fwd_packed.restype = i
-        L.conv2d_describe.argtypes = [i] * 12 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
+        L.conv2d_describe.argtypes = [i] * 13 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
+        L.conv2d_workspace_bytes.argtypes = [i] * 12
+        L.conv2d_workspace_bytes.restype = l
+        L.conv2d_fwd_ws.argtypes = [i] * 12 + [p, p, p, p, p, l, i, p, ctypes.c_size_t, p]
+        L.conv2d_fwd_ws.restype = i
         L.conv2d_describe.restype = i
         L.miconv_stack_create.argtypes = [p, i, ctypes.POINTER(p)]
         L.miconv_stack_size.argtypes = [p]
@@ -144,6 +152,9 @@ def _image_strided(t: torch.Tensor, name: str) -> int:
     N, K, P, Q = t.shape
     if t.stride()[1:] != (P * Q, Q, 1) and K * P * Q > 1:
         raise ValueError(f"{name} must be dense within each image")
+    if N > 1 and t.stride(0) < K * P * Q:
+        # e.g. an expanded view: images would overlap in memory
+        raise ValueError(f"{name}: images overlap (image stride {t.stride(0)} < {K * P * Q})")
     return t.stride(0) if N > 1 else K * P * Q
 
 
@@ -238,6 +249,63 @@ def conv2d_fwd_ex(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None
     return y
 
 
+def conv2d_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32",
+                           algo=ALGO_AUTO) -> int:
+    """Bytes of workspace conv2d_fwd_ws needs for this shape (any pointer alignment)."""
+    n = lib().conv2d_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups,
+                                     1 if dtype == "bf16" else 0, int(algo))
+    if n < 0:
+        raise MiconvError(int(n), "conv2d_workspace_bytes")
+    return n
+
+
+def workspace(nbytes: int, device="cuda") -> Optional[torch.Tensor]:
+    """A 256-byte aligned device buffer of at least nbytes (torch's caching
+    allocator returns such blocks), or None for 0."""
+    if nbytes <= 0:
+        return None
+    t = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if t.data_ptr() % 256:
+        raise RuntimeError("workspace not 256-byte aligned")
+    return t
+
+
+def conv2d_fwd_ws(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None, algo=ALGO_AUTO,
+                  ws=None, stream=None):
+    """conv2d_fwd_ex with a caller workspace: the fastest single-call plans
+    (split reductions, channel-last staging, per-call filter packing).  ws is
+    a uint8 device tensor of at least conv2d_workspace_bytes bytes; None
+    allocates one from torch's caching allocator (the library never
+    allocates)."""
+    xdt = torch.bfloat16 if x.dtype == torch.bfloat16 else torch.float32
+    _dev(x, xdt, "x", 4)
+    _dev(w, xdt, "w", 4)
+    if bias is not None:
+        _dev(bias, torch.float32, "bias", 1)
+    ys = _image_strided(y, "y")
+    if res is not None:
+        if _image_strided(res, "res") != ys or tuple(res.shape) != tuple(y.shape):
+            raise ValueError("res must have y's shape and strides")
+    N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if groups <= 0 or Cg * groups != C:
+        raise ValueError("w.shape[1] * groups must equal C")
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, K, P, Q):
+        raise ValueError(f"y must have shape {(N, K, P, Q)}, got {tuple(y.shape)}")
+    dt = 1 if xdt == torch.bfloat16 else 0
+    if ws is None:
+        ws = workspace(conv2d_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups,
+                                              "bf16" if dt else "f32", algo), x.device)
+    elif ws.device.type != "cuda" or ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise TypeError("ws must be a contiguous uint8 device tensor")
+    rc = lib().conv2d_fwd_ws(N, C, H, W, K, R, S, stride, pad, groups, dt, int(algo), _ptr(x), _ptr(w),
+                             _ptr(bias), _ptr(res), _ptr(y), ys, 1 if relu else 0, _ptr(ws),
+                             0 if ws is None else ws.numel(), _stream(stream))
+    _check(rc, "conv2d_fwd_ws")
+    return y
+
+
 class PackedFilters:
     """Filters packed once for repeated calls of one layer shape
     (conv2d_pack_weights); ``forward`` runs conv2d_fwd_packed.  Holds the
@@ -329,12 +397,17 @@ def cast_f32_to_bf16(x, y, stream=None):
     return y
 
 
-def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", algo=ALGO_AUTO):
-    """(kernel names, launch count) the library would use for this conv shape."""
+def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", algo=ALGO_AUTO,
+                    mode="ws"):
+    """(kernel names, launch count) the library would use for this conv shape
+    through the entry point of `mode`: "plain" (conv2d_fwd & co, no
+    workspace), "ws" (conv2d_fwd_ws), "packed" (conv2d_fwd_packed) or
+    "stack" (a miconv_stack layer)."""
     buf = ctypes.create_string_buffer(256)
     n = ctypes.c_int()
     rc = lib().conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups,
-                               1 if dtype == "bf16" else 0, int(algo), buf, 256, ctypes.byref(n))
+                               1 if dtype == "bf16" else 0, int(algo), _PLAN[mode], buf, 256,
+                               ctypes.byref(n))
     _check(rc, "conv2d_describe")
     return buf.value.decode(), n.value
 
@@ -441,11 +514,19 @@ class Stack:
 
 # Allocating conveniences (output buffers come from torch's caching allocator).
 
-def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO, stream=None):
+def conv2d(x, w, bias=None, stride=1, pad=0, groups=1, relu=False, algo=ALGO_AUTO, stream=None,
+           mode="ws"):
+    """y = act(conv(x, w) + bias) into a new tensor.  mode "ws": conv2d_fwd_ws
+    with a workspace from torch's caching allocator (the fastest plan);
+    "plain": conv2d_fwd / conv2d_fwd_bf16 (and *_algo), no workspace."""
     N, _, H, W = x.shape
     K, _, R, S = w.shape
     P, Q = out_dims(H, W, R, S, stride, pad)
     y = torch.empty((N, K, P, Q), device=x.device, dtype=torch.float32)
+    if mode == "ws":
+        return conv2d_fwd_ws(x, w, bias, y, stride, pad, groups, relu, algo=algo, stream=stream)
+    if mode != "plain":
+        raise ValueError(f"mode must be 'ws' or 'plain', got {mode!r}")
     if x.dtype == torch.bfloat16:
         if algo == ALGO_AUTO:
             return conv2d_fwd_bf16(x, w, bias, y, stride, pad, groups, relu, stream)

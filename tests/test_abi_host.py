@@ -22,6 +22,7 @@ def L():
 def test_exports_every_declared_symbol(L):
     names = miconv.header_functions()
     for expected in ("conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd", "conv2d_fwd_algo",
+                     "conv2d_workspace_bytes", "conv2d_fwd_ws",
                      "miconv_out_dims", "maxpool2d_fwd", "add_act_fwd", "cast_f32_to_bf16",
                      "miconv_strerror", "miconv_last_hip_error", "miconv_version"):
         assert expected in names
@@ -77,10 +78,10 @@ def test_algo_and_glue_errors(L):
 
 
 def test_strerror_and_version(L):
-    for s in range(0, -8, -1):
-        assert miconv.strerror(s)
+    for s in range(0, -9, -1):
+        assert miconv.strerror(s) != "unknown status", s
     assert miconv.strerror(-99) == "unknown status"
-    assert L.miconv_version() >= 100
+    assert L.miconv_version() >= 20000
     assert L.miconv_last_hip_error() == 0
 
 
@@ -139,3 +140,86 @@ def test_output_stride_validation(L):
     dw = (2, 32, 28, 28, 32, 3, 3, 1, 1, 32)
     assert L.conv2d_fwd_ex(*dw, 0, A, FAKE, FAKE, None, None, FAKE, 64 * 28 * 28, 0, None) == miconv.ERR_UNSUPPORTED
     assert L.conv2d_fwd_ex(*shape, 3, A, FAKE, FAKE, None, None, FAKE, 0, 0, None) == miconv.ERR_UNSUPPORTED
+
+
+def test_workspace_query(L):
+    """conv2d_workspace_bytes: 0 where the fastest plan needs no scratch,
+    the split partials / channel-last copy / packed filters otherwise, and
+    the validation errors of the conv entry points."""
+    f = miconv.conv2d_workspace_bytes
+    assert f(1, 1, 1, 1, 1, 1, 1, 1, 0) == 0                                   # one tap
+    assert f(1, 512, 7, 7, 512, 3, 3, 1, 1) >= 2 * 512 * 49 * 4               # split partials
+    # bf16 3x3 at batch 64: the channel-last copy of x and the KRSC filters
+    assert f(64, 128, 28, 28, 128, 3, 3, 1, 1, dtype="bf16") >= 64 * 128 * 28 * 28 * 2 + 128 * 128 * 9 * 2
+    with pytest.raises(miconv.MiconvError):
+        f(1, 64, 56, 56, 64, 3, 3, 1, 1, groups=3)
+    g = L.conv2d_workspace_bytes
+    assert g(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 2, 0) == miconv.ERR_UNSUPPORTED   # dtype
+    assert g(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 0, 9) == miconv.ERR_UNSUPPORTED   # algo
+    assert g(0, 64, 56, 56, 64, 3, 3, 1, 1, 1, 0, 0) == miconv.ERR_SHAPE
+
+
+def test_ws_entry_point_checks_the_workspace_first(L):
+    """A plan that needs scratch refuses a missing, short or unaligned
+    workspace before anything is enqueued (no GPU needed)."""
+    shape = (1, 512, 7, 7, 512, 3, 3, 1, 1, 1)
+    need = L.conv2d_workspace_bytes(*shape, 0, 0)
+    assert need > 0
+    A = miconv.ALGO_AUTO
+    call = lambda ws, n: L.conv2d_fwd_ws(*shape, 0, A, FAKE, FAKE, None, None, FAKE, 0, 0, ws, n, None)
+    assert call(None, 0) == miconv.ERR_WORKSPACE
+    assert call(FAKE, need - 1) == miconv.ERR_WORKSPACE
+    assert call(FAKE + 16, need) == miconv.ERR_WORKSPACE      # not 256-byte aligned
+    assert L.conv2d_fwd_ws(*shape, 0, A, None, FAKE, None, None, FAKE, 0, 0, FAKE, need, None) == miconv.ERR_NULL
+    assert L.conv2d_fwd_ws(*shape, 2, A, FAKE, FAKE, None, None, FAKE, 0, 0, FAKE, need, None) == \
+        miconv.ERR_UNSUPPORTED
+
+
+SCRATCH_KERNELS = ("splitk_reduce", "nchw_to_nhwc", "pack_")
+
+
+@pytest.mark.parametrize("config", [1, 2, 3, 4, 5, 6])
+def test_plain_plans_need_no_scratch(L, config):
+    """Every layer of every workload, as the plain entry points plan it, runs
+    without split partials, a channel-last copy or a filter-packing launch:
+    one kernel, reading only the caller's tensors.  The stack plans of the
+    same layers pack nothing per pass either."""
+    from paper_1907_02154_amd import workloads as wl
+    wk = wl.workload(config)
+    dt = "bf16" if wk.dtype == "bf16" else "f32"
+    for l in wk.layers:
+        if l.kind == "dw":
+            continue
+        name, n = miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad, l.groups,
+                                         dt, mode="plain")
+        assert n == 1 and not any(k in name for k in SCRATCH_KERNELS), (l.name, name)
+        name, n = miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad, l.groups,
+                                         dt, mode="packed")
+        assert n == 1 and not any(k in name for k in SCRATCH_KERNELS), (l.name, name)
+        name, _ = miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad, l.groups,
+                                         dt, mode="stack")
+        assert "pack_" not in name, (l.name, name)
+
+
+def test_no_allocation_or_sync_on_the_call_path():
+    """hipMalloc, hipFree and stream/device synchronisation appear only in the
+    stack executor's create/destroy, never in the code the conv entry points
+    reach."""
+    import glob
+    import os
+    import re
+    csrc = os.path.join(os.path.dirname(miconv.__file__), "csrc")
+    pat = re.compile(r"\b(hipMalloc\w*|hipFree\w*|hipStreamSynchronize|hipDeviceSynchronize|hipMemset\w*)\s*\(")
+    for path in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        with open(path) as f:
+            text = f.read()
+        hits = pat.findall(text)
+        if os.path.basename(path) == "stack.hip":
+            body = text[text.index("int miconv_stack_create"):]
+            for fn in ("miconv_stack_launch", "miconv_stack_capture", "miconv_stack_replay",
+                       "miconv_stack_launch_timed"):
+                seg = body[body.index(f"int {fn}("):]
+                seg = seg[:seg.index("\n}\n")]
+                assert not pat.search(seg), fn
+        else:
+            assert not hits, (path, hits)

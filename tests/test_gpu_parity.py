@@ -42,9 +42,9 @@ def dev_bf16_bits(bits):
     return t.view(torch.bfloat16)
 
 
-def gpu_conv(x, w, b, stride, pad, groups, relu, algo):
+def gpu_conv(x, w, b, stride, pad, groups, relu, algo, mode="ws"):
     y = miconv.conv2d(dev(x), dev(w), None if b is None else dev(b), stride, pad, groups, relu,
-                      algo=algo)
+                      algo=algo, mode=mode)
     torch.cuda.synchronize()
     return y.cpu().numpy()
 
@@ -87,7 +87,11 @@ DENSE_CASES = [
 @pytest.mark.parametrize("case", DENSE_CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("algo", [miconv.ALGO_DIRECT, miconv.ALGO_IGEMM, miconv.ALGO_WAVE,
                                   miconv.ALGO_AUTO])
-def test_dense_small_int_bitwise(oracle_lib, case, algo):
+@pytest.mark.parametrize("mode", ["ws", "plain"])
+def test_dense_small_int_bitwise(oracle_lib, case, algo, mode):
+    """Every fp32 algorithm through conv2d_fwd_ws (split reductions allowed)
+    and through the plain entry point (no workspace: filters read as given,
+    no split)."""
     N, C, H, W, K, R, S, st, pad, g = case
     seed = 1000 + sum(case)
     x = ints((N, C, H, W), -4, 4, seed)
@@ -95,9 +99,9 @@ def test_dense_small_int_bitwise(oracle_lib, case, algo):
     b = ints((K,), -8, 8, seed + 2)
     for relu in (False, True):
         ref = oracle_lib.conv2d(x, w, b, st, pad, g, relu)
-        y = gpu_conv(x, w, b, st, pad, g, relu, algo)
+        y = gpu_conv(x, w, b, st, pad, g, relu, algo, mode)
         np.testing.assert_array_equal(y, ref, err_msg=f"{case} relu={relu} algo={algo}")
-    y = gpu_conv(x, w, None, st, pad, g, False, algo)
+    y = gpu_conv(x, w, None, st, pad, g, False, algo, mode)
     np.testing.assert_array_equal(y, oracle_lib.conv2d(x, w, None, st, pad, g, False))
 
 
@@ -162,14 +166,15 @@ BF16_CASES = DENSE_CASES[:9] + [
 
 @pytest.mark.parametrize("case", BF16_CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("algo", [miconv.ALGO_AUTO, miconv.ALGO_IGEMM, miconv.ALGO_DIRECT])
-def test_bf16_small_int_bitwise(oracle_lib, case, algo):
+@pytest.mark.parametrize("mode", ["ws", "plain"])
+def test_bf16_small_int_bitwise(oracle_lib, case, algo, mode):
     N, C, H, W, K, R, S, st, pad, g = case
     seed = 3000 + sum(case)
     x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
     w = wl.to_bf16_bits(ints((K, C // g, R, S), -4, 4, seed + 1))
     b = ints((K,), -8, 8, seed + 2)
     ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
-    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True, algo=algo)
+    y = miconv.conv2d(dev_bf16_bits(x), dev_bf16_bits(w), dev(b), st, pad, g, True, algo=algo, mode=mode)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), ref)
 
@@ -182,29 +187,45 @@ OFFSET_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups) run on x and y at
 ]
 
 
+def _offset_bf16(bits, shape):
+    """A bf16 device tensor holding `bits` one element past a 16-byte boundary."""
+    buf = torch.empty(bits.size + 8, dtype=torch.int16, device="cuda")
+    buf[1:1 + bits.size] = torch.from_numpy(bits.reshape(-1).view(np.int16)).cuda()
+    t = buf[1:1 + bits.size].view(torch.bfloat16).view(shape)
+    assert t.data_ptr() % 16 == 2
+    return t
+
+
 @pytest.mark.parametrize("case", OFFSET_CASES, ids=lambda c: "x".join(map(str, c)))
-def test_bf16_offset_pointers_small_int_bitwise(oracle_lib, case):
+@pytest.mark.parametrize("which", ["xy", "w"])
+@pytest.mark.parametrize("mode", ["ws", "plain"])
+def test_bf16_offset_pointers_small_int_bitwise(oracle_lib, case, which, mode):
     """x one bf16 element and y one float past a 16-byte boundary: the
     channel-last copy falls back to reads that need no alignment, the 1x1
     layer that would read x in NCHW takes the copy, and the epilogue stores
-    element by element; results stay exact on small integers."""
+    element by element.  w one element past a 16-byte boundary: a 1x1 layer,
+    whose kernels read w as given with 16-byte loads, takes the gather kernel
+    instead.  Results stay exact on small integers, nothing is written
+    outside y."""
     N, C, H, W, K, R, S, st, pad, g = case
     seed = 3900 + sum(case)
     x = wl.to_bf16_bits(ints((N, C, H, W), -4, 4, seed))
     w = wl.to_bf16_bits(ints((K, C // g, R, S), -4, 4, seed + 1))
     b = ints((K,), -8, 8, seed + 2)
     ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
-    xb = torch.empty(x.size + 8, dtype=torch.int16, device="cuda")
-    xb[1:1 + x.size] = torch.from_numpy(x.reshape(-1).view(np.int16)).cuda()
-    tx = xb[1:1 + x.size].view(torch.bfloat16).view(N, C, H, W)
-    assert tx.data_ptr() % 16 == 2
+    tx = _offset_bf16(x, (N, C, H, W)) if which == "xy" else dev_bf16_bits(x)
+    tw = _offset_bf16(w, w.shape) if which == "w" else dev_bf16_bits(w)
     P, Q = miconv.out_dims(H, W, R, S, st, pad)
+    o = 1 if which == "xy" else 0
     yb = torch.full((N * K * P * Q + 4,), float("nan"), device="cuda")
-    ty = yb[1:1 + N * K * P * Q].view(N, K, P, Q)
-    miconv.conv2d_fwd_bf16(tx, dev_bf16_bits(w), dev(b), ty, st, pad, g, True)
+    ty = yb[o:o + N * K * P * Q].view(N, K, P, Q)
+    if mode == "ws":
+        miconv.conv2d_fwd_ws(tx, tw, dev(b), ty, st, pad, g, True)
+    else:
+        miconv.conv2d_fwd_bf16(tx, tw, dev(b), ty, st, pad, g, True)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(ty.cpu().numpy(), ref, err_msg=str(case))
-    assert torch.isnan(yb[0]) and torch.isnan(yb[-3:]).all()   # nothing written outside y
+    assert torch.isnan(yb[:o]).all() and torch.isnan(yb[o + N * K * P * Q:]).all()   # nothing outside y
 
 
 HALO_CASES = [  # (N, C, H, W, K, groups): bf16 3x3 stride-1 layers that take the halo-patch kernel
@@ -433,16 +454,27 @@ def test_wave_independent_tiles_small_int_bitwise(oracle_lib, case):
     epilogue stored straight from the accumulators: exact against the oracle
     on small integers."""
     N, C, H, W, K, st = case
-    name = miconv.conv2d_describe(N, C, H, W, K, 3, 3, st, 1, 1, "f32")[0]
+    name = miconv.conv2d_describe(N, C, H, W, K, 3, 3, st, 1, 1, "f32", mode="stack")[0]
     assert name.endswith("igemm_wave_f32_kernel<3, 3, 4, 2, 2, true>"), name
+    name = miconv.conv2d_describe(N, C, H, W, K, 3, 3, st, 1, 1, "f32", mode="plain")[0]
+    assert name.endswith("igemm_wave_f32_kcrs_kernel<3, 3, 4, 2, 2, true, 2>"), name
     seed = 4800 + sum(case)
     x = ints((N, C, H, W), -4, 4, seed)
     w = ints((K, C, 3, 3), -4, 4, seed + 1)
     b = ints((K,), -8, 8, seed + 2)
+    P, Q = miconv.out_dims(H, W, 3, 3, st, 1)
     for relu, bias in ((True, b), (False, None)):
         ref = oracle_lib.conv2d(x, w, bias, st, 1, 1, relu)
-        np.testing.assert_array_equal(gpu_conv(x, w, bias, st, 1, 1, relu, miconv.ALGO_AUTO), ref,
+        np.testing.assert_array_equal(gpu_conv(x, w, bias, st, 1, 1, relu, miconv.ALGO_AUTO, "plain"), ref,
                                       err_msg=f"{case} relu={relu}")
+        # packed filters (a one-layer stack)
+        y = torch.full((N, K, P, Q), float("nan"), device="cuda")
+        s = miconv.Stack([(miconv.OP_CONV_F32, dev(x), dev(w), None if bias is None else dev(bias), y,
+                           st, 1, 1, relu)])
+        s.launch()
+        torch.cuda.synchronize()
+        s.close()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"{case} relu={relu} stack")
 
 
 PACKED_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups, dtype): filters packed once
@@ -460,9 +492,9 @@ PACKED_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups, dtype): filters p
 
 @pytest.mark.parametrize("case", PACKED_CASES, ids=lambda c: "x".join(map(str, c)))
 def test_packed_filters_match_plain_calls(oracle_lib, case):
-    """conv2d_pack_weights + conv2d_fwd_packed run the kernel the plain entry
-    point runs, minus the packing launch: bitwise the same output, exact
-    against the oracle on small integers, for two calls on one packing."""
+    """conv2d_pack_weights + conv2d_fwd_packed (filters packed once, no
+    workspace): bitwise the output of the workspace entry point, exact against
+    the oracle on small integers, for two calls on one packing."""
     N, C, H, W, K, R, S, st, pad, g, dtype = case
     seed = 4600 + sum(case)
     x = ints((N, C, H, W), -4, 4, seed)
@@ -509,30 +541,111 @@ SPLIT_CASES = [  # batch-1 layers whose reduction the wave planner splits (ResNe
 
 
 def test_split_reduction_shared_workspace(oracle_lib):
-    """Split layers write their partials into the per-stream workspace, which
-    channel-last bf16 calls in between also use (for x's copy and their own
-    partials): calls of different shapes, repeated and interleaved, must all
-    stay exact on small integers."""
-    data = []
+    """Split layers write their partials into one caller workspace, which
+    channel-last bf16 calls in between also use (for x's copy, their packed
+    filters and their own partials): calls of different shapes, repeated and
+    interleaved on one stream, must all stay exact on small integers."""
+    data, need = [], 0
     for i, (N, C, H, W, K, R, S, st, pad, g) in enumerate(SPLIT_CASES):
         x = ints((N, C, H, W), -3, 3, 4100 + i)
         w = ints((K, C // g, R, S), -3, 3, 4200 + i)
         b = ints((K,), -8, 8, 4300 + i)
         name, launches = miconv.conv2d_describe(N, C, H, W, K, R, S, st, pad, g, "f32")
-        assert "igemm_wave_f32_kernel" in name and "splitk_reduce" in name, name
+        assert "igemm_wave_f32_kcrs_kernel" in name and "splitk_reduce" in name, name
+        need = max(need, miconv.conv2d_workspace_bytes(N, C, H, W, K, R, S, st, pad, g))
         data.append((x, w, b, st, pad, g, oracle_lib.conv2d(x, w, b, st, pad, g, True)))
     bx = wl.to_bf16_bits(ints((2, 64, 30, 30), -4, 4, 4400))
     bw = wl.to_bf16_bits(ints((64, 64, 3, 3), -4, 4, 4401))
     bb = ints((64,), -8, 8, 4402)
     bref = oracle_lib.conv2d_bf16(bx, bw, bb, 1, 1, 1, True)
+    need = max(need, miconv.conv2d_workspace_bytes(2, 64, 30, 30, 64, 3, 3, 1, 1, 1, "bf16"))
+    ws = miconv.workspace(need)
     for order in ([0, 1, 2, 0], [2, 1, 0, 2, 2]):
         for j in order:
             x, w, b, st, pad, g, ref = data[j]
-            y = miconv.conv2d(dev(x), dev(w), dev(b), st, pad, g, True)
-            yb = miconv.conv2d(dev_bf16_bits(bx), dev_bf16_bits(bw), dev(bb), 1, 1, 1, True)
+            P, Q = miconv.out_dims(x.shape[2], x.shape[3], w.shape[2], w.shape[3], st, pad)
+            y = torch.empty((x.shape[0], w.shape[0], P, Q), device="cuda")
+            miconv.conv2d_fwd_ws(dev(x), dev(w), dev(b), y, st, pad, g, True, ws=ws)
+            yb = torch.empty((2, 64, 30, 30), device="cuda")
+            miconv.conv2d_fwd_ws(dev_bf16_bits(bx), dev_bf16_bits(bw), dev(bb), yb, 1, 1, 1, True, ws=ws)
             torch.cuda.synchronize()
             np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"case {j}")
             np.testing.assert_array_equal(yb.cpu().numpy(), bref)
+
+
+# Kernel families for the graph-capture test: (N, C, H, W, K, R, S, stride, pad, groups, dtype)
+CAPTURE_CASES = [
+    (1, 64, 20, 20, 48, 3, 3, 1, 1, 1, "f32"),     # wave, (r, s, c) filter reads
+    (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32"),    # wave 1x1, 16-byte filter reads
+    (1, 3, 45, 47, 40, 7, 7, 2, 3, 1, "f32"),      # wave stem, (r, s, c4)
+    (3, 3, 224, 224, 64, 3, 3, 1, 1, 1, "f32"),    # one tile per wavefront
+    (1, 512, 7, 7, 512, 3, 3, 1, 1, 1, "f32"),     # split reduction (ws)
+    (1, 12, 9, 9, 18, 3, 3, 1, 1, 3, "f32"),       # direct
+    (2, 32, 12, 12, 32, 3, 3, 1, 1, 32, "f32"),    # depthwise
+    (4, 64, 56, 56, 256, 1, 1, 1, 0, 1, "bf16"),   # NCHW-operand 1x1
+    (8, 64, 28, 28, 128, 1, 1, 2, 0, 1, "bf16"),   # channel-last copy (ws) / gather (plain)
+    (21, 64, 56, 56, 64, 3, 3, 1, 1, 1, "bf16"),   # halo kernel (ws)
+    (1, 512, 7, 7, 512, 3, 3, 1, 1, 1, "bf16"),    # split (ws)
+    (1, 3, 224, 224, 64, 7, 7, 2, 3, 1, "bf16"),   # stem (ws: filters packed per call)
+]
+
+
+@pytest.mark.parametrize("case", CAPTURE_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
+@pytest.mark.parametrize("mode", ["plain", "ws"])
+def test_first_call_captured_in_a_graph(oracle_lib, case, mode):
+    """The very first call of a shape (nothing warmed up, nothing allocated
+    by the library) captured into a HIP graph, replayed three times with
+    eager work and synchronisation in between: every replay exact against
+    the oracle on small integers."""
+    N, C, H, W, K, R, S, st, pad, g, dt = case
+    seed = 5100 + sum(case[:10]) + (7 if mode == "ws" else 0)
+    x = ints((N, C, H, W), -4, 4, seed)
+    w = ints((K, C // g, R, S), -4, 4, seed + 1)
+    b = ints((K,), -8, 8, seed + 2)
+    if dt == "bf16":
+        x, w = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+        tx, tw = dev_bf16_bits(x), dev_bf16_bits(w)
+        ref = oracle_lib.conv2d_bf16(x, w, b, st, pad, g, True)
+    else:
+        tx, tw = dev(x), dev(w)
+        ref = oracle_lib.conv2d(x, w, b, st, pad, g, True)
+    tb = dev(b)
+    P, Q = miconv.out_dims(H, W, R, S, st, pad)
+    y = torch.empty((N, K, P, Q), device="cuda")
+    ws = None
+    if mode == "ws":
+        ws = miconv.workspace(miconv.conv2d_workspace_bytes(N, C, H, W, K, R, S, st, pad, g, dt))
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.graph(graph, stream=side):
+        if mode == "ws":
+            miconv.conv2d_fwd_ws(tx, tw, tb, y, st, pad, g, True, ws=ws, stream=side)
+        elif dt == "bf16":
+            miconv.conv2d_fwd_bf16(tx, tw, tb, y, st, pad, g, True, stream=side)
+        else:
+            miconv.conv2d_fwd(tx, tw, tb, y, st, pad, g, True, stream=side)
+    for rep in range(3):
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"replay {rep}")
+
+
+def test_workspace_too_small_launches_nothing():
+    N, C, H, W, K = 1, 512, 7, 7, 512
+    need = miconv.conv2d_workspace_bytes(N, C, H, W, K, 3, 3, 1, 1)
+    assert need > 0
+    x = torch.ones((N, C, H, W), device="cuda")
+    w = torch.ones((K, C, 3, 3), device="cuda")
+    y = torch.full((N, K, H, W), float("nan"), device="cuda")
+    ws = miconv.workspace(need)
+    with pytest.raises(miconv.MiconvError) as e:
+        miconv.conv2d_fwd_ws(x, w, None, y, 1, 1, ws=ws[:need - 256])
+    assert e.value.status == miconv.ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.isnan(y).all()
 
 
 def test_maxpool_add_cast(oracle_lib):
@@ -568,6 +681,19 @@ def test_rejects_wrong_shapes_from_python():
         miconv.conv2d_fwd(x, w, None, torch.zeros((1, 4, 7, 7), device="cuda"), 1, 1)
     with pytest.raises(TypeError):
         miconv.conv2d_fwd(x.double(), w, None, torch.zeros((1, 4, 8, 8), device="cuda"), 1, 1)
+    # an expanded y (image stride 0) would make every image land on one buffer
+    x4 = torch.zeros((4, 4, 8, 8), device="cuda")
+    y1 = torch.full((1, 4, 8, 8), float("nan"), device="cuda")
+    res = torch.zeros((4, 4, 8, 8), device="cuda")
+    for f in (miconv.conv2d_fwd_ex, miconv.conv2d_fwd_ws):
+        with pytest.raises(ValueError):
+            f(x4, w, None, y1.expand(4, 4, 8, 8), 1, 1)
+        with pytest.raises(ValueError):
+            f(x4, w, None, torch.empty((4, 4, 8, 8), device="cuda"), 1, 1, res=y1.expand(4, 4, 8, 8))
+    with pytest.raises(ValueError):
+        miconv.Stack([(miconv.OP_CONV_F32, x4, w, None, y1.expand(4, 4, 8, 8), 1, 1, 1, False)])
+    torch.cuda.synchronize()
+    assert torch.isnan(y1).all()
 
 
 def test_depthwise_batch64_sampled(oracle_lib):

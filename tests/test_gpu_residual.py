@@ -34,14 +34,14 @@ def dev_bf16_bits(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
 
 
-# (N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, kernel the call must use)
+# (N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, kernel conv2d_fwd_ws must use)
 RES_CASES = [
-    (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kernel<3, 3, 8, 1, 1, false>"),
-    (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", A, "igemm_wave_f32_kernel<1, 1, 8, 1, 1, false>"),
+    (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 1, false, 2>"),
+    (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<1, 1, 8, 1, 1, false, 1>"),
     (1, 512, 8, 8, 96, 3, 3, 1, 1, 1, "f32", A, "splitk_reduce_kernel"),        # 16-byte reduce
     (1, 1024, 7, 7, 40, 3, 3, 1, 1, 1, "f32", A, "splitk_reduce_kernel"),       # scalar reduce
-    (8, 3, 224, 224, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kernel<3, 3, 4, 2, 2, true>"),
-    (1, 3, 45, 47, 40, 7, 7, 2, 3, 1, "f32", A, "igemm_wave_f32_kernel<7, 7, 8, 1, 2, false>"),
+    (8, 3, 224, 224, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<3, 3, 4, 2, 2, true, 2>"),
+    (1, 3, 45, 47, 40, 7, 7, 2, 3, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<7, 7, 8, 1, 2, false, 2>"),
     (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", I, "igemm_f32_kernel<1, 1, 32, 64, 1, 2, 64>"),
     (1, 12, 9, 9, 18, 3, 3, 1, 1, 3, "f32", A, "conv_direct_kernel<float>"),
     (4, 64, 56, 56, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>"),
@@ -80,34 +80,45 @@ def _oracle(oracle_lib, case, x, w, b, res, relu):
     return f(x, w, b, st, pad, g, relu, res=res)
 
 
+def _join(tx, tw, tb, res, y, st, pad, g, relu, algo, mode):
+    if mode == "ws":
+        miconv.conv2d_fwd_ws(tx, tw, tb, y, st, pad, g, relu, res=res, algo=algo)
+    else:
+        miconv.conv2d_fwd_res(tx, tw, tb, res, y, st, pad, g, relu, algo=algo)
+
+
 @pytest.mark.parametrize("case", RES_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
-def test_residual_join_small_int_bitwise(oracle_lib, case):
+@pytest.mark.parametrize("mode", ["ws", "plain"])
+def test_residual_join_small_int_bitwise(oracle_lib, case, mode):
+    """conv2d_fwd_ws (the kernel named in the case) and conv2d_fwd_res (the
+    plan without a workspace) with the join in the epilogue."""
     N, C, H, W, K, R, S, st, pad, g, dt, algo, kernel = case
-    name = miconv.conv2d_describe(N, C, H, W, K, R, S, st, pad, g, dt, algo)[0]
-    assert kernel in name, name
+    name = miconv.conv2d_describe(N, C, H, W, K, R, S, st, pad, g, dt, algo, mode=mode)[0]
+    if mode == "ws":
+        assert kernel in name, name
     x, w, b, res, tx, tw = _inputs(case, 6000 + sum(case[:10]))
     tres = dev(res)
     for relu in (True, False):
         ref = _oracle(oracle_lib, case, x, w, b, res, relu)
         y = torch.full(res.shape, float("nan"), device="cuda")
-        miconv.conv2d_fwd_res(tx, tw, dev(b), tres, y, st, pad, g, relu, algo=algo)
+        _join(tx, tw, dev(b), tres, y, st, pad, g, relu, algo, mode)
         torch.cuda.synchronize()
         np.testing.assert_array_equal(y.cpu().numpy(), ref, err_msg=f"{name} relu={relu}")
     # in place: the residual is the output buffer itself
     y = tres.clone()
-    miconv.conv2d_fwd_res(tx, tw, dev(b), y, y, st, pad, g, True, algo=algo)
+    _join(tx, tw, dev(b), y, y, st, pad, g, True, algo, mode)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case, x, w, b, res, True),
                                   err_msg=f"{name} in place")
     # no residual: the plain operator
     y = torch.empty(res.shape, device="cuda")
-    miconv.conv2d_fwd_res(tx, tw, dev(b), None, y, st, pad, g, True, algo=algo)
+    _join(tx, tw, dev(b), None, y, st, pad, g, True, algo, mode)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case, x, w, b, np.zeros_like(res), True))
 
 
 @pytest.mark.parametrize("case", [c for c in RES_CASES if c[-1] in (
-    "igemm_wave_f32_kernel<1, 1, 8, 1, 1, false>", "splitk_reduce_kernel",
+    "igemm_wave_f32_kcrs_kernel<1, 1, 8, 1, 1, false, 1>", "splitk_reduce_kernel",
     "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>")][:4],
     ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
 def test_residual_offset_pointers(oracle_lib, case):
@@ -122,7 +133,7 @@ def test_residual_offset_pointers(oracle_lib, case):
     r = rb[1:1 + n].view(res.shape)
     r.copy_(dev(res))
     assert y.data_ptr() % 16 == 4 and r.data_ptr() % 16 == 4
-    miconv.conv2d_fwd_res(tx, tw, dev(b), r, y, st, pad, g, True, algo=algo)
+    miconv.conv2d_fwd_ws(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case, x, w, b, res, True))
     assert torch.isnan(yb[0]) and torch.isnan(yb[1 + n:]).all()
@@ -214,14 +225,49 @@ def test_output_image_stride(oracle_lib, case):
     case2 = (max(N, 2),) + case[1:]
     x, w, b, res, tx, tw = _inputs(case2, 7300 + sum(case[:10]))
     n2, _, P, Q = res.shape
-    for off, extra in ((4, 8), (3, 5)):       # y 16-byte aligned or not
+    for off, extra, mode in ((4, 8, "ws"), (3, 5, "ws"), (4, 8, "plain")):   # y 16-byte aligned or not
         big = torch.full((n2, K + extra, P, Q), float("nan"), device="cuda")
         rbig = torch.zeros((n2, K + extra, P, Q), device="cuda")
         y, r = big[:, off:off + K], rbig[:, off:off + K]
         r.copy_(dev(res))
-        miconv.conv2d_fwd_ex(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
+        if mode == "ws":
+            miconv.conv2d_fwd_ws(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
+        else:
+            miconv.conv2d_fwd_ex(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
         torch.cuda.synchronize()
-        name = miconv.conv2d_describe(n2, C, H, W, K, R, S, st, pad, g, dt, algo)[0]
+        name = miconv.conv2d_describe(n2, C, H, W, K, R, S, st, pad, g, dt, algo, mode=mode)[0]
         np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case2, x, w, b, res, True),
                                       err_msg=f"{name} offset {off}")
         assert torch.isnan(big[:, :off]).all() and torch.isnan(big[:, off + K:]).all()
+
+
+VEC_Y_CASES = [c for c in RES_CASES if c[-1] in (
+    "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>",
+    "igemm_bf16_halo_kernel<128, 64, 2, 2, 256, 1>",
+    "igemm_bf16_halo_kernel<128, 128, 2, 2, 192, 2>",
+    "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 1, false, 2>")]
+
+
+@pytest.mark.parametrize("case", VEC_Y_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
+def test_output_stride_misaligned_vector_planes(oracle_lib, case):
+    """y and res as channel ranges of a wider tensor whose base sits one float
+    past a 16-byte boundary, on planes (P*Q % 4 == 0) where the epilogues
+    would otherwise store 16 bytes at a time: the strided, misaligned rows
+    take the element-wise path, exactly, and the guard channels stay NaN."""
+    N, C, H, W, K, R, S, st, pad, g, dt, algo, kernel = case
+    case2 = (max(N, 2),) + case[1:]
+    x, w, b, res, tx, tw = _inputs(case2, 7600 + sum(case[:10]))
+    n2, _, P, Q = res.shape
+    assert (P * Q) % 4 == 0
+    extra = 6
+    flat = torch.full((n2 * (K + extra) * P * Q + 1,), float("nan"), device="cuda")
+    rflat = torch.zeros_like(flat)
+    big = flat[1:].view(n2, K + extra, P, Q)
+    rbig = rflat[1:].view(n2, K + extra, P, Q)
+    y, r = big[:, 2:2 + K], rbig[:, 2:2 + K]
+    assert y.data_ptr() % 16 != 0 and (y.data_ptr() - r.data_ptr()) % 16 == 0
+    r.copy_(dev(res))
+    miconv.conv2d_fwd_ws(tx, tw, dev(b), y, st, pad, g, True, res=r, algo=algo)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case2, x, w, b, res, True))
+    assert torch.isnan(big[:, :2]).all() and torch.isnan(big[:, 2 + K:]).all() and torch.isnan(flat[0])
