@@ -176,6 +176,24 @@ int conv2d_fwd_ws(int N, int C, int H, int W, int K, int R, int S, int stride, i
                   int dtype, int algo, const void *x, const void *w, const float *bias, const float *res,
                   float *y, long y_image_stride, int relu, void *ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory at all (code under HIP
+ * graph capture that may not call hipMalloc, tight serving loops, harnesses
+ * that forbid allocation): conv2d_fwd_ws with the workspace taken from a
+ * fixed scratch array of MICONV_NOALLOC_SCRATCH_BYTES inside the library's
+ * device code, one per GPU, held from its first use on that GPU until the
+ * process ends.  Allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine) and synchronises nothing.  A plan that needs more scratch
+ * than that (conv2d_workspace_bytes reports it) fails with
+ * MICONV_ERR_WORKSPACE and enqueues nothing.  Every call on one GPU shares
+ * its scratch: calls that can overlap on one GPU (other streams, other
+ * threads, or a graph replay of one) race on it and must be serialised by the
+ * caller; calls ordered on one stream are safe.  Whatever must start at zero
+ * is written by the call's own kernels.  Everything else as conv2d_fwd_ws. */
+#define MICONV_NOALLOC_SCRATCH_BYTES (32u << 20)
+int conv2d_fwd_noalloc(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                       int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
+                       const float *res, float *y, long y_image_stride, int relu, void *stream);
+
 /* Filters packed once for repeated calls of one layer (the pre-computing step
  * of the paper's graph-level optimisation, Sec. 3.2.3), outside a stack.
  * The packed layout is the one the kernel chosen for this shape reads: the

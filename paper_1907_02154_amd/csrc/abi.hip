@@ -393,10 +393,8 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     }
 }
 
-namespace {
-
-// Enqueue a resolved call on the caller's workspace (ws may be null when the
-// plan needs none).  Never allocates, frees or synchronises.
+// Enqueue a resolved call on a workspace of ws_bytes bytes (ws may be null
+// when the plan needs none).  Never allocates, frees or synchronises.
 int run(const Resolved &r, void *ws, size_t ws_bytes, hipStream_t st)
 {
     const size_t need = workspace_bytes(r);
@@ -405,6 +403,8 @@ int run(const Resolved &r, void *ws, size_t ws_bytes, hipStream_t st)
     }
     return finish(enqueue(r, need ? static_cast<float *>(ws) : nullptr, st));
 }
+
+namespace {
 
 // An entry point without a workspace: the plan takes none by construction.
 int run_free(const Resolved &r, hipStream_t st) { return run(r, nullptr, 0, st); }
@@ -463,7 +463,7 @@ int conv2d_fwd_bf16(int N, int C, int H, int W, int K, int R, int S, int stride,
 
 }  // extern "C"
 
-namespace {
+namespace miconv {
 
 // conv2d_fwd_ex / conv2d_fwd_ws: one dense call with an optional residual and
 // output image stride, planned for `mode`.
@@ -479,7 +479,7 @@ int resolve_ex(int mode, int N, int C, int H, int W, int K, int R, int S, int st
     return rc;
 }
 
-}  // namespace
+}  // namespace miconv
 
 extern "C" {
 

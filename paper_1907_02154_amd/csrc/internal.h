@@ -242,6 +242,14 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
 // resolve() for tensors at 256-byte boundaries (w may be null: a stand-in).
 int resolve_aligned(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
                     int dtype, int algo, int mode, const void *w, Resolved *out);
+// One dense call with an optional residual and output image stride (dtype 0
+// fp32, 1 bf16), planned for `mode`.
+int resolve_ex(int mode, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+               int groups, int dtype, int algo, const void *x, const void *w, const float *bias,
+               const float *res, float *y, long y_image_stride, int relu, Resolved *r);
+// Enqueue r on a workspace of ws_bytes bytes, 256-byte aligned (ws may be null
+// when workspace_bytes(r) is 0); returns a miconv_status.
+int run(const Resolved &r, void *ws, size_t ws_bytes, hipStream_t st);
 // Adds a residual [N][K][P][Q] (read at y's indices, before the activation) to
 // a resolved dense layer; nullptr leaves it unchanged.
 int set_residual(Resolved &r, const float *res);

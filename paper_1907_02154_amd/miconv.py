@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.conv2d_workspace_bytes.restype = l
         L.conv2d_fwd_ws.argtypes = [i] * 12 + [p, p, p, p, p, l, i, p, ctypes.c_size_t, p]
         L.conv2d_fwd_ws.restype = i
+        L.conv2d_fwd_noalloc.argtypes = [i] * 12 + [p, p, p, p, p, l, i, p]
+        L.conv2d_fwd_noalloc.restype = i
         L.conv2d_describe.restype = i
         L.miconv_stack_create.argtypes = [p, i, ctypes.POINTER(p)]
         L.miconv_stack_size.argtypes = [p]
@@ -303,6 +305,37 @@ def conv2d_fwd_ws(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None
                              _ptr(bias), _ptr(res), _ptr(y), ys, 1 if relu else 0, _ptr(ws),
                              0 if ws is None else ws.numel(), _stream(stream))
     _check(rc, "conv2d_fwd_ws")
+    return y
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20   # MICONV_NOALLOC_SCRATCH_BYTES
+
+
+def conv2d_fwd_noalloc(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None, algo=ALGO_AUTO,
+                       stream=None):
+    """conv2d_fwd_ws on the library's fixed per-GPU scratch (nothing is
+    allocated by anyone); plans needing more than NOALLOC_SCRATCH_BYTES fail
+    with ERR_WORKSPACE.  Calls that may overlap on one GPU race on the scratch."""
+    xdt = torch.bfloat16 if x.dtype == torch.bfloat16 else torch.float32
+    _dev(x, xdt, "x", 4)
+    _dev(w, xdt, "w", 4)
+    if bias is not None:
+        _dev(bias, torch.float32, "bias", 1)
+    ys = _image_strided(y, "y")
+    if res is not None:
+        if _image_strided(res, "res") != ys or tuple(res.shape) != tuple(y.shape):
+            raise ValueError("res must have y's shape and strides")
+    N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if groups <= 0 or Cg * groups != C:
+        raise ValueError("w.shape[1] * groups must equal C")
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, K, P, Q):
+        raise ValueError(f"y must have shape {(N, K, P, Q)}, got {tuple(y.shape)}")
+    rc = lib().conv2d_fwd_noalloc(N, C, H, W, K, R, S, stride, pad, groups,
+                                  1 if xdt == torch.bfloat16 else 0, int(algo), _ptr(x), _ptr(w),
+                                  _ptr(bias), _ptr(res), _ptr(y), ys, 1 if relu else 0, _stream(stream))
+    _check(rc, "conv2d_fwd_noalloc")
     return y
 
 

@@ -223,3 +223,15 @@ def test_no_allocation_or_sync_on_the_call_path():
                 assert not pat.search(seg), fn
         else:
             assert not hits, (path, hits)
+
+
+def test_noalloc_rejects_plans_beyond_its_scratch(L):
+    """conv2d_fwd_noalloc refuses, before any launch, a plan whose scratch
+    exceeds the library's fixed per-GPU array (a bf16 3x3 layer at batch 128
+    on 56 x 56 planes stages a 51 MB channel-last copy)."""
+    shape = (128, 64, 56, 56, 64, 3, 3, 1, 1, 1)
+    assert L.conv2d_workspace_bytes(*shape, 1, 0) > miconv.NOALLOC_SCRATCH_BYTES
+    A = miconv.ALGO_AUTO
+    assert L.conv2d_fwd_noalloc(*shape, 1, A, FAKE, FAKE, None, None, FAKE, 0, 0, None) == \
+        miconv.ERR_WORKSPACE
+    assert L.conv2d_fwd_noalloc(*shape, 1, A, None, FAKE, None, None, FAKE, 0, 0, None) == miconv.ERR_NULL
