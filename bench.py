@@ -16,7 +16,10 @@ Prints one JSON line with the conv TFLOP/s of the step (from the timed
 region), ms per image, the roofline of the dominant kernel (the kernel with
 the largest summed execution time; its traffic comes from the committed
 counter summary profiles/traffic.txt when that matches the kernel's source)
-and the CPU oracle timed on a bounded sample of the same stack.
+and the CPU oracle timed on a bounded sample of the same stack.  The default
+run (ResNet-50 at batch 1) also carries, under "b64", the same record for
+ResNet-50 at batch 64 with bf16 inputs (the metric's other half), and under
+"single_call" the single-layer configuration timed through each entry point.
 """
 from __future__ import annotations
 
@@ -108,6 +111,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget for the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--layers", action="store_true", help="also print a per-layer table to stderr")
+    ap.add_argument("--no-b64", action="store_true",
+                    help="with the default --config 2: skip the nested batch-64 bf16 record (config 5)")
     ap.add_argument("--profile-passes", type=int, default=0, metavar="N",
                     help="instead: run N eager passes of the stack and exit (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -312,45 +317,24 @@ def dw_sweep(args):
     print(json.dumps(out), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
-              "(there is no multi-GPU path)", file=sys.stderr)
-        sys.exit(2)
-    if args.dw_sweep:
-        dw_sweep(args)
-        return
-    if args.residual_join:
-        residual_join(args)
-        return
-    if args.copy_calibration:
-        import torch
-        torch.cuda.set_device(0)
-        src = torch.zeros(64 << 20, device="cuda")     # 256 MiB of fp32
-        dst = torch.empty_like(src)
-        for _ in range(4):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print("copy calibration: 4 copies of 268435456 bytes", flush=True)
-        return
-
+def stack_record(args, config: int, batch, steps: int, warmup: int, cpu_seconds: float,
+                 table: bool) -> dict:
+    """Time one configuration's conv stack: resident tensors for every layer,
+    `warmup` eager passes, then the timed region (one HIP graph of `steps`
+    passes, replayed once untimed and once timed), then `steps` eager passes
+    whose kernels carry runtime start/end stamps (per-kernel durations for the
+    roofline).  Returns the record printed as JSON."""
     import torch
     from paper_1907_02154_amd import miconv
     from paper_1907_02154_amd import workloads as wl
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    torch.cuda.set_device(0)
-    miconv.lib()
-    wk = wl.workload(args.config, args.batch)
+    wk = wl.workload(config, batch)
     bf16 = wk.dtype == "bf16"
 
     # Resident inputs, weights, biases and outputs for every layer.
     layers = []
     for i, l in enumerate(wk.layers):
-        x, w, b = wl.layer_tensors(args.config, i, l)
+        x, w, b = wl.layer_tensors(config, i, l)
         P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
         if bf16:
             tx = torch.from_numpy(wl.to_bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
@@ -372,7 +356,7 @@ def main():
         l = d["layer"]
         op = miconv.OP_CONV_BF16 if bf16 else (miconv.OP_DWCONV_F32 if l.kind == "dw" else miconv.OP_CONV_F32)
         ops.append((op, d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu))
-    stack = miconv.Stack(ops)          # plans every layer; packs 3x3 filters once (KRSC)
+    stack = miconv.Stack(ops)          # plans every layer; packs filters once
     for j, d in enumerate(layers):
         d["kernel"] = stack.describe(j)
     n_launch = stack.launches
@@ -384,14 +368,14 @@ def main():
             stack.launch(stream)
         torch.cuda.synchronize()
         print(f"{args.profile_passes} eager passes of {wk.name}", flush=True)
-        return
-    for _ in range(args.warmup):          # eager passes: planning, workspace, caches
+        sys.exit(0)
+    for _ in range(warmup):               # eager passes: caches, instruction caches
         stack.launch(stream)
     torch.cuda.synchronize()
 
     # The timed region: one HIP graph holding exactly K passes, replayed once
     # untimed (first replay of a fresh graph) and once timed.
-    K = args.steps
+    K = steps
     stack.capture(K, timed=False, stream=stream)
     stack.replay(stream)
     torch.cuda.synchronize()
@@ -465,17 +449,19 @@ def main():
                     frac=round(achieved / peak, 4))
     roof.update(traffic=measured_traffic(dom_name),
                 algorithmic_bytes_per_launch=round(dom["bytes"] / dom["launches"]),
+                algorithmic_flops_per_launch=round(dom["flops"] / dom["launches"]),
                 kernel=dom_name, launches_per_step=dom["launches"],
                 avg_launch_us=round(avg_launch_us, 3),
                 share_of_step=round(dom["ms"] / float(launch_ms.sum()), 4))
 
     # Stack-wide fraction of roofline: sum over layers of the time the layer
-    # needs at the binding peak (MFMA or HBM, whichever is slower for it),
-    # over the summed measured layer times.
+    # needs at the binding peak (MFMA or HBM, whichever is slower for it), over
+    # the graph-timed step (and, for reference, over the summed kernel stamps).
     t_roof = sum(max(d["flops"] / (peak * 1e12), d["bytes"] / (PEAK_HBM_GBS * 1e9)) for d in layers)
-    stack_roof_frac = t_roof / (float(layer_ms.sum()) * 1e-3)
+    stack_roof_frac = t_roof / (ms_per_step * 1e-3)
+    stack_roof_frac_kernels = t_roof / (float(layer_ms.sum()) * 1e-3)
 
-    if args.layers:
+    if table:
         # per layer: mean over the K passes (the launch parts), and the median,
         # 10th and 90th percentile of the layer's per-pass time
         parts = [[] for _ in layers]
@@ -495,7 +481,7 @@ def main():
 
     # CPU baseline: the oracle on a bounded prefix of the same layers.
     cpu = None
-    if args.cpu_seconds > 0:
+    if cpu_seconds > 0:
         import oracle
         done_flops, t_cpu, sample = 0, 0.0, []
         for d in layers:
@@ -512,37 +498,145 @@ def main():
             t_cpu += time.perf_counter() - t0
             done_flops += d["flops"]
             sample.append(l.name)
-            if t_cpu > args.cpu_seconds:
+            if t_cpu > cpu_seconds:
                 break
         cpu = dict(value=round(done_flops / t_cpu / 1e12, 6), unit="TFLOP/s",
                    cores=oracle.num_threads(), cpu=cpu_model(), kind="oracle",
                    sample=f"{len(sample)} of {len(layers)} layers ({sample[0]}..{sample[-1]}), "
                           f"{done_flops / 1e9:.3f} GFLOP in {t_cpu:.2f} s, fp64 accumulation")
 
-    out = {
-        "metric": "conv TFLOP/s and ms/image (ResNet-50 convs, b=1 & b=64); % MFMA/HBM peak",
+    rec = {
         "value": round(tflops, 4),
         "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup + K,
         "ms_per_step": round(ms_per_step, 5),
         "ms_per_image": round(ms_per_step / wk.layers[0].N, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
         "dtype": "bf16-in/f32-acc" if bf16 else "f32",
-        "data": "synthetic (seeded uniform/He-normal per layer, resident in HBM)",
         "config": {"workload": wk.name, "convs": len(layers), "batch": wk.layers[0].N,
-                   "gflop_per_step": round(step_flops / 1e9, 4), "device": gpu_info(torch),
+                   "gflop_per_step": round(step_flops / 1e9, 4),
                    "wall_s_timed": round(wall, 4),
                    "timing": "value: one HIP graph of K passes between two events; roofline: kernel "
                              "execution times stamped by the runtime on K eager passes",
+                   "launches_per_step": n_launch,
                    "kernel_ms_per_step": round(float(launch_ms.sum()), 5),
-                   "stack_roofline_frac": round(stack_roof_frac, 4)},
+                   "stack_roofline_frac": round(stack_roof_frac, 4),
+                   "stack_roofline_frac_kernel_stamps": round(stack_roof_frac_kernels, 4)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if bf16 and wk.layers[0].N >= 32:
+        # the compute-bound 3x3 layers of stages 3-5: fraction of bf16 MFMA peak
+        # per layer, copies and split reductions of the layer included
+        per = []
+        for j, d in enumerate(layers):
+            l = d["layer"]
+            if l.R == 3 and l.name[:2] in ("s3", "s4", "s5"):
+                t = float(layer_ms[j]) * 1e-3
+                per.append(dict(layer=l.name, us=round(t * 1e6, 2),
+                                mfma_frac=round(d["flops"] / t / 1e12 / peak, 4)))
+        rec["mfma_frac_3x3_s3_s5"] = per
+    return rec
+
+
+def single_call_times(steps: int) -> dict:
+    """The single-layer configuration (conv 64 -> 64 3x3 at 56 x 56, batch 1,
+    fp32) through each entry point, every variant timed as a HIP graph of
+    `steps` calls: conv2d_fwd (no workspace, filters as given),
+    conv2d_fwd_ws (caller workspace), conv2d_fwd_packed (filters packed once)
+    and a one-layer stack."""
+    import torch
+    from paper_1907_02154_amd import miconv
+    from paper_1907_02154_amd import workloads as wl
+
+    l = wl.workload(1).layers[0]
+    x, w, b = wl.layer_tensors(1, 0, l)
+    tx, tw, tb = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(), torch.from_numpy(b).cuda()
+    P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+    y = torch.empty((l.N, l.K, P, Q), device="cuda")
+    ws = miconv.workspace(miconv.conv2d_workspace_bytes(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad))
+    pk = miconv.PackedFilters(tw, tuple(tx.shape), l.stride, l.pad)
+    st = miconv.Stack([(miconv.OP_CONV_F32, tx, tw, tb, y, l.stride, l.pad, 1, l.relu)])
+    stream = torch.cuda.current_stream()
+    fns = {
+        "conv2d_fwd": lambda s: miconv.conv2d_fwd(tx, tw, tb, y, l.stride, l.pad, 1, l.relu, stream=s),
+        "conv2d_fwd_ws": lambda s: miconv.conv2d_fwd_ws(tx, tw, tb, y, l.stride, l.pad, 1, l.relu, ws=ws,
+                                                        stream=s),
+        "conv2d_fwd_packed": lambda s: pk.forward(tx, tb, y, l.relu, stream=s),
+        "stack": lambda s: st.launch(s),
+    }
+    out = {}
+    for name, fn in fns.items():
+        for _ in range(5):
+            fn(stream)
+        torch.cuda.synchronize()
+        out[name + "_us"] = round(_graph_ms(torch, fn, steps, stream) * 1e3, 3)
+    st.close()
+    fl = wl.flops(l, P, Q)
+    out["workload"] = "conv 64->64 3x3 @56x56 b1 fp32 (231.2 MFLOP)"
+    out["kernels"] = {m: miconv.conv2d_describe(l.N, l.C, l.H, l.W, l.K, l.R, l.S, l.stride, l.pad,
+                                                mode=m)[0] for m in ("plain", "ws", "packed", "stack")}
+    out["tflops_stack"] = round(fl / (out["stack_us"] * 1e-6) / 1e12, 3)
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
+              "(there is no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+    if args.dw_sweep:
+        dw_sweep(args)
+        return
+    if args.residual_join:
+        residual_join(args)
+        return
+    if args.copy_calibration:
+        import torch
+        torch.cuda.set_device(0)
+        src = torch.zeros(64 << 20, device="cuda")     # 256 MiB of fp32
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print("copy calibration: 4 copies of 268435456 bytes", flush=True)
+        return
+
+    import torch
+    from paper_1907_02154_amd import miconv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    miconv.lib()
+
+    rec = stack_record(args, args.config, args.batch, args.steps, args.warmup, args.cpu_seconds, args.layers)
+    out = {
+        "metric": "conv TFLOP/s and ms/image (ResNet-50 convs, b=1 & b=64); % MFMA/HBM peak",
+        "value": rec["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": rec["ms_per_step"],
+        "ms_per_image": rec["ms_per_image"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": rec["dtype"],
+        "data": "synthetic (seeded uniform/He-normal per layer, resident in HBM)",
+        "config": dict(rec["config"], device=gpu_info(torch)),
+        "roofline": rec["roofline"],
+        "cpu_baseline": rec["cpu_baseline"],
+    }
+    if "mfma_frac_3x3_s3_s5" in rec:
+        out["mfma_frac_3x3_s3_s5"] = rec["mfma_frac_3x3_s3_s5"]
+    if args.config == 2 and args.batch is None and not args.no_b64:
+        # the metric's batch-64 half: ResNet-50 at batch 64, bf16 inputs, fp32
+        # accumulation and outputs, timed the same way (its own warm-up, K passes)
+        out["b64"] = stack_record(args, 5, None, args.steps, args.warmup, min(args.cpu_seconds, 15.0), False)
+    if args.config in (1, 2) and args.batch is None:
+        out["single_call"] = single_call_times(args.steps)
     print(json.dumps(out), flush=True)
 
 

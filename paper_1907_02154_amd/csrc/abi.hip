@@ -227,6 +227,12 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
             // filters packed ahead in the wavefront load order, else read as given
             r.wplan.kc = !(mode & MODE_PREPACK);
             r.wlayout = r.wplan.kc ? WL_GIVEN : WL_WAVE;
+            // Read as given, a filter row holds its taps in (c, r, s) order:
+            // reducing in that order makes a half-block's 4 taps one 16-byte
+            // load (the (r, s, c) order would take four 4-byte loads R*S
+            // floats apart), for one padding test per tap on the pixel side.
+            if (r.wplan.kc && r.wplan.order == 1 && R * S > 1 && r.p.Kred % 4 == 0 && (uintptr_t)w % 16 == 0)
+                r.wplan.order = 0;
         }
     } else {
         return MICONV_ERR_UNSUPPORTED;

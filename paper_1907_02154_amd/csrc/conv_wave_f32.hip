@@ -403,7 +403,7 @@ template <int R_, int S_, int WAVES, int BJ, int ORD, bool IND = false>
 void launch_wave(const ConvArgs &a, int kc, dim3 grid, hipStream_t st)
 {
     if (kc == 1) {
-        if constexpr (ORD == 1 && R_ == 1 && S_ == 1 && !IND)
+        if constexpr ((ORD == 0 || (ORD == 1 && R_ == 1 && S_ == 1)) && !IND)
             launch_kernel((igemm_wave_f32_kcrs_kernel<R_, S_, WAVES, BJ, ORD, IND, 1>), grid, dim3(64 * WAVES), 0,
                           st, a);
     } else if (kc == 2) {
@@ -438,6 +438,14 @@ void launch_rs(const ConvArgs &a, int waves, int bj, bool ind, int kc, dim3 grid
 int rs_template(int v) { return (v == 1 || v == 3 || v == 7) ? v : 0; }
 
 }  // namespace
+
+// Filters read as given: the 4 taps of a half-block are consecutive in a
+// filter row, and 16-byte aligned, in the (c, r, s) order and for 1x1 layers.
+bool wave_kc_vector(const ConvProblem &p, const WavePlan &plan, const void *w)
+{
+    const bool contiguous = plan.order == 0 || (plan.order == 1 && p.R == 1 && p.S == 1);
+    return contiguous && !plan.ind && p.Kred % 4 == 0 && (uintptr_t)w % 16 == 0;
+}
 
 bool wave_fits(const ConvProblem &p)
 {
@@ -505,12 +513,13 @@ void describe_wave_f32(const ConvProblem &p, const WavePlan &plan, char *buf, in
 {
     int R = rs_template(p.R), S = rs_template(p.S);
     if (R == 0 || S == 0 || R != S) R = S = 0;
-    if (plan.order == 1 && R != 3 && R != 1) R = S = 0;
+    if ((plan.order == 0 || plan.order == 1) && R != 3 && R != 1) R = S = 0;
     if (plan.order == 2 && R != 3 && R != 7) R = S = 0;
     const bool gen = p.res || p.ysn != (long)p.K * p.P * p.Q;
     if (plan.kc) {
         // the 16-byte filter loads need w 16-byte aligned: named as for an aligned w
-        const int kc = plan.order == 1 && p.R == 1 && p.S == 1 && !plan.ind ? 1 : 2;
+        alignas(16) static const float stand_in[4] = {};
+        const int kc = wave_kc_vector(p, plan, stand_in) ? 1 : 2;
         snprintf(buf, len, "igemm_wave_f32_kcrs_kernel<%d, %d, %d, %d, %d, %s, %d>%s", R, S, plan.waves,
                  plan.bj, plan.order, plan.ind ? "true" : "false", kc,
                  plan.splits > 1 ? " + splitk_reduce_kernel" : "");
@@ -528,8 +537,7 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
 {
     // filters as given: one 16-byte load per half-block where the 4 taps are
     // consecutive and aligned (1x1, C/groups % 8 == 0), else four 4-byte loads
-    const int kc = !plan.kc ? 0
-                   : plan.order == 1 && p.R == 1 && p.S == 1 && !plan.ind && (uintptr_t)w % 16 == 0 ? 1 : 2;
+    const int kc = !plan.kc ? 0 : wave_kc_vector(p, plan, w) ? 1 : 2;
     ConvArgs a = make_args(p);
     a.x = x;
     a.w = w;
@@ -565,6 +573,8 @@ hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const flo
             launch_rs<0, 0, 2>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     } else if (p.R == 1 && p.S == 1) {
         launch_rs<1, 1, 0>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
+    } else if (p.R == 3 && p.S == 3) {
+        launch_rs<3, 3, 0>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     } else {
         launch_rs<0, 0, 0>(a, plan.waves, plan.bj, plan.ind, kc, grid, st);
     }

@@ -131,6 +131,8 @@ struct WavePlan {
 // The wave kernel addresses x and its packed filters with 32-bit offsets.
 bool wave_fits(const ConvProblem &p);
 WavePlan plan_wave_f32(const ConvProblem &p, int num_cus, int max_splits);
+// The kernel reading w as given loads a half-block's 4 taps as one 16-byte load.
+bool wave_kc_vector(const ConvProblem &p, const WavePlan &plan, const void *w);
 hipError_t launch_wave_f32(const ConvProblem &p, const WavePlan &plan, const float *x,
                            const float *w, const float *bias, float *y, float *ws,
                            hipStream_t st, const LaunchHook *hook = nullptr);

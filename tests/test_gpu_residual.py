@@ -36,7 +36,7 @@ def dev_bf16_bits(bits):
 
 # (N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, kernel conv2d_fwd_ws must use)
 RES_CASES = [
-    (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 1, false, 2>"),
+    (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 0, false, 1>"),
     (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<1, 1, 8, 1, 1, false, 1>"),
     (1, 512, 8, 8, 96, 3, 3, 1, 1, 1, "f32", A, "splitk_reduce_kernel"),        # 16-byte reduce
     (1, 1024, 7, 7, 40, 3, 3, 1, 1, 1, "f32", A, "splitk_reduce_kernel"),       # scalar reduce
@@ -245,7 +245,7 @@ VEC_Y_CASES = [c for c in RES_CASES if c[-1] in (
     "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>",
     "igemm_bf16_halo_kernel<128, 64, 2, 2, 256, 1>",
     "igemm_bf16_halo_kernel<128, 128, 2, 2, 192, 2>",
-    "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 1, false, 2>")]
+    "igemm_wave_f32_kcrs_kernel<3, 3, 8, 1, 0, false, 1>")]
 
 
 @pytest.mark.parametrize("case", VEC_Y_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
