@@ -17,4 +17,6 @@ from .ref import (  # noqa: F401
     add_act,
     f32_to_bf16,
     bf16_to_f32,
+    conv2d_bf16_cl,
+    maxpool2d_bf16_cl,
 )

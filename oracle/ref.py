@@ -199,3 +199,31 @@ def bf16_to_f32(bits):
     """bf16 bit patterns -> exact fp32 values (bf16 is the upper half of fp32)."""
     bits = _c(bits, np.uint16)
     return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def conv2d_bf16_cl(x_bits, w_bits, bias=None, stride=1, pad=0, groups=1, relu=False, res_bits=None):
+    """One layer of a network whose activations stay bf16 and channel-last
+    between layers (the graph-level layout choice and operator fusion of
+    Sec. 3.2.3): x bf16 bits [N][H][W][C], w bf16 bits [K][C/groups][R][S],
+    bias fp32 [K], res bf16 bits [N][P][Q][K] or None; returns bf16 bits
+    [N][P][Q][K].
+
+    Reading: the layer's value is the definition above, act(conv + bias +
+    res) summed in fp64 and rounded once to fp32 (conv2d_bf16 with the
+    residual widened exactly), then rounded to bf16, nearest even
+    (f32_to_bf16).  The layout change is a transpose, no arithmetic."""
+    x = np.ascontiguousarray(np.transpose(_c(x_bits, np.uint16), (0, 3, 1, 2)))
+    res = None
+    if res_bits is not None:
+        res = bf16_to_f32(np.ascontiguousarray(np.transpose(_c(res_bits, np.uint16), (0, 3, 1, 2))))
+    y = conv2d_bf16(x, w_bits, bias, stride, pad, groups, relu, res=res)
+    return f32_to_bf16(np.ascontiguousarray(np.transpose(y, (0, 2, 3, 1))))
+
+
+def maxpool2d_bf16_cl(x_bits, R, S, stride, pad=0):
+    """Max-pool of bf16 channel-last bits [N][H][W][C] -> [N][P][Q][C]: the
+    maxima of the exactly widened values are input values, so they convert
+    back to bf16 without rounding."""
+    x = bf16_to_f32(np.ascontiguousarray(np.transpose(_c(x_bits, np.uint16), (0, 3, 1, 2))))
+    y = maxpool2d(x, R, S, stride, pad)
+    return f32_to_bf16(np.ascontiguousarray(np.transpose(y, (0, 2, 3, 1))))

@@ -338,3 +338,64 @@ def test_residual_small_integers_exact(oracle_lib):
                                   oracle_lib.conv2d(x, w, b, 2, 1, 2, True))
     with pytest.raises(ValueError):
         oracle_lib.conv2d(x, w, b, 2, 1, 2, res=res[:, :2])
+
+
+# ---- channel-last bf16 layers (conv2d_bf16_cl, maxpool2d_bf16_cl) ----
+
+def _bits(t):
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def test_channel_last_layer_against_torch(oracle_lib):
+    """conv2d_bf16_cl against torch: float64 conv2d of the exactly widened
+    bf16 values, plus bias and the widened bf16 residual, activation, then
+    torch's cast to float32 and to bfloat16, in channel-last order.  Over 120
+    random tiny shapes (groups, strides, padding) every output bit agrees."""
+    rng = np.random.default_rng(11)
+    for case in range(120):
+        N = int(rng.integers(1, 3))
+        g = int(rng.choice([1, 2]))
+        Cg, Kg = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        C, K = Cg * g, Kg * g
+        R, S = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        H, W = int(rng.integers(R, 8)), int(rng.integers(S, 8))
+        st, pad = int(rng.integers(1, 3)), int(rng.integers(0, 2))
+        torch.manual_seed(1100 + case)
+        xb = torch.randn(N, H, W, C).to(torch.bfloat16)
+        wb = torch.randn(K, Cg, R, S).to(torch.bfloat16)
+        b = torch.randn(K) * 0.1
+        P, Q = oracle_lib.out_dims(H, W, R, S, st, pad)
+        rb = torch.randn(N, P, Q, K).to(torch.bfloat16) if case % 2 else None
+        relu = bool(case % 3)
+        ref = F.conv2d(xb.permute(0, 3, 1, 2).double(), wb.double(), b.double(), st, pad, 1, g)
+        if rb is not None:
+            ref = ref + rb.permute(0, 3, 1, 2).double()
+        if relu:
+            ref = ref.clamp_min(0)
+        want = _bits(ref.float().to(torch.bfloat16).permute(0, 2, 3, 1))
+        got = oracle_lib.conv2d_bf16_cl(_bits(xb), _bits(wb), b.numpy(), st, pad, g, relu,
+                                        None if rb is None else _bits(rb))
+        np.testing.assert_array_equal(got, want, err_msg=f"case {case}")
+
+
+def test_channel_last_layer_rounds_through_fp32(oracle_lib):
+    """The reading fixed for a bf16 output: the fp64 sum is rounded to fp32
+    first, then to bf16.  x = (1, 2^-8, 2^-30), w = 1 (a 1x1 conv over three
+    channels) sums to 1 + 2^-8 + 2^-30; fp32 drops the 2^-30, leaving
+    1 + 2^-8, exactly half a bf16 step above 1, which ties to even: 1.0 (bits
+    0x3F80).  Rounding the fp64 sum straight to bf16 would give 1.0078125."""
+    x = torch.tensor([1.0, 2.0 ** -8, 2.0 ** -30]).to(torch.bfloat16).view(1, 1, 1, 3)
+    w = torch.ones(1, 3, 1, 1).to(torch.bfloat16)
+    got = oracle_lib.conv2d_bf16_cl(_bits(x), _bits(w))
+    assert got.shape == (1, 1, 1, 1) and int(got[0, 0, 0, 0]) == 0x3F80
+
+
+def test_channel_last_maxpool_against_torch(oracle_lib):
+    """maxpool2d_bf16_cl equals torch's max_pool2d of the bf16 values in
+    channel-last order, bit for bit (a maximum is one of the inputs)."""
+    torch.manual_seed(12)
+    for R, st, pad in ((3, 2, 1), (2, 2, 0), (3, 1, 1)):
+        xb = torch.randn(2, 9, 11, 16).to(torch.bfloat16)
+        want = F.max_pool2d(xb.permute(0, 3, 1, 2).float(), R, st, pad).to(torch.bfloat16)
+        got = oracle_lib.maxpool2d_bf16_cl(_bits(xb), R, R, st, pad)
+        np.testing.assert_array_equal(got, _bits(want.permute(0, 2, 3, 1)))
