@@ -226,7 +226,49 @@ int conv2d_fwd_packed(int N, int C, int H, int W, int K, int R, int S, int strid
                       int groups, int dtype, const void *x, const void *packed, const float *bias,
                       float *y, int relu, void *stream);
 
+/* ---- Channel-last bf16 activations between layers ----
+ *
+ * The paper's graph tuner chooses each operator's data layout for the whole
+ * network and its fusion merges element-wise work into the conv (Sec. 3.2.3).
+ * Here that is a bf16 channel-last activation layout kept from layer to
+ * layer: a layer reads the previous layer's bf16 [N][H][W][C] output as given
+ * (no transposing copy) and its epilogue writes its own output as bf16
+ * [N][P][Q][K], bias, residual join and ReLU applied in fp32 before one
+ * round-to-nearest-even to bf16: half the output bytes of fp32 NCHW. */
+enum miconv_layout {
+    MICONV_LAYOUT_NCHW = 0,          /* x bf16 NCHW, y fp32 NCHW: conv2d_fwd_bf16 */
+    MICONV_LAYOUT_X_NHWC = 1,        /* x bf16 [N][H][W][C] */
+    MICONV_LAYOUT_Y_NHWC_BF16 = 2    /* y (and res) bf16 [N][P][Q][K] */
+};
+
+/* bf16 conv2d with channel-last x and/or y (enum miconv_layout flags, or-ed):
+ *   y = act(conv(x, w) + bias + res),  summed in fp32; with
+ *   MICONV_LAYOUT_Y_NHWC_BF16 the result is rounded once to bf16 (nearest
+ *   even) and res, when given, is bf16 [N][P][Q][K] like y.
+ * w bf16 [K][C/groups][R][S] and bias fp32 [K] as everywhere.  Supported:
+ *  - MICONV_LAYOUT_X_NHWC (with or without a channel-last y): C/groups % 64
+ *    == 0, x 16-byte aligned (and w for 1x1 filters); with a channel-last y
+ *    K/groups % 8 == 0 and y, res 16-byte aligned;
+ *  - MICONV_LAYOUT_Y_NHWC_BF16 alone (x NCHW): the 7x7 stride-2 stem on at
+ *    most 4 channels with 112 output columns (ResNet's first layer), K % 4
+ *    == 0, no residual;
+ * anything else MICONV_ERR_UNSUPPORTED (MICONV_ERR_ALIGN for alignment).
+ * Workspace as for conv2d_fwd_ws, sized by conv2d_cl_workspace_bytes (split
+ * partials and per-call packed filters; never a copy of x). */
+long conv2d_cl_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                               int groups, int layout);
+int conv2d_fwd_cl(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                  int layout, const uint16_t *x, const uint16_t *w, const float *bias, const void *res,
+                  void *y, int relu, void *ws, size_t ws_bytes, void *stream);
+
 /* Glue operators of the evaluated networks (not part of the conv operator). */
+
+/* Max-pool on bf16 channel-last tensors: x [N][H][W][C] -> y [N][P][Q][C],
+ * R x S window, stride, symmetric pad (pad < R and pad < S); padded positions
+ * never win, so y holds input values exactly.  C % 8 == 0, x and y 16-byte
+ * aligned. */
+int maxpool2d_nhwc_bf16(int N, int C, int H, int W, int R, int S, int stride, int pad,
+                        const uint16_t *x, uint16_t *y, void *stream);
 
 /* Max-pool fp32 NCHW with an R x S window, stride and symmetric pad
  * (pad < R and pad < S); padded positions never win. y [N][C][P][Q]. */
@@ -251,8 +293,11 @@ int cast_f32_to_bf16(long count, const float *x, uint16_t *y, void *stream);
 
 enum miconv_op {
     MICONV_OP_CONV_F32 = 0,    /* conv2d_fwd */
-    MICONV_OP_CONV_BF16 = 1,   /* conv2d_fwd_bf16 (x, w are bf16 bit patterns) */
-    MICONV_OP_DWCONV_F32 = 2   /* dwconv2d_fwd */
+    MICONV_OP_CONV_BF16 = 1,   /* conv2d_fwd_bf16 (x, w are bf16 bit patterns), or with
+                                  `layout` conv2d_fwd_cl */
+    MICONV_OP_DWCONV_F32 = 2,  /* dwconv2d_fwd */
+    MICONV_OP_MAXPOOL_BF16_NHWC = 3   /* maxpool2d_nhwc_bf16: R x S window, stride, pad; K = C,
+                                         w, bias, res NULL (glue between channel-last layers) */
 };
 
 typedef struct miconv_conv_desc {
@@ -261,10 +306,11 @@ typedef struct miconv_conv_desc {
     const void *x;             /* device, layout as the matching entry point */
     const void *w;
     const float *bias;         /* may be NULL */
-    float *y;
-    const float *res;          /* residual joined before the activation, as in
-                                  conv2d_fwd_res (dense ops only); may be NULL */
+    void *y;                   /* fp32 NCHW, or bf16 channel-last per `layout` */
+    const void *res;           /* residual joined before the activation, as in
+                                  conv2d_fwd_res / conv2d_fwd_cl (dense ops only); may be NULL */
     long y_image_stride;       /* as in conv2d_fwd_ex; 0 = dense y */
+    int layout;                /* MICONV_OP_CONV_BF16: enum miconv_layout flags, as in conv2d_fwd_cl */
 } miconv_conv_desc;
 
 typedef struct miconv_stack miconv_stack;

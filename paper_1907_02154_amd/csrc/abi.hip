@@ -48,6 +48,7 @@ ConvArgs make_args(const ConvProblem &p)
     a.relu = p.relu;
     a.res = p.res;
     a.ysn = p.ysn;
+    a.ycl = p.ycl;
     a.dv_pq = make_fastdiv(p.P * p.Q);
     a.dv_q = make_fastdiv(p.Q);
     return a;
@@ -140,10 +141,47 @@ int set_hip_error(hipError_t e) { return hip_fail(e); }
 // the call may use besides its tensors (enum PlanMode): without a workspace
 // there is no split reduction, no channel-last copy and no per-call filter
 // packing, and filters are read as given unless they were packed ahead.
+// Max-pool over bf16 channel-last tensors, as a stack layer (K = C, no filters).
+static int resolve_pool(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                        const void *x, float *y, Resolved *out)
+{
+    if (!x || !y) return MICONV_ERR_NULL;
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || R <= 0 || S <= 0 || stride < 1 || pad < 0 || pad >= R ||
+        pad >= S)
+        return MICONV_ERR_SHAPE;
+    if (K != C) return MICONV_ERR_GROUPS;
+    if (C % 8) return MICONV_ERR_UNSUPPORTED;
+    const long P = extent(H, R, stride, pad), Q = extent(W, S, stride, pad);
+    if (P < 1 || Q < 1) return MICONV_ERR_SHAPE;
+    if ((long)N * C * H * W > INT_MAX || (long)N * C * P * Q > INT_MAX) return MICONV_ERR_TOO_LARGE;
+    if ((uintptr_t)x % 16 || (uintptr_t)y % 16) return MICONV_ERR_ALIGN;
+    Resolved r{};
+    r.kind = OP_MAXPOOL_BF16_NHWC;
+    r.impl = IMPL_POOL_NHWC;
+    r.p.N = N;
+    r.p.C = C;
+    r.p.H = H;
+    r.p.W = W;
+    r.p.K = K;
+    r.p.R = R;
+    r.p.S = S;
+    r.p.stride = stride;
+    r.p.pad = pad;
+    r.p.groups = 1;
+    r.p.P = (int)P;
+    r.p.Q = (int)Q;
+    r.p.xcl = r.p.ycl = 1;
+    r.x = x;
+    r.y = y;
+    *out = r;
+    return MICONV_OK;
+}
+
 int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int R, int S, int stride,
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
-            int relu, Resolved *out)
+            int relu, Resolved *out, int layout)
 {
+    if (kind == OP_MAXPOOL_BF16_NHWC) return resolve_pool(N, C, H, W, K, R, S, stride, pad, x, y, out);
     Resolved r{};
     const size_t elem = kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, elem, &r.p);
@@ -162,6 +200,34 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
     r.bias = bias;
     r.y = y;
     const bool depthwise = groups > 1 && groups == C && K == C;
+    if (layout & ~(LAYOUT_X_NHWC | LAYOUT_Y_NHWC_BF16)) return MICONV_ERR_UNSUPPORTED;
+    if (layout) {
+        // Channel-last bf16 layers of a channel-last network: x [N][H][W][C]
+        // read as given by the direct-to-LDS kernels, and/or y (and the
+        // residual) bf16 [N][P][Q][K] written by their channel-last epilogue;
+        // x in NCHW with a channel-last y is the 7x7 stem's kernel.
+        if (kind != OP_DENSE_BF16 || algo != MICONV_ALGO_AUTO) return MICONV_ERR_UNSUPPORTED;
+        r.p.xcl = (layout & LAYOUT_X_NHWC) ? 1 : 0;
+        r.p.ycl = (layout & LAYOUT_Y_NHWC_BF16) ? 1 : 0;
+        if (r.p.ycl && (uintptr_t)y % 16) return MICONV_ERR_ALIGN;
+        if (r.p.xcl) {
+            const bool fits = (long)N * C * H * W * 2 < (1L << 31) && (long)K * r.p.Kred * 2 < (1L << 31);
+            if (r.p.Cg % 64 || !fits || (R * S > 1 && !can_pack)) return MICONV_ERR_UNSUPPORTED;
+            if (r.p.ycl && r.p.Kg % 8) return MICONV_ERR_UNSUPPORTED;
+            if (R * S == 1 && (uintptr_t)w % 16) return MICONV_ERR_ALIGN;
+            if ((uintptr_t)x % 16) return MICONV_ERR_ALIGN;
+            r.impl = IMPL_NHWC_BF16;
+            r.nplan = plan_nhwc_bf16(r.p, cu_count(), x, max_splits, true);
+            r.wlayout = R * S == 1 ? WL_GIVEN : r.nplan.halo ? WL_KRSC_BLOCK : WL_KRSC;
+        } else {
+            if (!r.p.ycl || !can_pack || !stem_bf16_eligible(r.p, y) || K % 4) return MICONV_ERR_UNSUPPORTED;
+            r.impl = IMPL_STEM_BF16;
+            r.wlayout = WL_STEM;
+        }
+        r.pack_per_call = r.wlayout != WL_GIVEN && !(mode & MODE_PREPACK);
+        *out = r;
+        return MICONV_OK;
+    }
     if (kind == OP_DW_F32) {
         if (!depthwise) return MICONV_ERR_GROUPS;
         if (R > 7 || S > 7) return MICONV_ERR_UNSUPPORTED;
@@ -245,6 +311,14 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
 int set_residual(Resolved &r, const float *res)
 {
     if (!res) return MICONV_OK;
+    if (r.impl == IMPL_POOL_NHWC) return MICONV_ERR_UNSUPPORTED;
+    if (r.p.ycl) {
+        // bf16 [N][P][Q][K] like y, read with 16-byte loads; the stem takes none
+        if ((uintptr_t)res % 16) return MICONV_ERR_ALIGN;
+        if (r.impl != IMPL_NHWC_BF16) return MICONV_ERR_UNSUPPORTED;
+        r.p.res = res;
+        return MICONV_OK;
+    }
     // Kernels read it with the same (possibly 16-byte) accesses as they write y.
     if ((uintptr_t)res % sizeof(float) || ((uintptr_t)res - (uintptr_t)r.y) % 16)
         return MICONV_ERR_ALIGN;
@@ -257,6 +331,7 @@ int set_output_stride(Resolved &r, long ysn)
 {
     const long dense = (long)r.p.K * r.p.P * r.p.Q;
     if (ysn == 0 || ysn == dense) return MICONV_OK;
+    if (r.p.ycl || r.impl == IMPL_POOL_NHWC) return MICONV_ERR_UNSUPPORTED;   // channel-last y is dense
     if (ysn < dense) return MICONV_ERR_SHAPE;                  // images would overlap
     if ((long)(r.p.N - 1) * ysn + dense > INT_MAX) return MICONV_ERR_TOO_LARGE;
     if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
@@ -350,6 +425,10 @@ hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHo
     }
     switch (r.impl) {
     case IMPL_DW: return launch_dwconv_f32(r.p, xf, wf, r.bias, r.y, st);
+    case IMPL_POOL_NHWC:
+        return launch_maxpool_nhwc_bf16(r.p.N, r.p.C, r.p.H, r.p.W, r.p.R, r.p.S, r.p.stride, r.p.pad, r.p.P,
+                                        r.p.Q, static_cast<const uint16_t *>(r.x), reinterpret_cast<uint16_t *>(r.y),
+                                        st);
     default:
         if (r.kind == OP_DENSE_BF16)
             return launch_conv_direct_bf16(r.p, static_cast<const uint16_t *>(r.x),
@@ -395,6 +474,10 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     case IMPL_IGEMM_BF16: describe_igemm_bf16(r.p, r.plan, r.bfast, r.bva, buf, len, launches); break;
     case IMPL_NHWC_BF16: describe_nhwc_bf16(r.p, r.nplan, buf, len, launches); break;
     case IMPL_STEM_BF16: describe_stem_bf16(buf, len, launches); break;
+    case IMPL_POOL_NHWC:
+        snprintf(buf, len, "maxpool_nhwc_bf16_kernel");
+        *launches = 1;
+        break;
     default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;
     }
 }
@@ -539,6 +622,37 @@ int conv2d_fwd_ws(int N, int C, int H, int W, int K, int R, int S, int stride, i
     const int rc = resolve_ex(MODE_SCRATCH, N, C, H, W, K, R, S, stride, pad, groups, dtype, algo, x, w,
                               bias, res, y, y_image_stride, relu, &r);
     return rc != MICONV_OK ? rc : run(r, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+long conv2d_cl_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                               int groups, int layout)
+{
+    if (layout == 0) return conv2d_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups, 1, MICONV_ALGO_AUTO);
+    alignas(256) static const float stand_in[64] = {};
+    Resolved r;
+    const int rc = resolve(OP_DENSE_BF16, MICONV_ALGO_AUTO, MODE_SCRATCH, N, C, H, W, K, R, S, stride, pad,
+                           groups, stand_in, stand_in, nullptr, const_cast<float *>(stand_in), 0, &r, layout);
+    return rc != MICONV_OK ? rc : (long)workspace_bytes(r);
+}
+
+int conv2d_fwd_cl(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                  int layout, const uint16_t *x, const uint16_t *w, const float *bias, const void *res,
+                  void *y, int relu, void *ws, size_t ws_bytes, void *stream)
+{
+    Resolved r;
+    int rc = resolve(OP_DENSE_BF16, MICONV_ALGO_AUTO, MODE_SCRATCH, N, C, H, W, K, R, S, stride, pad, groups,
+                     x, w, bias, static_cast<float *>(y), relu, &r, layout);
+    if (rc == MICONV_OK) rc = set_residual(r, static_cast<const float *>(res));
+    return rc != MICONV_OK ? rc : run(r, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int maxpool2d_nhwc_bf16(int N, int C, int H, int W, int R, int S, int stride, int pad, const uint16_t *x,
+                        uint16_t *y, void *stream)
+{
+    Resolved r;
+    const int rc = resolve(OP_MAXPOOL_BF16_NHWC, MICONV_ALGO_AUTO, MODE_FREE, N, C, H, W, C, R, S, stride, pad,
+                           1, x, nullptr, nullptr, reinterpret_cast<float *>(y), 0, &r);
+    return rc != MICONV_OK ? rc : run_free(r, static_cast<hipStream_t>(stream));
 }
 
 long conv2d_packed_weight_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,

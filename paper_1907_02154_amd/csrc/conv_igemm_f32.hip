@@ -193,6 +193,64 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
 // eight splits before it adds any of them: the launch costs one memory round
 // trip, not one per split.  Partials are read through a buffer resource, so
 // the slots past the last split read as zeros (adding them changes nothing).
+// Channel-last bf16 output: the split partials are [splits][M][K] fp32; a
+// thread sums 8 consecutive channels of one pixel over the splits in split
+// order, adds bias and the bf16 residual (the layout of y), applies the
+// activation, rounds to bf16 and stores 16 bytes.
+__global__ __launch_bounds__(256) void splitk_reduce_cl_kernel(ConvArgs a)
+{
+    const int K8 = a.K / 8;
+    const long units = (long)a.M * K8;
+    const long plane = (long)a.M * a.K;
+    const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
+    uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < units; i += (long)gridDim.x * blockDim.x) {
+        const int o = (int)(i % K8);
+        const long m = i / K8;
+        const long off = m * a.K + 8 * o;
+        float s[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] = 0.f;
+        for (int sp = 0; sp < a.splits; ++sp) {
+            const float4 lo = *reinterpret_cast<const float4 *>(a.ws + sp * plane + off);
+            const float4 hi = *reinterpret_cast<const float4 *>(a.ws + sp * plane + off + 4);
+            s[0] += lo.x;
+            s[1] += lo.y;
+            s[2] += lo.z;
+            s[3] += lo.w;
+            s[4] += hi.x;
+            s[5] += hi.y;
+            s[6] += hi.z;
+            s[7] += hi.w;
+        }
+        uint32_t rr[4] = {0, 0, 0, 0};
+        if (res) {
+            const uint4 r = *reinterpret_cast<const uint4 *>(res + off);
+            rr[0] = r.x;
+            rr[1] = r.y;
+            rr[2] = r.z;
+            rr[3] = r.w;
+        }
+        uint32_t d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int k = 8 * o + 2 * e;
+            float v0 = s[2 * e] + (a.bias ? a.bias[k] : 0.f);
+            float v1 = s[2 * e + 1] + (a.bias ? a.bias[k + 1] : 0.f);
+            if (res) {
+                v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
+                v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
+            }
+            if (a.relu) {
+                v0 = fmaxf(v0, 0.f);
+                v1 = fmaxf(v1, 0.f);
+            }
+            d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+        }
+        *reinterpret_cast<uint4 *>(y + off) = make_uint4(d[0], d[1], d[2], d[3]);
+    }
+}
+
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvArgs a)
 {
     constexpr int kGroup = 8;
@@ -362,6 +420,15 @@ hipError_t launch_igemm_f32(const ConvProblem &p, const IgemmPlan &plan, const f
 
 hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
 {
+    if (a.ycl) {
+        // channel-last bf16 output: partials [splits][M][K], 8 channels per thread
+        const long units = (long)a.M * (a.K / 8);
+        if ((long)a.splits * a.M * a.K * 4 >= (1L << 31) || a.K % 8) return hipErrorInvalidValue;
+        long blocks = (units + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        launch_kernel(splitk_reduce_cl_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);
+        return hipGetLastError();
+    }
     const long total = (long)a.K * a.M;
     // 32-bit offsets, also for the zero-reading slots of the last group of 8
     if ((long)(a.splits + 7) * total * 4 >= (1L << 31)) return hipErrorInvalidValue;

@@ -537,6 +537,88 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 
+// Channel-last bf16 epilogue (layers inside a channel-last network: y and
+// the residual are bf16 [N*P*Q][K]).  In these instantiations the MFMA runs
+// with the filters as its A operand, so accumulator register v of lane l
+// holds channel 8*(v/4) + 4*(l/32) + v%4 of the channel block and pixel l%32
+// of the pixel block: four consecutive channels of one pixel, written to LDS
+// as one 16-byte store into a pixel-major tile [BPX][BKC + 4] fp32 (16 lanes
+// of a store phase cover the 64 banks once).  Each thread then takes 8
+// consecutive channels of one pixel: bias, the bf16 residual, activation,
+// round to bf16 (nearest even), one 16-byte store.  With a reduction split
+// the raw fp32 sums go to this split's partials [M][K] instead (two 16-byte
+// stores) for splitk_reduce_cl_kernel.  Requires K/groups % 8 == 0 and y,
+// res 16-byte aligned (checked on the host).
+template <int BPX, int BKC, int NT, int TPX, int TCH, int BJ, int BI>
+__device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][BI], float *ot, int tid,
+                                   int wpx, int wch, int h, int ll, int k0, int m0, int g, int split)
+{
+    constexpr int CP = BKC + 4;
+    constexpr int C8 = BKC / 8;
+    static_assert(NT % C8 == 0, "a thread keeps one channel octet");
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int kl = wch * TCH + bi * 32 + 8 * q4 + 4 * h;
+                const int pl = wpx * TPX + bj * 32 + ll;
+                *reinterpret_cast<float4 *>(ot + pl * CP + kl) =
+                    make_float4(acc[bj][bi][4 * q4], acc[bj][bi][4 * q4 + 1], acc[bj][bi][4 * q4 + 2],
+                                acc[bj][bi][4 * q4 + 3]);
+            }
+    __syncthreads();
+    const int o = tid % C8;
+    const int k = k0 + 8 * o;
+    if (k >= a.Kg) return;                      // K/groups % 8 == 0: the octet is whole
+    const int kg = g * a.Kg + k;
+    float bv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bv[e] = (a.splits == 1 && a.bias) ? a.bias[kg + e] : 0.f;
+    const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
+    uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
+    for (int pl = tid / C8; pl < BPX; pl += NT / C8) {
+        const int m = m0 + pl;
+        if (m >= a.M) break;
+        const float4 lo = *reinterpret_cast<const float4 *>(ot + pl * CP + 8 * o);
+        const float4 hi = *reinterpret_cast<const float4 *>(ot + pl * CP + 8 * o + 4);
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const long off = (long)m * a.K + kg;
+        if (a.splits > 1) {
+            float *dst = a.ws + (long)split * a.M * a.K + off;
+            *reinterpret_cast<float4 *>(dst) = lo;
+            *reinterpret_cast<float4 *>(dst + 4) = hi;
+            continue;
+        }
+        uint32_t rr[4] = {0, 0, 0, 0};
+        if (res) {
+            const uint4 r = *reinterpret_cast<const uint4 *>(res + off);
+            rr[0] = r.x;
+            rr[1] = r.y;
+            rr[2] = r.z;
+            rr[3] = r.w;
+        }
+        uint32_t d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float v0 = v[2 * e] + bv[2 * e], v1 = v[2 * e + 1] + bv[2 * e + 1];
+            if (res) {
+                v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
+                v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
+            }
+            if (a.relu) {
+                v0 = fmaxf(v0, 0.f);
+                v1 = fmaxf(v1, 0.f);
+            }
+            d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+        }
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 dv = {d[0], d[1], d[2], d[3]};
+        __builtin_nontemporal_store(dv, reinterpret_cast<u32x4 *>(y + off));
+    }
+}
+
 // NCHWB (1x1, stride 1, H*W % 8 == 0, 128-pixel tiles): the pixel operand is
 // read from the NCHW input itself, no channel-last copy.  A chunk's pixel tile
 // is staged as 64 channel rows of 128 pixels (16 units of 8 pixels, unit s of
@@ -552,7 +634,7 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // channel row, each lane fetching the pixel pair its LDS dword holds under
 // the unit permutation.  Same bandwidth per byte through the load path,
 // 4x the instructions.
-template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC, bool RES>
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC, bool RES, bool YCL>
 __device__ __forceinline__ void dma_body(const ConvArgs &a)
 {
     constexpr int NT = 64 * WPX * WCH;
@@ -569,7 +651,8 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
     static_assert(KRC == 64 || KRC == 32, "reduction chunk");
 
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
-    constexpr int SMEM = NST * (UA + UB) > BKC * OP / 4 ? NST * (UA + UB) : BKC * OP / 4;
+    constexpr int EPI = YCL ? BPX * (BKC + 4) / 4 : BKC * OP / 4;   // epilogue tile, 16-byte units
+    constexpr int SMEM = NST * (UA + UB) > EPI ? NST * (UA + UB) : EPI;
     __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];
 
     const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
@@ -767,9 +850,14 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
 #pragma unroll
             for (int bj = 0; bj < BJ; ++bj)
 #pragma unroll
-                for (int bi = 0; bi < BI; ++bi)
-                    acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
-                                                                         acc[bj][bi], 0, 0, 0);
+                for (int bi = 0; bi < BI; ++bi) {
+                    if constexpr (YCL)   // filters as the A operand: a lane holds channels of one pixel
+                        acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[ks][bi], xv[ks][bj],
+                                                                             acc[bj][bi], 0, 0, 0);
+                    else
+                        acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
+                                                                             acc[bj][bi], 0, 0, 0);
+                }
     };
 
     const int nchunks = kr_end > kr_begin ? (kr_end - kr_begin) / KRC : 0;
@@ -787,6 +875,12 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
         compute(t);
     }
 
+    if constexpr (YCL) {
+        __syncthreads();   // every wavefront is done with the operand stages
+        epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch, h,
+                                                    ll, k0, m0, g, split);
+        return;
+    }
     // Epilogue through LDS: the tile (BKC channels x BPX pixels, fp32, bias and
     // activation applied) is laid out channel-major in the shared buffer, free
     // once every wavefront has passed the barrier, then each channel row is
@@ -830,7 +924,14 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
 template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs a)
 {
-    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, false>(a);
+    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, false, false>(a);
+}
+
+// Channel-last bf16 output (and residual): the epilogue_cl instantiation.
+template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_cl_kernel(ConvArgs a)
+{
+    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, false, true>(a);
 }
 
 // The same kernel with the residual join in its epilogue (layers without a
@@ -839,7 +940,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
 __global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_dma_res_kernel(ConvArgs a)
 {
-    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, true>(a);
+    dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, true, false>(a);
 }
 
 // 3x3, stride 1, padding 1 (the middle layers of bottleneck blocks): the
@@ -860,7 +961,7 @@ __global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_dma_res_kernel(C
 // last tap of the current one.  PR = patch rows allocated (BPX + 2W + 2 used).
 // NPB = 1 (one channel block, C/groups == 64): a single patch buffer, loaded
 // once, which keeps a 128 x 64 tile at 48 KB of LDS (three work-groups per CU).
-template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB, bool RES>
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB, bool RES, bool YCL>
 __device__ __forceinline__ void halo_body(const ConvArgs &a)
 {
     constexpr int NT = 64 * WPX * WCH;
@@ -872,7 +973,8 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UP % NT == 0, "tile shape");
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
     static_assert(NPB == 1 || NPB == 2, "patch buffers");
-    constexpr int SMEM = 2 * UA + NPB * UP > BKC * OP / 4 ? 2 * UA + NPB * UP : BKC * OP / 4;
+    constexpr int EPI = YCL ? BPX * (BKC + 4) / 4 : BKC * OP / 4;   // epilogue tile, 16-byte units
+    constexpr int SMEM = 2 * UA + NPB * UP > EPI ? 2 * UA + NPB * UP : EPI;
     __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];   // [A 0][A 1][patch 0][patch 1]
     if (NPB == 1 && a.Cg != 64) return;                 // the launcher never sends such a layer
 
@@ -1007,9 +1109,14 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
 #pragma unroll
             for (int bj = 0; bj < BJ; ++bj)
 #pragma unroll
-                for (int bi = 0; bi < BI; ++bi)
-                    acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
-                                                                         acc[bj][bi], 0, 0, 0);
+                for (int bi = 0; bi < BI; ++bi) {
+                    if constexpr (YCL)   // filters as the A operand, as in epilogue_cl
+                        acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[ks][bi], xv[ks][bj],
+                                                                             acc[bj][bi], 0, 0, 0);
+                    else
+                        acc[bj][bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xv[ks][bj], wv[ks][bi],
+                                                                             acc[bj][bi], 0, 0, 0);
+                }
     };
 
     if (t_begin < t_end) {
@@ -1028,6 +1135,12 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
         compute(t);
     }
 
+    if constexpr (YCL) {
+        __syncthreads();   // every wavefront is done with the filter stages and patches
+        epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch, h,
+                                                    ll, k0, m0, g, split);
+        return;
+    }
     // Epilogue through LDS, as in igemm_bf16_dma_kernel.
     float rv[RES ? BKC * (BPX / 4) / NT : 1][4];
     if constexpr (RES) load_res_tile<BPX, BKC, NT>(a, tid, k0, m0, g, rv);
@@ -1067,19 +1180,33 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
 template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
 __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_kernel(ConvArgs a)
 {
-    halo_body<BPX, BKC, WPX, WCH, PR, NPB, false>(a);
+    halo_body<BPX, BKC, WPX, WCH, PR, NPB, false, false>(a);
 }
 
 // With the residual join in the epilogue (no reduction split).
 template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
 __global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_halo_res_kernel(ConvArgs a)
 {
-    halo_body<BPX, BKC, WPX, WCH, PR, NPB, true>(a);
+    halo_body<BPX, BKC, WPX, WCH, PR, NPB, true, false>(a);
+}
+
+// Channel-last bf16 output (and residual).
+template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
+__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_halo_cl_kernel(ConvArgs a)
+{
+    halo_body<BPX, BKC, WPX, WCH, PR, NPB, false, true>(a);
 }
 
 template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
 void launch_dma(const ConvArgs &a, dim3 grid, hipStream_t st)
 {
+    if constexpr (NCHWB == 0) {
+        if (a.ycl) {
+            launch_kernel((igemm_bf16_dma_cl_kernel<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC>), grid,
+                          dim3(64 * WPX * WCH), 0, st, a);
+            return;
+        }
+    }
     if (a.res && a.splits == 1)
         launch_kernel((igemm_bf16_dma_res_kernel<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC>), grid,
                       dim3(64 * WPX * WCH), 0, st, a);
@@ -1091,7 +1218,10 @@ void launch_dma(const ConvArgs &a, dim3 grid, hipStream_t st)
 template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB = 2>
 void launch_halo_k(const ConvArgs &a, dim3 grid, hipStream_t st)
 {
-    if (a.res && a.splits == 1)
+    if (a.ycl)
+        launch_kernel((igemm_bf16_halo_cl_kernel<BPX, BKC, WPX, WCH, PR, NPB>), grid, dim3(64 * WPX * WCH), 0,
+                      st, a);
+    else if (a.res && a.splits == 1)
         launch_kernel((igemm_bf16_halo_res_kernel<BPX, BKC, WPX, WCH, PR, NPB>), grid,
                       dim3(64 * WPX * WCH), 0, st, a);
     else
@@ -1252,11 +1382,12 @@ bool nhwc_bf16_eligible(const ConvProblem &p) { return p.Cg % 32 == 0; }
 // CU; below that, 128 x 64 while it still covers every CU, then 64 x 64.
 // Filters of at most 64 channels take the 64-wide channel tiles.  A launch
 // with fewer than half as many 64 x 64 tiles as CUs splits the reduction.
-static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int max_splits)
+static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int max_splits, bool x_nhwc)
 {
     NhwcPlan plan{};
     plan.dma = 1;
     plan.krc = 64;
+    plan.x_nhwc = x_nhwc ? 1 : 0;
     auto wgs = [&](int t) {
         return (long)ceil_div(p.M, kTilesD[t].bpx) * ceil_div(p.Kg, kTilesD[t].bkc) * p.groups;
     };
@@ -1294,7 +1425,7 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
     // the load instructions, which pays off only for short reductions
     // (measured at batch 64, 14x14: 256 -> 1024 channels 26.4 + 6.7 us copy ->
     // 32.2 us; 1024 -> 256 channels 15.7 + 11.3 us copy -> 28.7 us)
-    const bool nchw_ok = p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && plan.tile <= 1;
+    const bool nchw_ok = !x_nhwc && p.R == 1 && p.S == 1 && p.stride == 1 && p.pad == 0 && plan.tile <= 1;
     plan.nchwb = nchw_ok && (p.H * p.W) % 8 == 0 && (uintptr_t)x % 16 == 0 ? 1
                  : nchw_ok && (p.H * p.W) % 2 == 0 && (uintptr_t)x % 4 == 0 && chunks <= 8 ? 2 : 0;
     // A 128 x 64 grid that fits in two work-groups per CU loses no occupancy
@@ -1316,17 +1447,17 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
              splits == 1 && 128 + 2 * p.W + 2 <= 256)
         plan.halo = 256;
     const ConvProblem cp = copied_problem(p);
-    plan.xcl_bytes = plan.nchwb ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
+    plan.xcl_bytes = plan.nchwb || x_nhwc ? 0 : (size_t)cp.N * cp.C * cp.H * cp.W * sizeof(uint16_t);
     plan.copy_cb = plane_copy_block(p, num_cus);
     return plan;
 }
 
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits)
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits, bool x_nhwc)
 {
     // the direct-to-LDS kernel addresses x and w through 32-bit buffer offsets
     const bool fits = (long)p.N * p.C * p.H * p.W * 2 < (1L << 31) &&
                       (long)p.K * p.Cg * p.R * p.S * 2 < (1L << 31);
-    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus, x, max_splits);
+    if (p.Cg % 64 == 0 && fits) return plan_dma(p, num_cus, x, max_splits, x_nhwc);
     NhwcPlan plan{};
     plan.krc = p.Cg % 64 == 0 ? 64 : 32;
     plan.tile = 1;
@@ -1361,29 +1492,29 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     char tname[64];
     const int rv = copy_read_width(p, nullptr);
     if (rv == 0)
-        snprintf(tname, sizeof tname, "nchw_to_nhwc_plane_bf16_kernel");
+        snprintf(tname, sizeof tname, "nchw_to_nhwc_plane_bf16_kernel + ");
     else
-        snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d>", rv);
+        snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d> + ", rv);
+    const bool copy = !plan.nchwb && !plan.x_nhwc;
+    const char *variant = p.ycl ? "_cl" : p.res && plan.splits == 1 ? "_res" : "";
+    const char *reduce = plan.splits == 1 ? "" : p.ycl ? " + splitk_reduce_cl_kernel" : " + splitk_reduce_kernel";
     if (plan.dma && plan.halo) {
         const TileD &d = kTilesD[plan.tile];
-        snprintf(buf, len, "%s + igemm_bf16_halo%s_kernel<%d, %d, 2, 2, %d, %d>%s", tname,
-                 p.res && plan.splits == 1 ? "_res" : "", d.bpx, d.bkc, plan.halo,
-                 d.bkc == 64 ? 1 : 2, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
-        *launches = 2 + (plan.splits > 1 ? 1 : 0);
+        snprintf(buf, len, "%sigemm_bf16_halo%s_kernel<%d, %d, 2, 2, %d, %d>%s", copy ? tname : "", variant,
+                 d.bpx, d.bkc, plan.halo, d.bkc == 64 ? 1 : 2, reduce);
+        *launches = (copy ? 2 : 1) + (plan.splits > 1 ? 1 : 0);
         return;
     }
     if (plan.dma) {
         const TileD &d = kTilesD[plan.tile];
         // the instantiation's full name, reduction chunk included (every launch uses 64)
-        snprintf(buf, len, "%s%sigemm_bf16_dma%s_kernel<%d, %d, %d, %d, %d, %d, %d, %d, 64>%s",
-                 plan.nchwb ? "" : tname, plan.nchwb ? "" : " + ", p.res && plan.splits == 1 ? "_res" : "",
-                 R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst,
-                 plan.nchwb, plan.splits > 1 ? " + splitk_reduce_kernel" : "");
-        *launches = (plan.nchwb ? 1 : 2) + (plan.splits > 1 ? 1 : 0);
+        snprintf(buf, len, "%sigemm_bf16_dma%s_kernel<%d, %d, %d, %d, %d, %d, %d, %d, 64>%s", copy ? tname : "",
+                 variant, R, S, d.bpx, d.bkc, d.wpx, d.wch, d.nst, plan.nchwb, reduce);
+        *launches = (copy ? 2 : 1) + (plan.splits > 1 ? 1 : 0);
         return;
     } else {
         const TileN &t = kTilesN[plan.tile];
-        snprintf(buf, len, "%s + igemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s", tname, R, S, t.bkc,
+        snprintf(buf, len, "%sigemm_bf16_nhwc_kernel<%d, %d, %d, %d, %d>%s", tname, R, S, t.bkc,
                  t.bpx, plan.krc,
                  plan.splits > 1 ? " + splitk_reduce_kernel" : "");
     }
@@ -1408,6 +1539,28 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
         const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
         if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
         launch_dma_nchw(a, plan.tile, plan.nchwb, dim3((unsigned)wgs), st);
+        if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
+        if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+        return launch_splitk_reduce(a, st);
+    }
+    if (plan.x_nhwc) {
+        // x is already channel-last: the GEMM reads it as given, strides included
+        if (!plan.dma) return hipErrorInvalidValue;
+        ConvArgs a = make_args(p);
+        a.x = x;
+        a.w = w_krsc;
+        a.bias = bias;
+        a.y = y;
+        a.ws = plan.splits > 1 ? partials : nullptr;
+        a.splits = plan.splits;
+        a.kr_per_split = plan.kr_per_split;
+        const TileD &d = kTilesD[plan.tile];
+        const long wgs = (long)ceil_div(p.M, d.bpx) * ceil_div(p.Kg, d.bkc) * p.groups * plan.splits;
+        if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
+        if (plan.halo) {
+            if ((e = launch_halo(a, d.bkc, plan.halo, dim3((unsigned)wgs), st)) != hipSuccess) return e;
+        } else
+            launch_dma(a, plan.tile, dim3((unsigned)wgs), st);
         if ((e = hipGetLastError()) != hipSuccess || plan.splits == 1) return e;
         if (hook && (e = hook->before_launch(hook->ctx, st)) != hipSuccess) return e;
         return launch_splitk_reduce(a, st);

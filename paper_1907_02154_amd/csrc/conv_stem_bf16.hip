@@ -23,7 +23,8 @@
 // A work-group computes 4 output rows (448 pixels = 14 blocks of 32) x 64
 // filters with 7 wavefronts, each 2 pixel blocks x 2 filter blocks of
 // v_mfma_f32_32x32x16_bf16 with filters as the A operand and pixels as B, so
-// each store instruction writes runs of 32 consecutive output pixels.
+// each store instruction writes runs of 32 consecutive output pixels (NCHW
+// fp32), or 4 consecutive channels of each of 32 pixels (channel-last bf16).
 #include "internal.h"
 
 #include <cstdio>
@@ -54,6 +55,7 @@ struct StemArgs {
     int N, C, H, W, K, P;
     int relu;
     int vec;                  // W % 8 == 0 and x 16-byte aligned: 16-byte row loads
+    int ycl;                  // y bf16 channel-last [N][P][kQ][K] (no residual)
 };
 
 __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
@@ -147,6 +149,39 @@ __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
     // v of lane l is filter 8*(v/4) + 4*h + v%4 of the filter block and pixel
     // l%32 of the pixel block: each store instruction writes 32 consecutive
     // pixels (128 bytes) of two filter planes.
+    if (a.ycl) {
+        // channel-last bf16: register group v/4 holds 4 consecutive channels
+        // of pixel l%32, stored as one 8-byte write
+        uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int k = k0 + f * 32 + 8 * q4 + 4 * h;
+                if (k >= a.K) continue;                      // K % 4 == 0 (checked on the host)
+                float bv[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) bv[e] = a.bias ? a.bias[k + e] : 0.f;
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const long pix = ((long)n * a.P + p0) * kQ + 32 * (2 * wave + b) + ll;
+                    uint32_t d[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        float v0 = acc[b][f][4 * q4 + 2 * e] + bv[2 * e];
+                        float v1 = acc[b][f][4 * q4 + 2 * e + 1] + bv[2 * e + 1];
+                        if (a.relu) {
+                            v0 = fmaxf(v0, 0.f);
+                            v1 = fmaxf(v1, 0.f);
+                        }
+                        d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+                    }
+                    *reinterpret_cast<uint2 *>(y + pix * a.K + k) = make_uint2(d[0], d[1]);
+                }
+            }
+        }
+        return;
+    }
     const long plane = (long)a.P * kQ;
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
@@ -226,6 +261,8 @@ hipError_t launch_stem_bf16(const ConvProblem &p, const uint16_t *x, const uint1
     a.P = p.P;
     a.relu = p.relu;
     a.vec = p.W % 8 == 0 && (uintptr_t)x % 16 == 0;
+    a.ycl = p.ycl;
+    if (p.ycl && (p.res || p.K % 4 || (uintptr_t)y % 8)) return hipErrorInvalidValue;
     const long wgs = (long)(p.P / kRows) * p.N * ceil_div(p.K, 64);
     launch_kernel(stem7_bf16_kernel, dim3((unsigned)wgs), dim3(kThreads), 0, st, a);
     return hipGetLastError();

@@ -1,5 +1,6 @@
 // Glue operators of the evaluated networks, outside the conv operator:
-// max-pool (ResNet stem 3x3/2 pad 1, VGG 2x2/2), the residual join
+// max-pool (ResNet stem 3x3/2 pad 1, VGG 2x2/2; fp32 NCHW, and bf16
+// channel-last between the layers of a channel-last network), the residual join
 // act(a + b) of a bottleneck block, and the fp32 -> bf16 rounding that feeds
 // a bf16 conv from an fp32 activation.  All are elementwise or near it and
 // bound by HBM bandwidth; lanes walk contiguous memory.
@@ -63,22 +64,55 @@ __global__ __launch_bounds__(256) void add_act_kernel(const float *a, const floa
     }
 }
 
-// Round to nearest even on the raw bits: add 0x7FFF plus the lowest kept bit,
-// then keep the upper half.  A NaN keeps its sign and gets the quiet bit.
-__device__ inline uint16_t f32_to_bf16_rne(float f)
-{
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
-        return (uint16_t)((u >> 16) | 0x0040u);
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
 __global__ __launch_bounds__(256) void cast_bf16_kernel(const float *__restrict__ x,
                                                         uint16_t *__restrict__ y, long n)
 {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (long)gridDim.x * blockDim.x)
         y[i] = f32_to_bf16_rne(x[i]);
+}
+
+// Max-pool over bf16 channel-last tensors: a thread takes 8 channels of one
+// output pixel (16-byte loads and store); the maximum of bf16 values is one
+// of them, so the result is exact.  Padded positions never win.
+__global__ __launch_bounds__(256) void maxpool_nhwc_bf16_kernel(const uint16_t *__restrict__ x,
+                                                                uint16_t *__restrict__ y, int C, int H,
+                                                                int W, int R, int S, int stride, int pad,
+                                                                int P, int Q, long total)
+{
+    const int C8 = C / 8;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const int o = (int)(i % C8);
+        const long pix = i / C8;
+        const int q = (int)(pix % Q);
+        const long t = pix / Q;
+        const int p = (int)(t % P);
+        const long n = t / P;
+        float m[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
+        for (int r = 0; r < R; ++r) {
+            const int h = p * stride - pad + r;
+            if ((unsigned)h >= (unsigned)H) continue;
+            for (int s = 0; s < S; ++s) {
+                const int w = q * stride - pad + s;
+                if ((unsigned)w >= (unsigned)W) continue;
+                const uint4 v = *reinterpret_cast<const uint4 *>(x + ((n * H + h) * W + w) * C + 8 * o);
+                const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    m[2 * e] = fmaxf(m[2 * e], bf16_to_f32((uint16_t)(d[e] & 0xFFFFu)));
+                    m[2 * e + 1] = fmaxf(m[2 * e + 1], bf16_to_f32((uint16_t)(d[e] >> 16)));
+                }
+            }
+        }
+        uint32_t d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            d[e] = (uint32_t)f32_to_bf16_rne(m[2 * e]) | ((uint32_t)f32_to_bf16_rne(m[2 * e + 1]) << 16);
+        *reinterpret_cast<uint4 *>(y + pix * C + 8 * o) = make_uint4(d[0], d[1], d[2], d[3]);
+    }
 }
 
 unsigned grid_for(long n)
@@ -120,6 +154,19 @@ hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t
 {
     if (count == 0) return hipSuccess;
     launch_kernel(cast_bf16_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, y, count);
+    return hipGetLastError();
+}
+
+}  // namespace miconv
+
+namespace miconv {
+
+hipError_t launch_maxpool_nhwc_bf16(int N, int C, int H, int W, int R, int S, int stride, int pad, int P,
+                                    int Q, const uint16_t *x, uint16_t *y, hipStream_t st)
+{
+    const long total = (long)N * P * Q * (C / 8);
+    launch_kernel(maxpool_nhwc_bf16_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, y, C, H, W, R, S,
+                  stride, pad, P, Q, total);
     return hipGetLastError();
 }
 

@@ -34,8 +34,31 @@ struct ConvProblem {
     int M;           // N * P * Q: the GEMM pixel extent
     int relu;
     const float *res;  // [N][K][P][Q] added to the conv + bias before the activation, or nullptr
+                       // (with ycl: bf16 [N][P][Q][K], the layout of y)
     long ysn;          // elements from one image of y (and res) to the next: K*P*Q when dense
+    int xcl;           // x is bf16 channel-last [N][H][W][C] (else NCHW)
+    int ycl;           // y (and res) bf16 channel-last [N][P][Q][K] (else fp32 NCHW)
 };
+
+// fp32 -> bf16 bits, round to nearest even on the raw bits: add 0x7FFF plus
+// the lowest kept bit, keep the upper half.  A NaN keeps its sign and gets the
+// quiet bit.
+__host__ __device__ inline uint16_t f32_to_bf16_rne(float f)
+{
+    uint32_t u;
+    __builtin_memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
+        return (uint16_t)((u >> 16) | 0x0040u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__host__ __device__ inline float bf16_to_f32(uint16_t b)
+{
+    const uint32_t u = (uint32_t)b << 16;
+    float f;
+    __builtin_memcpy(&f, &u, 4);
+    return f;
+}
 
 // Division by a divisor d >= 1 fixed at launch, for numerators below 2^31:
 // n / d = (mulhi(n, mul) + n) >> shift with shift = ceil(log2 d) and
@@ -79,6 +102,7 @@ struct ConvArgs {
     const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may
                           // be y itself (every element is read and written by one thread)
     long ysn;             // elements from one image of y (and res) to the next (>= K*P*Q)
+    int ycl;              // y and res bf16 [N*P*Q][K]; split partials then [splits][M][K]
 };
 
 ConvArgs make_args(const ConvProblem &p);
@@ -161,9 +185,11 @@ struct NhwcPlan {
     int copy_cb;          // channels per work-group of the whole-plane copy
     int halo;             // 3x3 stride-1 layers: patch rows of the halo kernel (0: not used);
                           // its filters are packed in 64-channel blocks
+    int x_nhwc;           // x is already channel-last: no copy
 };
 bool nhwc_bf16_eligible(const ConvProblem &p);
-NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits);
+// x_nhwc: x is given channel-last (direct-to-LDS kernels only, C/groups % 64 == 0).
+NhwcPlan plan_nhwc_bf16(const ConvProblem &p, int num_cus, const void *x, int max_splits, bool x_nhwc = false);
 hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const uint16_t *x,
                             const uint16_t *w_krsc, const float *bias, float *y, uint16_t *xcl,
                             float *partials, hipStream_t st, const LaunchHook *hook = nullptr);
@@ -193,10 +219,15 @@ hipError_t launch_maxpool_f32(int N, int C, int H, int W, int R, int S, int stri
 hipError_t launch_add_act_f32(long count, const float *a, const float *b, float *y, int relu,
                               hipStream_t st);
 hipError_t launch_cast_bf16(long count, const float *x, uint16_t *y, hipStream_t st);
+// Max-pool on bf16 channel-last tensors, x [N][H][W][C] -> y [N][P][Q][C].
+hipError_t launch_maxpool_nhwc_bf16(int N, int C, int H, int W, int R, int S, int stride, int pad, int P,
+                                    int Q, const uint16_t *x, uint16_t *y, hipStream_t st);
 
 // A validated conv call with its kernel fixed (what the ABI entry points and
 // the stack executor enqueue).
-enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2 };
+enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2, OP_MAXPOOL_BF16_NHWC = 3 };
+// Layout flags of a bf16 dense layer (enum miconv_layout).
+enum LayoutFlags { LAYOUT_X_NHWC = 1, LAYOUT_Y_NHWC_BF16 = 2 };
 enum Impl {
     IMPL_DIRECT = 0,
     IMPL_IGEMM = 1,
@@ -204,7 +235,8 @@ enum Impl {
     IMPL_WAVE = 3,
     IMPL_IGEMM_BF16 = 4,
     IMPL_NHWC_BF16 = 5,
-    IMPL_STEM_BF16 = 6
+    IMPL_STEM_BF16 = 6,
+    IMPL_POOL_NHWC = 7
 };
 // What a call may use besides its tensors.
 enum PlanMode {
@@ -240,7 +272,7 @@ struct Resolved {
 };
 int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int R, int S, int stride,
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
-            int relu, Resolved *out);
+            int relu, Resolved *out, int layout = 0);
 // resolve() for tensors at 256-byte boundaries (w may be null: a stand-in).
 int resolve_aligned(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
                     int dtype, int algo, int mode, const void *w, Resolved *out);

@@ -169,9 +169,10 @@ int miconv_stack_create(const miconv_conv_desc *layers, int n, miconv_stack **ou
         const miconv_conv_desc &d = layers[i];
         Resolved r;
         int rc = resolve(d.op, MICONV_ALGO_AUTO, MODE_SCRATCH | MODE_PREPACK, d.N, d.C, d.H, d.W, d.K, d.R,
-                         d.S, d.stride, d.pad, d.groups, d.x, d.w, d.bias, d.y, d.relu, &r);
+                         d.S, d.stride, d.pad, d.groups, d.x, d.w, d.bias, static_cast<float *>(d.y), d.relu,
+                         &r, d.layout);
         if (rc == MICONV_OK) rc = set_output_stride(r, d.y_image_stride);
-        if (rc == MICONV_OK) rc = set_residual(r, d.res);
+        if (rc == MICONV_OK) rc = set_residual(r, static_cast<const float *>(d.res));
         if (rc != MICONV_OK) {
             miconv_stack_destroy(s);
             return rc;

@@ -72,6 +72,12 @@ def lib() -> ctypes.CDLL:
         L.conv2d_fwd_ws.restype = i
         L.conv2d_fwd_noalloc.argtypes = [i] * 12 + [p, p, p, p, p, l, i, p]
         L.conv2d_fwd_noalloc.restype = i
+        L.conv2d_cl_workspace_bytes.argtypes = [i] * 11
+        L.conv2d_cl_workspace_bytes.restype = l
+        L.conv2d_fwd_cl.argtypes = [i] * 11 + [p, p, p, p, p, i, p, ctypes.c_size_t, p]
+        L.conv2d_fwd_cl.restype = i
+        L.maxpool2d_nhwc_bf16.argtypes = [i] * 8 + [p, p, p]
+        L.maxpool2d_nhwc_bf16.restype = i
         L.conv2d_describe.restype = i
         L.miconv_stack_create.argtypes = [p, i, ctypes.POINTER(p)]
         L.miconv_stack_size.argtypes = [p]
@@ -445,7 +451,9 @@ def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", alg
     return buf.value.decode(), n.value
 
 
-OP_CONV_F32, OP_CONV_BF16, OP_DWCONV_F32 = 0, 1, 2
+OP_CONV_F32, OP_CONV_BF16, OP_DWCONV_F32, OP_MAXPOOL_BF16_NHWC = 0, 1, 2, 3
+# enum miconv_layout flags
+LAYOUT_NCHW, LAYOUT_X_NHWC, LAYOUT_Y_NHWC_BF16 = 0, 1, 2
 
 
 class ConvDesc(ctypes.Structure):
@@ -453,7 +461,73 @@ class ConvDesc(ctypes.Structure):
                                          ("N", "C", "H", "W", "K", "R", "S", "stride", "pad",
                                           "groups", "relu")] + \
                [("x", ctypes.c_void_p), ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
-                ("y", ctypes.c_void_p), ("res", ctypes.c_void_p), ("y_image_stride", ctypes.c_long)]
+                ("y", ctypes.c_void_p), ("res", ctypes.c_void_p), ("y_image_stride", ctypes.c_long),
+                ("layout", ctypes.c_int)]
+
+
+def _cl_shapes(x, w, y, stride, pad, groups, layout):
+    """Extents of a channel-last bf16 layer from its tensors: x [N][H][W][C]
+    (MICONV_LAYOUT_X_NHWC) or [N][C][H][W] bf16, y [N][P][Q][K] bf16
+    (MICONV_LAYOUT_Y_NHWC_BF16) or [N][K][P][Q] fp32; checks y's shape."""
+    _dev(x, torch.bfloat16, "x", 4)
+    _dev(w, torch.bfloat16, "w", 4)
+    if layout & LAYOUT_X_NHWC:
+        N, H, W, C = x.shape
+    else:
+        N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if groups <= 0 or Cg * groups != C:
+        raise ValueError("w.shape[1] * groups must equal C")
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if layout & LAYOUT_Y_NHWC_BF16:
+        _dev(y, torch.bfloat16, "y", 4)
+        want = (N, P, Q, K)
+    else:
+        _dev(y, torch.float32, "y", 4)
+        want = (N, K, P, Q)
+    if tuple(y.shape) != want:
+        raise ValueError(f"y must have shape {want}, got {tuple(y.shape)}")
+    return N, C, H, W, K, R, S
+
+
+def conv2d_cl_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups=1, layout=LAYOUT_X_NHWC | LAYOUT_Y_NHWC_BF16):
+    n = lib().conv2d_cl_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups, int(layout))
+    if n < 0:
+        raise MiconvError(int(n), "conv2d_cl_workspace_bytes")
+    return n
+
+
+def conv2d_fwd_cl(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None,
+                  layout=LAYOUT_X_NHWC | LAYOUT_Y_NHWC_BF16, ws=None, stream=None):
+    """bf16 conv with channel-last x and/or y (conv2d_fwd_cl); res like y.
+    ws None: a workspace from torch's caching allocator."""
+    N, C, H, W, K, R, S = _cl_shapes(x, w, y, stride, pad, groups, layout)
+    if bias is not None:
+        _dev(bias, torch.float32, "bias", 1)
+    if res is not None:
+        _dev(res, y.dtype, "res", 4)
+        if tuple(res.shape) != tuple(y.shape):
+            raise ValueError("res must have y's shape")
+    if ws is None:
+        ws = workspace(conv2d_cl_workspace_bytes(N, C, H, W, K, R, S, stride, pad, groups, layout), x.device)
+    rc = lib().conv2d_fwd_cl(N, C, H, W, K, R, S, stride, pad, groups, int(layout), _ptr(x), _ptr(w),
+                             _ptr(bias), _ptr(res), _ptr(y), 1 if relu else 0, _ptr(ws),
+                             0 if ws is None else ws.numel(), _stream(stream))
+    _check(rc, "conv2d_fwd_cl")
+    return y
+
+
+def maxpool2d_nhwc_bf16(x, y, R, S, stride, pad=0, stream=None):
+    """Max-pool on bf16 channel-last tensors: x [N][H][W][C] -> y [N][P][Q][C]."""
+    _dev(x, torch.bfloat16, "x", 4)
+    _dev(y, torch.bfloat16, "y", 4)
+    N, H, W, C = x.shape
+    P, Q = out_dims(H, W, R, S, stride, pad)
+    if tuple(y.shape) != (N, P, Q, C):
+        raise ValueError(f"y must have shape {(N, P, Q, C)}")
+    _check(lib().maxpool2d_nhwc_bf16(N, C, H, W, R, S, stride, pad, _ptr(x), _ptr(y), _stream(stream)),
+           "maxpool2d_nhwc_bf16")
+    return y
 
 
 class Stack:
@@ -470,8 +544,41 @@ class Stack:
         self._keep = []
         descs = (ConvDesc * len(layers))()
         for d, layer in zip(descs, layers):
+            if layer[0] == "maxpool":
+                # ("maxpool", x, y, R, S, stride, pad): bf16 channel-last glue
+                _, x, y, R, S, stride, pad = layer
+                _dev(x, torch.bfloat16, "x", 4)
+                _dev(y, torch.bfloat16, "y", 4)
+                N, H, W, C = x.shape
+                P, Q = out_dims(H, W, R, S, stride, pad)
+                if tuple(y.shape) != (N, P, Q, C):
+                    raise ValueError(f"y must have shape {(N, P, Q, C)}")
+                d.op, d.N, d.C, d.H, d.W, d.K, d.R, d.S = OP_MAXPOOL_BF16_NHWC, N, C, H, W, C, R, S
+                d.stride, d.pad, d.groups, d.relu = stride, pad, 1, 0
+                d.x, d.y = x.data_ptr(), y.data_ptr()
+                self._keep.append((x, y))
+                continue
             op, x, w, bias, y, stride, pad, groups, relu = layer[:9]
             res = layer[9] if len(layer) > 9 else None
+            layout = layer[10] if len(layer) > 10 else 0
+            if layout:
+                # a channel-last bf16 layer (conv2d_fwd_cl)
+                if op != OP_CONV_BF16:
+                    raise ValueError("a layout applies to bf16 convolutions only")
+                N, C, H, W, K, R, S = _cl_shapes(x, w, y, stride, pad, groups, layout)
+                if bias is not None:
+                    _dev(bias, torch.float32, "bias", 1)
+                if res is not None:
+                    _dev(res, y.dtype, "res", 4)
+                    if tuple(res.shape) != tuple(y.shape):
+                        raise ValueError("res must have y's shape")
+                d.op, d.N, d.C, d.H, d.W, d.K, d.R, d.S = op, N, C, H, W, K, R, S
+                d.stride, d.pad, d.groups, d.relu = stride, pad, groups, 1 if relu else 0
+                d.x, d.w, d.bias, d.y = x.data_ptr(), w.data_ptr(), _ptr(bias), y.data_ptr()
+                d.res = _ptr(res)
+                d.layout = int(layout)
+                self._keep.append((x, w, bias, y, res))
+                continue
             ys = _image_strided(y, "y")
             if res is not None:
                 if _image_strided(res, "res") != ys or tuple(res.shape) != tuple(y.shape):
