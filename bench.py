@@ -111,6 +111,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget for the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--layers", action="store_true", help="also print a per-layer table to stderr")
+    ap.add_argument("--chain", choices=["resnet50_b64", "resnet50_b1", "mobilenet_b1"], default=None,
+                    help="instead: a whole-network pass (layers chained, glue and joins included); "
+                         "resnet50_b64 keeps bf16 channel-last activations between layers")
     ap.add_argument("--no-b64", action="store_true",
                     help="with the default --config 2: skip the nested batch-64 bf16 record (config 5)")
     ap.add_argument("--profile-passes", type=int, default=0, metavar="N",
@@ -578,6 +581,102 @@ def single_call_times(steps: int) -> dict:
     return out
 
 
+def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bool = False) -> dict:
+    """A whole-network pass (paper_1907_02154_amd.networks): every layer reads
+    the previous layers' outputs, with the network's glue (ResNet's max-pool)
+    in the same stack and the shortcut joins fused into the convs.  Timed like
+    stack_record: one HIP graph of K passes; per-kernel durations from K eager
+    passes with runtime stamps.  net: "resnet50_b64" (bf16, layout "bf16_cl"
+    or fp32 NCHW at batch 64 is not offered), "resnet50_b1" or "mobilenet_b1"
+    (fp32)."""
+    import torch
+    from paper_1907_02154_amd import miconv
+    from paper_1907_02154_amd import networks as nets
+    from paper_1907_02154_amd import workloads as wl
+
+    config = {"resnet50_b64": 5, "resnet50_b1": 2, "mobilenet_b1": 3}[net]
+    graph = nets.mobilenet_graph() if net == "mobilenet_b1" else nets.resnet50_graph(config)
+    bf16 = layout == "bf16_cl"
+    x0, _, _ = wl.layer_tensors(config, 0, wl.workload(config).layers[0])
+    params = {}
+    for node in graph:
+        if node.kind == "conv":
+            _, w, b = wl.layer_tensors(config, node.index, node.layer)
+            tw = (torch.from_numpy(wl.to_bf16_bits(w).view(np.int16)).cuda().view(torch.bfloat16) if bf16
+                  else torch.from_numpy(w).cuda())
+            params[node.name] = (tw, torch.from_numpy(b).cuda())
+    tx = (torch.from_numpy(wl.to_bf16_bits(x0).view(np.int16)).cuda().view(torch.bfloat16) if bf16
+          else torch.from_numpy(x0).cuda())
+    ops, outs = nets.build_stack(graph, tx, params, layout)
+    stack = miconv.Stack(ops)
+    n_launch = stack.launches
+    launch_info = [stack.launch_info(j) for j in range(n_launch)]
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        stack.launch(stream)
+    torch.cuda.synchronize()
+    stack.capture(steps, timed=False, stream=stream)
+    stack.replay(stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    stack.replay(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / steps
+    stack.launch_timed(steps, stream)
+    torch.cuda.synchronize()
+    launch_ms = stack.times().mean(axis=0)
+    names = [n.name for n in graph]
+    flops, nbytes, layer_ms = {}, {}, np.zeros(len(graph))
+    elem = 2 if bf16 else 4
+    for node in graph:
+        if node.kind != "conv":
+            continue
+        l = node.layer
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        flops[node.name] = wl.flops(l, P, Q)
+        xin = l.N * l.C * l.H * l.W * (2 if bf16 else 4)
+        yout = l.N * l.K * P * Q * elem
+        nbytes[node.name] = xin + l.K * (l.C // l.groups) * l.R * l.S * (2 if bf16 else 4) + 4 * l.K + yout + \
+            (yout if node.res else 0)
+    conv_ms, pool_ms, per_kernel = 0.0, 0.0, {}
+    for j in range(n_launch):
+        li, kname = launch_info[j]
+        layer_ms[li] += launch_ms[j]
+        if graph[li].kind == "conv":
+            conv_ms += float(launch_ms[j])
+        else:
+            pool_ms += float(launch_ms[j])
+        k = per_kernel.setdefault(kname, [0.0, 0])
+        k[0] += float(launch_ms[j])
+        k[1] += 1
+    if table:
+        for i, node in enumerate(graph):
+            extra = ""
+            if node.kind == "conv":
+                t = float(layer_ms[i]) * 1e-3
+                extra = (f"{flops[node.name] / t / 1e12:8.2f} TFLOP/s {nbytes[node.name] / t / 1e9:8.1f} GB/s")
+            print(f"{i:3d} {node.name:10s} {stack.describe(i):60s} {layer_ms[i] * 1e3:9.2f} us {extra}",
+                  file=sys.stderr)
+    stack.close()
+    total_flops = sum(flops.values())
+    peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
+    t_roof = sum(max(flops[n] / (peak * 1e12), nbytes[n] / (PEAK_HBM_GBS * 1e9)) for n in flops)
+    dom = max(per_kernel.items(), key=lambda kv: kv[1][0])
+    N = graph[0].layer.N
+    return {
+        "workload": f"{net} network pass ({layout}): {len(flops)} convs"
+                    + (" + max-pool" if len(flops) < len(graph) else "") + ", shortcut joins fused",
+        "value": round(total_flops / (ms_per_step * 1e-3) / 1e12, 4), "unit": "TFLOP/s",
+        "ms_per_step": round(ms_per_step, 5), "ms_per_image": round(ms_per_step / N, 5),
+        "gflop_per_step": round(total_flops / 1e9, 4), "launches_per_step": n_launch,
+        "conv_kernel_ms": round(conv_ms, 5), "glue_kernel_ms": round(pool_ms, 5),
+        "stack_roofline_frac": round(t_roof / (ms_per_step * 1e-3), 4),
+        "dominant_kernel": {"kernel": dom[0], "ms_per_step": round(dom[1][0], 5), "launches": dom[1][1]},
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -589,6 +688,15 @@ def main():
         return
     if args.residual_join:
         residual_join(args)
+        return
+    if args.chain:
+        import torch
+        torch.cuda.set_device(0)
+        layout = "bf16_cl" if args.chain == "resnet50_b64" else "f32"
+        rec = chain_record(args, args.chain, layout, args.steps, args.warmup, args.layers)
+        rec.update(metric="network pass TFLOP/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+                   higher_is_better=True, dtype="bf16" if layout == "bf16_cl" else "f32", data="synthetic")
+        print(json.dumps(rec), flush=True)
         return
     if args.copy_calibration:
         import torch
@@ -635,6 +743,10 @@ def main():
         # the metric's batch-64 half: ResNet-50 at batch 64, bf16 inputs, fp32
         # accumulation and outputs, timed the same way (its own warm-up, K passes)
         out["b64"] = stack_record(args, 5, None, args.steps, args.warmup, min(args.cpu_seconds, 15.0), False)
+        # the same network at batch 64 as one chained pass with bf16
+        # channel-last activations between layers (no per-layer copies, bf16
+        # outputs, joins fused)
+        out["b64_chained"] = chain_record(args, "resnet50_b64", "bf16_cl", args.steps, args.warmup)
     if args.config in (1, 2) and args.batch is None:
         out["single_call"] = single_call_times(args.steps)
     print(json.dumps(out), flush=True)

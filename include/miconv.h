@@ -296,8 +296,9 @@ enum miconv_op {
     MICONV_OP_CONV_BF16 = 1,   /* conv2d_fwd_bf16 (x, w are bf16 bit patterns), or with
                                   `layout` conv2d_fwd_cl */
     MICONV_OP_DWCONV_F32 = 2,  /* dwconv2d_fwd */
-    MICONV_OP_MAXPOOL_BF16_NHWC = 3   /* maxpool2d_nhwc_bf16: R x S window, stride, pad; K = C,
+    MICONV_OP_MAXPOOL_BF16_NHWC = 3,  /* maxpool2d_nhwc_bf16: R x S window, stride, pad; K = C,
                                          w, bias, res NULL (glue between channel-last layers) */
+    MICONV_OP_MAXPOOL_F32 = 4         /* maxpool2d_fwd on fp32 NCHW, the same fields */
 };
 
 typedef struct miconv_conv_desc {

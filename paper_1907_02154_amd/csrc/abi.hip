@@ -141,8 +141,8 @@ int set_hip_error(hipError_t e) { return hip_fail(e); }
 // the call may use besides its tensors (enum PlanMode): without a workspace
 // there is no split reduction, no channel-last copy and no per-call filter
 // packing, and filters are read as given unless they were packed ahead.
-// Max-pool over bf16 channel-last tensors, as a stack layer (K = C, no filters).
-static int resolve_pool(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+// Max-pool as a stack layer (K = C, no filters): bf16 channel-last, or fp32 NCHW.
+static int resolve_pool(int kind, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                         const void *x, float *y, Resolved *out)
 {
     if (!x || !y) return MICONV_ERR_NULL;
@@ -150,14 +150,16 @@ static int resolve_pool(int N, int C, int H, int W, int K, int R, int S, int str
         pad >= S)
         return MICONV_ERR_SHAPE;
     if (K != C) return MICONV_ERR_GROUPS;
-    if (C % 8) return MICONV_ERR_UNSUPPORTED;
+    const bool cl = kind == OP_MAXPOOL_BF16_NHWC;
+    if (cl && C % 8) return MICONV_ERR_UNSUPPORTED;
     const long P = extent(H, R, stride, pad), Q = extent(W, S, stride, pad);
     if (P < 1 || Q < 1) return MICONV_ERR_SHAPE;
     if ((long)N * C * H * W > INT_MAX || (long)N * C * P * Q > INT_MAX) return MICONV_ERR_TOO_LARGE;
-    if ((uintptr_t)x % 16 || (uintptr_t)y % 16) return MICONV_ERR_ALIGN;
+    if (cl ? ((uintptr_t)x % 16 || (uintptr_t)y % 16) : ((uintptr_t)x % 4 || (uintptr_t)y % 4))
+        return MICONV_ERR_ALIGN;
     Resolved r{};
-    r.kind = OP_MAXPOOL_BF16_NHWC;
-    r.impl = IMPL_POOL_NHWC;
+    r.kind = kind;
+    r.impl = cl ? IMPL_POOL_NHWC : IMPL_POOL_F32;
     r.p.N = N;
     r.p.C = C;
     r.p.H = H;
@@ -170,7 +172,7 @@ static int resolve_pool(int N, int C, int H, int W, int K, int R, int S, int str
     r.p.groups = 1;
     r.p.P = (int)P;
     r.p.Q = (int)Q;
-    r.p.xcl = r.p.ycl = 1;
+    r.p.xcl = r.p.ycl = cl ? 1 : 0;
     r.x = x;
     r.y = y;
     *out = r;
@@ -181,7 +183,8 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
             int pad, int groups, const void *x, const void *w, const float *bias, float *y,
             int relu, Resolved *out, int layout)
 {
-    if (kind == OP_MAXPOOL_BF16_NHWC) return resolve_pool(N, C, H, W, K, R, S, stride, pad, x, y, out);
+    if (kind == OP_MAXPOOL_BF16_NHWC || kind == OP_MAXPOOL_F32)
+        return resolve_pool(kind, N, C, H, W, K, R, S, stride, pad, x, y, out);
     Resolved r{};
     const size_t elem = kind == OP_DENSE_BF16 ? sizeof(uint16_t) : sizeof(float);
     int rc = validate(N, C, H, W, K, R, S, stride, pad, groups, x, w, y, elem, &r.p);
@@ -311,7 +314,7 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
 int set_residual(Resolved &r, const float *res)
 {
     if (!res) return MICONV_OK;
-    if (r.impl == IMPL_POOL_NHWC) return MICONV_ERR_UNSUPPORTED;
+    if (r.impl == IMPL_POOL_NHWC || r.impl == IMPL_POOL_F32) return MICONV_ERR_UNSUPPORTED;
     if (r.p.ycl) {
         // bf16 [N][P][Q][K] like y, read with 16-byte loads; the stem takes none
         if ((uintptr_t)res % 16) return MICONV_ERR_ALIGN;
@@ -331,7 +334,8 @@ int set_output_stride(Resolved &r, long ysn)
 {
     const long dense = (long)r.p.K * r.p.P * r.p.Q;
     if (ysn == 0 || ysn == dense) return MICONV_OK;
-    if (r.p.ycl || r.impl == IMPL_POOL_NHWC) return MICONV_ERR_UNSUPPORTED;   // channel-last y is dense
+    if (r.p.ycl || r.impl == IMPL_POOL_NHWC || r.impl == IMPL_POOL_F32)
+        return MICONV_ERR_UNSUPPORTED;   // channel-last y is dense; pools take no stride
     if (ysn < dense) return MICONV_ERR_SHAPE;                  // images would overlap
     if ((long)(r.p.N - 1) * ysn + dense > INT_MAX) return MICONV_ERR_TOO_LARGE;
     if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
@@ -425,6 +429,9 @@ hipError_t enqueue(const Resolved &r0, float *ws, hipStream_t st, const LaunchHo
     }
     switch (r.impl) {
     case IMPL_DW: return launch_dwconv_f32(r.p, xf, wf, r.bias, r.y, st);
+    case IMPL_POOL_F32:
+        return launch_maxpool_f32(r.p.N, r.p.C, r.p.H, r.p.W, r.p.R, r.p.S, r.p.stride, r.p.pad, r.p.P, r.p.Q,
+                                  static_cast<const float *>(r.x), r.y, st);
     case IMPL_POOL_NHWC:
         return launch_maxpool_nhwc_bf16(r.p.N, r.p.C, r.p.H, r.p.W, r.p.R, r.p.S, r.p.stride, r.p.pad, r.p.P,
                                         r.p.Q, static_cast<const uint16_t *>(r.x), reinterpret_cast<uint16_t *>(r.y),
@@ -476,6 +483,10 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     case IMPL_STEM_BF16: describe_stem_bf16(buf, len, launches); break;
     case IMPL_POOL_NHWC:
         snprintf(buf, len, "maxpool_nhwc_bf16_kernel");
+        *launches = 1;
+        break;
+    case IMPL_POOL_F32:
+        snprintf(buf, len, "maxpool_kernel");
         *launches = 1;
         break;
     default: describe_direct(r.kind == OP_DENSE_BF16, buf, len, launches); break;

@@ -225,7 +225,7 @@ hipError_t launch_maxpool_nhwc_bf16(int N, int C, int H, int W, int R, int S, in
 
 // A validated conv call with its kernel fixed (what the ABI entry points and
 // the stack executor enqueue).
-enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2, OP_MAXPOOL_BF16_NHWC = 3 };
+enum OpKind { OP_DENSE_F32 = 0, OP_DENSE_BF16 = 1, OP_DW_F32 = 2, OP_MAXPOOL_BF16_NHWC = 3, OP_MAXPOOL_F32 = 4 };
 // Layout flags of a bf16 dense layer (enum miconv_layout).
 enum LayoutFlags { LAYOUT_X_NHWC = 1, LAYOUT_Y_NHWC_BF16 = 2 };
 enum Impl {
@@ -236,7 +236,8 @@ enum Impl {
     IMPL_IGEMM_BF16 = 4,
     IMPL_NHWC_BF16 = 5,
     IMPL_STEM_BF16 = 6,
-    IMPL_POOL_NHWC = 7
+    IMPL_POOL_NHWC = 7,
+    IMPL_POOL_F32 = 8
 };
 // What a call may use besides its tensors.
 enum PlanMode {

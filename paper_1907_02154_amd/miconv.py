@@ -451,7 +451,7 @@ def conv2d_describe(N, C, H, W, K, R, S, stride, pad, groups=1, dtype="f32", alg
     return buf.value.decode(), n.value
 
 
-OP_CONV_F32, OP_CONV_BF16, OP_DWCONV_F32, OP_MAXPOOL_BF16_NHWC = 0, 1, 2, 3
+OP_CONV_F32, OP_CONV_BF16, OP_DWCONV_F32, OP_MAXPOOL_BF16_NHWC, OP_MAXPOOL_F32 = 0, 1, 2, 3, 4
 # enum miconv_layout flags
 LAYOUT_NCHW, LAYOUT_X_NHWC, LAYOUT_Y_NHWC_BF16 = 0, 1, 2
 
@@ -545,15 +545,22 @@ class Stack:
         descs = (ConvDesc * len(layers))()
         for d, layer in zip(descs, layers):
             if layer[0] == "maxpool":
-                # ("maxpool", x, y, R, S, stride, pad): bf16 channel-last glue
+                # ("maxpool", x, y, R, S, stride, pad): glue, bf16 channel-last
+                # ([N][H][W][C] tensors) or fp32 NCHW
                 _, x, y, R, S, stride, pad = layer
-                _dev(x, torch.bfloat16, "x", 4)
-                _dev(y, torch.bfloat16, "y", 4)
-                N, H, W, C = x.shape
+                cl = x.dtype == torch.bfloat16
+                _dev(x, x.dtype if cl else torch.float32, "x", 4)
+                _dev(y, x.dtype, "y", 4)
+                if cl:
+                    N, H, W, C = x.shape
+                else:
+                    N, C, H, W = x.shape
                 P, Q = out_dims(H, W, R, S, stride, pad)
-                if tuple(y.shape) != (N, P, Q, C):
-                    raise ValueError(f"y must have shape {(N, P, Q, C)}")
-                d.op, d.N, d.C, d.H, d.W, d.K, d.R, d.S = OP_MAXPOOL_BF16_NHWC, N, C, H, W, C, R, S
+                want = (N, P, Q, C) if cl else (N, C, P, Q)
+                if tuple(y.shape) != want:
+                    raise ValueError(f"y must have shape {want}")
+                d.op = OP_MAXPOOL_BF16_NHWC if cl else OP_MAXPOOL_F32
+                d.N, d.C, d.H, d.W, d.K, d.R, d.S = N, C, H, W, C, R, S
                 d.stride, d.pad, d.groups, d.relu = stride, pad, 1, 0
                 d.x, d.y = x.data_ptr(), y.data_ptr()
                 self._keep.append((x, y))
