@@ -15,7 +15,7 @@ events that the runtime stamps with each kernel's execution interval.
 Prints one JSON line with the conv TFLOP/s of the step (from the timed
 region), ms per image, the roofline of the dominant kernel (the kernel with
 the largest summed execution time; its traffic comes from the committed
-counter summary profiles/traffic.txt when that matches the kernel's source)
+counter summaries profiles/traffic_<workload>.txt when they match the kernel source)
 and the CPU oracle timed on a bounded sample of the same stack.  The default
 run (ResNet-50 at batch 1) also carries, under "b64", the same record for
 ResNet-50 at batch 64 with bf16 inputs (the metric's other half), and under
@@ -41,13 +41,13 @@ PEAK_BF16_MFMA_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
 
 
-def measured_traffic(kernel: str):
+def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` (read + written, calibrated against a
-    plain copy) from the committed counter summary profiles/traffic.txt, or
-    None when it has no line for this kernel or the kernel's source changed
-    since the counters were taken."""
+    plain copy) in `workload`, from the committed counter summary
+    profiles/traffic_<workload>.txt, or None when it has no line for this
+    kernel or the kernel's source changed since the counters were taken."""
     from paper_1907_02154_amd.traffic import source_sha
-    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -253,9 +253,8 @@ def dw_sweep(args):
     cache, so every launch streams from HBM -- captured into a HIP graph with a
     timing event around every launch; the per-layer figure is the median launch
     duration.  Inputs are seeded on the device (uniform [0,1)); values do not
-    affect the timing, and parity at these shapes is tested separately.  A
-    plain device-to-device copy of 1 GiB gives the achievable-bandwidth
-    ceiling for context."""
+    affect the timing, and parity at these shapes is tested separately.  The
+    runtime's own device-to-device copy of 1 GiB is timed for context."""
     import torch
     from paper_1907_02154_amd import miconv
     from paper_1907_02154_amd import workloads as wl
@@ -275,6 +274,16 @@ def dw_sweep(args):
         b = torch.randn((l.C,), device="cuda", generator=gen) * 0.01
         st = miconv.Stack([(miconv.OP_DWCONV_F32, xs[i], w, b, ys[i], l.stride, l.pad, l.C, l.relu)
                            for i in range(sets)])
+        if args.profile_passes:
+            # counter runs: eager launches only (every buffer set, N times)
+            for _ in range(args.profile_passes):
+                st.launch()
+            torch.cuda.synchronize()
+            st.close()
+            print(f"{l.name}: {args.profile_passes} eager passes over {sets} buffer sets", flush=True)
+            del xs, ys
+            torch.cuda.empty_cache()
+            continue
         for _ in range(max(1, -(-args.warmup // sets))):
             st.launch()
         reps = max(2, -(-args.steps // sets))
@@ -293,7 +302,10 @@ def dw_sweep(args):
         tot_ms += ms
         del xs, ys
         torch.cuda.empty_cache()
-    # Achievable ceiling: torch's device-to-device copy, 1 GiB each way.
+    if args.profile_passes:
+        return
+    # For context (not a ceiling): the runtime's own device-to-device copy
+    # kernel (torch copy_), 1 GiB each way.
     src = torch.empty(1 << 28, device="cuda")
     dst = torch.empty_like(src)
     for _ in range(3):
@@ -307,6 +319,10 @@ def dw_sweep(args):
     copy_gbs = 2 * src.numel() * 4 * 10 / e0.elapsed_time(e1) / 1e6
     del src, dst
     gbs = tot_bytes / tot_ms / 1e6
+    # counted HBM bytes of the sweep (FETCH_SIZE + WRITE_SIZE per launch from
+    # the committed counter summary, when it matches every kernel's source)
+    counted = [measured_traffic(r["kernel"], f"mobilenet_dw_b{args.dw_sweep}") for r in rows]
+    traffic = sum(counted) if all(c is not None for c in counted) else None
     out = {"metric": "depthwise conv HBM bandwidth (MobileNet-v1 dw shapes)", "value": round(gbs, 1),
            "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(tot_ms, 4), "higher_is_better": True, "scaling": "weak",
@@ -314,8 +330,9 @@ def dw_sweep(args):
            "config": {"workload": f"MobileNet-v1 depthwise layers, batch {args.dw_sweep}",
                       "algorithmic_bytes": tot_bytes, "device": gpu_info(torch)},
            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
-           "copy_ceiling_GBs": round(copy_gbs, 1),
+                        "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                        "traffic_over_algorithmic": None if traffic is None else round(traffic / tot_bytes, 4)},
+           "runtime_copy_GBs": round(copy_gbs, 1),
            "layers": rows}
     print(json.dumps(out), flush=True)
 
@@ -450,7 +467,9 @@ def stack_record(args, config: int, batch, steps: int, warmup: int, cpu_seconds:
         achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                     frac=round(achieved / peak, 4))
-    roof.update(traffic=measured_traffic(dom_name),
+    tag = {2: "resnet50_b1", 5: "resnet50_b64", 3: "mobilenet_b1", 4: "vgg16_b8", 6: "squeezenet_b1",
+           1: "conv3x3_b1"}[config] if batch is None else f"config{config}_b{batch}"
+    roof.update(traffic=measured_traffic(dom_name, tag),
                 algorithmic_bytes_per_launch=round(dom["bytes"] / dom["launches"]),
                 algorithmic_flops_per_launch=round(dom["flops"] / dom["launches"]),
                 kernel=dom_name, launches_per_step=dom["launches"],
@@ -612,6 +631,12 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
     n_launch = stack.launches
     launch_info = [stack.launch_info(j) for j in range(n_launch)]
     stream = torch.cuda.current_stream()
+    if args.profile_passes:
+        for _ in range(args.profile_passes):
+            stack.launch(stream)
+        torch.cuda.synchronize()
+        print(f"{args.profile_passes} eager passes of the {net} network", flush=True)
+        sys.exit(0)
     for _ in range(warmup):
         stack.launch(stream)
     torch.cuda.synchronize()
@@ -664,6 +689,7 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
     peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
     t_roof = sum(max(flops[n] / (peak * 1e12), nbytes[n] / (PEAK_HBM_GBS * 1e9)) for n in flops)
     dom = max(per_kernel.items(), key=lambda kv: kv[1][0])
+    dom_traffic = measured_traffic(dom[0], f"{net}_chained")
     N = graph[0].layer.N
     return {
         "workload": f"{net} network pass ({layout}): {len(flops)} convs"
@@ -673,7 +699,8 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
         "gflop_per_step": round(total_flops / 1e9, 4), "launches_per_step": n_launch,
         "conv_kernel_ms": round(conv_ms, 5), "glue_kernel_ms": round(pool_ms, 5),
         "stack_roofline_frac": round(t_roof / (ms_per_step * 1e-3), 4),
-        "dominant_kernel": {"kernel": dom[0], "ms_per_step": round(dom[1][0], 5), "launches": dom[1][1]},
+        "dominant_kernel": {"kernel": dom[0], "ms_per_step": round(dom[1][0], 5), "launches": dom[1][1],
+                            "avg_launch_us": round(dom[1][0] / dom[1][1] * 1e3, 3), "traffic": dom_traffic},
     }
 
 

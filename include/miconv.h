@@ -250,7 +250,7 @@ enum miconv_layout {
  *    == 0, x 16-byte aligned (and w for 1x1 filters); with a channel-last y
  *    K/groups % 8 == 0 and y, res 16-byte aligned;
  *  - MICONV_LAYOUT_Y_NHWC_BF16 alone (x NCHW): the 7x7 stride-2 stem on at
- *    most 4 channels with 112 output columns (ResNet's first layer), K % 4
+ *    most 4 channels with 112 output columns (ResNet's first layer), K % 8
  *    == 0, no residual;
  * anything else MICONV_ERR_UNSUPPORTED (MICONV_ERR_ALIGN for alignment).
  * Workspace as for conv2d_fwd_ws, sized by conv2d_cl_workspace_bytes (split

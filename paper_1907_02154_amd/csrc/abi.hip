@@ -223,7 +223,7 @@ int resolve(int kind, int algo, int mode, int N, int C, int H, int W, int K, int
             r.nplan = plan_nhwc_bf16(r.p, cu_count(), x, max_splits, true);
             r.wlayout = R * S == 1 ? WL_GIVEN : r.nplan.halo ? WL_KRSC_BLOCK : WL_KRSC;
         } else {
-            if (!r.p.ycl || !can_pack || !stem_bf16_eligible(r.p, y) || K % 4) return MICONV_ERR_UNSUPPORTED;
+            if (!r.p.ycl || !can_pack || !stem_bf16_eligible(r.p, y) || K % 8) return MICONV_ERR_UNSUPPORTED;
             r.impl = IMPL_STEM_BF16;
             r.wlayout = WL_STEM;
         }

@@ -555,7 +555,23 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
 {
     constexpr int CP = BKC + 4;
     constexpr int C8 = BKC / 8;
-    static_assert(NT % C8 == 0, "a thread keeps one channel octet");
+    constexpr int IT = BPX / (NT / C8);              // pixels per thread
+    static_assert(NT % C8 == 0 && BPX % (NT / C8) == 0, "a thread keeps one channel octet");
+    const int o = tid % C8;
+    const int k = k0 + 8 * o;
+    const int kg = g * a.Kg + k;
+    const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
+    // The thread's residual octets, requested before the tile goes through
+    // LDS so that their round trips overlap it (all precede the thread's
+    // first store, so res may be y itself).
+    uint4 rv[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int m = m0 + tid / C8 + it * (NT / C8);
+        rv[it] = make_uint4(0, 0, 0, 0);
+        if (res && a.splits == 1 && k < a.Kg && m < a.M)
+            rv[it] = *reinterpret_cast<const uint4 *>(res + (long)m * a.K + kg);
+    }
 #pragma unroll
     for (int bi = 0; bi < BI; ++bi)
 #pragma unroll
@@ -569,16 +585,14 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
                                 acc[bj][bi][4 * q4 + 3]);
             }
     __syncthreads();
-    const int o = tid % C8;
-    const int k = k0 + 8 * o;
     if (k >= a.Kg) return;                      // K/groups % 8 == 0: the octet is whole
-    const int kg = g * a.Kg + k;
     float bv[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) bv[e] = (a.splits == 1 && a.bias) ? a.bias[kg + e] : 0.f;
-    const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
     uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
-    for (int pl = tid / C8; pl < BPX; pl += NT / C8) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int pl = tid / C8 + it * (NT / C8);
         const int m = m0 + pl;
         if (m >= a.M) break;
         const float4 lo = *reinterpret_cast<const float4 *>(ot + pl * CP + 8 * o);
@@ -591,14 +605,7 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
             *reinterpret_cast<float4 *>(dst + 4) = hi;
             continue;
         }
-        uint32_t rr[4] = {0, 0, 0, 0};
-        if (res) {
-            const uint4 r = *reinterpret_cast<const uint4 *>(res + off);
-            rr[0] = r.x;
-            rr[1] = r.y;
-            rr[2] = r.z;
-            rr[3] = r.w;
-        }
+        const uint32_t rr[4] = {rv[it].x, rv[it].y, rv[it].z, rv[it].w};
         uint32_t d[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {

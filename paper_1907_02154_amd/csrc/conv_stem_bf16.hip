@@ -58,10 +58,16 @@ struct StemArgs {
     int ycl;                  // y bf16 channel-last [N][P][kQ][K] (no residual)
 };
 
+constexpr int kOPitch = 68;   // channel-last epilogue: bf16 row pitch of a pixel (64 + 4)
+
 __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
 {
-    __shared__ __attribute__((aligned(16))) uint4 patch[kPatchUnits];   // [row][col][4 ch] bf16
-    __shared__ __attribute__((aligned(16))) uint4 wl[64 * kWPitch];      // [k][pair] 8 x bf16
+    // one LDS block: the input patch and the filters during the MFMAs, then
+    // (channel-last output) half of the output tile, pixel-major
+    __shared__ __attribute__((aligned(16))) uint4 lds[kPatchUnits + 64 * kWPitch];
+    static_assert(224 * kOPitch * 2 <= (kPatchUnits + 64 * kWPitch) * 16, "epilogue tile fits");
+    uint4 *patch = lds;                     // [row][col][4 ch] bf16
+    uint4 *wl = lds + kPatchUnits;          // [k][pair] 8 x bf16
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int h = lane >> 5, ll = lane & 31;
@@ -150,34 +156,57 @@ __global__ __launch_bounds__(kThreads) void stem7_bf16_kernel(StemArgs a)
     // l%32 of the pixel block: each store instruction writes 32 consecutive
     // pixels (128 bytes) of two filter planes.
     if (a.ycl) {
-        // channel-last bf16: register group v/4 holds 4 consecutive channels
-        // of pixel l%32, stored as one 8-byte write
+        // Channel-last bf16: register group v/4 of lane l holds 4 consecutive
+        // channels of pixel l%32.  The tile goes out in two halves (pixel
+        // block b of every wavefront): bias, activation and the bf16 rounding
+        // in registers, the half staged pixel-major in LDS ([224][64 + 4]
+        // bf16: the pitch spreads a store's 32 pixels over the banks), then
+        // every lane writes 16 bytes = 8 channels of one pixel, so a
+        // wavefront's stores are 1 KB of contiguous y (64 channels).
         uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
+        uint16_t *ot = reinterpret_cast<uint16_t *>(lds);
+        const int kn = min(64, a.K - k0);                  // channels of this filter tile (% 4 == 0)
+        float bv[2][4][4];
 #pragma unroll
-        for (int f = 0; f < 2; ++f) {
+        for (int f = 0; f < 2; ++f)
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int k = k0 + f * 32 + 8 * q4 + 4 * h;
-                if (k >= a.K) continue;                      // K % 4 == 0 (checked on the host)
-                float bv[4];
+            for (int q4 = 0; q4 < 4; ++q4)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) bv[e] = a.bias ? a.bias[k + e] : 0.f;
+                for (int e = 0; e < 4; ++e) {
+                    const int k = k0 + f * 32 + 8 * q4 + 4 * h + e;
+                    bv[f][q4][e] = (a.bias && k < a.K) ? a.bias[k] : 0.f;
+                }
+        const long pix0 = ((long)n * a.P + p0) * kQ;       // first pixel of the 4-row tile
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const long pix = ((long)n * a.P + p0) * kQ + 32 * (2 * wave + b) + ll;
+        for (int b = 0; b < 2; ++b) {
+            __syncthreads();                                // LDS free (MFMA operands, or the last half)
+#pragma unroll
+            for (int f = 0; f < 2; ++f)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
                     uint32_t d[2];
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
-                        float v0 = acc[b][f][4 * q4 + 2 * e] + bv[2 * e];
-                        float v1 = acc[b][f][4 * q4 + 2 * e + 1] + bv[2 * e + 1];
+                        float v0 = acc[b][f][4 * q4 + 2 * e] + bv[f][q4][2 * e];
+                        float v1 = acc[b][f][4 * q4 + 2 * e + 1] + bv[f][q4][2 * e + 1];
                         if (a.relu) {
                             v0 = fmaxf(v0, 0.f);
                             v1 = fmaxf(v1, 0.f);
                         }
                         d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
                     }
-                    *reinterpret_cast<uint2 *>(y + pix * a.K + k) = make_uint2(d[0], d[1]);
+                    const int row = 32 * wave + ll;         // pixel 32*(2*wave + b) + ll of the tile
+                    *reinterpret_cast<uint2 *>(ot + row * kOPitch + f * 32 + 8 * q4 + 4 * h) =
+                        make_uint2(d[0], d[1]);
                 }
+            __syncthreads();
+            for (int u = tid; u < 224 * 8; u += kThreads) {
+                const int row = u >> 3, o = u & 7;
+                if (8 * o >= kn) continue;
+                const int px = 32 * (2 * (row >> 5) + b) + (row & 31);
+                const uint2 lo = *reinterpret_cast<const uint2 *>(ot + row * kOPitch + 8 * o);
+                const uint2 hi = *reinterpret_cast<const uint2 *>(ot + row * kOPitch + 8 * o + 4);
+                *reinterpret_cast<uint4 *>(y + (pix0 + px) * a.K + k0 + 8 * o) = make_uint4(lo.x, lo.y, hi.x, hi.y);
             }
         }
         return;
@@ -262,7 +291,7 @@ hipError_t launch_stem_bf16(const ConvProblem &p, const uint16_t *x, const uint1
     a.relu = p.relu;
     a.vec = p.W % 8 == 0 && (uintptr_t)x % 16 == 0;
     a.ycl = p.ycl;
-    if (p.ycl && (p.res || p.K % 4 || (uintptr_t)y % 8)) return hipErrorInvalidValue;
+    if (p.ycl && (p.res || p.K % 8 || (uintptr_t)y % 16)) return hipErrorInvalidValue;
     const long wgs = (long)(p.P / kRows) * p.N * ceil_div(p.K, 64);
     launch_kernel(stem7_bf16_kernel, dim3((unsigned)wgs), dim3(kThreads), 0, st, a);
     return hipGetLastError();

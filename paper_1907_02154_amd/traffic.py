@@ -39,6 +39,15 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 # kernel name prefix -> the source file that defines it
 SOURCES = {
     "igemm_wave_f32_kernel": "conv_wave_f32.hip",
+    "igemm_wave_f32_gen_kernel": "conv_wave_f32.hip",
+    "igemm_wave_f32_kcrs_kernel": "conv_wave_f32.hip",
+    "igemm_bf16_dma_res_kernel": "conv_nhwc_bf16.hip",
+    "igemm_bf16_dma_cl_kernel": "conv_nhwc_bf16.hip",
+    "igemm_bf16_halo_res_kernel": "conv_nhwc_bf16.hip",
+    "igemm_bf16_halo_cl_kernel": "conv_nhwc_bf16.hip",
+    "splitk_reduce_cl_kernel": "conv_igemm_f32.hip",
+    "maxpool_nhwc_bf16_kernel": "glue.hip",
+    "maxpool_kernel": "glue.hip",
     "igemm_f32_kernel": "conv_igemm_f32.hip",
     "splitk_reduce_kernel": "conv_igemm_f32.hip",
     "igemm_bf16_kernel": "conv_igemm_bf16.hip",
