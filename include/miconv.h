@@ -261,6 +261,12 @@ int conv2d_fwd_cl(int N, int C, int H, int W, int K, int R, int S, int stride, i
                   int layout, const uint16_t *x, const uint16_t *w, const float *bias, const void *res,
                   void *y, int relu, void *ws, size_t ws_bytes, void *stream);
 
+/* The kernels conv2d_fwd_cl would launch for this shape and layout (with its
+ * workspace), as conv2d_describe names them; validates like conv2d_fwd_cl
+ * (pointers taken as 256-byte aligned); enqueues nothing. */
+int conv2d_cl_describe(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                       int layout, char *buf, int buflen, int *launches);
+
 /* Glue operators of the evaluated networks (not part of the conv operator). */
 
 /* Max-pool on bf16 channel-last tensors: x [N][H][W][C] -> y [N][P][Q][C],

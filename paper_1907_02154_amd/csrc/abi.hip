@@ -657,6 +657,20 @@ int conv2d_fwd_cl(int N, int C, int H, int W, int K, int R, int S, int stride, i
     return rc != MICONV_OK ? rc : run(r, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
+int conv2d_cl_describe(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int groups,
+                       int layout, char *buf, int buflen, int *launches)
+{
+    if (!buf || buflen <= 0 || !launches) return MICONV_ERR_NULL;
+    buf[0] = 0;
+    alignas(256) static const float stand_in[64] = {};
+    Resolved r;
+    const int rc = resolve(OP_DENSE_BF16, MICONV_ALGO_AUTO, MODE_SCRATCH, N, C, H, W, K, R, S, stride, pad,
+                           groups, stand_in, stand_in, nullptr, const_cast<float *>(stand_in), 0, &r, layout);
+    if (rc != MICONV_OK) return rc;
+    describe(r, buf, buflen, launches);
+    return MICONV_OK;
+}
+
 int maxpool2d_nhwc_bf16(int N, int C, int H, int W, int R, int S, int stride, int pad, const uint16_t *x,
                         uint16_t *y, void *stream)
 {

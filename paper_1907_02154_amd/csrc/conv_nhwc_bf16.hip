@@ -1443,6 +1443,15 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
     // planner takes them only when 128 x 64 leaves CUs idle), so tile 2 always
     // has three stages (1024-channel 1x1, stride 2, 14x14 -> 7x7: 17.7 -> 14.1 us).
     if (plan.nchwb != 1 && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
+    // Channel-last 1x1 layers with at most 4 reduction chunks and at least
+    // 256 output channels (ResNet's expansions and projections) are bound by
+    // each tile's load -> epilogue latency: 128 x 64 tiles (three work-groups
+    // per CU, so one's epilogue overlaps another's loads) beat 128 x 128
+    // (measured at batch 64, bf16 channel-last: 64 -> 256 at 56x56 with the
+    // residual 61 -> 54 us, 128 -> 512 at 28x28 38 -> 35 us, 256 -> 1024 at
+    // 14x14 25.5 -> 24.4 us); with more chunks 128 x 128 stays ahead.
+    if (x_nhwc && p.R == 1 && p.S == 1 && chunks <= 4 && p.Kg >= 256 && splits == 1 && wgs(1) >= num_cus)
+        plan.tile = 1;
     // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
     // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
     // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With

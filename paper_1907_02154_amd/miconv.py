@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
         L.conv2d_cl_workspace_bytes.restype = l
         L.conv2d_fwd_cl.argtypes = [i] * 11 + [p, p, p, p, p, i, p, ctypes.c_size_t, p]
         L.conv2d_fwd_cl.restype = i
+        L.conv2d_cl_describe.argtypes = [i] * 11 + [ctypes.c_char_p, i, ctypes.POINTER(i)]
+        L.conv2d_cl_describe.restype = i
         L.maxpool2d_nhwc_bf16.argtypes = [i] * 8 + [p, p, p]
         L.maxpool2d_nhwc_bf16.restype = i
         L.conv2d_describe.restype = i
@@ -515,6 +517,16 @@ def conv2d_fwd_cl(x, w, bias, y, stride=1, pad=0, groups=1, relu=False, res=None
                              0 if ws is None else ws.numel(), _stream(stream))
     _check(rc, "conv2d_fwd_cl")
     return y
+
+
+def conv2d_cl_describe(N, C, H, W, K, R, S, stride, pad, groups=1,
+                       layout=LAYOUT_X_NHWC | LAYOUT_Y_NHWC_BF16):
+    """(kernel names, launch count) of conv2d_fwd_cl for this shape and layout."""
+    buf = ctypes.create_string_buffer(256)
+    n = ctypes.c_int()
+    _check(lib().conv2d_cl_describe(N, C, H, W, K, R, S, stride, pad, groups, int(layout), buf, 256,
+                                    ctypes.byref(n)), "conv2d_cl_describe")
+    return buf.value.decode(), n.value
 
 
 def maxpool2d_nhwc_bf16(x, y, R, S, stride, pad=0, stream=None):

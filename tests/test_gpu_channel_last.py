@@ -50,8 +50,9 @@ def nhwc(a):
 # (N, C, H, W, K, R, S, stride, pad, groups, layout, kernel the call must use)
 CL_CASES = [
     (4, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
-    (16, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 3, 0, 64>"),
-    (64, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 128, 2, 2, 2, 0, 64>"),
+    (16, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 2, 0, 64>"),
+    (16, 256, 28, 28, 128, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
+    (64, 512, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 128, 2, 2, 2, 0, 64>"),
     (4, 256, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, "),
     (8, 256, 28, 28, 128, 1, 1, 2, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, "),                # stride 2
     (3, 64, 9, 11, 72, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, "),                   # ragged M, K
