@@ -549,29 +549,47 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // the raw fp32 sums go to this split's partials [M][K] instead (two 16-byte
 // stores) for splitk_reduce_cl_kernel.  Requires K/groups % 8 == 0 and y,
 // res 16-byte aligned (checked on the host).
-template <int BPX, int BKC, int NT, int TPX, int TCH, int BJ, int BI>
-__device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][BI], float *ot, int tid,
-                                   int wpx, int wch, int h, int ll, int k0, int m0, int g, int split)
+template <int BPX, int BKC, int NT>
+struct ClRes {
+    static constexpr int C8 = BKC / 8;
+    static constexpr int IT = BPX / (NT / C8);       // pixels per thread
+    uint4 rv[IT];
+};
+
+// The thread's residual octets (the ones its epilogue_cl stores), requested
+// ahead so that their round trips overlap other work (all precede the
+// thread's first store, so res may be y itself).
+template <int BPX, int BKC, int NT>
+__device__ inline void cl_res_load(const ConvArgs &a, ClRes<BPX, BKC, NT> &r, int tid, int k0, int m0, int g)
 {
-    constexpr int CP = BKC + 4;
     constexpr int C8 = BKC / 8;
-    constexpr int IT = BPX / (NT / C8);              // pixels per thread
+    constexpr int IT = BPX / (NT / C8);
     static_assert(NT % C8 == 0 && BPX % (NT / C8) == 0, "a thread keeps one channel octet");
     const int o = tid % C8;
     const int k = k0 + 8 * o;
     const int kg = g * a.Kg + k;
     const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
-    // The thread's residual octets, requested before the tile goes through
-    // LDS so that their round trips overlap it (all precede the thread's
-    // first store, so res may be y itself).
-    uint4 rv[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
         const int m = m0 + tid / C8 + it * (NT / C8);
-        rv[it] = make_uint4(0, 0, 0, 0);
+        r.rv[it] = make_uint4(0, 0, 0, 0);
         if (res && a.splits == 1 && k < a.Kg && m < a.M)
-            rv[it] = *reinterpret_cast<const uint4 *>(res + (long)m * a.K + kg);
+            r.rv[it] = *reinterpret_cast<const uint4 *>(res + (long)m * a.K + kg);
     }
+}
+
+template <int BPX, int BKC, int NT, int TPX, int TCH, int BJ, int BI>
+__device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][BI], float *ot, int tid,
+                                   int wpx, int wch, int h, int ll, int k0, int m0, int g, int split,
+                                   const ClRes<BPX, BKC, NT> &cr)
+{
+    constexpr int CP = BKC + 4;
+    constexpr int C8 = BKC / 8;
+    constexpr int IT = BPX / (NT / C8);              // pixels per thread
+    const int o = tid % C8;
+    const int k = k0 + 8 * o;
+    const int kg = g * a.Kg + k;
+    const uint4 *rv = cr.rv;
 #pragma unroll
     for (int bi = 0; bi < BI; ++bi)
 #pragma unroll
@@ -610,7 +628,7 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float v0 = v[2 * e] + bv[2 * e], v1 = v[2 * e + 1] + bv[2 * e + 1];
-            if (res) {
+            if (a.res) {
                 v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
                 v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
             }
@@ -652,7 +670,7 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
     constexpr int LA = UA / NT, LB = UB / NT;           // load instructions per lane per chunk
     constexpr int LOADS = LA + (NCHWB == 2 ? KRC / (WPX * WCH) : LB);
     static_assert(BJ >= 1 && BI >= 1 && UA % NT == 0 && UB % NT == 0, "tile shape");
-    static_assert(NST >= 2 && NST <= 8 && (NST - 2) * LOADS <= 63, "pipeline depth");
+    static_assert(NST >= 1 && NST <= 8 && (NST - 2) * LOADS <= 63, "pipeline depth");
     static_assert(!NCHWB || (BPX == 128 && R_ == 1 && S_ == 1 && KRC == 64), "NCHW pixel operand: 1x1, 128-pixel tiles");
     static_assert(NCHWB != 2 || (KRC / WPX / WCH) * WPX * WCH == KRC, "one channel row per load");
     static_assert(KRC == 64 || KRC == 32, "reduction chunk");
@@ -867,25 +885,42 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
                 }
     };
 
+    // the residual of the channel-last epilogue: the work-group's first
+    // requests, landed by the time the first reduction chunk has
+    ClRes<BPX, BKC, NT> cr;
+    if constexpr (YCL) cl_res_load<BPX, BKC, NT>(a, cr, tid, k0, m0, g);
+
     const int nchunks = kr_end > kr_begin ? (kr_end - kr_begin) / KRC : 0;
+    if constexpr (NST == 1) {
+        // one stage (layers of one or two chunks): no overlap inside the
+        // work-group, a third of the LDS, more work-groups per CU
+        for (int t = 0; t < nchunks; ++t) {
+            if (t) asm volatile("s_barrier" ::: "memory");   // every wavefront is done with chunk t-1
+            issue(t);
+            wait_vmcnt<0>();
+            asm volatile("s_barrier" ::: "memory");
+            compute(t);
+        }
+    } else {
 #pragma unroll
-    for (int t = 0; t < NST - 1; ++t)
-        if (t < nchunks) issue(t);
-    for (int t = 0; t < nchunks; ++t) {
-        // this lane's loads of chunk t are done once at most `ahead` later
-        // chunks' loads are outstanding
-        const int ahead = min(NST - 2, nchunks - 1 - t);
-        wait_ahead<LOADS, NST - 2>(ahead);
-        // every lane's chunk t is in LDS, and every wavefront is done with chunk t-1
-        asm volatile("s_barrier" ::: "memory");
-        if (t + NST - 1 < nchunks) issue(t + NST - 1);
-        compute(t);
+        for (int t = 0; t < NST - 1; ++t)
+            if (t < nchunks) issue(t);
+        for (int t = 0; t < nchunks; ++t) {
+            // this lane's loads of chunk t are done once at most `ahead` later
+            // chunks' loads are outstanding
+            const int ahead = min(NST - 2, nchunks - 1 - t);
+            wait_ahead<LOADS, NST - 2>(ahead);
+            // every lane's chunk t is in LDS, and every wavefront is done with chunk t-1
+            asm volatile("s_barrier" ::: "memory");
+            if (t + NST - 1 < nchunks) issue(t + NST - 1);
+            compute(t);
+        }
     }
 
     if constexpr (YCL) {
         __syncthreads();   // every wavefront is done with the operand stages
         epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch, h,
-                                                    ll, k0, m0, g, split);
+                                                    ll, k0, m0, g, split, cr);
         return;
     }
     // Epilogue through LDS: the tile (BKC channels x BPX pixels, fp32, bias and
@@ -1126,6 +1161,11 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
                 }
     };
 
+    // the residual of the channel-last epilogue: the work-group's first
+    // requests, landed by the time the first reduction chunk has
+    ClRes<BPX, BKC, NT> cr;
+    if constexpr (YCL) cl_res_load<BPX, BKC, NT>(a, cr, tid, k0, m0, g);
+
     if (t_begin < t_end) {
         issue_a(t_begin);
         issue_patch(t_begin / 9);
@@ -1145,7 +1185,7 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     if constexpr (YCL) {
         __syncthreads();   // every wavefront is done with the filter stages and patches
         epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch, h,
-                                                    ll, k0, m0, g, split);
+                                                    ll, k0, m0, g, split, cr);
         return;
     }
     // Epilogue through LDS, as in igemm_bf16_dma_kernel.
@@ -1323,6 +1363,8 @@ const TileD kTilesD[] = {
     {128, 64, 2, 2, 2},    // 48 KB: three per CU, wavefront tile 64 x 32
     {64, 64, 2, 2, 3},     // 48 KB: three per CU, wavefront tile 32 x 32, three stages
     {128, 64, 2, 2, 3},    // tile 1 with a third stage: 72 KB, two per CU
+    {128, 64, 2, 2, 1},    // one stage (1x1 only): 34 KB with the channel-last epilogue, four per CU
+    {64, 64, 2, 2, 1},     // one stage (1x1 only): 17 KB, eight per CU
 };
 
 template <int R_, int S_>
@@ -1332,7 +1374,19 @@ void launch_dma_rs(const ConvArgs &a, int tile, dim3 grid, hipStream_t st)
     case 0: launch_dma<R_, S_, 128, 128, 2, 2, 2, 0>(a, grid, st); break;
     case 1: launch_dma<R_, S_, 128, 64, 2, 2, 2, 0>(a, grid, st); break;
     case 2: launch_dma<R_, S_, 64, 64, 2, 2, 3, 0>(a, grid, st); break;
-    default: launch_dma<R_, S_, 128, 64, 2, 2, 3, 0>(a, grid, st); break;
+    case 3: launch_dma<R_, S_, 128, 64, 2, 2, 3, 0>(a, grid, st); break;
+    default:
+        // tiles 4 and 5 are instantiated with one stage for 1x1 layers only
+        // (the planner's choice); any other layer gets the same tile shape
+        // pipelined
+        if constexpr (R_ == 1 && S_ == 1) {
+            if (tile == 4) launch_dma<1, 1, 128, 64, 2, 2, 1, 0>(a, grid, st);
+            else launch_dma<1, 1, 64, 64, 2, 2, 1, 0>(a, grid, st);
+        } else {
+            if (tile == 4) launch_dma<R_, S_, 128, 64, 2, 2, 2, 0>(a, grid, st);
+            else launch_dma<R_, S_, 64, 64, 2, 2, 3, 0>(a, grid, st);
+        }
+        break;
     }
 }
 
@@ -1443,15 +1497,18 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
     // planner takes them only when 128 x 64 leaves CUs idle), so tile 2 always
     // has three stages (1024-channel 1x1, stride 2, 14x14 -> 7x7: 17.7 -> 14.1 us).
     if (plan.nchwb != 1 && plan.tile == 1 && wgs(1) * splits <= 2L * num_cus) plan.tile = 3;
-    // Channel-last 1x1 layers with at most 4 reduction chunks and at least
-    // 256 output channels (ResNet's expansions and projections) are bound by
-    // each tile's load -> epilogue latency: 128 x 64 tiles (three work-groups
-    // per CU, so one's epilogue overlaps another's loads) beat 128 x 128
-    // (measured at batch 64, bf16 channel-last: 64 -> 256 at 56x56 with the
-    // residual 61 -> 54 us, 128 -> 512 at 28x28 38 -> 35 us, 256 -> 1024 at
-    // 14x14 25.5 -> 24.4 us); with more chunks 128 x 128 stays ahead.
-    if (x_nhwc && p.R == 1 && p.S == 1 && chunks <= 4 && p.Kg >= 256 && splits == 1 && wgs(1) >= num_cus)
-        plan.tile = 1;
+    // Channel-last 1x1 layers with at most 4 reduction chunks (ResNet's
+    // expansions and projections, the 256-channel reductions at 56x56) are
+    // bound by HBM and by each tile's load -> epilogue latency.  One LDS stage
+    // (no overlap inside a work-group) leaves room for four 128 x 64 or eight
+    // 64 x 64 work-groups per CU, whose loads overlap each other's epilogues
+    // (measured at batch 64, bf16 channel-last, against the best two-stage
+    // tile: 64 -> 256 at 56x56 with the residual 56.0 -> 51.2 us, 64 -> 256
+    // projection 48.6 -> 40.5 us, 128 -> 512 at 28x28 34.7 -> 31.7 us,
+    // 256 -> 1024 at 14x14 24.4 -> 21.6 us, 256 -> 64 at 56x56 on 64 x 64
+    // tiles 35.3 -> 30.2 us); with more chunks the pipelined tiles stay ahead.
+    if (x_nhwc && p.R == 1 && p.S == 1 && chunks <= 4 && splits == 1 && wgs(4) >= num_cus)
+        plan.tile = p.Kg >= 128 ? 4 : 5;
     // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
     // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
     // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With

@@ -7,7 +7,8 @@ fp64 sum rounded to fp32, then to bf16 (oracle.conv2d_bf16_cl).  On small
 integers every fp32 sum is exact, so both sides round the same value and
 must agree bit for bit, for every kernel instantiation (1x1 and 3x3
 direct-to-LDS tiles, the halo kernel, strided 1x1 and 3x3, split reductions
-with their channel-last reduce, groups, ragged tiles, the 7x7 stem).
+with their channel-last reduce, groups, ragged tiles, the one-stage 1x1
+tiles, the 7x7 stem).
 """
 import numpy as np
 import pytest
@@ -50,7 +51,9 @@ def nhwc(a):
 # (N, C, H, W, K, R, S, stride, pad, groups, layout, kernel the call must use)
 CL_CASES = [
     (4, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
-    (16, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 2, 0, 64>"),
+    (16, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),   # one stage
+    (17, 128, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),  # 2 chunks, ragged M
+    (42, 64, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 1, 0, 64>"),     # one stage, 64 x 64
     (16, 256, 28, 28, 128, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
     (64, 512, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 128, 2, 2, 2, 0, 64>"),
     (4, 256, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, "),
