@@ -18,6 +18,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmiconv.so")
 HEADER = os.path.join(os.path.dirname(_PKG), "include", "miconv.h")
+HEADERS = [HEADER, os.path.join(os.path.dirname(_PKG), "include", "mivision.h")]
 
 OK = 0
 (ERR_NULL, ERR_SHAPE, ERR_GROUPS, ERR_UNSUPPORTED, ERR_TOO_LARGE, ERR_ALIGN, ERR_HIP,
@@ -111,11 +112,14 @@ def lib() -> ctypes.CDLL:
 
 
 def header_functions() -> list:
-    """Names of the functions ``include/miconv.h`` declares."""
-    with open(HEADER) as f:
-        text = f.read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+    """Names of the functions ``include/miconv.h`` and ``include/mivision.h`` declare."""
+    names = set()
+    for h in HEADERS:
+        with open(h) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
 
 
 def strerror(status: int) -> str:

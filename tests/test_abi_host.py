@@ -1,6 +1,7 @@
 """Host-side checks of the C-ABI library (no GPU needed).
 
-The library must load, export every function ``include/miconv.h`` declares,
+The library must load, export every function ``include/miconv.h`` and
+``include/mivision.h`` declare,
 and reject invalid arguments before any HIP call (so these run on a machine
 without a GPU).  The fake pointers below are never dereferenced: every call
 here fails validation first.
@@ -24,7 +25,8 @@ def test_exports_every_declared_symbol(L):
     for expected in ("conv2d_fwd", "conv2d_fwd_bf16", "dwconv2d_fwd", "conv2d_fwd_algo",
                      "conv2d_workspace_bytes", "conv2d_fwd_ws",
                      "miconv_out_dims", "maxpool2d_fwd", "add_act_fwd", "cast_f32_to_bf16",
-                     "miconv_strerror", "miconv_last_hip_error", "miconv_version"):
+                     "miconv_strerror", "miconv_last_hip_error", "miconv_version",
+                     "vision_scan_i32", "vision_segmented_argsort", "vision_box_nms"):
         assert expected in names
     for n in names:
         assert hasattr(L, n), n
@@ -235,3 +237,37 @@ def test_noalloc_rejects_plans_beyond_its_scratch(L):
     assert L.conv2d_fwd_noalloc(*shape, 1, A, FAKE, FAKE, None, None, FAKE, 0, 0, None) == \
         miconv.ERR_WORKSPACE
     assert L.conv2d_fwd_noalloc(*shape, 1, A, None, FAKE, None, None, FAKE, 0, 0, None) == miconv.ERR_NULL
+
+
+def test_vision_validation(L):
+    """The vision entry points reject bad scalars before any HIP call."""
+    from paper_1907_02154_amd import vision
+    V = vision.lib()
+    assert V.vision_scan_workspace_bytes(0, 10) == miconv.ERR_SHAPE
+    assert V.vision_scan_workspace_bytes(1, 0) == miconv.ERR_SHAPE
+    assert V.vision_scan_workspace_bytes(1 << 16, 1 << 16) == miconv.ERR_TOO_LARGE
+    assert V.vision_scan_workspace_bytes(300, 1000) == 0          # one work-group per row: no workspace
+    assert V.vision_scan_workspace_bytes(1, 1 << 20) > 0          # across work-groups: tile sums
+    assert V.vision_scan_i32(1, 10, None, FAKE, 0, None, 0, None) == miconv.ERR_NULL
+    assert V.vision_scan_i32(1, 1 << 20, FAKE, FAKE, 0, None, 0, None) == miconv.ERR_WORKSPACE
+    assert V.vision_scan_i32(1, 1 << 20, FAKE, FAKE, 0, FAKE + 16, 1 << 30, None) == miconv.ERR_WORKSPACE
+    assert V.vision_argsort_workspace_bytes(0, 1) == miconv.ERR_SHAPE
+    assert V.vision_argsort_workspace_bytes(10, 0) == miconv.ERR_SHAPE
+    assert V.vision_argsort_workspace_bytes(2048, 1) == 0         # one block: sorted in place in LDS
+    assert V.vision_argsort_workspace_bytes(4096, 3) >= 4096 * 24
+    assert V.vision_segmented_argsort(100, 1, FAKE, None, 1, FAKE, None, 0, None) == miconv.ERR_NULL
+    assert V.vision_segmented_argsort(5000, 1, FAKE, FAKE, 1, FAKE, None, 0, None) == miconv.ERR_WORKSPACE
+    assert V.vision_box_nms_workspace_bytes(1, 5000, 6, -1) == miconv.ERR_UNSUPPORTED
+    assert V.vision_box_nms_workspace_bytes(1, 5000, 6, 4096) > 0
+    assert V.vision_box_nms_workspace_bytes(0, 5000, 6, 400) == miconv.ERR_SHAPE
+    nms = lambda **k: V.vision_box_nms(*[k.get(n, d) for n, d in (
+        ("B", 1), ("N", 100), ("W", 6), ("data", FAKE), ("out", FAKE), ("ov", 0.5), ("va", 0.0), ("topk", 50),
+        ("idx", 0), ("score", 1), ("coord", 2), ("force", 0), ("ws", FAKE), ("wsb", 1 << 30), ("st", None))])
+    assert nms(data=None) == miconv.ERR_NULL
+    assert nms(coord=3) == miconv.ERR_SHAPE
+    assert nms(score=6) == miconv.ERR_SHAPE
+    assert nms(idx=6) == miconv.ERR_SHAPE
+    assert nms(topk=-1, N=5000) == miconv.ERR_UNSUPPORTED
+    assert nms(data=FAKE + 2) == miconv.ERR_ALIGN
+    assert nms(ws=None) == miconv.ERR_WORKSPACE
+    assert nms(wsb=16) == miconv.ERR_WORKSPACE

@@ -1,0 +1,216 @@
+"""GPU: the vision operators (include/mivision.h) against the oracle
+(oracle/vision.py), through the C ABI.
+
+Integer and index results must match bit for bit: the prefix sums, the
+argsort's local indices (ties are broken by position on both sides, so the
+answer is unique), and box_nms's output, whose kept rows are copies of input
+rows and whose every other value is -1.  IoU is evaluated in fp32 with the
+same operations in the same order on both sides, so the threshold decisions
+agree.  Cases span single and several tiles, ragged tails, the one-row and
+across-work-group scan paths, empty and long segments, ties, signed zeros,
+NaN and infinite keys, topk limits, classes, force_suppress, no class field,
+several images, the largest candidate count, and the SSD-like detection
+workload at full size.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_1907_02154_amd import detections as det
+from paper_1907_02154_amd import miconv
+from paper_1907_02154_amd import vision
+
+pytestmark = pytest.mark.gpu
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "vision_examples.json")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    vision.lib()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+# ---------------------------------------------------------------- scan
+
+SCAN_CASES = [
+    (1, 1), (1, 4095), (1, 4096), (1, 4097), (3, 10000), (1, 16384), (1, 16385),   # one work-group per row
+    (2, 100000), (1, 1 << 20), (5, 70001),                                            # across work-groups
+    (300, 1000), (64, 20000),                                                          # many rows
+]
+
+
+@pytest.mark.parametrize("rows,n", SCAN_CASES, ids=[f"{r}x{n}" for r, n in SCAN_CASES])
+def test_scan_bitwise(oracle_lib, rows, n):
+    x = det.scan_values((rows, n), seed=rows * 7 + n)
+    assert vision.scan_workspace_bytes(rows, n) >= 0
+    tx = dev(x)
+    for exclusive in (False, True):
+        y = vision.scan_i32(tx, exclusive=exclusive)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        f = oracle_lib.scan_exclusive_i32 if exclusive else oracle_lib.scan_inclusive_i32
+        for r in range(rows):
+            np.testing.assert_array_equal(got[r], f(x[r]), err_msg=f"row {r} exclusive={exclusive}")
+
+
+def test_scan_in_place_and_hand_example(oracle_lib):
+    with open(GOLD) as f:
+        g = json.load(f)["scan"]
+    t = dev(np.int32(g["x"]))
+    vision.scan_i32(t, t)
+    torch.cuda.synchronize()
+    assert t.cpu().tolist() == g["inclusive"]
+    x = det.scan_values((2, 50000), seed=5)
+    t = dev(x)
+    vision.scan_i32(t, t, exclusive=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(t.cpu().numpy()[1], oracle_lib.scan_exclusive_i32(x[1]))
+
+
+# ---------------------------------------------------------------- argsort
+
+def _check_argsort(oracle_lib, keys, off, descending):
+    out = vision.segmented_argsort(dev(keys), dev(off), descending)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy(), oracle_lib.segmented_argsort(keys, off, descending))
+
+
+ARGSORT_CASES = [   # (n, segments, ties)
+    (7, 2, False), (2048, 1, False), (2049, 3, True), (5000, 40, True), (30000, 1, False),
+    (100000, 700, False), (100000, 13, True), (262144, 2000, False), (1000, 1000, True),
+]
+
+
+@pytest.mark.parametrize("n,segments,ties", ARGSORT_CASES, ids=[f"{a}-{b}-{c}" for a, b, c in ARGSORT_CASES])
+def test_segmented_argsort_bitwise(oracle_lib, n, segments, ties):
+    keys = det.keys(n, seed=n + segments, ties=ties)
+    off = det.segment_offsets(segments, n, seed=segments)
+    for descending in (True, False):
+        _check_argsort(oracle_lib, keys, off, descending)
+
+
+def test_argsort_hand_examples_and_special_keys(oracle_lib):
+    with open(GOLD) as f:
+        for c in json.load(f)["argsort"]:
+            out = vision.segmented_argsort(dev(np.float32(c["keys"])), dev(np.int32(c["offsets"])), c["descending"])
+            torch.cuda.synchronize()
+            assert out.cpu().tolist() == c["expect"], c
+    keys = np.float32([0.0, -0.0, np.inf, -np.inf, np.nan, 1.0, -1.0, np.nan, 0.0, -0.0] * 500)
+    off = det.segment_offsets(17, keys.size, seed=3)
+    for descending in (True, False):
+        _check_argsort(oracle_lib, keys, off, descending)
+
+
+def test_argsort_positions_past_the_segments():
+    """Positions at or past offsets[segments] belong to no segment: -1."""
+    keys = det.keys(5000, seed=1)
+    off = np.int32([0, 1000, 3000])
+    out = vision.segmented_argsort(dev(keys), dev(off)).cpu().numpy()
+    assert np.all(out[3000:] == -1)
+    assert sorted(out[:1000].tolist()) == list(range(1000))
+
+
+# ---------------------------------------------------------------- box_nms
+
+def _check_nms(oracle_lib, data, **kw):
+    got = vision.box_nms(dev(data), **kw)
+    torch.cuda.synchronize()
+    ref = oracle_lib.box_nms(data, **kw)
+    np.testing.assert_array_equal(got.cpu().numpy(), ref)
+    return ref
+
+
+def test_nms_hand_examples(oracle_lib):
+    with open(GOLD) as f:
+        for c in json.load(f)["nms"]:
+            d = np.float32(c["data"])[None]
+            _check_nms(oracle_lib, d, overlap_thresh=c["overlap_thresh"], valid_thresh=c["valid_thresh"],
+                       topk=c["topk"], force_suppress=c["force_suppress"])
+
+
+NMS_CASES = [   # (batch, num, topk, force, id_index, thresh)
+    (1, 50, -1, False, 0, 0.5),
+    (2, 1000, 64, False, 0, 0.45),
+    (3, 2000, 65, True, 0, 0.3),
+    (1, 4096, -1, False, 0, 0.5),       # the largest candidate count
+    (4, 5000, 400, False, -1, 0.45),    # no class field
+    (2, 3000, 129, False, 0, 0.0),      # any overlap suppresses
+    (1, 700, 0, False, 0, 0.5),         # topk 0: everything invalid
+]
+
+
+@pytest.mark.parametrize("case", NMS_CASES, ids=["-".join(map(str, c)) for c in NMS_CASES])
+def test_box_nms_bitwise(oracle_lib, case):
+    B, N, topk, force, id_index, thr = case
+    data = det.detection_rows(B, N, classes=5, objects=8, seed=N + B, object_frac=0.3)
+    if id_index < 0:
+        data = np.ascontiguousarray(data[..., 1:])   # [score, x1, y1, x2, y2]
+        ref = _check_nms(oracle_lib, data, overlap_thresh=thr, valid_thresh=0.01, topk=topk, id_index=-1,
+                         score_index=0, coord_start=1, force_suppress=force)
+    else:
+        ref = _check_nms(oracle_lib, data, overlap_thresh=thr, valid_thresh=0.01, topk=topk,
+                         force_suppress=force)
+    kept = np.all(ref != -1, axis=2).sum(axis=1)
+    assert kept.min() > 0 if topk != 0 else kept.max() == 0
+
+
+def test_box_nms_detection_workload(oracle_lib):
+    """The SSD-like workload at full size: 24564 rows per image, 20 classes,
+    scores above 0.01, the best 400 compared, IoU threshold 0.45; one image
+    and a batch of 4."""
+    for B in (1, 4):
+        data = det.detection_rows(B, seed=B)
+        ref = _check_nms(oracle_lib, data, overlap_thresh=0.45, valid_thresh=0.01, topk=400)
+        kept = np.all(ref != -1, axis=2).sum(axis=1)
+        assert kept.min() >= 5 and kept.max() < 400
+
+
+def test_box_nms_repeated_calls_share_workspace(oracle_lib):
+    """A second call on the same workspace (left holding the first call's
+    state) with a smaller input gives the second input's answer."""
+    ws = miconv.workspace(vision.box_nms_workspace_bytes(2, 3000, 6, 300))
+    d1 = det.detection_rows(2, 3000, seed=21, object_frac=0.3)
+    d2 = det.detection_rows(1, 1000, seed=22, object_frac=0.3)
+    for d in (d1, d2):
+        got = vision.box_nms(dev(d), 0.45, 0.01, 300, ws=ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(got.cpu().numpy(), oracle_lib.box_nms(d, 0.45, 0.01, 300))
+
+
+def test_box_nms_graph_capture_replays(oracle_lib):
+    """The whole pipeline captured into a HIP graph on its first call and
+    replayed: every replay equals the oracle."""
+    d = dev(det.detection_rows(2, 6000, seed=9, object_frac=0.2))
+    ref = oracle_lib.box_nms(d.cpu().numpy(), 0.45, 0.01, 256)
+    out = torch.empty_like(d)
+    ws = miconv.workspace(vision.box_nms_workspace_bytes(2, 6000, 6, 256))
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            vision.box_nms(d, 0.45, 0.01, 256, out=out, ws=ws)
+    for rep in range(3):
+        out.fill_(7.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(out.cpu().numpy(), ref, err_msg=f"replay {rep}")
+
+
+def test_vision_rejections():
+    d = torch.zeros((1, 10, 6), device="cuda")
+    with pytest.raises(miconv.MiconvError) as e:
+        vision.box_nms(d, coord_start=3)
+    assert e.value.status == miconv.ERR_SHAPE
+    with pytest.raises(miconv.MiconvError) as e:
+        vision.box_nms(torch.zeros((1, 5000, 6), device="cuda"), topk=-1)
+    assert e.value.status == miconv.ERR_UNSUPPORTED
