@@ -18,8 +18,11 @@ the largest summed execution time; its traffic comes from the committed
 counter summaries profiles/traffic_<workload>.txt when they match the kernel source)
 and the CPU oracle timed on a bounded sample of the same stack.  The default
 run (ResNet-50 at batch 1) also carries, under "b64", the same record for
-ResNet-50 at batch 64 with bf16 inputs (the metric's other half), and under
-"single_call" the single-layer configuration timed through each entry point.
+ResNet-50 at batch 64 with bf16 inputs (the metric's other half), under
+"b64_chained" that network as one pass with bf16 channel-last activations,
+under "single_call" the single-layer configuration timed through each entry
+point, and under "vision" the detection post-processing operators (box_nms,
+segmented argsort, prefix sum) on their own workloads.
 """
 from __future__ import annotations
 
@@ -123,6 +126,10 @@ def parse():
     ap.add_argument("--dw-sweep", type=int, default=0, metavar="N",
                     help="instead: HBM bandwidth of the depthwise kernel on the 13 MobileNet "
                          "depthwise shapes at batch N (e.g. 256)")
+    ap.add_argument("--vision", action="store_true",
+                    help="instead: only the vision operators (box_nms, segmented argsort, prefix sum)")
+    ap.add_argument("--no-vision", action="store_true",
+                    help="skip the nested vision-operator record of the default run")
     ap.add_argument("--residual-join", action="store_true",
                     help="instead: the ResNet-50 join layers (last 1x1 of each bottleneck block) "
                          "with the shortcut add + ReLU fused into the conv epilogue, against the "
@@ -704,6 +711,74 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
     }
 
 
+def vision_record(steps: int, cpu_seconds: float) -> dict:
+    """The vision operators of Sec. 3.1.1 on their own workloads, each timed
+    as a HIP graph of `steps` calls with inputs resident in HBM:
+      * box_nms on SSD-style detection rows (24564 anchors per image, 20
+        classes, score > 0.01, best 400 compared, IoU 0.45) at batch 1
+        (latency) and batch 32 (throughput);
+      * segmented argsort of 2^22 normal keys in 4096 segments of varying
+        length (keys/s; the merge passes move 12 bytes per key each way);
+      * the three-stage prefix sum of one row of 2^26 int32 (the across-
+        work-group path), against HBM bandwidth (algorithmic bytes: 4 read
+        + 4 written per value);
+    plus the oracle timed on a bounded sample of the box_nms workload."""
+    import torch
+    from paper_1907_02154_amd import detections as det
+    from paper_1907_02154_amd import miconv, vision
+
+    stream = torch.cuda.current_stream()
+    rec = {"workload": "SSD-style detection rows, 24564 x [class, score, x1, y1, x2, y2], 20 classes; "
+                       "valid_thresh 0.01, topk 400, overlap 0.45"}
+    for B in (1, 32):
+        data = torch.from_numpy(det.detection_rows(B, seed=100 + B)).cuda()
+        out = torch.empty_like(data)
+        ws = miconv.workspace(vision.box_nms_workspace_bytes(B, data.shape[1], 6, 400))
+        fn = lambda s, d=data, o=out, w=ws: vision.box_nms(d, 0.45, 0.01, 400, out=o, ws=w, stream=s)  # noqa: E731
+        fn(stream)
+        ms = _graph_ms(torch, fn, steps, stream)
+        rec[f"box_nms_b{B}_us"] = round(ms * 1e3, 2)
+        if B > 1:
+            rec[f"box_nms_b{B}_images_per_s"] = round(B / (ms * 1e-3), 1)
+    n, S = 1 << 22, 4096
+    keys = torch.from_numpy(det.keys(n, seed=5)).cuda()
+    off = torch.from_numpy(det.segment_offsets(S, n, seed=5)).cuda()
+    idx = torch.empty(n, dtype=torch.int32, device="cuda")
+    ws = miconv.workspace(vision.argsort_workspace_bytes(n, S))
+    fn = lambda s: vision.segmented_argsort(keys, off, True, out=idx, ws=ws, stream=s)  # noqa: E731
+    fn(stream)
+    ms = _graph_ms(torch, fn, max(steps // 5, 3), stream)
+    passes = 0
+    L = 2048
+    while L < n:
+        passes, L = passes + 1, 2 * L
+    rec["argsort"] = {"n": n, "segments": S, "us": round(ms * 1e3, 1), "Mkeys_per_s": round(n / (ms * 1e3), 1),
+                      "merge_passes": passes}
+    n = 1 << 26
+    x = torch.ones(n, dtype=torch.int32, device="cuda")
+    y = torch.empty_like(x)
+    ws = miconv.workspace(vision.scan_workspace_bytes(1, n))
+    fn = lambda s: vision.scan_i32(x, y, ws=ws, stream=s)  # noqa: E731
+    fn(stream)
+    ms = _graph_ms(torch, fn, max(steps // 5, 3), stream)
+    gbs = 8.0 * n / (ms * 1e-3) / 1e9
+    rec["scan"] = {"n": n, "us": round(ms * 1e3, 1), "GBs_algorithmic": round(gbs, 1)}
+    rec["roofline"] = {"kernel": "scan (upsweep + tile sums + downsweep)", "bound": "hbm",
+                       "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                       "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None}
+    if cpu_seconds > 0:
+        import oracle
+        data = det.detection_rows(1, seed=101)
+        t0, k = time.perf_counter(), 0
+        while k < 200 and time.perf_counter() - t0 < cpu_seconds:
+            oracle.box_nms(data, 0.45, 0.01, 400)
+            k += 1
+        dt = (time.perf_counter() - t0) / k
+        rec["cpu_baseline"] = {"value": round(dt * 1e3, 3), "unit": "ms/image", "cores": 1, "kind": "oracle",
+                               "sample": f"box_nms oracle on {k} calls of the batch-1 workload"}
+    return rec
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -715,6 +790,13 @@ def main():
         return
     if args.residual_join:
         residual_join(args)
+        return
+    if args.vision:
+        import torch
+        torch.cuda.set_device(0)
+        rec = vision_record(args.steps, min(args.cpu_seconds, 5.0))
+        rec.update(metric="vision operator latency", n_gpus=1, steps=args.steps, warmup=args.warmup, data="synthetic")
+        print(json.dumps(rec), flush=True)
         return
     if args.chain:
         import torch
@@ -776,6 +858,9 @@ def main():
         out["b64_chained"] = chain_record(args, "resnet50_b64", "bf16_cl", args.steps, args.warmup)
     if args.config in (1, 2) and args.batch is None:
         out["single_call"] = single_call_times(args.steps)
+    if args.config == 2 and args.batch is None and not args.no_vision:
+        # the vision operators of detection post-processing (Sec. 3.1.1)
+        out["vision"] = vision_record(args.steps, min(args.cpu_seconds, 5.0))
     print(json.dumps(out), flush=True)
 
 

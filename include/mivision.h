@@ -64,7 +64,8 @@ int vision_scan_i32(int rows, long n, const int32_t *x, int32_t *y, int exclusiv
  * 2048 outputs of a merge at the split points of its merge path; a pair
  * whose two runs meet at a segment boundary is already in order and is
  * copied.  Errors: MICONV_ERR_NULL, MICONV_ERR_SHAPE (n < 1, segments < 1),
- * MICONV_ERR_TOO_LARGE (n >= 2^31), MICONV_ERR_WORKSPACE. */
+ * MICONV_ERR_TOO_LARGE (n >= 2^31 or segments >= 2^21 - 1),
+ * MICONV_ERR_WORKSPACE. */
 long vision_argsort_workspace_bytes(long n, int segments);
 int vision_segmented_argsort(long n, int segments, const float *keys, const int32_t *offsets, int descending,
                              int32_t *out, void *ws, size_t ws_bytes, void *stream);
@@ -97,7 +98,8 @@ int vision_segmented_argsort(long n, int segments, const float *keys, const int3
  * index outside the row),
  * MICONV_ERR_UNSUPPORTED (more than MIVISION_NMS_MAX_CANDIDATES candidates
  * per image possible: min(topk, num), or num when topk < 0),
- * MICONV_ERR_TOO_LARGE, MICONV_ERR_WORKSPACE. */
+ * MICONV_ERR_TOO_LARGE (batch * num * width >= 2^31, batch >= 2^21 - 1),
+ * MICONV_ERR_WORKSPACE. */
 long vision_box_nms_workspace_bytes(int batch, int num, int width, int topk);
 int vision_box_nms(int batch, int num, int width, const float *data, float *out, float overlap_thresh,
                    float valid_thresh, int topk, int id_index, int score_index, int coord_start,

@@ -23,9 +23,10 @@ namespace {
 
 // ----------------------------------------------------------------- scan
 
-constexpr int kScanThreads = 256;
+constexpr int kScanThreads = 256;                     // work-groups across a row
 constexpr int kScanItems = 16;                        // values per thread (register block)
 constexpr int kScanTile = kScanThreads * kScanItems;  // 4096 values per tile
+constexpr int kScanWide = 1024;                       // a work-group owning one of few rows
 
 // One spare LDS word per 16: thread t's values t*16 .. t*16+15 start in
 // distinct banks.
@@ -66,33 +67,55 @@ __device__ int wg_scan_incl(int v, int *wsum, int *total)
 
 // Sources of scanned values: an int32 array, or the candidate flag of a
 // detection row (score > threshold).
+// SrcI32 can also be read four values per 16-byte load where aligned.
 struct SrcI32 {
+    static constexpr bool kVec = true;
     const int32_t *x;
     __device__ int operator()(long i) const { return x[i]; }
+    __device__ bool aligned(long i) const { return (((uintptr_t)(x + i)) & 15) == 0; }
+    __device__ int4 vec(long i) const { return *reinterpret_cast<const int4 *>(x + i); }
 };
 struct SrcScore {
+    static constexpr bool kVec = false;
     const float *data;
     int width, score_index;
     float thresh;
     __device__ int operator()(long i) const { return data[i * width + score_index] > thresh ? 1 : 0; }
+    __device__ bool aligned(long) const { return false; }
+    __device__ int4 vec(long) const { return int4{}; }
 };
 
-// The three stages on one tile [base, base + len) (len <= kScanTile), carry =
-// sum of everything before the tile.  Up-sweep: thread t scans its
+// The three stages on one tile [base, base + len) (len <= NT * kScanItems),
+// carry = sum of everything before the tile.  Up-sweep: thread t scans its
 // kScanItems consecutive values sequentially in registers; scan: Hillis-
 // Steele over the thread totals; down-sweep: each value gets the scanned
 // total of the threads before its own.  Loads and stores are striped over
 // the threads (coalesced) and transposed through LDS.  Returns carry + the
 // tile's sum.
-template <class Src>
+template <int NT, class Src>
 __device__ int scan_tile(const Src &src, long base, int len, int32_t *y, int carry, bool exclusive, int *tile,
                          int *wsum)
 {
     const int t = threadIdx.x;
+    if (Src::kVec && len == NT * kScanItems && src.aligned(base)) {
+        // whole aligned tile: 16-byte loads, four values each (a group of
+        // four never straddles a pad word)
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        const int i = j * kScanThreads + t;
-        tile[pad16(i)] = i < len ? src(base + i) : 0;
+        for (int j = 0; j < kScanItems / 4; ++j) {
+            const int i4 = j * NT + t;
+            const int4 q = src.vec(base + 4L * i4);
+            const int o = pad16(4 * i4);
+            tile[o] = q.x;
+            tile[o + 1] = q.y;
+            tile[o + 2] = q.z;
+            tile[o + 3] = q.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int i = j * NT + t;
+            tile[pad16(i)] = i < len ? src(base + i) : 0;
+        }
     }
     __syncthreads();
     int x0[kScanItems], v[kScanItems];
@@ -104,16 +127,25 @@ __device__ int scan_tile(const Src &src, long base, int len, int32_t *y, int car
         v[k] = run;
     }
     int total;
-    const int incl = wg_scan_incl<kScanThreads>(run, wsum, &total);
+    const int incl = wg_scan_incl<NT>(run, wsum, &total);
     const int before = incl - run + carry;
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k)
         tile[pad16(t * kScanItems + k)] = before + (exclusive ? v[k] - x0[k] : v[k]);
     __syncthreads();
+    if (len == NT * kScanItems && (((uintptr_t)(y + base)) & 15) == 0) {
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        const int i = j * kScanThreads + t;
-        if (i < len) y[base + i] = tile[pad16(i)];
+        for (int j = 0; j < kScanItems / 4; ++j) {
+            const int i4 = j * NT + t;
+            const int o = pad16(4 * i4);
+            *reinterpret_cast<int4 *>(y + base + 4L * i4) = int4{tile[o], tile[o + 1], tile[o + 2], tile[o + 3]};
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int i = j * NT + t;
+            if (i < len) y[base + i] = tile[pad16(i)];
+        }
     }
     __syncthreads();   // the tile buffer is free
     return carry + total;
@@ -122,17 +154,19 @@ __device__ int scan_tile(const Src &src, long base, int len, int32_t *y, int car
 // One work-group per row, its tiles in order with a running carry: the three
 // stages inside the work-group, nothing shared across work-groups.  Row r is
 // elements [r*n, r*n + n).  row_totals[r] (if given) gets the row's sum.
-template <class Src>
-__global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(Src src, long n, int32_t *y, int exclusive,
-                                                                 int32_t *row_totals)
+// NT = 1024 when the rows are few (a tile of 16384 values per round trip).
+template <int NT, class Src>
+__global__ __launch_bounds__(NT) void scan_rows_kernel(Src src, long n, int32_t *y, int exclusive,
+                                                       int32_t *row_totals)
 {
-    __shared__ int tile[kScanTile + kScanTile / 16];
-    __shared__ int wsum[kScanThreads / 64];
+    constexpr int TILE = NT * kScanItems;
+    __shared__ int tile[TILE + TILE / 16];
+    __shared__ int wsum[NT / 64];
     const long row = blockIdx.x;
     int carry = 0;
-    for (long b = 0; b < n; b += kScanTile)
-        carry = scan_tile(src, row * n + b, (int)(n - b < kScanTile ? n - b : kScanTile), y, carry, exclusive != 0,
-                          tile, wsum);
+    for (long b = 0; b < n; b += TILE)
+        carry = scan_tile<NT>(src, row * n + b, (int)(n - b < TILE ? n - b : TILE), y, carry, exclusive != 0,
+                              tile, wsum);
     if (row_totals && threadIdx.x == 0) row_totals[row] = carry;
 }
 
@@ -146,10 +180,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_upsweep_kernel(Src src, lon
     const long rem = n - (long)blockIdx.x * kScanTile;
     const int len = (int)(rem < kScanTile ? rem : kScanTile);
     int s = 0;
+    if (Src::kVec && len == kScanTile && src.aligned(base)) {
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        const int i = j * kScanThreads + threadIdx.x;
-        if (i < len) s += src(base + i);
+        for (int j = 0; j < kScanItems / 4; ++j) {
+            const int4 q = src.vec(base + 4L * (j * kScanThreads + threadIdx.x));
+            s += q.x + q.y + q.z + q.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int i = j * kScanThreads + threadIdx.x;
+            if (i < len) s += src(base + i);
+        }
     }
     int total;
     wg_scan_incl<kScanThreads>(s, wsum, &total);
@@ -165,8 +207,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_tile_sums_kernel(int32_t *t
     const long row = blockIdx.x;
     int carry = 0;
     for (int b = 0; b < tiles; b += kScanTile)
-        carry = scan_tile(SrcI32{tile_sums}, row * tiles + b, tiles - b < kScanTile ? tiles - b : kScanTile,
-                          tile_sums, carry, true, tile, wsum);
+        carry = scan_tile<kScanThreads>(SrcI32{tile_sums}, row * tiles + b,
+                                        tiles - b < kScanTile ? tiles - b : kScanTile, tile_sums, carry, true, tile,
+                                        wsum);
 }
 
 // Down-sweep: each tile scanned again with the prefix of the tiles before it.
@@ -178,7 +221,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_downsweep_kernel(Src src, l
     __shared__ int wsum[kScanThreads / 64];
     const long base = (long)blockIdx.y * n + (long)blockIdx.x * kScanTile;
     const long rem = n - (long)blockIdx.x * kScanTile;
-    scan_tile(src, base, (int)(rem < kScanTile ? rem : kScanTile), y,
+    scan_tile<kScanThreads>(src, base, (int)(rem < kScanTile ? rem : kScanTile), y,
               tile_prefix[(long)blockIdx.y * gridDim.x + blockIdx.x], exclusive != 0, tile, wsum);
 }
 
@@ -199,8 +242,12 @@ hipError_t launch_scan(const Src &src, int rows, long n, int32_t *y, bool exclus
                        void *ws, hipStream_t st)
 {
     if (!scan_across(rows, n) || row_totals) {
-        launch_kernel(scan_rows_kernel<Src>, dim3((unsigned)rows), dim3(kScanThreads), 0, st, src, n, y,
-                      exclusive ? 1 : 0, row_totals);
+        if (rows < 256 && n > kScanTile)
+            launch_kernel(scan_rows_kernel<kScanWide, Src>, dim3((unsigned)rows), dim3(kScanWide), 0, st, src, n, y,
+                          exclusive ? 1 : 0, row_totals);
+        else
+            launch_kernel(scan_rows_kernel<kScanThreads, Src>, dim3((unsigned)rows), dim3(kScanThreads), 0, st, src,
+                          n, y, exclusive ? 1 : 0, row_totals);
         return hipGetLastError();
     }
     const int tiles = (int)((n + kScanTile - 1) / kScanTile);
@@ -267,62 +314,157 @@ __device__ __forceinline__ int32_t local_index(uint64_t k, int v, const int32_t 
     return (int32_t)(v - seg_at(off, s, n));
 }
 
+// The same search by a whole wavefront for a uniform i: 64 probes per round,
+// so a table of S offsets costs about log64(S) dependent round trips.
+__device__ int find_segment_wave(const int32_t *off, int S, long n, long i)
+{
+    const int lane = threadIdx.x & 63;
+    int lo = 0, hi = S - 1;   // the answer is in [lo, hi]
+    while (lo < hi) {
+        const int span = hi - lo;                   // probes lo + 1 .. hi
+        const int step = (span + 63) / 64;
+        const int m = lo + 1 + lane * step;
+        const bool f = m <= hi && seg_at(off, m, n) <= i;   // true ... true false ... false
+        const uint64_t bal = __ballot(f);
+        if (!bal) {
+            hi = lo;                                // no probe at or below i: the answer is lo
+        } else {
+            const int l = 63 - __clzll((long long)bal);   // last true probe
+            const int ml = lo + 1 + l * step;
+            lo = ml;
+            const int next = ml + step;             // the first false probe (if any) bounds hi
+            hi = next - 1 < hi ? next - 1 : hi;
+        }
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int d)
+{
+    const int lo = __shfl_xor((int)(uint32_t)v, d), hi = __shfl_xor((int)(uint32_t)(v >> 32), d);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// One step of the bitonic network between elements J apart (J < 8) held by
+// one thread (elements 8t .. 8t+7 in x): the pair is put in ascending order
+// where bit k of its index is clear, descending where it is set.
+template <int J>
+__device__ __forceinline__ void bitonic_regs(uint64_t (&x)[kSortItems], int t, int k)
+{
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        if ((r & J) == 0) {
+            const bool up = ((kSortItems * t + r) & k) == 0;
+            const uint64_t p = x[r], q = x[r + J];
+            if ((p > q) == up) {
+                x[r] = q;
+                x[r + J] = p;
+            }
+        }
+    }
+}
+
 // Equal blocks sorted locally: block b of the flattened array (kSortTile
-// positions) is loaded with composite keys (segment << 32 | key bits),
-// positions past the last segment as padding, and sorted in LDS by a bitonic
-// network.  Segments stay in order, each segment's part of the block is
-// sorted.  With a single block the answers are written directly (out).
+// positions) is sorted by a bitonic network over one 64-bit word per element,
+// (segment: 21 bits | key bits: 32 | position in the block: 11), which orders
+// by segment, key, position and is unique; positions past the last segment
+// get segment 2^21 - 1 and all-ones key bits, so they sort last.  Segments
+// stay in order, each segment's part of the block is sorted.
+//   Thread t holds elements 8t .. 8t+7 in registers: network steps between
+// elements less than 8 apart stay in registers, steps up to 511 apart are
+// lane shuffles within the wavefront, and only the three steps of 512 and
+// 1024 go through LDS.  The segments overlapping the block are found once
+// (two wavefront searches) and their offsets staged in LDS, where each
+// element looks up its own.  The result leaves as (segment << 32 | key bits,
+// position) for the merge passes, or, with a single block, as the answers.
+constexpr uint64_t kPackPadSeg = 0x1FFFFFull;
+
 __global__ __launch_bounds__(kSortThreads) void segsort_block_kernel(const float *keys, const int32_t *off, int S,
                                                                      long n, int descending, uint64_t *K, int32_t *V,
                                                                      int32_t *out)
 {
     __shared__ uint64_t sk[kSortTile];
-    __shared__ int32_t sv[kSortTile];
-    const int t = threadIdx.x;
+    __shared__ long soff[kSortTile + 1];
+    __shared__ int seg_lo, seg_cnt;
+    const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
     const long base = (long)blockIdx.x * kSortTile;
     const long end = seg_at(off, S, n);   // positions >= end belong to no segment
-#pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
-        const int i = j * kSortThreads + t;
-        const long g = base + i;
-        if (g < end) {
-            const int s = find_segment(off, S, n, g);
-            sk[i] = ((uint64_t)(uint32_t)s << 32) | key_bits(keys[g], descending);
-            sv[i] = (int32_t)g;
-        } else {
-            sk[i] = kPadKey;
-            sv[i] = g < n ? (int32_t)g : INT_MAX;
+    const long last = (base + kSortTile < end ? base + kSortTile : end) - 1;
+    if (wid == 0 && base <= last) {
+        const int lo = find_segment_wave(off, S, n, base);
+        const int hi = find_segment_wave(off, S, n, last);
+        const int cnt = hi - lo + 1;
+        if (lane == 0) {
+            seg_lo = lo;
+            seg_cnt = cnt;
         }
+        if (cnt <= kSortTile)
+            for (int q = lane; q < cnt; q += 64) soff[q] = seg_at(off, lo + q, n);
     }
     __syncthreads();
-    for (int k = 2; k <= kSortTile; k <<= 1)
-        for (int j = k >> 1; j > 0; j >>= 1) {
+    uint64_t x[kSortItems];
 #pragma unroll
-            for (int q = 0; q < kSortTile / 2 / kSortThreads; ++q) {
-                const int p = q * kSortThreads + t;
-                const int i = 2 * p - (p & (j - 1));   // the pair (i, i + j), bit j of i clear
-                const int l = i + j;
-                const bool up = (i & k) == 0;
-                const uint64_t a = sk[i], b = sk[l];
-                const int va = sv[i], vb = sv[l];
-                if (elem_less(b, vb, a, va) == up) {
-                    sk[i] = b;
-                    sk[l] = a;
-                    sv[i] = vb;
-                    sv[l] = va;
+    for (int r = 0; r < kSortItems; ++r) {
+        const int e = kSortItems * t + r;
+        const long g = base + e;
+        x[r] = (kPackPadSeg << 43) | (0xFFFFFFFFull << 11) | (uint64_t)e;
+        if (g < end) {
+            int sg;
+            if (seg_cnt <= kSortTile) {      // last q with soff[q] <= g
+                int lo = 0, hi = seg_cnt - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (soff[mid] <= g) lo = mid;
+                    else hi = mid - 1;
                 }
+                sg = seg_lo + lo;
+            } else {
+                sg = find_segment(off, S, n, g);
             }
-            __syncthreads();
+            x[r] = ((uint64_t)sg << 43) | ((uint64_t)key_bits(keys[g], descending) << 11) | (uint64_t)e;
         }
+    }
+    for (int k = 2; k <= kSortTile; k <<= 1) {
+        for (int j = k >> 1; j >= kSortItems; j >>= 1) {
+            // partner of element e = 8t + r is e ^ j = 8(t ^ (j/8)) + r
+            const bool up = ((kSortItems * t) & k) == 0;
+            const bool lower = ((kSortItems * t) & j) == 0;
+            uint64_t y[kSortItems];
+            if (j < 64 * kSortItems) {
 #pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
-        const int i = j * kSortThreads + t;
-        const long g = base + i;
+                for (int r = 0; r < kSortItems; ++r) y[r] = shfl_xor64(x[r], j / kSortItems);
+            } else {
+                __syncthreads();   // everyone is done reading the previous LDS step
+#pragma unroll
+                for (int r = 0; r < kSortItems; ++r) sk[kSortItems * t + r] = x[r];
+                __syncthreads();
+#pragma unroll
+                for (int r = 0; r < kSortItems; ++r) y[r] = sk[(kSortItems * t + r) ^ j];
+            }
+#pragma unroll
+            for (int r = 0; r < kSortItems; ++r) {
+                const bool keep_min = lower == up;
+                const uint64_t mn = x[r] < y[r] ? x[r] : y[r], mx = x[r] < y[r] ? y[r] : x[r];
+                x[r] = keep_min ? mn : mx;
+            }
+        }
+        // steps between a thread's own elements
+        if (k > 4) bitonic_regs<4>(x, t, k);
+        if (k > 2) bitonic_regs<2>(x, t, k);
+        bitonic_regs<1>(x, t, k);
+    }
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const long g = base + kSortItems * t + r;
         if (g >= n) continue;
-        if (out) out[g] = local_index(sk[i], sv[i], off, n);
+        const uint64_t w = x[r];
+        const bool pad = (w >> 43) == kPackPadSeg;
+        const uint64_t key = pad ? kPadKey : ((w >> 43) << 32) | ((w >> 11) & 0xFFFFFFFFull);
+        const int32_t v = (int32_t)(base + (long)(w & 0x7FF));
+        if (out) out[g] = local_index(key, v, off, n);
         else {
-            K[g] = sk[i];
-            V[g] = sv[i];
+            K[g] = key;
+            V[g] = v;
         }
     }
 }
@@ -504,6 +646,9 @@ struct NmsArgs {
     float *ckey;              // [B*N] compacted scores
     int32_t *corig;           // [B*N] compacted row index within the image
     int32_t *rank;            // [B*N] segmented argsort of ckey: rank r of image b -> local slot
+    float4 *cbox;             // [B][mrows] box of the candidate of rank r
+    float *ccls;              // [B][mrows] its class
+    int32_t *crow;            // [B][mrows] its input row
     uint64_t *mask;           // [B][mrows][capw]
 };
 
@@ -559,16 +704,20 @@ __device__ __forceinline__ int nms_row(const NmsArgs &a, int b, int r)
 }
 
 // IoU of two corner-encoded boxes, each operation rounded to fp32 in the
-// order of the definition (no contraction into fused multiply-adds).
+// order of the definition.  Contraction into fused multiply-adds is switched
+// off here: the compiler would otherwise fold the area products into the
+// union's sums, whose single rounding moves the IoU by an ulp and flips
+// comparisons at the threshold.
 __device__ __forceinline__ float box_iou(float4 p, float4 q)
 {
-    const float iw = fmaxf(0.f, __fsub_rn(fminf(p.z, q.z), fmaxf(p.x, q.x)));
-    const float ih = fmaxf(0.f, __fsub_rn(fminf(p.w, q.w), fmaxf(p.y, q.y)));
-    const float inter = __fmul_rn(iw, ih);
-    const float ap = __fmul_rn(fmaxf(0.f, __fsub_rn(p.z, p.x)), fmaxf(0.f, __fsub_rn(p.w, p.y)));
-    const float aq = __fmul_rn(fmaxf(0.f, __fsub_rn(q.z, q.x)), fmaxf(0.f, __fsub_rn(q.w, q.y)));
-    const float uni = __fsub_rn(__fadd_rn(ap, aq), inter);
-    return uni <= 0.f ? 0.f : __fdiv_rn(inter, uni);
+#pragma clang fp contract(off)
+    const float iw = fmaxf(0.f, fminf(p.z, q.z) - fmaxf(p.x, q.x));
+    const float ih = fmaxf(0.f, fminf(p.w, q.w) - fmaxf(p.y, q.y));
+    const float inter = iw * ih;
+    const float ap = fmaxf(0.f, p.z - p.x) * fmaxf(0.f, p.w - p.y);
+    const float aq = fmaxf(0.f, q.z - q.x) * fmaxf(0.f, q.w - q.y);
+    const float uni = (ap + aq) - inter;
+    return uni <= 0.f ? 0.f : inter / uni;
 }
 
 __device__ __forceinline__ float4 load_box(const NmsArgs &a, int b, int i, float *cls)
@@ -579,13 +728,30 @@ __device__ __forceinline__ float4 load_box(const NmsArgs &a, int b, int i, float
     return make_float4(c[0], c[1], c[2], c[3]);
 }
 
+// The compared candidates in rank order: box, class and input row of rank r
+// of image b (r < the image's candidate count), gathered once so that the
+// mask and walk kernels read them with one request each.
+__global__ __launch_bounds__(256) void nms_gather_kernel(NmsArgs a)
+{
+    const int b = blockIdx.y;
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= nms_count(a, b)) return;
+    const int i = nms_row(a, b, r);
+    float c;
+    const long k = (long)b * a.mrows + r;
+    a.cbox[k] = load_box(a, b, i, &c);
+    a.ccls[k] = c;
+    a.crow[k] = i;
+}
+
 // Suppression masks: work-group (column block cb, row block rb, image b),
-// one wavefront.  Lane t takes candidate i = 64*rb + t (the loop above the
-// innermost one, on work-groups and lanes) and tests it against the 64
-// candidates j of block cb staged in LDS (the innermost loop): bit j - 64*cb
-// of mask[b][i][cb] is set when j comes later and i, once kept, suppresses
-// it.  Blocks below the diagonal are never read and not computed.
-__global__ __launch_bounds__(64) void nms_mask_kernel(NmsArgs a)
+// four wavefronts.  Lane t of wavefront q takes candidate i = 64*rb + t (the
+// loop above the innermost one, on work-groups and lanes) and tests it
+// against the 16 candidates j = 64*cb + 16*q .. + 15 staged in LDS (the
+// innermost loop): bit j - 64*cb of mask[b][i][cb] is set when j comes later
+// and i, once kept, suppresses it.  Each wavefront writes its 16 bits of the
+// word.  Blocks below the diagonal are never read and not computed.
+__global__ __launch_bounds__(256) void nms_mask_kernel(NmsArgs a)
 {
     __shared__ float4 cbox[64];
     __shared__ float ccls[64];
@@ -593,72 +759,117 @@ __global__ __launch_bounds__(64) void nms_mask_kernel(NmsArgs a)
     if (cb < rb) return;
     const int count = nms_count(a, b);
     if (rb * 64 >= count) return;
-    const int t = threadIdx.x;
-    const int j = cb * 64 + t;
-    if (j < count) {
-        float c;
-        cbox[t] = load_box(a, b, nms_row(a, b, j), &c);
-        ccls[t] = c;
+    const int t = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const long base = (long)b * a.mrows;
+    if (threadIdx.x < 64) {
+        const int j = cb * 64 + t;
+        if (j < count) {
+            cbox[t] = a.cbox[base + j];
+            ccls[t] = a.ccls[base + j];
+        }
     }
     __syncthreads();
     const int i = rb * 64 + t;
     if (i >= count) return;
-    float ci;
-    const float4 bi = load_box(a, b, nms_row(a, b, i), &ci);
+    const float4 bi = a.cbox[base + i];
+    const float ci = a.ccls[base + i];
     const bool any_class = a.force || a.id_index < 0;
-    uint64_t bits = 0;
-    const int jn = count - cb * 64 < 64 ? count - cb * 64 : 64;
+    uint32_t bits = 0;
+    const int j0 = cb * 64 + 16 * q;
+    const int jn = count - j0 < 16 ? count - j0 : 16;
     for (int jj = 0; jj < jn; ++jj) {
-        const int jg = cb * 64 + jj;
+        const int jg = j0 + jj;
         if (jg <= i) continue;
-        if (!any_class && !(ccls[jj] == ci)) continue;
-        if (box_iou(bi, cbox[jj]) > a.overlap) bits |= 1ull << jj;
+        if (!any_class && !(ccls[16 * q + jj] == ci)) continue;
+        if (box_iou(bi, cbox[16 * q + jj]) > a.overlap) bits |= 1u << jj;
     }
-    a.mask[((long)b * a.mrows + i) * a.capw + cb] = bits;
+    // bits 16q .. 16q+15 of the 64-bit word (little-endian halves of halves)
+    reinterpret_cast<uint16_t *>(a.mask)[((base + i) * a.capw + cb) * 4 + q] = (uint16_t)bits;
 }
 
-// The greedy walk, one wavefront per image: lane w holds word w of the
-// removed set.  Candidate i (rank order) is kept unless its bit is set; a
-// kept candidate ORs its mask row (words from its own on) into the set.
-// Mask rows are staged through LDS 64 at a time, all requested at once, so
-// the walk waits for memory once per 64 candidates.  Kept rows are then
-// copied to the first output rows of the image.
-__global__ __launch_bounds__(64) void nms_sweep_kernel(NmsArgs a)
+// The greedy walk, one work-group per image.  The mask rows of the image's
+// candidates are staged in LDS by all 256 threads at once (as many rows as
+// fit; all requests in flight together), then the first wavefront walks:
+// lane w holds word w of the removed set, candidate i (rank order) is kept
+// unless its bit is set (the word is read from its lane with readlane, i
+// being uniform), and a kept candidate ORs its mask row (words from its own
+// on) into the set.  The kept ranks are listed in LDS, and afterwards all
+// threads copy the kept rows, one value each, to the first output rows.
+// The 64-bit value v of lane w (uniform w), as a scalar.
+__device__ __forceinline__ uint64_t lane_word(uint64_t v, int w)
 {
-    extern __shared__ uint64_t rows[];          // [64][capw]
-    __shared__ int kept_rows[kNmsMax];
-    const int b = blockIdx.x, lane = threadIdx.x;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, w);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), w);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+constexpr int kSweepThreads = 256;
+constexpr int kSweepWords = 6144;   // 48 KB of mask rows per staging round
+
+__global__ __launch_bounds__(kSweepThreads) void nms_sweep_kernel(NmsArgs a)
+{
+    __shared__ uint64_t rows[kSweepWords];
+    __shared__ int kept_rank[kNmsMax];
+    __shared__ int kept_n;
+    const int b = blockIdx.x, t = threadIdx.x, lane = t & 63;
     const int count = nms_count(a, b);
+    const long base = (long)b * a.mrows;
+    const int per = kSweepWords / a.capw / 64 * 64;   // rows per staging round: whole words, >= 64
     uint64_t removed = 0;
     int kept = 0;
-    for (int r0 = 0; r0 < count; r0 += 64) {
-        const int nr = count - r0 < 64 ? count - r0 : 64;
+    for (int r0 = 0; r0 < count; r0 += per) {
+        const int nr = count - r0 < per ? count - r0 : per;
+        const int words = nr * a.capw;
         __syncthreads();
-        for (int e = lane; e < nr * a.capw; e += 64) {
-            const int rr = e / a.capw, w = e - rr * a.capw;
-            // words left of the row's own block are never written; read as 0
-            rows[e] = w >= (r0 + rr) / 64 ? a.mask[((long)b * a.mrows + r0 + rr) * a.capw + w] : 0;
+        for (int e0 = 0; e0 < words; e0 += kSweepThreads * 8) {
+            uint64_t v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int e = e0 + k * kSweepThreads + t;
+                const int rr = e / a.capw, w = e - rr * a.capw;
+                // words left of the row's own block are never written; read as 0
+                v[k] = e < words && w >= (r0 + rr) / 64 ? a.mask[(base + r0 + rr) * a.capw + w] : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int e = e0 + k * kSweepThreads + t;
+                if (e < words) rows[e] = v[k];
+            }
         }
         __syncthreads();
-        for (int rr = 0; rr < nr; ++rr) {
-            const int i = r0 + rr;
-            const uint64_t word = __shfl(removed, i >> 6);
-            if ((word >> (i & 63)) & 1) continue;
-            if (lane == 0) kept_rows[kept] = nms_row(a, b, i);
-            ++kept;
-            if (lane < a.capw) removed |= rows[rr * a.capw + lane];
+        if (t < 64) {
+            // word by word: the next candidate not yet removed is the lowest
+            // clear bit above the last one taken, so removed candidates cost
+            // nothing and the walk takes one step per kept candidate
+            for (int w = r0 >> 6; w * 64 < r0 + nr; ++w) {
+                const int valid = r0 + nr - w * 64 < 64 ? r0 + nr - w * 64 : 64;
+                const uint64_t live = valid == 64 ? ~0ull : (1ull << valid) - 1;
+                uint64_t cur = lane_word(removed, w);
+                uint64_t avail = ~cur & live;
+                while (avail) {
+                    const int bit = __builtin_ctzll(avail);
+                    const int i = w * 64 + bit;
+                    if (lane == 0) kept_rank[kept] = i;
+                    ++kept;
+                    if (lane < a.capw) removed |= rows[(i - r0) * a.capw + lane];
+                    cur = lane_word(removed, w);
+                    avail = ~cur & live & ~((2ull << bit) - 1);   // bits above `bit` (none when bit = 63)
+                }
+            }
         }
     }
+    if (t == 0) kept_n = kept;
     __syncthreads();
-    for (int k = lane; k < kept; k += 64) {
-        const float *src = a.data + ((long)b * a.N + kept_rows[k]) * a.width;
-        float *dst = a.out + ((long)b * a.N + k) * a.width;
-        for (int c = 0; c < a.width; ++c) dst[c] = src[c];
+    const int nk = kept_n;
+    for (int e = t; e < nk * a.width; e += kSweepThreads) {
+        const int k = e / a.width, c = e - k * a.width;
+        const float *src = a.data + ((long)b * a.N + a.crow[base + kept_rank[k]]) * a.width;
+        a.out[((long)b * a.N + k) * a.width + c] = src[c];
     }
 }
 
 struct NmsLayout {
-    long pos, seg_off, ckey, corig, rank, sort, mask, total;
+    long pos, seg_off, ckey, corig, rank, sort, cbox, ccls, crow, mask, total;
 };
 
 NmsLayout nms_layout(int B, int N, int cap)
@@ -679,8 +890,15 @@ NmsLayout nms_layout(int B, int N, int cap)
     o += align256(n * 4);
     l.sort = o;
     o += align256(argsort_ws_bytes(n));
+    const long mrows = (long)B * capw * 64;
+    l.cbox = o;
+    o += align256(mrows * 16);
+    l.ccls = o;
+    o += align256(mrows * 4);
+    l.crow = o;
+    o += align256(mrows * 4);
     l.mask = o;
-    o += align256((long)B * capw * 64 * capw * 8);
+    o += align256(mrows * capw * 8);
     l.total = o;
     return l;
 }
@@ -722,7 +940,7 @@ int vision_scan_i32(int rows, long n, const int32_t *x, int32_t *y, int exclusiv
 long vision_argsort_workspace_bytes(long n, int segments)
 {
     if (n < 1 || segments < 1) return MICONV_ERR_SHAPE;
-    if (n >= (1L << 31) || segments >= (1 << 30)) return MICONV_ERR_TOO_LARGE;
+    if (n >= (1L << 31) || segments >= (1 << 21) - 1) return MICONV_ERR_TOO_LARGE;
     return argsort_ws_bytes(n);
 }
 
@@ -741,7 +959,7 @@ int vision_segmented_argsort(long n, int segments, const float *keys, const int3
 long vision_box_nms_workspace_bytes(int batch, int num, int width, int topk)
 {
     if (batch < 1 || num < 1 || width < 1) return MICONV_ERR_SHAPE;
-    if ((long)batch * num * width >= (1L << 31)) return MICONV_ERR_TOO_LARGE;
+    if ((long)batch * num * width >= (1L << 31) || batch >= (1 << 21) - 1) return MICONV_ERR_TOO_LARGE;
     const int cap = nms_cap(num, topk);
     if (cap > kNmsMax) return MICONV_ERR_UNSUPPORTED;
     return nms_layout(batch, num, cap).total;
@@ -783,6 +1001,9 @@ int vision_box_nms(int batch, int num, int width, const float *data, float *out,
     a.ckey = reinterpret_cast<float *>(w + l.ckey);
     a.corig = reinterpret_cast<int32_t *>(w + l.corig);
     a.rank = reinterpret_cast<int32_t *>(w + l.rank);
+    a.cbox = reinterpret_cast<float4 *>(w + l.cbox);
+    a.ccls = reinterpret_cast<float *>(w + l.ccls);
+    a.crow = reinterpret_cast<int32_t *>(w + l.crow);
     a.mask = reinterpret_cast<uint64_t *>(w + l.mask);
     const long n = (long)batch * num;
     const long vals = n * width;
@@ -801,9 +1022,11 @@ int vision_box_nms(int batch, int num, int width, const float *data, float *out,
     if ((e = launch_segsort(a.ckey, seg, batch, n, 1, a.rank, w + l.sort, st)) != hipSuccess)
         return set_hip_error(e);
     if (a.capw > 0) {   // topk == 0: no candidate, the output stays invalid
-        launch_kernel(nms_mask_kernel, dim3((unsigned)a.capw, (unsigned)a.capw, (unsigned)batch), dim3(64), 0, st,
+        launch_kernel(nms_gather_kernel, dim3((unsigned)((a.mrows + 255) / 256), (unsigned)batch), dim3(256), 0, st,
                       a);
-        launch_kernel(nms_sweep_kernel, dim3((unsigned)batch), dim3(64), (uint32_t)(64 * a.capw * 8), st, a);
+        launch_kernel(nms_mask_kernel, dim3((unsigned)a.capw, (unsigned)a.capw, (unsigned)batch), dim3(256), 0, st,
+                      a);
+        launch_kernel(nms_sweep_kernel, dim3((unsigned)batch), dim3(kSweepThreads), 0, st, a);
     }
     e = hipGetLastError();
     return e == hipSuccess ? MICONV_OK : set_hip_error(e);

@@ -163,6 +163,29 @@ def test_box_nms_bitwise(oracle_lib, case):
     assert kept.min() > 0 if topk != 0 else kept.max() == 0
 
 
+def test_box_nms_iou_rounding_at_threshold(oracle_lib):
+    """4096 images of two same-class boxes whose IoU lies within a few ulps
+    of the 0.5 threshold (B is A shifted right by about a third of its
+    width): the keep / suppress decision follows the fp32 rounding of every
+    product and sum, so a kernel that fused a product into the union's sums
+    (one rounding fewer) disagrees with the oracle on some of them."""
+    rng = np.random.default_rng(44)
+    f = np.float32
+    B = 4096
+    d = np.zeros((B, 2, 6), np.float32)
+    x0, y0 = rng.uniform(0, 1, B).astype(f), rng.uniform(0, 1, B).astype(f)
+    w, h = rng.uniform(0.05, 0.5, B).astype(f), rng.uniform(0.05, 0.5, B).astype(f)
+    dx = (w / f(3)).astype(f)
+    dx = (dx + rng.integers(-3, 4, B).astype(f) * np.spacing(dx)).astype(f)
+    d[:, :, 0] = 1
+    d[:, 0, 1], d[:, 1, 1] = 0.9, 0.8
+    d[:, 0, 2:6] = np.stack([x0, y0, x0 + w, y0 + h], 1)
+    d[:, 1, 2:6] = np.stack([x0 + dx, y0, x0 + dx + w, y0 + h], 1)
+    ref = _check_nms(oracle_lib, d, overlap_thresh=0.5, valid_thresh=0.0, topk=-1)
+    kept2 = np.all(ref[:, 1] != -1, axis=1)
+    assert 0 < kept2.sum() < B   # both decisions occur
+
+
 def test_box_nms_detection_workload(oracle_lib):
     """The SSD-like workload at full size: 24564 rows per image, 20 classes,
     scores above 0.01, the best 400 compared, IoU threshold 0.45; one image
