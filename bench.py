@@ -20,6 +20,7 @@ and the CPU oracle timed on a bounded sample of the same stack.  The default
 run (ResNet-50 at batch 1) also carries, under "b64", the same record for
 ResNet-50 at batch 64 with bf16 inputs (the metric's other half), under
 "b64_chained" that network as one pass with bf16 channel-last activations,
+under "b1_chained" the batch-1 network as one pass (fp32),
 under "single_call" the single-layer configuration timed through each entry
 point, and under "vision" the detection post-processing operators (box_nms,
 segmented argsort, prefix sum) on their own workloads.
@@ -200,6 +201,8 @@ def residual_join(args):
         elems += res.numel()
         conv_flops += wl.flops(l, P, Q)
     sf, sp = miconv.Stack(fused), miconv.Stack(plain)
+    sf.overlap(False)   # unrelated layers: timed in order, one at a time
+    sp.overlap(False)
     stream = torch.cuda.current_stream()
     for _ in range(max(1, args.warmup)):
         sf.launch(stream)
@@ -281,6 +284,7 @@ def dw_sweep(args):
         b = torch.randn((l.C,), device="cuda", generator=gen) * 0.01
         st = miconv.Stack([(miconv.OP_DWCONV_F32, xs[i], w, b, ys[i], l.stride, l.pad, l.C, l.relu)
                            for i in range(sets)])
+        st.overlap(False)   # the buffer sets rotate through one layer: one launch at a time
         if args.profile_passes:
             # counter runs: eager launches only (every buffer set, N times)
             for _ in range(args.profile_passes):
@@ -384,6 +388,10 @@ def stack_record(args, config: int, batch, steps: int, warmup: int, cpu_seconds:
         op = miconv.OP_CONV_BF16 if bf16 else (miconv.OP_DWCONV_F32 if l.kind == "dw" else miconv.OP_CONV_F32)
         ops.append((op, d["x"], d["w"], d["b"], d["y"], l.stride, l.pad, l.groups, l.relu))
     stack = miconv.Stack(ops)          # plans every layer; packs filters once
+    # each layer has its own input, so none depends on another: they stay in
+    # order on one stream (the step is the sum of the layers' latencies, as
+    # a network runs them), never overlapped
+    stack.overlap(False)
     for j, d in enumerate(layers):
         d["kernel"] = stack.describe(j)
     n_launch = stack.launches
@@ -647,15 +655,24 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
     for _ in range(warmup):
         stack.launch(stream)
     torch.cuda.synchronize()
-    stack.capture(steps, timed=False, stream=stream)
-    stack.replay(stream)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    stack.replay(stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = e0.elapsed_time(e1) / steps
+
+    def graph_ms():
+        stack.capture(steps, timed=False, stream=stream)
+        stack.replay(stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        stack.replay(stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    # the pass in one stream, and, for comparison, with the layers the
+    # network's dependencies allow on a second stream
+    overlapped = stack.overlap(True)
+    ms_two = graph_ms()
+    stack.overlap(False)
+    ms_per_step = graph_ms()
     stack.launch_timed(steps, stream)
     torch.cuda.synchronize()
     launch_ms = stack.times().mean(axis=0)
@@ -703,6 +720,7 @@ def chain_record(args, net: str, layout: str, steps: int, warmup: int, table: bo
                     + (" + max-pool" if len(flops) < len(graph) else "") + ", shortcut joins fused",
         "value": round(total_flops / (ms_per_step * 1e-3) / 1e12, 4), "unit": "TFLOP/s",
         "ms_per_step": round(ms_per_step, 5), "ms_per_image": round(ms_per_step / N, 5),
+        "two_streams": {"layers_on_second_stream": overlapped, "ms_per_step": round(ms_two, 5)},
         "gflop_per_step": round(total_flops / 1e9, 4), "launches_per_step": n_launch,
         "conv_kernel_ms": round(conv_ms, 5), "glue_kernel_ms": round(pool_ms, 5),
         "stack_roofline_frac": round(t_roof / (ms_per_step * 1e-3), 4),
@@ -856,6 +874,10 @@ def main():
         # channel-last activations between layers (no per-layer copies, bf16
         # outputs, joins fused)
         out["b64_chained"] = chain_record(args, "resnet50_b64", "bf16_cl", args.steps, args.warmup)
+    if args.config == 2 and args.batch is None:
+        # the batch-1 network as one chained pass (stem, max-pool, blocks with
+        # the join fused; projection shortcuts beside the block's first convs)
+        out["b1_chained"] = chain_record(args, "resnet50_b1", "f32", args.steps, args.warmup)
     if args.config in (1, 2) and args.batch is None:
         out["single_call"] = single_call_times(args.steps)
     if args.config == 2 and args.batch is None and not args.no_vision:

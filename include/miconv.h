@@ -348,6 +348,19 @@ int miconv_stack_launch(miconv_stack *s, void *stream);
  * captured graph. */
 int miconv_stack_launch_timed(miconv_stack *s, int steps, void *stream);
 
+/* Overlap of independent layers in untimed captures (off by default): at
+ * create every layer's dependencies are derived from the byte ranges of x,
+ * res and y it shares with earlier layers (read after write, write after
+ * write, write after read); with enable != 0 a layer that its successor does
+ * not depend on runs on a second stream, joined by event waits (graph
+ * edges), each stream with its own half of the workspace; passes never
+ * overlap each other.  In ResNet the projection shortcut then runs beside
+ * the first two convs of its block.  On MI355X the cross-stream edges cost
+ * more than the overlap gains on ResNet-50 (batch 1 and 64), hence the
+ * default.  Takes effect at the next capture.  Returns the number of layers
+ * on the second stream when enabled (0 when nothing can overlap), else 0. */
+int miconv_stack_overlap(miconv_stack *s, int enable);
+
 /* Capture `steps` consecutive passes into one HIP graph, replacing any
  * previous capture (nothing executes; the NULL stream is served by a private
  * capture stream).  With timed != 0 an event is recorded before every kernel

@@ -93,10 +93,11 @@ def lib() -> ctypes.CDLL:
         L.miconv_stack_replay.argtypes = [p, p]
         L.miconv_stack_times.argtypes = [p, p, l]
         L.miconv_stack_destroy.argtypes = [p]
+        L.miconv_stack_overlap.argtypes = [p, i]
         for f in ("miconv_stack_create", "miconv_stack_size", "miconv_stack_describe",
                   "miconv_stack_launches", "miconv_stack_launch_info",
                   "miconv_stack_launch", "miconv_stack_launch_timed", "miconv_stack_capture", "miconv_stack_replay",
-                  "miconv_stack_times", "miconv_stack_destroy"):
+                  "miconv_stack_times", "miconv_stack_destroy", "miconv_stack_overlap"):
             getattr(L, f).restype = i
         L.miconv_strerror.argtypes = [i]
         L.miconv_strerror.restype = ctypes.c_char_p
@@ -648,6 +649,14 @@ class Stack:
         _check(lib().miconv_stack_launch_timed(self._h, steps, _stream(stream)),
                "miconv_stack_launch_timed")
         self.steps = steps
+
+    def overlap(self, enable: bool) -> int:
+        """Overlap independent layers on a second stream in the next untimed
+        capture (off by default); returns how many layers run there."""
+        rc = lib().miconv_stack_overlap(self._h, 1 if enable else 0)
+        if rc < 0:
+            _check(rc, "miconv_stack_overlap")
+        return rc
 
     def capture(self, steps: int, timed: bool, stream=None):
         _check(lib().miconv_stack_capture(self._h, steps, 1 if timed else 0, _stream(stream)),

@@ -142,28 +142,42 @@ def _check_chain(oracle_lib, graph, config, layout, images, tol, batch=None):
 
 def test_resnet50_b64_bf16_channel_last_chain(oracle_lib):
     """ResNet-50 at batch 64 with bf16 channel-last activations: per-layer
-    gate 2e-2 on images 0 and 63; the stack's graph replays equal its eager
-    pass bit for bit."""
+    gate 2e-2 on images 0 and 63; the stack's graph replays (projection
+    shortcuts overlapped, or not) equal its eager pass bit for bit."""
     graph = nets.resnet50_graph(5)
     s, outs, drift = _check_chain(oracle_lib, graph, 5, "bf16_cl", images=[0, 63], tol=2e-2)
     assert drift[-1][1] < 0.2, drift[-1]
-    last = outs[graph[-1].name].clone()
-    s.capture(2, timed=False)
-    for rep in range(2):
-        outs[graph[-1].name].fill_(float("nan"))
-        torch.cuda.synchronize()
-        s.replay()
-        torch.cuda.synchronize()
-        assert torch.equal(outs[graph[-1].name], last), f"replay {rep}"
+    _replays_match_eager(s, outs, graph)
     s.close()
+
+
+def _replays_match_eager(s, outs, graph):
+    """Graph replays of the pass -- with the four projection shortcuts on the
+    second stream, and all in one stream -- reproduce the eager pass bit for
+    bit, every node's output."""
+    eager = {k: v.clone() for k, v in outs.items()}
+    for overlap in (True, False):
+        n_side = s.overlap(overlap)
+        assert n_side == (4 if overlap else 0), n_side
+        s.capture(2, timed=False)
+        for rep in range(2):
+            for k, v in outs.items():
+                if k != "input":
+                    v.fill_(float("nan"))
+            torch.cuda.synchronize()
+            s.replay()
+            torch.cuda.synchronize()
+            for k, v in outs.items():
+                assert torch.equal(v, eager[k]), f"overlap={overlap} replay {rep} node {k}"
 
 
 def test_resnet50_b1_f32_chain(oracle_lib):
     """ResNet-50 at batch 1, fp32 NCHW: stem, max-pool, bottlenecks with the
     join fused into each block's last conv; per-layer gate 1e-4."""
     graph = nets.resnet50_graph(2)
-    s, _, drift = _check_chain(oracle_lib, graph, 2, "f32", images=[0], tol=1e-4)
+    s, outs, drift = _check_chain(oracle_lib, graph, 2, "f32", images=[0], tol=1e-4)
     assert drift[-1][1] < 1e-3, drift[-1]
+    _replays_match_eager(s, outs, graph)
     s.close()
 
 
@@ -172,4 +186,5 @@ def test_mobilenet_b1_f32_chain(oracle_lib):
     graph = nets.mobilenet_graph()
     s, _, drift = _check_chain(oracle_lib, graph, 3, "f32", images=[0], tol=1e-4)
     assert drift[-1][1] < 1e-3, drift[-1]
+    assert s.overlap(True) == 0          # a chain: nothing can overlap
     s.close()
