@@ -83,15 +83,22 @@ def _oracle(oracle_lib, case, x, w, b, res, relu):
 def _join(tx, tw, tb, res, y, st, pad, g, relu, algo, mode):
     if mode == "ws":
         miconv.conv2d_fwd_ws(tx, tw, tb, y, st, pad, g, relu, res=res, algo=algo)
+    elif mode == "stack":   # a one-layer stack: filters packed at create
+        op = miconv.OP_CONV_BF16 if tx.dtype == torch.bfloat16 else miconv.OP_CONV_F32
+        s = miconv.Stack([(op, tx, tw, tb, y, st, pad, g, relu, res)])
+        s.launch()
+        torch.cuda.synchronize()
+        s.close()
     else:
         miconv.conv2d_fwd_res(tx, tw, tb, res, y, st, pad, g, relu, algo=algo)
 
 
 @pytest.mark.parametrize("case", RES_CASES, ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
-@pytest.mark.parametrize("mode", ["ws", "plain"])
+@pytest.mark.parametrize("mode", ["ws", "plain", "stack"])
 def test_residual_join_small_int_bitwise(oracle_lib, case, mode):
-    """conv2d_fwd_ws (the kernel named in the case) and conv2d_fwd_res (the
-    plan without a workspace) with the join in the epilogue."""
+    """conv2d_fwd_ws (the kernel named in the case), conv2d_fwd_res (the
+    plan without a workspace) and a one-layer stack (packed filters) with the
+    join in the epilogue."""
     N, C, H, W, K, R, S, st, pad, g, dt, algo, kernel = case
     name = miconv.conv2d_describe(N, C, H, W, K, R, S, st, pad, g, dt, algo, mode=mode)[0]
     if mode == "ws":

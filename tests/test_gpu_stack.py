@@ -194,14 +194,19 @@ RAGGED = [  # (N, C, H, W, K, R, S, stride, pad, groups): small layers that take
     (2, 12, 8, 8, 20, 5, 5, 1, 2, 1),      # 5x5, two images, reduction 300
     (1, 64, 7, 7, 96, 1, 1, 1, 0, 1),
     (1, 512, 7, 7, 64, 3, 3, 1, 1, 1),     # long reduction: split across work-groups
+    (1, 256, 7, 7, 40, 3, 3, 1, 1, 2),     # split, two groups of 20 filters
+    (1, 1024, 5, 5, 33, 1, 1, 1, 0, 1),    # split, 25 pixels, K = 33
+    (1, 300, 9, 9, 70, 3, 3, 1, 1, 1),     # split, reduction order (c, r, s)
 ]
+SPLIT = RAGGED[-4:]
 
 
 def test_stack_wave_packed_filters_ragged(oracle_lib):
     """Wave-kernel layers in a stack read filters packed once in the kernel's
     operand order (zero-padded blocks of 32 filters x 8 taps): exact against
     the oracle on small integers for ragged filter counts, reductions, groups
-    and strides, eager and replayed."""
+    and strides, eager and replayed; the last four split their reduction
+    across work-groups (a reduce launch sums the partials)."""
     ops, refs = [], []
     for i, (N, C, H, W, K, R, S, st, pad, g) in enumerate(RAGGED):
         x = wl.small_ints((N, C, H, W), -3, 3, 900 + i)
@@ -216,7 +221,8 @@ def test_stack_wave_packed_filters_ragged(oracle_lib):
     names = [s.describe(j) for j in range(len(ops))]
     assert all(n.startswith("igemm_wave_f32_kernel") for n in names), names
     assert not any("pack_wave" in n for n in names), names   # packed once, at stack creation
-    assert any("splitk_reduce" in n for n in names), names
+    for shape, n in zip(RAGGED, names):
+        assert ("splitk_reduce" in n) == (shape in SPLIT), (shape, n)
     for replay in (False, True):
         if replay:
             for o in ops:
@@ -229,4 +235,41 @@ def test_stack_wave_packed_filters_ragged(oracle_lib):
         for o, (x, w, b, st, pad, g, relu), shape in zip(ops, refs, RAGGED):
             want = oracle_lib.conv2d(x, w, b, st, pad, g, relu)
             np.testing.assert_array_equal(o[4].cpu().numpy(), want, err_msg=f"{shape} replay={replay}")
+    s.close()
+
+
+def test_stack_split_replays_bitwise(oracle_lib):
+    """ResNet-50 batch-1 layers whose reductions are split across 2-9
+    work-groups: the partials are summed in split order, so an eager pass and
+    three replays of a graph holding three passes (eager work and
+    synchronisation between them) give the same bits; and they meet the
+    1e-4 gate."""
+    idxs = [12, 25, 28, 43, 44, 46]
+    ops, refs = [], []
+    for i in idxs:
+        l = wl.workload(2).layers[i]
+        x, w, b = wl.layer_tensors(2, i, l)
+        P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+        y = torch.full((l.N, l.K, P, Q), float("nan"), device="cuda")
+        ops.append((miconv.OP_CONV_F32, torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda(),
+                    torch.from_numpy(b).cuda(), y, l.stride, l.pad, l.groups, l.relu))
+        refs.append((l, x, w, b))
+    s = miconv.Stack(ops)
+    assert s.launches == 2 * len(ops), [s.describe(j) for j in range(len(ops))]   # conv + reduce
+    s.launch()
+    torch.cuda.synchronize()
+    first = [o[4].clone() for o in ops]
+    for o, (l, x, w, b) in zip(ops, refs):
+        want = oracle_lib.conv2d(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        got = o[4].cpu().numpy().astype(np.float64)
+        assert np.max(np.abs(got - want)) / np.max(np.abs(want)) <= 1e-4, l.name
+    s.capture(3, timed=False)
+    for rep in range(3):
+        for o in ops:
+            o[4].fill_(float("nan"))
+        torch.cuda.synchronize()
+        s.replay()
+        torch.cuda.synchronize()
+        for o, f, (l, *_r) in zip(ops, first, refs):
+            assert torch.equal(o[4], f), (l.name, rep)
     s.close()
