@@ -245,7 +245,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_cl_kernel(ConvArgs a)
                 v0 = fmaxf(v0, 0.f);
                 v1 = fmaxf(v1, 0.f);
             }
-            d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+            d[e] = pack_bf16x2(v0, v1);
         }
         *reinterpret_cast<uint4 *>(y + off) = make_uint4(d[0], d[1], d[2], d[3]);
     }

@@ -636,7 +636,7 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
                 v0 = fmaxf(v0, 0.f);
                 v1 = fmaxf(v1, 0.f);
             }
-            d[e] = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+            d[e] = pack_bf16x2(v0, v1);
         }
         typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
         const u32x4 dv = {d[0], d[1], d[2], d[3]};

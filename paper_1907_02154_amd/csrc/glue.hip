@@ -110,7 +110,7 @@ __global__ __launch_bounds__(256) void maxpool_nhwc_bf16_kernel(const uint16_t *
         uint32_t d[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            d[e] = (uint32_t)f32_to_bf16_rne(m[2 * e]) | ((uint32_t)f32_to_bf16_rne(m[2 * e + 1]) << 16);
+            d[e] = pack_bf16x2(m[2 * e], m[2 * e + 1]);
         *reinterpret_cast<uint4 *>(y + pix * C + 8 * o) = make_uint4(d[0], d[1], d[2], d[3]);
     }
 }
