@@ -1401,6 +1401,8 @@ void launch_dma_nchw(const ConvArgs &a, int tile, int mode, dim3 grid, hipStream
             launch_dma<1, 1, 128, 64, 2, 2, 2, 2>(a, grid, st);
     } else if (tile == 0) {
         launch_dma<1, 1, 128, 128, 2, 2, 2, 1>(a, grid, st);
+    } else if (tile == 4) {
+        launch_dma<1, 1, 128, 64, 2, 2, 1, 1>(a, grid, st);
     } else {
         launch_dma<1, 1, 128, 64, 2, 2, 2, 1>(a, grid, st);
     }
@@ -1509,6 +1511,11 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
     // tiles 35.3 -> 30.2 us); with more chunks the pipelined tiles stay ahead.
     if (x_nhwc && p.R == 1 && p.S == 1 && chunks <= 4 && splits == 1 && wgs(4) >= num_cus)
         plan.tile = p.Kg >= 128 ? 4 : 5;
+    // The same for 1x1 layers reading NCHW x with 16-byte loads (fp32 NCHW
+    // output): 128 x 64 one-stage tiles, four per CU (measured at batch 64:
+    // 64 -> 256 at 56x56 58.2 -> 54.5 us, 128 -> 512 at 28x28 38.1 -> 34.8 us;
+    // the 4-byte-load layers at 14x14 even, so they keep their tiles).
+    if (plan.nchwb == 1 && chunks <= 4 && splits == 1 && wgs(4) >= num_cus) plan.tile = 4;
     // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
     // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
     // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With

@@ -64,12 +64,17 @@ __global__ __launch_bounds__(256) void add_act_kernel(const float *a, const floa
     }
 }
 
+// A thread rounds a pair of elements with one conversion instruction.
 __global__ __launch_bounds__(256) void cast_bf16_kernel(const float *__restrict__ x,
                                                         uint16_t *__restrict__ y, long n)
 {
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (long)gridDim.x * blockDim.x)
-        y[i] = f32_to_bf16_rne(x[i]);
+    for (long i = 2 * ((long)blockIdx.x * blockDim.x + threadIdx.x); i < n;
+         i += 2 * (long)gridDim.x * blockDim.x) {
+        const bool two = i + 1 < n;
+        const uint32_t d = pack_bf16x2(x[i], two ? x[i + 1] : 0.f);
+        y[i] = (uint16_t)d;
+        if (two) y[i + 1] = (uint16_t)(d >> 16);
+    }
 }
 
 // Max-pool over bf16 channel-last tensors: a thread takes 8 channels of one

@@ -259,10 +259,12 @@ def test_bf16_halo_small_int_bitwise(oracle_lib, case):
 
 
 NCHW_1X1_CASES = [  # (N, C, H, W, K, groups, loads): 1x1 stride-1 layers whose pixel operand comes from NCHW x
-    (3, 64, 56, 56, 520, 1, 1),     # image boundaries inside pixel tiles, ragged M and K (128 x 64 tiles)
-    (4, 64, 56, 56, 512, 1, 1),     # 128 x 128 tiles
-    (2, 192, 64, 64, 256, 1, 1),    # three reduction chunks
+    (3, 64, 56, 56, 520, 1, 1),     # image boundaries inside pixel tiles, ragged M and K (one-stage 128 x 64 tiles)
+    (4, 64, 56, 56, 512, 1, 1),     # one-stage tiles
+    (2, 192, 64, 64, 256, 1, 1),    # three reduction chunks, one stage
     (8, 128, 64, 64, 256, 2, 1),    # two groups of 64 channels
+    (8, 384, 56, 56, 256, 1, 1),    # six chunks: pipelined 128 x 128 tiles
+    (4, 384, 56, 56, 200, 1, 1),    # six chunks: pipelined 128 x 64 tiles, ragged K
     (64, 64, 14, 14, 256, 1, 2),    # 196-pixel planes: 8-pixel groups straddle images, 4-byte loads
     (64, 256, 14, 14, 1024, 1, 2),  # ResNet-50 s4 expansion layer, 128 x 128 tiles
     (200, 64, 10, 13, 256, 1, 2),   # 130-pixel planes, ragged last tile
@@ -672,6 +674,31 @@ def test_maxpool_add_cast(oracle_lib):
     miconv.cast_f32_to_bf16(dev(f), y)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.view(torch.int16).cpu().numpy().view(np.uint16), oracle_lib.f32_to_bf16(f))
+
+
+def test_cast_bf16_rounding_every_class(oracle_lib):
+    """The device's bf16 rounding (one conversion instruction for a pair of
+    values, used by every bf16 epilogue) against the oracle's on the cases
+    that decide rounding: signed zeros, infinities, quiet and signalling NaNs
+    of both signs and several payloads, denormals, the largest finite values
+    (which round to infinity), every exponent with a dropped half of exactly
+    0x8000 (ties, both parities of the kept bit) and its neighbours, and 2^22
+    random bit patterns; odd and even lengths."""
+    specials = [0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0xFFC00000, 0x7F800001,
+                0xFF800001, 0x7FBFFFFF, 0xFFFFFFFF, 0x7FFF8000, 0x00000001, 0x80000001, 0x007FFFFF,
+                0x00008000, 0x00018000, 0x80008000, 0x7F7FFFFF, 0xFF7FFFFF, 0x7F7F8000, 0x7F7F7FFF]
+    e = np.arange(256, dtype=np.uint32) << 23
+    ties = np.concatenate([e | 0x8000, e | 0x18000, e | 0x7FFF, e | 0x8001, e | 0x17FFF, e | 0x18001])
+    ties = np.concatenate([ties, ties | 0x80000000])
+    rng = np.random.default_rng(7)
+    rand = rng.integers(0, 2 ** 32, 1 << 22, dtype=np.uint64).astype(np.uint32)
+    bits = np.concatenate([np.uint32(specials), ties, rand])
+    for n in (bits.size, bits.size - 1, 1, 3):
+        f = bits[:n].view(np.float32)
+        y = torch.empty(f.shape, device="cuda", dtype=torch.bfloat16)
+        miconv.cast_f32_to_bf16(dev(f), y)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.view(torch.int16).cpu().numpy().view(np.uint16), oracle_lib.f32_to_bf16(f))
 
 
 def test_rejects_wrong_shapes_from_python():

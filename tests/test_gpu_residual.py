@@ -44,7 +44,7 @@ RES_CASES = [
     (1, 3, 45, 47, 40, 7, 7, 2, 3, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<7, 7, 8, 1, 2, false, 2>"),
     (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", I, "igemm_f32_kernel<1, 1, 32, 64, 1, 2, 64>"),
     (1, 12, 9, 9, 18, 3, 3, 1, 1, 3, "f32", A, "conv_direct_kernel<float>"),
-    (4, 64, 56, 56, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>"),
+    (4, 64, 56, 56, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 1, 1, 64>"),
     (64, 64, 14, 14, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 3, 2, 64>"),
     (8, 64, 28, 28, 128, 1, 1, 2, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
     (32, 64, 14, 14, 128, 3, 3, 1, 1, 1, "bf16", A, "igemm_bf16_dma_kernel<3, 3, 64, 64, 2, 2, 3, 0, 64>"),
@@ -56,6 +56,7 @@ RES_CASES = [
     (1, 40, 19, 19, 70, 3, 3, 1, 1, 1, "bf16", A, "splitk_reduce_kernel"),
     (1, 3, 224, 224, 64, 7, 7, 2, 3, 1, "bf16", A, "stem7_bf16_kernel"),
     (1, 12, 9, 9, 18, 3, 3, 1, 1, 3, "bf16", D, "conv_direct_kernel<unsigned short>"),
+    (4, 384, 56, 56, 200, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>"),   # six chunks: pipelined
 ]
 
 
@@ -126,7 +127,7 @@ def test_residual_join_small_int_bitwise(oracle_lib, case, mode):
 
 @pytest.mark.parametrize("case", [c for c in RES_CASES if c[-1] in (
     "igemm_wave_f32_kcrs_kernel<1, 1, 8, 1, 1, false, 1>", "splitk_reduce_kernel",
-    "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>")][:4],
+    "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 1, 1, 64>")][:4],
     ids=lambda c: "x".join(map(str, c[:10])) + "-" + c[10])
 def test_residual_offset_pointers(oracle_lib, case):
     """y and res one float past a 16-byte boundary (same offset): the kernels
@@ -249,6 +250,7 @@ def test_output_image_stride(oracle_lib, case):
 
 
 VEC_Y_CASES = [c for c in RES_CASES if c[-1] in (
+    "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 1, 1, 64>",
     "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>",
     "igemm_bf16_halo_kernel<128, 64, 2, 2, 256, 1>",
     "igemm_bf16_halo_kernel<128, 128, 2, 2, 192, 2>",
