@@ -44,6 +44,28 @@ struct NhwcCopyArgs {
     FastDiv dv_hw, dv_pq, dv_q;
 };
 
+// Writes a staged tile ([64 channels][64 pixels], channel row c at row
+// c ^ ((c >> 3) & 7)) to the channel-last copy: a lane gathers 8 channels of
+// one pixel and stores them as 16 bytes.
+__device__ __forceinline__ void copy_tile_out(const NhwcCopyArgs &a, const uint16_t (*tile)[64 + 8], int c0,
+                                              int p0, int t)
+{
+    auto row = [](int c) { return c ^ ((c >> 3) & 7); };
+#pragma unroll
+    for (int i = 0; i < 64 / 32; ++i) {   // 64 pixels x 8 channel octets
+        const int id = t + 256 * i;
+        const int px = id >> 3, o = id & 7;
+        if (c0 + 8 * o < a.C && p0 + px < a.npq) {
+            uint32_t d[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                d[e] = (uint32_t)tile[row(8 * o + 2 * e)][px] | ((uint32_t)tile[row(8 * o + 2 * e + 1)][px] << 16);
+            *reinterpret_cast<uint4 *>(a.xt + (long)(p0 + px) * a.C + c0 + 8 * o) =
+                make_uint4(d[0], d[1], d[2], d[3]);
+        }
+    }
+}
+
 template <int RV>
 __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
 {
@@ -93,19 +115,49 @@ __global__ __launch_bounds__(256) void nchw_to_nhwc_bf16_kernel(NhwcCopyArgs a)
         }
     }
     __syncthreads();
+    copy_tile_out(a, tile, c0, p0, t);
+}
+
+// Stride-2 subsampling copy (1x1 stride-2 layers) reading G sampled pixels
+// per load: output pixels q .. q+G-1 of a row sample input columns 2q ..
+// 2q+2G-2, so one 4G-byte load of 2G consecutive input pixels holds them at
+// its even positions.  Requires Q % G == 0 (a group stays in one output row),
+// W % G == 0 and H*W % 2G == 0 (every load aligned) and W = 2Q (a load never
+// passes the end of its input row).
+template <int G>
+__global__ __launch_bounds__(256) void nchw_to_nhwc_sampled_bf16_kernel(NhwcCopyArgs a)
+{
+    static_assert(G == 2 || G == 4, "8- or 16-byte loads");
+    constexpr int PX = 64;
+    __shared__ __attribute__((aligned(16))) uint16_t tile[64][PX + 8];
+    auto row = [](int c) { return c ^ ((c >> 3) & 7); };
+    const int t = threadIdx.x;
+    const int c0 = (blockIdx.x % a.tiles_c) * 64;
+    const int p0 = (blockIdx.x / a.tiles_c) * PX;
+    constexpr int GR = PX / G;                  // sampled groups per channel row
 #pragma unroll
-    for (int i = 0; i < PX / 32; ++i) {   // PX pixels x 8 channel octets
+    for (int i = 0; i < 64 * GR / 256; ++i) {
         const int id = t + 256 * i;
-        const int px = id >> 3, o = id & 7;
-        if (c0 + 8 * o < a.C && p0 + px < a.npq) {
-            uint32_t d[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                d[e] = (uint32_t)tile[row(8 * o + 2 * e)][px] | ((uint32_t)tile[row(8 * o + 2 * e + 1)][px] << 16);
-            *reinterpret_cast<uint4 *>(a.xt + (long)(p0 + px) * a.C + c0 + 8 * o) =
-                make_uint4(d[0], d[1], d[2], d[3]);
+        const int c = id / GR, o = id % GR;
+        const int px = p0 + G * o;
+        const bool ok = c0 + c < a.C && px < a.npq;
+        const unsigned m = ok ? px : 0;
+        const unsigned n = fdiv(m, a.dv_pq);
+        const unsigned pq = m - n * a.PQ;
+        const unsigned pp = fdiv(pq, a.dv_q);
+        const unsigned q = pq - pp * a.Q;
+        const uint16_t *src = a.x + ((long)n * a.C + c0 + c) * a.HW + (long)(2 * pp) * a.W + 2 * q;
+        if constexpr (G == 4) {
+            const uint4 v = ok ? *reinterpret_cast<const uint4 *>(src) : make_uint4(0, 0, 0, 0);
+            *reinterpret_cast<uint2 *>(&tile[row(c)][4 * o]) =
+                make_uint2((v.x & 0xFFFFu) | (v.y << 16), (v.z & 0xFFFFu) | (v.w << 16));
+        } else {
+            const uint2 v = ok ? *reinterpret_cast<const uint2 *>(src) : make_uint2(0, 0);
+            *reinterpret_cast<uint32_t *>(&tile[row(c)][2 * o]) = (v.x & 0xFFFFu) | (v.y << 16);
         }
     }
+    __syncthreads();
+    copy_tile_out(a, tile, c0, p0, t);
 }
 
 // Small planes (32*H*W <= kPlaneElems): a work-group moves one image's block
@@ -1323,7 +1375,13 @@ int copy_read_width(const ConvProblem &p, const void *x)
     const int HW = p.H * p.W;
     const bool scalar = copy_subsamples(p) || HW % 4 != 0;
     if (scalar && 32 * HW <= kPlaneElems && p.C % 8 == 0 && xa % 16 == 0) return 0;
-    if (copy_subsamples(p)) return 1;
+    if (copy_subsamples(p)) {
+        // stride 2: negative = sampled pixels per load (8- or 16-byte loads)
+        const bool s2 = p.stride == 2 && p.W == 2 * p.Q;
+        if (s2 && p.Q % 4 == 0 && p.W % 4 == 0 && HW % 8 == 0 && xa % 16 == 0) return -4;
+        if (s2 && p.Q % 2 == 0 && p.W % 2 == 0 && HW % 4 == 0 && xa % 8 == 0) return -2;
+        return 1;
+    }
     if (HW % 8 == 0 && xa % 16 == 0) return 8;
     if (HW % 4 == 0 && xa % 8 == 0) return 4;
     return 1;
@@ -1573,6 +1631,8 @@ void describe_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, char *buf, i
     const int rv = copy_read_width(p, nullptr);
     if (rv == 0)
         snprintf(tname, sizeof tname, "nchw_to_nhwc_plane_bf16_kernel + ");
+    else if (rv < 0)
+        snprintf(tname, sizeof tname, "nchw_to_nhwc_sampled_bf16_kernel<%d> + ", -rv);
     else
         snprintf(tname, sizeof tname, "nchw_to_nhwc_bf16_kernel<%d> + ", rv);
     const bool copy = !plan.nchwb && !plan.x_nhwc;
@@ -1677,6 +1737,10 @@ hipError_t launch_nhwc_bf16(const ConvProblem &p, const NhwcPlan &plan, const ui
         launch_kernel(nchw_to_nhwc_bf16_kernel<8>, tg, tb, 0, st, ca);
     else if (rv == 4)
         launch_kernel(nchw_to_nhwc_bf16_kernel<4>, tg, tb, 0, st, ca);
+    else if (rv == -4)
+        launch_kernel(nchw_to_nhwc_sampled_bf16_kernel<4>, tg, tb, 0, st, ca);
+    else if (rv == -2)
+        launch_kernel(nchw_to_nhwc_sampled_bf16_kernel<2>, tg, tb, 0, st, ca);
     else
         launch_kernel(nchw_to_nhwc_bf16_kernel<1>, tg, tb, 0, st, ca);
     if ((e = hipGetLastError()) != hipSuccess) return e;

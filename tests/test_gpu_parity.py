@@ -161,6 +161,10 @@ BF16_CASES = DENSE_CASES[:9] + [
     (32, 256, 63, 63, 16, 1, 1, 2, 0, 1),    # large sampled copy: 256-pixel tiles
     (24, 256, 45, 45, 16, 1, 1, 1, 0, 1),    # large copy of odd planes: 256-pixel tiles, scalar reads
     (2, 64, 21, 23, 64, 3, 3, 1, 1, 1),      # 483-pixel planes: whole-plane copy in 32-channel blocks
+    (3, 96, 56, 56, 40, 1, 1, 2, 0, 1),      # stride-2 copy, 4 sampled pixels per 16-byte load, ragged channels
+    (2, 64, 28, 28, 72, 1, 1, 2, 0, 1),      # stride-2 copy, 2 sampled pixels per 8-byte load (Q = 14)
+    (2, 64, 20, 36, 64, 1, 1, 2, 0, 1),      # 10 x 18 sampled rows: 8-byte loads
+    (2, 64, 30, 30, 64, 1, 1, 2, 0, 1),      # odd Q = 15: sampled copy reads pixel by pixel
 ]
 
 
@@ -184,6 +188,7 @@ OFFSET_CASES = [  # (N, C, H, W, K, R, S, stride, pad, groups) run on x and y at
     (2, 64, 14, 14, 96, 3, 3, 1, 1, 1),
     (2, 64, 14, 14, 64, 1, 1, 2, 0, 1),
     (1, 64, 16, 16, 128, 1, 1, 1, 0, 1),
+    (2, 64, 28, 28, 64, 1, 1, 2, 0, 1),      # stride-2 copy: the grouped loads need an aligned x
 ]
 
 
