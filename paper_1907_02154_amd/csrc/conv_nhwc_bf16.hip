@@ -438,29 +438,53 @@ __device__ inline void store_tile(const ConvArgs &a, const float *ot, int tid, i
     float *out = split_out ? a.ws + (long)split * a.K * a.M : a.y;
     const bool vec = split_out ? (a.M & 3) == 0 : ((a.PQ & 3) == 0 && ((uintptr_t)a.y & 15) == 0 && (a.ysn & 3) == 0);
     constexpr int C4 = BPX / 4;
-    for (int idx = tid; idx < BKC * C4; idx += NT) {
-        const int kl = idx / C4, c4 = idx - kl * C4;
+    constexpr int KS = NT / C4;                     // filter rows per pass of the work-group
+    constexpr int IT = BKC / KS;                    // passes
+    static_assert(NT % C4 == 0 && BKC % KS == 0, "epilogue rows per thread");
+    // A thread's rows share one quad of pixels, m .. m+3 (c4 = tid % C4), and
+    // step through the filters KS at a time.
+    const int c4 = tid % C4, kl0 = tid / C4;
+    const int m = m0 + 4 * c4;
+    if (m >= a.M) return;
+    if (vec && m + 3 < a.M) {
+        // the quad lies in one image plane (P*Q % 4 == 0): one image index and
+        // one base offset; every row is a constant stride further
+        const int n = split_out ? 0 : (int)fdiv(m, a.dv_pq);
+        const long kstride = split_out ? (long)a.M : (long)a.PQ;
+        const long base = split_out ? (long)m : (long)n * a.ysn + (m - n * a.PQ);
+        float *dst = out + base + ((long)g * a.Kg + k0 + kl0) * kstride;
+        const long step = KS * kstride;
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        constexpr int B = IT < 8 ? IT : 8;          // LDS reads in flight per batch
+        static_assert(IT % B == 0, "batches");
+#pragma unroll
+        for (int i0 = 0; i0 < IT; i0 += B) {
+            f32x4 v[B];
+#pragma unroll
+            for (int i = 0; i < B; ++i)
+                v[i] = *reinterpret_cast<const f32x4 *>(ot + (kl0 + (i0 + i) * KS) * OP + 4 * c4);
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                if (k0 + kl0 + (i0 + i) * KS < a.Kg)
+                    __builtin_nontemporal_store(v[i], reinterpret_cast<f32x4 *>(dst + (i0 + i) * step));
+            }
+        }
+        return;
+    }
+    for (int it = 0; it < IT; ++it) {
+        const int kl = kl0 + it * KS;
         const int k = k0 + kl;
-        const int m = m0 + 4 * c4;
-        if (k >= a.Kg || m >= a.M) continue;
+        if (k >= a.Kg) break;
         const int kg = g * a.Kg + k;
         const float4 v = *reinterpret_cast<const float4 *>(ot + kl * OP + 4 * c4);
         const float ve[4] = {v.x, v.y, v.z, v.w};
-        if (vec && m + 3 < a.M) {
-            const int n = split_out ? 0 : (int)fdiv(m, a.dv_pq);
-            const long off = split_out ? (long)kg * a.M + m : ((long)n * a.ysn + (long)kg * a.PQ) + (m - n * a.PQ);
-            typedef float f32x4 __attribute__((ext_vector_type(4)));
-            const f32x4 nv = {v.x, v.y, v.z, v.w};
-            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4 *>(out + off));
-        } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int mm = m + e;
-                if (mm >= a.M) break;
-                const int n = split_out ? 0 : (int)fdiv(mm, a.dv_pq);
-                const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.ysn + (long)kg * a.PQ) + (mm - n * a.PQ);
-                out[off] = ve[e];
-            }
+        for (int e = 0; e < 4; ++e) {
+            const int mm = m + e;
+            if (mm >= a.M) break;
+            const int n = split_out ? 0 : (int)fdiv(mm, a.dv_pq);
+            const long off = split_out ? (long)kg * a.M + mm : ((long)n * a.ysn + (long)kg * a.PQ) + (mm - n * a.PQ);
+            out[off] = ve[e];
         }
     }
 }
