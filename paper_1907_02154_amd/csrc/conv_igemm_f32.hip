@@ -199,30 +199,22 @@ __global__ __launch_bounds__(64 * WK * WP) void igemm_f32_kernel(ConvArgs a)
 // activation, rounds to bf16 and stores 16 bytes.
 __global__ __launch_bounds__(256) void splitk_reduce_cl_kernel(ConvArgs a)
 {
-    const int K8 = a.K / 8;
-    const long units = (long)a.M * K8;
-    const long plane = (long)a.M * a.K;
+    constexpr int kGroup = 4;                   // splits whose loads are in flight together
+    constexpr unsigned kOut = 0x80000000u;      // past the partials: reads as zeros
+    const unsigned K8 = (unsigned)a.K / 8;
+    const unsigned units = (unsigned)a.M * K8;  // below 2^31, as every offset here (the launcher checks)
+    const unsigned plane = (unsigned)a.M * a.K;
+    const __amdgpu_buffer_rsrc_t wsr = __builtin_amdgcn_make_buffer_rsrc(
+        a.ws, (short)0, (int)(a.splits * plane * 4u), 0x00020000);
     const uint16_t *res = reinterpret_cast<const uint16_t *>(a.res);
     uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < units; i += (long)gridDim.x * blockDim.x) {
-        const int o = (int)(i % K8);
-        const long m = i / K8;
-        const long off = m * a.K + 8 * o;
-        float s[8];
+    for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < units; i += gridDim.x * blockDim.x) {
+        const unsigned m = fdiv(i, a.dv_kt);    // division by K/8
+        const unsigned o = i - m * K8;
+        const unsigned off = m * a.K + 8 * o;
+        float bv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s[e] = 0.f;
-        for (int sp = 0; sp < a.splits; ++sp) {
-            const float4 lo = *reinterpret_cast<const float4 *>(a.ws + sp * plane + off);
-            const float4 hi = *reinterpret_cast<const float4 *>(a.ws + sp * plane + off + 4);
-            s[0] += lo.x;
-            s[1] += lo.y;
-            s[2] += lo.z;
-            s[3] += lo.w;
-            s[4] += hi.x;
-            s[5] += hi.y;
-            s[6] += hi.z;
-            s[7] += hi.w;
-        }
+        for (int e = 0; e < 8; ++e) bv[e] = a.bias ? a.bias[8 * o + e] : 0.f;
         uint32_t rr[4] = {0, 0, 0, 0};
         if (res) {
             const uint4 r = *reinterpret_cast<const uint4 *>(res + off);
@@ -231,12 +223,35 @@ __global__ __launch_bounds__(256) void splitk_reduce_cl_kernel(ConvArgs a)
             rr[2] = r.z;
             rr[3] = r.w;
         }
+        // split order from zero, kGroup splits' loads requested before any add
+        float s[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] = 0.f;
+        for (int sp = 0; sp < a.splits; sp += kGroup) {
+            float4 lo[kGroup], hi[kGroup];
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                const unsigned b = sp + u < a.splits ? ((sp + u) * plane + off) * 4u : kOut;
+                lo[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(wsr, b, 0, 0));
+                hi[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(wsr, b + 16u, 0, 0));
+            }
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                s[0] += lo[u].x;
+                s[1] += lo[u].y;
+                s[2] += lo[u].z;
+                s[3] += lo[u].w;
+                s[4] += hi[u].x;
+                s[5] += hi[u].y;
+                s[6] += hi[u].z;
+                s[7] += hi[u].w;
+            }
+        }
         uint32_t d[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int k = 8 * o + 2 * e;
-            float v0 = s[2 * e] + (a.bias ? a.bias[k] : 0.f);
-            float v1 = s[2 * e + 1] + (a.bias ? a.bias[k + 1] : 0.f);
+            float v0 = s[2 * e] + bv[2 * e];
+            float v1 = s[2 * e + 1] + bv[2 * e + 1];
             if (res) {
                 v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
                 v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
@@ -424,6 +439,7 @@ hipError_t launch_splitk_reduce(ConvArgs a, hipStream_t st)
         // channel-last bf16 output: partials [splits][M][K], 8 channels per thread
         const long units = (long)a.M * (a.K / 8);
         if ((long)a.splits * a.M * a.K * 4 >= (1L << 31) || a.K % 8) return hipErrorInvalidValue;
+        a.dv_kt = make_fastdiv(a.K / 8);
         long blocks = (units + 255) / 256;
         if (blocks > 8192) blocks = 8192;
         launch_kernel(splitk_reduce_cl_kernel, dim3((unsigned)blocks), dim3(256), 0, st, a);

@@ -109,6 +109,7 @@ struct ConvArgs {
     FastDiv dv_pq, dv_q;  // division by P*Q and by Q
     FastDiv dv_m;         // division by M (split-K reduce)
     FastDiv dv_mt, dv_kt, dv_g, dv_cb;   // wave kernel: pixel tiles, filter tiles, groups, C/groups/8
+                                         // (dv_kt: K/8 in the channel-last split reduce)
     // Last, so that the fields every kernel reads first keep their offsets at
     // the front of the argument block (batch-1 kernels run a few microseconds).
     const float *res;     // [N][K][P][Q] residual added before the activation, or nullptr; it may

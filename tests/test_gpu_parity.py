@@ -81,6 +81,7 @@ DENSE_CASES = [
     (2, 2, 19, 17, 33, 3, 3, 2, 1, 1),       # two channels padded to four
     (1, 4, 13, 13, 20, 5, 5, 1, 2, 1),       # four channels, generic 5x5
     (1, 8, 12, 10, 64, 3, 2, 1, 1, 2),       # C/groups = 4 in each of two groups, R != S
+    (4, 512, 7, 7, 64, 3, 3, 1, 1, 1),       # split over four images: the reduction's pixel quads span images
 ]
 
 
@@ -165,6 +166,7 @@ BF16_CASES = DENSE_CASES[:9] + [
     (2, 64, 28, 28, 72, 1, 1, 2, 0, 1),      # stride-2 copy, 2 sampled pixels per 8-byte load (Q = 14)
     (2, 64, 20, 36, 64, 1, 1, 2, 0, 1),      # 10 x 18 sampled rows: 8-byte loads
     (2, 64, 30, 30, 64, 1, 1, 2, 0, 1),      # odd Q = 15: sampled copy reads pixel by pixel
+    (4, 512, 7, 7, 256, 3, 3, 1, 1, 1),      # split over four images: the reduction's pixel quads span images
 ]
 
 
