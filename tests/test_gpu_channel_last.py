@@ -54,6 +54,11 @@ CL_CASES = [
     (16, 64, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),   # one stage
     (17, 128, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),  # 2 chunks, ragged M
     (42, 64, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 1, 0, 64>"),     # one stage, 64 x 64
+    (32, 64, 56, 56, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),   # 3136 tiles
+    (128, 64, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 1, 0, 64>"),    # 1568 tiles
+    (16, 128, 28, 28, 256, 1, 1, 1, 0, 2, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),  # two groups
+    (64, 256, 28, 28, 200, 1, 1, 2, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),  # stride 2, ragged K
+    (32, 64, 30, 30, 136, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 64, 2, 2, 1, 0, 64>"),   # K = 136: a partial filter tile
     (16, 256, 28, 28, 128, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
     (64, 512, 28, 28, 256, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, 128, 128, 2, 2, 2, 0, 64>"),
     (4, 256, 28, 28, 64, 1, 1, 1, 0, 1, XY, "igemm_bf16_dma_cl_kernel<1, 1, "),
