@@ -654,7 +654,9 @@ __device__ inline void cl_res_load(const ConvArgs &a, ClRes<BPX, BKC, NT> &r, in
     }
 }
 
-template <int BPX, int BKC, int NT, int TPX, int TCH, int BJ, int BI>
+// NH = 2: the tile is staged in two passes of half its pixels (each the
+// pixels of one column of wavefronts, WPX = 2), which halves the staging LDS.
+template <int BPX, int BKC, int NT, int TPX, int TCH, int BJ, int BI, int NH = 1>
 __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][BI], float *ot, int tid,
                                    int wpx, int wch, int h, int ll, int k0, int m0, int g, int split,
                                    const ClRes<BPX, BKC, NT> &cr)
@@ -662,61 +664,69 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
     constexpr int CP = BKC + 4;
     constexpr int C8 = BKC / 8;
     constexpr int IT = BPX / (NT / C8);              // pixels per thread
+    constexpr int PH = BPX / NH;                     // pixels per pass
+    static_assert(NH == 1 || (NH == 2 && TPX == PH && IT % 2 == 0), "a pass is one column of wavefronts");
     const int o = tid % C8;
     const int k = k0 + 8 * o;
     const int kg = g * a.Kg + k;
+    const bool kok = k < a.Kg;                       // K/groups % 8 == 0: the octet is whole
     const uint4 *rv = cr.rv;
-#pragma unroll
-    for (int bi = 0; bi < BI; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < BJ; ++bj)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int kl = wch * TCH + bi * 32 + 8 * q4 + 4 * h;
-                const int pl = wpx * TPX + bj * 32 + ll;
-                *reinterpret_cast<float4 *>(ot + pl * CP + kl) =
-                    make_float4(acc[bj][bi][4 * q4], acc[bj][bi][4 * q4 + 1], acc[bj][bi][4 * q4 + 2],
-                                acc[bj][bi][4 * q4 + 3]);
-            }
-    __syncthreads();
-    if (k >= a.Kg) return;                      // K/groups % 8 == 0: the octet is whole
     float bv[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) bv[e] = (a.splits == 1 && a.bias) ? a.bias[kg + e] : 0.f;
+    for (int e = 0; e < 8; ++e) bv[e] = (kok && a.splits == 1 && a.bias) ? a.bias[kg + e] : 0.f;
     uint16_t *y = reinterpret_cast<uint16_t *>(a.y);
 #pragma unroll
-    for (int it = 0; it < IT; ++it) {
-        const int pl = tid / C8 + it * (NT / C8);
-        const int m = m0 + pl;
-        if (m >= a.M) break;
-        const float4 lo = *reinterpret_cast<const float4 *>(ot + pl * CP + 8 * o);
-        const float4 hi = *reinterpret_cast<const float4 *>(ot + pl * CP + 8 * o + 4);
-        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        const long off = (long)m * a.K + kg;
-        if (a.splits > 1) {
-            float *dst = a.ws + (long)split * a.M * a.K + off;
-            *reinterpret_cast<float4 *>(dst) = lo;
-            *reinterpret_cast<float4 *>(dst + 4) = hi;
-            continue;
-        }
-        const uint32_t rr[4] = {rv[it].x, rv[it].y, rv[it].z, rv[it].w};
-        uint32_t d[4];
+    for (int hp = 0; hp < NH; ++hp) {
+        if (hp) __syncthreads();                     // every thread is done reading the last pass
+        if (NH == 1 || wpx == hp) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            float v0 = v[2 * e] + bv[2 * e], v1 = v[2 * e + 1] + bv[2 * e + 1];
-            if (a.res) {
-                v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
-                v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
-            }
-            if (a.relu) {
-                v0 = fmaxf(v0, 0.f);
-                v1 = fmaxf(v1, 0.f);
-            }
-            d[e] = pack_bf16x2(v0, v1);
+            for (int bi = 0; bi < BI; ++bi)
+#pragma unroll
+                for (int bj = 0; bj < BJ; ++bj)
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const int kl = wch * TCH + bi * 32 + 8 * q4 + 4 * h;
+                        const int pl = wpx * TPX + bj * 32 + ll - hp * PH;
+                        *reinterpret_cast<float4 *>(ot + pl * CP + kl) =
+                            make_float4(acc[bj][bi][4 * q4], acc[bj][bi][4 * q4 + 1], acc[bj][bi][4 * q4 + 2],
+                                        acc[bj][bi][4 * q4 + 3]);
+                    }
         }
-        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-        const u32x4 dv = {d[0], d[1], d[2], d[3]};
-        __builtin_nontemporal_store(dv, reinterpret_cast<u32x4 *>(y + off));
+        __syncthreads();
+#pragma unroll
+        for (int it = hp * (IT / NH); it < (hp + 1) * (IT / NH); ++it) {
+            const int pl = tid / C8 + it * (NT / C8);
+            const int m = m0 + pl;
+            if (!kok || m >= a.M) continue;
+            const float4 lo = *reinterpret_cast<const float4 *>(ot + (pl - hp * PH) * CP + 8 * o);
+            const float4 hi = *reinterpret_cast<const float4 *>(ot + (pl - hp * PH) * CP + 8 * o + 4);
+            float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            const long off = (long)m * a.K + kg;
+            if (a.splits > 1) {
+                float *dst = a.ws + (long)split * a.M * a.K + off;
+                *reinterpret_cast<float4 *>(dst) = lo;
+                *reinterpret_cast<float4 *>(dst + 4) = hi;
+                continue;
+            }
+            const uint32_t rr[4] = {rv[it].x, rv[it].y, rv[it].z, rv[it].w};
+            uint32_t d[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float v0 = v[2 * e] + bv[2 * e], v1 = v[2 * e + 1] + bv[2 * e + 1];
+                if (a.res) {
+                    v0 += bf16_to_f32((uint16_t)(rr[e] & 0xFFFFu));
+                    v1 += bf16_to_f32((uint16_t)(rr[e] >> 16));
+                }
+                if (a.relu) {
+                    v0 = fmaxf(v0, 0.f);
+                    v1 = fmaxf(v1, 0.f);
+                }
+                d[e] = pack_bf16x2(v0, v1);
+            }
+            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 dv = {d[0], d[1], d[2], d[3]};
+            __builtin_nontemporal_store(dv, reinterpret_cast<u32x4 *>(y + off));
+        }
     }
 }
 
@@ -752,7 +762,10 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
     static_assert(KRC == 64 || KRC == 32, "reduction chunk");
 
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
-    constexpr int EPI = YCL ? BPX * (BKC + 4) / 4 : BKC * OP / 4;   // epilogue tile, 16-byte units
+    // one-stage 128-pixel channel-last tiles stage their epilogue in two
+    // passes, so the operand stage sets the LDS size
+    constexpr int NHE = YCL && NST == 1 && BPX == 128 && WPX == 2 ? 2 : 1;
+    constexpr int EPI = YCL ? BPX / NHE * (BKC + 4) / 4 : BKC * OP / 4;   // epilogue tile, 16-byte units
     constexpr int SMEM = NST * (UA + UB) > EPI ? NST * (UA + UB) : EPI;
     __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];
 
@@ -995,8 +1008,8 @@ __device__ __forceinline__ void dma_body(const ConvArgs &a)
 
     if constexpr (YCL) {
         __syncthreads();   // every wavefront is done with the operand stages
-        epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch, h,
-                                                    ll, k0, m0, g, split, cr);
+        epilogue_cl<BPX, BKC, NT, TPX, TCH, BJ, BI, NHE>(a, acc, reinterpret_cast<float *>(smem), tid, wpx, wch,
+                                                         h, ll, k0, m0, g, split, cr);
         return;
     }
     // Epilogue through LDS: the tile (BKC channels x BPX pixels, fp32, bias and
@@ -1047,7 +1060,7 @@ __global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_kernel(ConvArgs
 
 // Channel-last bf16 output (and residual): the epilogue_cl instantiation.
 template <int R_, int S_, int BPX, int BKC, int WPX, int WCH, int NST, int NCHWB, int KRC = 64>
-__global__ __launch_bounds__(64 * WPX * WCH) void igemm_bf16_dma_cl_kernel(ConvArgs a)
+__global__ __launch_bounds__(64 * WPX * WCH, NST == 1 && BPX == 128 ? 5 : 1) void igemm_bf16_dma_cl_kernel(ConvArgs a)
 {
     dma_body<R_, S_, BPX, BKC, WPX, WCH, NST, NCHWB, KRC, false, true>(a);
 }
