@@ -327,6 +327,9 @@ int set_residual(Resolved &r, const float *res)
         return MICONV_ERR_ALIGN;
     if (r.impl == IMPL_DW) return MICONV_ERR_UNSUPPORTED;
     r.p.res = res;
+    // the plan of a 1x1 layer reading NCHW x depends on the residual (tile choice)
+    if (r.impl == IMPL_NHWC_BF16 && r.nplan.nchwb)
+        r.nplan = plan_nhwc_bf16(r.p, cu_count(), r.x, (r.mode & MODE_SCRATCH) ? 64 : 1);
     return MICONV_OK;
 }
 

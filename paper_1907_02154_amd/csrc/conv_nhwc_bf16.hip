@@ -1610,7 +1610,8 @@ static NhwcPlan plan_dma(const ConvProblem &p, int num_cus, const void *x, int m
     // output): 128 x 64 one-stage tiles, four per CU (measured at batch 64:
     // 64 -> 256 at 56x56 58.2 -> 54.5 us, 128 -> 512 at 28x28 38.1 -> 34.8 us;
     // the 4-byte-load layers at 14x14 even, so they keep their tiles).
-    if (plan.nchwb == 1 && chunks <= 4 && splits == 1 && wgs(4) >= num_cus) plan.tile = 4;
+    // Not with a residual: its kernel's registers allow two work-groups per CU.
+    if (plan.nchwb == 1 && !p.res && chunks <= 4 && splits == 1 && wgs(4) >= num_cus) plan.tile = 4;
     // 3x3 stride-1 layers on 128 x 128 tiles stage one input patch per
     // 64-channel block for all nine taps (igemm_bf16_halo_kernel; measured at
     // batch 64: 28x28 24.5 -> 22.4 us, 7x7 23.2 -> 21.8 us per launch).  With

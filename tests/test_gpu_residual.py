@@ -44,6 +44,7 @@ RES_CASES = [
     (1, 3, 45, 47, 40, 7, 7, 2, 3, 1, "f32", A, "igemm_wave_f32_kcrs_kernel<7, 7, 8, 1, 2, false, 2>"),
     (2, 64, 15, 13, 130, 1, 1, 1, 0, 1, "f32", I, "igemm_f32_kernel<1, 1, 32, 64, 1, 2, 64>"),
     (1, 12, 9, 9, 18, 3, 3, 1, 1, 3, "f32", A, "conv_direct_kernel<float>"),
+    # named without the residual; with it the two-stage tile runs (test_residual_plan_keeps_two_stage_tile)
     (4, 64, 56, 56, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 1, 1, 64>"),
     (64, 64, 14, 14, 256, 1, 1, 1, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 3, 2, 64>"),
     (8, 64, 28, 28, 128, 1, 1, 2, 0, 1, "bf16", A, "igemm_bf16_dma_kernel<1, 1, 64, 64, 2, 2, 3, 0, 64>"),
@@ -123,6 +124,24 @@ def test_residual_join_small_int_bitwise(oracle_lib, case, mode):
     _join(tx, tw, dev(b), None, y, st, pad, g, True, algo, mode)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y.cpu().numpy(), _oracle(oracle_lib, case, x, w, b, np.zeros_like(res), True))
+
+
+def test_residual_plan_keeps_two_stage_tile():
+    """A 1x1 layer reading NCHW x with few reduction chunks takes the
+    one-stage tile alone, but with a residual the planner keeps the two-stage
+    one: the one-stage kernel's residual epilogue leaves room for two
+    work-groups per CU only."""
+    x = torch.zeros((4, 64, 56, 56), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((256, 64, 1, 1), dtype=torch.bfloat16, device="cuda")
+    y = torch.zeros((4, 256, 56, 56), device="cuda")
+    res = torch.zeros_like(y)
+    names = []
+    for r in (None, res):
+        s = miconv.Stack([(miconv.OP_CONV_BF16, x, w, None, y, 1, 0, 1, True, r)])
+        names.append(s.describe(0))
+        s.close()
+    assert names[0] == "igemm_bf16_dma_kernel<1, 1, 128, 64, 2, 2, 1, 1, 64>", names[0]
+    assert names[1] == "igemm_bf16_dma_res_kernel<1, 1, 128, 64, 2, 2, 2, 1, 64>", names[1]
 
 
 @pytest.mark.parametrize("case", [c for c in RES_CASES if c[-1] in (
