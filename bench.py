@@ -135,6 +135,10 @@ def parse():
                     help="instead: the ResNet-50 join layers (last 1x1 of each bottleneck block) "
                          "with the shortcut add + ReLU fused into the conv epilogue, against the "
                          "same convs followed by a separate add kernel (--config 2 or 5)")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="instead: the vendor bf16 GEMM (torch.matmul, hipBLASLt) on the ResNet-50 b64 "
+                         "layer shapes as plain [M, C*R*S] x [C*R*S, K] products, im2col excluded "
+                         "(context for the conv kernels, not part of the library)")
     return ap.parse_args()
 
 
@@ -157,6 +161,53 @@ def _graph_ms(torch, fn, steps, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / steps
+
+
+def vendor_gemm(args):
+    """The ResNet-50 batch-64 layer shapes (configuration 5) as plain bf16 GEMMs
+    through torch.matmul (hipBLASLt), each distinct shape timed as a HIP graph of
+    `steps` products over four rotating input/output sets, fp32 accumulation,
+    bf16 output.  The operand of a 3x3 or strided layer is taken as an already
+    formed [M, C*R*S] matrix, so this is a lower bound on an im2col + GEMM
+    convolution: it skips the im2col, the bias, ReLU and residual join."""
+    import torch
+    from paper_1907_02154_amd import workloads as wl
+    torch.cuda.set_device(0)
+    torch.backends.cuda.matmul.allow_bf16_reduced_precision_reduction = False
+    stream = torch.cuda.current_stream()
+    rows, seen, total = [], {}, 0.0
+    for l in wl.workload(5).layers:
+        P, Q = (l.H + 2 * l.pad - l.R) // l.stride + 1, (l.W + 2 * l.pad - l.S) // l.stride + 1
+        M, Kred = l.N * P * Q, l.C * l.R * l.S
+        key = (M, Kred, l.K)
+        if key not in seen:
+            b = torch.randn(Kred, l.K, device="cuda", dtype=torch.bfloat16)
+            sets = [(torch.randn(M, Kred, device="cuda", dtype=torch.bfloat16),
+                     torch.empty(M, l.K, device="cuda", dtype=torch.bfloat16)) for _ in range(4)]
+            it = [0]
+
+            def one(s, sets=sets, b=b, it=it):
+                x, y = sets[it[0] % 4]
+                it[0] += 1
+                torch.matmul(x, b, out=y)
+
+            with torch.cuda.stream(torch.cuda.Stream()):
+                for _ in range(args.warmup):
+                    one(None)
+            torch.cuda.synchronize()
+            seen[key] = _graph_ms(torch, one, args.steps, stream) * 1e3
+            del sets
+        us = seen[key]
+        total += us
+        fl = 2.0 * M * Kred * l.K
+        rows.append({"layer": l.name, "M": M, "CRS": Kred, "K": l.K, "us": round(us, 2),
+                     "mfma_frac": round(fl / us / 1e6 / PEAK_BF16_MFMA_TFLOPS, 4)})
+    print(json.dumps({"metric": "vendor GEMM time on the ResNet-50 b64 layer shapes (im2col excluded)",
+                      "value": round(total / 1e3, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps,
+                      "warmup": args.warmup, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+                      "config": {"workload": "ResNet-50 v1 b64 layer shapes as plain GEMMs",
+                                 "library": "torch.matmul (hipBLASLt)", "device": gpu_info(torch)},
+                      "layers": rows}), flush=True)
 
 
 def residual_join(args):
@@ -808,6 +859,9 @@ def main():
         return
     if args.residual_join:
         residual_join(args)
+        return
+    if args.vendor_gemm:
+        vendor_gemm(args)
         return
     if args.vision:
         import torch
