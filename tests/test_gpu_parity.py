@@ -392,6 +392,61 @@ def test_config5_resnet_bf16_sampled(oracle_lib):
         _check_layer(oracle_lib, 5, i, l, images=[0, l.N - 1], kmax=24, tol=TOL_BF16)
 
 
+def _stack_layer(config, i, l):
+    """One layer through a one-layer stack (filters packed at create, a
+    workspace of its own): the kernels the bench's layer-by-layer passes run.
+    Returns (kernel names, y on the host, the oracle's x, w, bias)."""
+    x, w, b = wl.layer_tensors(config, i, l)
+    bf16 = wl.workload(config).dtype == "bf16"
+    if bf16:
+        x, w = wl.to_bf16_bits(x), wl.to_bf16_bits(w)
+        tx, tw, op = dev_bf16_bits(x), dev_bf16_bits(w), miconv.OP_CONV_BF16
+    else:
+        tx, tw, op = dev(x), dev(w), miconv.OP_CONV_F32
+    P, Q = miconv.out_dims(l.H, l.W, l.R, l.S, l.stride, l.pad)
+    y = torch.full((l.N, l.K, P, Q), float("nan"), device="cuda")
+    st = miconv.Stack([(op, tx, tw, dev(b), y, l.stride, l.pad, l.groups, l.relu)])
+    name = st.describe(0)
+    st.launch()
+    torch.cuda.synchronize()
+    st.close()
+    return name, y.cpu().numpy(), x, w, b
+
+
+def test_config5_stack_whole_layer_per_kernel(oracle_lib):
+    """ResNet-50 at batch 64, bf16 x and w, as the bench's layer-by-layer stack
+    runs it: for every distinct kernel sequence the stack picks, its first
+    layer checked on the whole output (all 64 images, every channel) against
+    the oracle, e <= 2e-2."""
+    picked = {}
+    for i, l in _layers(5):
+        N, C, H, W, K, R, S = l.N, l.C, l.H, l.W, l.K, l.R, l.S
+        name = miconv.conv2d_describe(N, C, H, W, K, R, S, l.stride, l.pad, l.groups, "bf16", mode="stack")[0]
+        picked.setdefault(name, (i, l))
+    assert len(picked) >= 8, sorted(picked)
+    for name, (i, l) in picked.items():
+        print(f"config 5 layer {i} {l.name}: {name}", flush=True)
+        got_name, y, x, w, b = _stack_layer(5, i, l)
+        assert got_name == name, (got_name, name)
+        ref = oracle_lib.conv2d_bf16(x, w, b, l.stride, l.pad, l.groups, l.relu)
+        e = err_inf(y, ref)
+        assert e <= TOL_BF16, f"layer {i} {l.name} ({name}): e={e:.3e}"
+
+
+def test_config4_vgg_batch32_stack_sampled(oracle_lib):
+    """VGG-16 at batch 32 (the bench's --batch 32 run) through one-layer
+    stacks: images 0, 13 and 31, 24 output channels per layer, e <= 1e-4."""
+    for i, l in _layers(4):
+        l = l.with_batch(32)
+        name, y, x, w, b = _stack_layer(4, i, l)
+        print(f"config 4 b32 layer {i} {l.name}: {name}", flush=True)
+        ks = np.unique(np.linspace(0, l.K - 1, 24).astype(int))
+        for n in (0, 13, 31):
+            ref = oracle_lib.conv2d(x[n:n + 1], w[ks], b[ks], l.stride, l.pad, l.groups, l.relu)
+            e = err_inf(y[n:n + 1, ks], ref)
+            assert e <= TOL_F32, f"layer {i} {l.name} image {n}: e={e:.3e}"
+
+
 ERROR_BOUND_CASES = [  # (config, layer index): layers on seeded random data
     (1, 0),     # 64 -> 64 3x3 at 56x56, batch 1
     (2, 0),     # ResNet-50 stem, 7x7 over 3 channels
