@@ -263,7 +263,10 @@ __global__ __launch_bounds__(kThreads, 4) void stem7_bf16_kernel(StemArgs a)
             continue;
         }
         // NCHW fp32: each store instruction writes 32 consecutive pixels
-        // (128 bytes) of two filter planes.
+        // (128 bytes) of two filter planes.  Non-temporal: at batch 64 the
+        // output (205 MB) nearly fills the last-level cache, and written
+        // normally its dirty lines are written back during the following
+        // kernels, slowing them.
         const long plane = (long)a.P * kQ;
 #pragma unroll
         for (int f = 0; f < 2; ++f) {
@@ -279,7 +282,7 @@ __global__ __launch_bounds__(kThreads, 4) void stem7_bf16_kernel(StemArgs a)
                     const long o = yo + 32 * (2 * wave + b) + ll;
                     float val = acc[b][f][v] + bv;
                     if (a.res) val += a.res[o];
-                    a.y[o] = a.relu ? fmaxf(val, 0.f) : val;
+                    __builtin_nontemporal_store(a.relu ? fmaxf(val, 0.f) : val, &a.y[o]);
                 }
             }
         }
