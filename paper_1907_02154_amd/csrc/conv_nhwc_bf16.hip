@@ -723,9 +723,9 @@ __device__ inline void epilogue_cl(const ConvArgs &a, const floatx16 (&acc)[BJ][
                 }
                 d[e] = pack_bf16x2(v0, v1);
             }
-            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-            const u32x4 dv = {d[0], d[1], d[2], d[3]};
-            __builtin_nontemporal_store(dv, reinterpret_cast<u32x4 *>(y + off));
+            // plain stores: the next layer reads y, and the lines it finds in
+            // the last-level cache it does not fetch from HBM
+            *reinterpret_cast<uint4 *>(y + off) = make_uint4(d[0], d[1], d[2], d[3]);
         }
     }
 }
