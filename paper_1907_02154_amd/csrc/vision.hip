@@ -199,17 +199,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_upsweep_kernel(Src src, lon
 }
 
 // Scan: the tile sums of each row become exclusive prefixes, in place (one
-// work-group per row, the same three stages).
-__global__ __launch_bounds__(kScanThreads) void scan_tile_sums_kernel(int32_t *tile_sums, int tiles)
+// 1024-thread work-group per row, the same three stages over chunks of 16384
+// sums: a 2^26-value row in one pass).
+__global__ __launch_bounds__(kScanWide) void scan_tile_sums_kernel(int32_t *tile_sums, int tiles)
 {
-    __shared__ int tile[kScanTile + kScanTile / 16];
-    __shared__ int wsum[kScanThreads / 64];
+    constexpr int kChunk = kScanWide * kScanItems;
+    __shared__ int tile[kChunk + kChunk / 16];
+    __shared__ int wsum[kScanWide / 64];
     const long row = blockIdx.x;
     int carry = 0;
-    for (int b = 0; b < tiles; b += kScanTile)
-        carry = scan_tile<kScanThreads>(SrcI32{tile_sums}, row * tiles + b,
-                                        tiles - b < kScanTile ? tiles - b : kScanTile, tile_sums, carry, true, tile,
-                                        wsum);
+    for (int b = 0; b < tiles; b += kChunk)
+        carry = scan_tile<kScanWide>(SrcI32{tile_sums}, row * tiles + b, tiles - b < kChunk ? tiles - b : kChunk,
+                                     tile_sums, carry, true, tile, wsum);
 }
 
 // Down-sweep: each tile scanned again with the prefix of the tiles before it.
@@ -254,7 +255,7 @@ hipError_t launch_scan(const Src &src, int rows, long n, int32_t *y, bool exclus
     int32_t *sums = static_cast<int32_t *>(ws);
     launch_kernel(scan_upsweep_kernel<Src>, dim3((unsigned)tiles, (unsigned)rows), dim3(kScanThreads), 0, st, src,
                   n, sums);
-    launch_kernel(scan_tile_sums_kernel, dim3((unsigned)rows), dim3(kScanThreads), 0, st, sums, tiles);
+    launch_kernel(scan_tile_sums_kernel, dim3((unsigned)rows), dim3(kScanWide), 0, st, sums, tiles);
     launch_kernel(scan_downsweep_kernel<Src>, dim3((unsigned)tiles, (unsigned)rows), dim3(kScanThreads), 0, st,
                   src, n, static_cast<const int32_t *>(sums), y, exclusive ? 1 : 0);
     return hipGetLastError();
