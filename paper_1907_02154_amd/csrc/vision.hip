@@ -90,9 +90,9 @@ struct SrcScore {
 // kScanItems consecutive values sequentially in registers; scan: Hillis-
 // Steele over the thread totals; down-sweep: each value gets the scanned
 // total of the threads before its own.  Loads and stores are striped over
-// the threads (coalesced) and transposed through LDS.  Returns carry + the
-// tile's sum.
-template <int NT, class Src>
+// the threads (coalesced) and transposed through LDS; NTS: whole tiles are
+// stored non-temporally.  Returns carry + the tile's sum.
+template <int NT, class Src, bool NTS = false>
 __device__ int scan_tile(const Src &src, long base, int len, int32_t *y, int carry, bool exclusive, int *tile,
                          int *wsum)
 {
@@ -138,7 +138,12 @@ __device__ int scan_tile(const Src &src, long base, int len, int32_t *y, int car
         for (int j = 0; j < kScanItems / 4; ++j) {
             const int i4 = j * NT + t;
             const int o = pad16(4 * i4);
-            *reinterpret_cast<int4 *>(y + base + 4L * i4) = int4{tile[o], tile[o + 1], tile[o + 2], tile[o + 3]};
+            typedef int i32x4 __attribute__((ext_vector_type(4)));
+            const i32x4 q = {tile[o], tile[o + 1], tile[o + 2], tile[o + 3]};
+            if constexpr (NTS)
+                __builtin_nontemporal_store(q, reinterpret_cast<i32x4 *>(y + base + 4L * i4));
+            else
+                *reinterpret_cast<i32x4 *>(y + base + 4L * i4) = q;
         }
     } else {
 #pragma unroll
@@ -214,16 +219,20 @@ __global__ __launch_bounds__(kScanWide) void scan_tile_sums_kernel(int32_t *tile
 }
 
 // Down-sweep: each tile scanned again with the prefix of the tiles before it.
+// The tiles are taken last first: the up-sweep has just read them in order,
+// so the last ones are still in the last-level cache; y is stored
+// non-temporally so that it does not evict them (2^26 values: 158 -> 134 us).
 template <class Src>
 __global__ __launch_bounds__(kScanThreads) void scan_downsweep_kernel(Src src, long n, const int32_t *tile_prefix,
                                                                       int32_t *y, int exclusive)
 {
     __shared__ int tile[kScanTile + kScanTile / 16];
     __shared__ int wsum[kScanThreads / 64];
-    const long base = (long)blockIdx.y * n + (long)blockIdx.x * kScanTile;
-    const long rem = n - (long)blockIdx.x * kScanTile;
-    scan_tile<kScanThreads>(src, base, (int)(rem < kScanTile ? rem : kScanTile), y,
-              tile_prefix[(long)blockIdx.y * gridDim.x + blockIdx.x], exclusive != 0, tile, wsum);
+    const long bx = gridDim.x - 1 - blockIdx.x;
+    const long base = (long)blockIdx.y * n + bx * kScanTile;
+    const long rem = n - bx * kScanTile;
+    scan_tile<kScanThreads, Src, true>(src, base, (int)(rem < kScanTile ? rem : kScanTile), y,
+                                       tile_prefix[(long)blockIdx.y * gridDim.x + bx], exclusive != 0, tile, wsum);
 }
 
 // Rows this long or more, fewer than this many of them, go across work-groups.
