@@ -485,7 +485,7 @@ void describe_kernel(const Resolved &r, char *buf, int len, int *launches)
     case IMPL_NHWC_BF16: describe_nhwc_bf16(r.p, r.nplan, buf, len, launches); break;
     case IMPL_STEM_BF16: describe_stem_bf16(buf, len, launches); break;
     case IMPL_POOL_NHWC:
-        snprintf(buf, len, "maxpool_nhwc_bf16_kernel");
+        snprintf(buf, len, r.p.R == 3 && r.p.S == 3 ? "maxpool_nhwc_bf16_kernel<3, 3>" : "maxpool_nhwc_bf16_kernel<0, 0>");
         *launches = 1;
         break;
     case IMPL_POOL_F32:

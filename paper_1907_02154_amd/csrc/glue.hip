@@ -79,36 +79,65 @@ __global__ __launch_bounds__(256) void cast_bf16_kernel(const float *__restrict_
 
 // Max-pool over bf16 channel-last tensors: a thread takes 8 channels of one
 // output pixel (16-byte loads and store); the maximum of bf16 values is one
-// of them, so the result is exact.  Padded positions never win.
+// of them, so the result is exact.  Padded positions never win.  Every offset
+// fits in 32 bits (the host checks both tensors' sizes), and the index
+// divisions use launch-time fast dividers; R_ = S_ = 0 takes the window from
+// the arguments, otherwise the window's loads are all issued before the
+// maxima.
+__device__ __forceinline__ void max_bf16x8(float (&m)[8], uint4 v)
+{
+    const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        m[2 * e] = fmaxf(m[2 * e], bf16_to_f32((uint16_t)(d[e] & 0xFFFFu)));
+        m[2 * e + 1] = fmaxf(m[2 * e + 1], bf16_to_f32((uint16_t)(d[e] >> 16)));
+    }
+}
+
+template <int R_, int S_>
 __global__ __launch_bounds__(256) void maxpool_nhwc_bf16_kernel(const uint16_t *__restrict__ x,
                                                                 uint16_t *__restrict__ y, int C, int H,
-                                                                int W, int R, int S, int stride, int pad,
-                                                                int P, int Q, long total)
+                                                                int W, int Rr, int Sr, int stride, int pad,
+                                                                int P, int Q, unsigned total, FastDiv dv_c8,
+                                                                FastDiv dv_q, FastDiv dv_p)
 {
-    const int C8 = C / 8;
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (long)gridDim.x * blockDim.x) {
-        const int o = (int)(i % C8);
-        const long pix = i / C8;
-        const int q = (int)(pix % Q);
-        const long t = pix / Q;
-        const int p = (int)(t % P);
-        const long n = t / P;
+    const int R = R_ ? R_ : Rr, S = S_ ? S_ : Sr;
+    const unsigned C8 = (unsigned)C / 8;
+    for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const unsigned pix = fdiv(i, dv_c8);
+        const unsigned o = i - pix * C8;
+        const unsigned t = fdiv(pix, dv_q);
+        const int q = (int)(pix - t * (unsigned)Q);
+        const unsigned n = fdiv(t, dv_p);
+        const int p = (int)(t - n * (unsigned)P);
+        const int h0 = p * stride - pad, w0 = q * stride - pad;
         float m[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
-        for (int r = 0; r < R; ++r) {
-            const int h = p * stride - pad + r;
-            if ((unsigned)h >= (unsigned)H) continue;
-            for (int s = 0; s < S; ++s) {
-                const int w = q * stride - pad + s;
-                if ((unsigned)w >= (unsigned)W) continue;
-                const uint4 v = *reinterpret_cast<const uint4 *>(x + ((n * H + h) * W + w) * C + 8 * o);
-                const uint32_t d[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    m[2 * e] = fmaxf(m[2 * e], bf16_to_f32((uint16_t)(d[e] & 0xFFFFu)));
-                    m[2 * e + 1] = fmaxf(m[2 * e + 1], bf16_to_f32((uint16_t)(d[e] >> 16)));
+        for (int r = 0; r < R; ++r) {
+            const int h = h0 + r;
+            if constexpr (S_ != 0) {
+                uint4 v[S_];
+                bool ok[S_];
+#pragma unroll
+                for (int s = 0; s < S_; ++s) {
+                    const int w = w0 + s;
+                    ok[s] = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+                    v[s] = ok[s] ? *reinterpret_cast<const uint4 *>(
+                                       x + ((n * (unsigned)H + h) * (unsigned)W + w) * (unsigned)C + 8 * o)
+                                 : make_uint4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int s = 0; s < S_; ++s)
+                    if (ok[s]) max_bf16x8(m, v[s]);
+            } else {
+                if ((unsigned)h >= (unsigned)H) continue;
+                for (int s = 0; s < S; ++s) {
+                    const int w = w0 + s;
+                    if ((unsigned)w < (unsigned)W)
+                        max_bf16x8(m, *reinterpret_cast<const uint4 *>(
+                                          x + ((n * (unsigned)H + h) * (unsigned)W + w) * (unsigned)C + 8 * o));
                 }
             }
         }
@@ -116,7 +145,7 @@ __global__ __launch_bounds__(256) void maxpool_nhwc_bf16_kernel(const uint16_t *
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             d[e] = pack_bf16x2(m[2 * e], m[2 * e + 1]);
-        *reinterpret_cast<uint4 *>(y + pix * C + 8 * o) = make_uint4(d[0], d[1], d[2], d[3]);
+        *reinterpret_cast<uint4 *>(y + pix * (unsigned)C + 8 * o) = make_uint4(d[0], d[1], d[2], d[3]);
     }
 }
 
@@ -170,8 +199,14 @@ hipError_t launch_maxpool_nhwc_bf16(int N, int C, int H, int W, int R, int S, in
                                     int Q, const uint16_t *x, uint16_t *y, hipStream_t st)
 {
     const long total = (long)N * P * Q * (C / 8);
-    launch_kernel(maxpool_nhwc_bf16_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, y, C, H, W, R, S,
-                  stride, pad, P, Q, total);
+    if ((long)N * H * W * C > INT_MAX || (long)N * P * Q * C > INT_MAX) return hipErrorInvalidValue;
+    const FastDiv dc = make_fastdiv(C / 8), dq = make_fastdiv(Q), dp = make_fastdiv(P);
+    if (R == 3 && S == 3)
+        launch_kernel(maxpool_nhwc_bf16_kernel<3, 3>, dim3(grid_for(total)), dim3(256), 0, st, x, y, C, H, W, R, S,
+                      stride, pad, P, Q, (unsigned)total, dc, dq, dp);
+    else
+        launch_kernel(maxpool_nhwc_bf16_kernel<0, 0>, dim3(grid_for(total)), dim3(256), 0, st, x, y, C, H, W, R, S,
+                      stride, pad, P, Q, (unsigned)total, dc, dq, dp);
     return hipGetLastError();
 }
 

@@ -139,9 +139,11 @@ def test_channel_last_small_int_bitwise(oracle_lib, case):
 
 
 def test_channel_last_maxpool_bitwise(oracle_lib):
-    """ResNet's stem pool (3x3, stride 2, pad 1) and a 2x2/2 pool on bf16
+    """ResNet's stem pool (3x3, stride 2, pad 1), a 2x2/2 pool, and 3x3 pools
+    on odd planes (windows cut by the padding on every side) on bf16
     channel-last data: every output is the oracle's maximum, bit for bit."""
-    for (N, C, H, W, R, st, pad) in ((4, 64, 112, 112, 3, 2, 1), (2, 32, 15, 17, 2, 2, 0), (1, 8, 7, 9, 3, 1, 1)):
+    for (N, C, H, W, R, st, pad) in ((4, 64, 112, 112, 3, 2, 1), (2, 32, 15, 17, 2, 2, 0), (1, 8, 7, 9, 3, 1, 1),
+                                     (3, 24, 13, 11, 3, 2, 1)):
         xb = wl.to_bf16_bits(wl.normal((N, H, W, C), 1.0, 8300 + C))
         P, Q = miconv.out_dims(H, W, R, R, st, pad)
         y = torch.empty((N, P, Q, C), device="cuda", dtype=torch.bfloat16)
