@@ -44,7 +44,7 @@ def dev(a):
 SCAN_CASES = [
     (1, 1), (1, 4095), (1, 4096), (1, 4097), (3, 10000), (1, 16384), (1, 16385),   # one work-group per row
     (2, 100000), (1, 1 << 20), (5, 70001),                                            # across work-groups
-    (300, 1000), (64, 20000),                                                          # many rows
+    (300, 1000), (64, 20000), (70, 30000),                                             # many rows
 ]
 
 
@@ -145,6 +145,7 @@ NMS_CASES = [   # (batch, num, topk, force, id_index, thresh)
     (4, 5000, 400, False, -1, 0.45),    # no class field
     (2, 3000, 129, False, 0, 0.0),      # any overlap suppresses
     (1, 700, 0, False, 0, 0.5),         # topk 0: everything invalid
+    (2, 30000, 200, False, 0, 0.45),    # candidate flags of a row over two scan tiles
 ]
 
 
