@@ -1091,7 +1091,9 @@ __global__ __launch_bounds__(64 * WPX * WCH, 2) void igemm_bf16_dma_res_kernel(C
 // double-buffered by block parity, the next block's patch loaded with the
 // last tap of the current one.  PR = patch rows allocated (BPX + 2W + 2 used).
 // NPB = 1 (one channel block, C/groups == 64): a single patch buffer, loaded
-// once, which keeps a 128 x 64 tile at 48 KB of LDS (three work-groups per CU).
+// once, and a single filter stage, which keeps a 128 x 64 tile at 40 KB of
+// LDS: four work-groups per CU, each waiting for a tap's filters while the
+// others compute.
 template <int BPX, int BKC, int WPX, int WCH, int PR, int NPB, bool RES, bool YCL>
 __device__ __forceinline__ void halo_body(const ConvArgs &a)
 {
@@ -1105,8 +1107,9 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     constexpr int OP = BPX + 4;                          // output tile row pitch (floats)
     static_assert(NPB == 1 || NPB == 2, "patch buffers");
     constexpr int EPI = YCL ? BPX * (BKC + 4) / 4 : BKC * OP / 4;   // epilogue tile, 16-byte units
-    constexpr int SMEM = 2 * UA + NPB * UP > EPI ? 2 * UA + NPB * UP : EPI;
-    __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];   // [A 0][A 1][patch 0][patch 1]
+    constexpr int FA = NPB == 1 ? UA : 2 * UA;           // filter stages (one with one patch buffer)
+    constexpr int SMEM = FA + NPB * UP > EPI ? FA + NPB * UP : EPI;
+    __shared__ __attribute__((aligned(16))) uint4 smem[SMEM];   // [A 0][A 1 (NPB 2)][patch 0][patch 1 (NPB 2)]
     if (NPB == 1 && a.Cg != 64) return;                 // the launcher never sends such a layer
 
     const uint16_t *__restrict__ xcl = static_cast<const uint16_t *>(a.x);   // [N][H][W][C]
@@ -1153,7 +1156,7 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     }
     auto issue_a = [&](int t) {
         const int kr0 = __builtin_amdgcn_readfirstlane(t * 64);
-        uint4 *st = smem + (t & 1) * UA;
+        uint4 *st = smem + (NPB == 1 ? 0 : (t & 1) * UA);
 #pragma unroll
         for (int i = 0; i < LA; ++i) {
             const unsigned off = aok[i] ? aoffs[i] + 2u * kr0 : kOutside;
@@ -1167,7 +1170,7 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     if (prow > PR) return;                              // the launcher never sends such a layer
     const int pinstr = (prow * 8 + NT - 1) / NT;        // uniform
     auto issue_patch = [&](int cb) {
-        uint4 *pb = smem + 2 * UA + (NPB == 2 ? (cb & 1) * UP : 0);
+        uint4 *pb = smem + FA + (NPB == 2 ? (cb & 1) * UP : 0);
         const int cbase = g * a.Cg + cb * 64;
         for (int i = 0; i < pinstr; ++i) {
             const int u = i * NT + tid;
@@ -1208,8 +1211,8 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     auto compute = [&](int t) {
         const int cb = t / 9, tap = t - cb * 9;
         const int r = tap / 3, s = tap - r * 3;
-        const uint4 *sa = smem + (t & 1) * UA;
-        const uint4 *pb = smem + 2 * UA + (NPB == 2 ? (cb & 1) * UP : 0);
+        const uint4 *sa = smem + (NPB == 1 ? 0 : (t & 1) * UA);
+        const uint4 *pb = smem + FA + (NPB == 2 ? (cb & 1) * UP : 0);
         bf16x8 wv[4][BI], xv[4][BJ];
         int prow_l[BJ];
         bool ok[BJ];
@@ -1255,6 +1258,19 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
     ClRes<BPX, BKC, NT> cr;
     if constexpr (YCL) cl_res_load<BPX, BKC, NT>(a, cr, tid, k0, m0, g);
 
+    if constexpr (NPB == 1) {
+        // one filter stage: a tap's filters are requested once every
+        // wavefront is done with the last tap's; the other work-groups on
+        // the CU (four fit) cover the round trip
+        issue_patch(0);
+        for (int t = t_begin; t < t_end; ++t) {
+            if (t > t_begin) asm volatile("s_barrier" ::: "memory");
+            issue_a(t);
+            wait_vmcnt<0>();
+            asm volatile("s_barrier" ::: "memory");
+            compute(t);
+        }
+    } else {
     if (t_begin < t_end) {
         issue_a(t_begin);
         issue_patch(t_begin / 9);
@@ -1269,6 +1285,7 @@ __device__ __forceinline__ void halo_body(const ConvArgs &a)
             if ((t + 1) % 9 == 0) issue_patch((t + 1) / 9);
         }
         compute(t);
+    }
     }
 
     if constexpr (YCL) {
@@ -1506,7 +1523,7 @@ void launch_dma_nchw(const ConvArgs &a, int tile, int mode, dim3 grid, hipStream
 // Halo kernel instances: 128 x 128 tiles with patches of up to 192 rows
 // (BPX + 2W + 2 rows: W <= 31; 80 KB of LDS, two work-groups per CU), and
 // 128 x 64 tiles over one 64-channel block with one patch of up to 256 rows
-// (W <= 63; 48 KB, three per CU).
+// and one filter stage (W <= 63; 40 KB, four per CU).
 hipError_t launch_halo(const ConvArgs &a, int bkc, int pr, dim3 grid, hipStream_t st)
 {
     if (128 + 2 * a.W + 2 > pr || a.R != 3 || a.S != 3 || a.stride != 1 || a.pad != 1 || a.Cg % 64 != 0)
